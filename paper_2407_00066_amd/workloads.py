@@ -1,0 +1,195 @@
+"""Seeded synthetic inputs for the batched multi-adapter linear layer.
+
+This module draws random numbers and lays them out; it holds none of the
+method's arithmetic.  Both the GPU tests/benchmark and the CPU oracle tests
+take their inputs from here, and from nowhere else.
+
+Recipe (one independent numpy PCG64 stream per tensor):
+  seed = 240700066 + 1000 * config_index + stream_id
+Gaussians are drawn in float64, scaled to the stated variance ("N(0, s)" means
+variance s), then cast to float32, or cast to float32 and rounded to nearest
+even bfloat16.  bfloat16 arrays are returned as uint16 bit patterns.
+Shared bases U_k, V_k are the Q factors of a float64 QR of a Gaussian matrix.
+Clusters are a seeded balanced assignment: a permutation of the adapters cut
+into K groups of n/K.  "Zipf(s)" is the finite law P(rank k) ~ k^-s over
+k = 1..n, rank k meaning adapter k-1.
+
+The shapes mirror the paper's serving setting: Mistral-7B-sized layers,
+rank-16 LoRAs, up to ~1000 adapters, random adapters per request, and the
+compression settings it reports (JD-Full, 25 clusters at ~1000 LoRAs).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+SEED_BASE = 240700066
+
+# stream ids
+_S_W, _S_U, _S_V, _S_SIG, _S_X, _S_IDS, _S_CLU, _S_A, _S_B, _S_LEN, _S_SEQ = range(1, 12)
+
+
+def _rng(cfg: int, stream: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(SEED_BASE + 1000 * cfg + stream))
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round float32 to the nearest bfloat16 (ties to even); returns uint16 bits."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    rounded = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _cast(a64: np.ndarray, dtype: str) -> np.ndarray:
+    a32 = a64.astype(np.float32)
+    return a32 if dtype == "f32" else f32_to_bf16_bits(a32)
+
+
+def _gauss(rng: np.random.Generator, shape, var: float, dtype: str, chunk_rows: int = 64) -> np.ndarray:
+    """N(0, var) of the given shape, drawn row-block by row-block along axis 0
+    (the values equal one big draw; chunking only bounds the float64 temporary)."""
+    out = np.empty(shape, np.float32 if dtype == "f32" else np.uint16)
+    std = float(np.sqrt(var))
+    for i in range(0, shape[0], chunk_rows):
+        j = min(shape[0], i + chunk_rows)
+        out[i:j] = _cast(rng.standard_normal((j - i,) + tuple(shape[1:])) * std, dtype)
+    return out
+
+
+def _orthonormal(rng: np.random.Generator, K: int, rows: int, r: int) -> np.ndarray:
+    """K independent rows x r matrices with orthonormal columns (float64)."""
+    out = np.empty((K, rows, r), np.float64)
+    for k in range(K):
+        q, _ = np.linalg.qr(rng.standard_normal((rows, r)))
+        out[k] = q
+    return out
+
+
+def balanced_clusters(rng: np.random.Generator, n: int, K: int) -> np.ndarray:
+    """cluster_of[n]: a random permutation of adapters cut into K groups of n//K
+    (the first n % K groups get one extra)."""
+    perm = rng.permutation(n)
+    cluster_of = np.empty(n, np.int32)
+    sizes = [n // K + (1 if g < n % K else 0) for g in range(K)]
+    pos = 0
+    for g, s in enumerate(sizes):
+        cluster_of[perm[pos:pos + s]] = g
+        pos += s
+    return cluster_of
+
+
+def zipf_ids(rng: np.random.Generator, n: int, size: int, s: float = 1.1) -> np.ndarray:
+    p = np.arange(1, n + 1, dtype=np.float64) ** (-s)
+    p /= p.sum()
+    return rng.choice(n, size=size, p=p).astype(np.int32)
+
+
+def prefill_lengths(rng: np.random.Generator, n_seq: int, total: int, lo: int, hi: int) -> np.ndarray:
+    """n_seq lengths drawn uniformly from {lo..hi}, rescaled to sum to `total`:
+    scale by total/sum, floor, clamp to [lo, hi], then add (or remove) one
+    token per sequence in sequence order, staying inside [lo, hi]."""
+    raw = rng.integers(lo, hi + 1, size=n_seq).astype(np.float64)
+    lens = np.clip(np.floor(raw * total / raw.sum()).astype(np.int64), lo, hi)
+    i = 0
+    while lens.sum() != total:
+        step = 1 if lens.sum() < total else -1
+        if lo <= lens[i] + step <= hi:
+            lens[i] += step
+        i = (i + 1) % n_seq
+    return lens
+
+
+@dataclass
+class Workload:
+    """One batch of one multi-adapter linear layer.
+
+    Layouts: x[T][d_in], W[d_out][d_in], U[K][d_out][r], Vt[K][r][d_in] (= V_k^T),
+    Sigma[n][r][r] (applied as z' = Sigma_i z), A[n][r_l][d_in], B[n][d_out][r_l],
+    adapter_id[T], cluster_of[n].  Float arrays are float32 (dtype "f32") or
+    bfloat16 bits in uint16 (dtype "bf16").
+    """
+    name: str
+    dtype: str
+    T: int
+    d_in: int
+    d_out: int
+    r: int
+    n: int
+    K: int
+    r_l: int
+    x: np.ndarray
+    W: np.ndarray
+    U: np.ndarray
+    Vt: np.ndarray
+    Sigma: np.ndarray
+    adapter_id: np.ndarray
+    cluster_of: np.ndarray
+    A: np.ndarray | None = None
+    B: np.ndarray | None = None
+    meta: dict = field(default_factory=dict)
+
+
+def synthetic(name: str, cfg: int, *, T: int, d_in: int, d_out: int, r: int, n: int, K: int,
+              r_l: int = 16, dtype: str = "bf16", ids: str = "uniform", w_var: float | None = None,
+              sigma_var: float | None = None, a_var: float | None = None, b_var: float | None = None,
+              x_var: float = 1.0, with_lora: bool = True, n_seq: int = 32,
+              seq_len: tuple[int, int] = (32, 256)) -> Workload:
+    """General seeded workload.  ids: "uniform" (per token), "zipf" (Zipf(1.1)
+    per token), or "prefill" (n_seq sequences of lengths U{seq_len} rescaled to
+    T, one Zipf(1.1) adapter per sequence, tokens contiguous per sequence)."""
+    w_var = 1.0 / d_in if w_var is None else w_var
+    sigma_var = 1.0 / r if sigma_var is None else sigma_var
+    a_var = 1.0 / d_in if a_var is None else a_var
+    b_var = 1.0 / (64.0 * r_l) if b_var is None else b_var
+
+    W = _gauss(_rng(cfg, _S_W), (d_out, d_in), w_var, dtype)
+    U = _cast(_orthonormal(_rng(cfg, _S_U), K, d_out, r), dtype)
+    Vt = _cast(np.ascontiguousarray(_orthonormal(_rng(cfg, _S_V), K, d_in, r).transpose(0, 2, 1)), dtype)
+    Sigma = _gauss(_rng(cfg, _S_SIG), (n, r, r), sigma_var, dtype)
+    x = _gauss(_rng(cfg, _S_X), (T, d_in), x_var, dtype)
+    cluster_of = balanced_clusters(_rng(cfg, _S_CLU), n, K)
+    meta = {}
+    rid = _rng(cfg, _S_IDS)
+    if ids == "uniform":
+        adapter_id = rid.integers(0, n, size=T).astype(np.int32)
+    elif ids == "zipf":
+        adapter_id = zipf_ids(rid, n, T)
+    elif ids == "prefill":
+        lens = prefill_lengths(_rng(cfg, _S_LEN), n_seq, T, seq_len[0], seq_len[1])
+        seq_ad = zipf_ids(_rng(cfg, _S_SEQ), n, n_seq)
+        adapter_id = np.repeat(seq_ad, lens).astype(np.int32)
+        meta["seq_lens"] = lens
+        meta["seq_adapters"] = seq_ad
+    else:
+        raise ValueError(ids)
+    A = B = None
+    if with_lora:
+        A = _gauss(_rng(cfg, _S_A), (n, r_l, d_in), a_var, dtype, chunk_rows=8)
+        B = _gauss(_rng(cfg, _S_B), (n, d_out, r_l), b_var, dtype, chunk_rows=8)
+    return Workload(name, dtype, T, d_in, d_out, r, n, K, r_l, x, W, U, Vt, Sigma,
+                    adapter_id, cluster_of, A, B, meta)
+
+
+# The named workloads.  The index is the seed's config index.
+CONFIGS = {
+    # d=256 fp32; 8 rank-4 LoRAs ~N(0,1/16); one r=16 cluster; 32 uniform tokens.
+    "tiny_fp32": dict(cfg=0, T=32, d_in=256, d_out=256, r=16, n=8, K=1, r_l=4, dtype="f32",
+                      ids="uniform", sigma_var=1.0 / 16, a_var=1.0 / 16, b_var=1.0 / 16),
+    # 7B-shaped q_proj decode: d=4096, 100 LoRAs, one r=64 cluster, 64 uniform tokens.
+    "decode_q": dict(cfg=1, T=64, d_in=4096, d_out=4096, r=64, n=100, K=1, ids="uniform"),
+    # Prefill mix: 1000 LoRAs in 25 clusters (r=64), 32 sequences, 4096 tokens.
+    "prefill_mix": dict(cfg=2, T=4096, d_in=4096, d_out=4096, r=64, n=1000, K=25, ids="prefill"),
+    # MLP gate/up: 4096 -> 14336, 1000 LoRAs in 50 clusters (r=128), 256 Zipf tokens.
+    "mlp_up": dict(cfg=3, T=256, d_in=4096, d_out=14336, r=128, n=1000, K=50, ids="zipf"),
+}
+
+
+def make(name: str, **overrides) -> Workload:
+    spec = dict(CONFIGS[name])
+    spec.update(overrides)
+    return synthetic(name, **spec)
