@@ -1,0 +1,137 @@
+/*
+ * cts.h -- C ABI of the MI355X library for the batched multi-adapter linear
+ * layer of "Compress then Serve: Serving Thousands of LoRA Adapters with
+ * Little Overhead" (arXiv 2407.00066).
+ *
+ * The layer.  A batch holds T tokens; token t carries its own LoRA id
+ * i(t) = adapter_id[t] (App. D: each request names the LoRA it wants).  The
+ * n LoRAs were compressed offline into K clusters (Sec. 3.2); LoRA i belongs
+ * to cluster k(i) = cluster_of[i], whose shared bases U_k, V_k are resident
+ * on the GPU while Sigma_i is the LoRA's own r x r core (Sec. 3.1).  Then
+ *
+ *     y_t = W x_t + U_k Sigma_{i(t)} V_k^T x_t,        k = cluster_of[i(t)]
+ *
+ * i.e. (W_0 + Delta_i) x_t with Delta_i = U_k Sigma_i V_k^T (Sec. 3 and
+ * Sec. 3.1 objective; the base term is computed once for the batch and the
+ * adapter term per token, App. D).  The comparison path computes the same
+ * layer with the uncompressed LoRAs, y_t = W x_t + B_i A_i x_t (Sec. 3).
+ *
+ * Layouts (row-major, element type given by cts_problem.dtype):
+ *   x      [T][d_in]              W      [d_out][d_in]
+ *   U      [K][d_out][r]          Vt     [K][r][d_in]   (V_k transposed)
+ *   Sigma  [n][r][r]              applied as z' = Sigma_i z
+ *   A      [n][r_lora][d_in]      B      [n][d_out][r_lora]
+ *   y      [T][d_out]             element type cts_problem.out_dtype
+ *   adapter_id int32 [T], cluster_of int32 [n]
+ * There is no scale argument: a LoRA scale such as alpha/r is folded into
+ * Sigma_i (or B_i) by the caller.
+ *
+ * Memory and ownership.  Every array pointer is DEVICE memory owned by the
+ * caller; `p` is HOST memory, read during the call only.  The library never
+ * allocates, frees or synchronises in these calls: the caller provides a
+ * device workspace of at least cts_workspace_size(p) (resp.
+ * cts_workspace_size_uncompressed(p)) bytes, which may be reused between
+ * calls on the same stream.  `stream` is a hipStream_t (NULL = the null
+ * stream); calls only enqueue work on it and return.  Results are valid once
+ * the stream has reached that point.  Concurrent calls need distinct
+ * workspaces and outputs.
+ *
+ * Errors.  Every argument error is detected on the host before any HIP call
+ * and reported by the return code; nothing is launched then.  T == 0 is a
+ * valid no-op.  Device launch failures give CTS_ERR_HIP.  Ids are a
+ * precondition like pointer validity in BLAS: 0 <= adapter_id[t] < n and
+ * 0 <= cluster_of[i] < K.  The kernels clamp out-of-range ids so that they
+ * never access memory outside the arrays, but the output rows of such tokens
+ * are unspecified; cts_validate_ids checks the ids (synchronously).
+ * A token that should see only the base layer can use an adapter whose
+ * Sigma_i is zero: U_k * 0 adds exactly nothing.
+ */
+#ifndef CTS_H
+#define CTS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CTS_OK = 0,
+    CTS_ERR_INVALID_ARG = 1,   /* null pointer, non-positive size, overlap */
+    CTS_ERR_UNSUPPORTED = 2,   /* valid but outside this library's limits */
+    CTS_ERR_WORKSPACE = 3,     /* workspace smaller than required */
+    CTS_ERR_HIP = 4,           /* a HIP call or kernel launch failed */
+    CTS_ERR_BAD_IDS = 5        /* cts_validate_ids found an id out of range */
+} cts_status;
+
+typedef enum { CTS_F32 = 0, CTS_BF16 = 1 } cts_dtype;
+
+/* Problem description (host memory).  Limits (else CTS_ERR_UNSUPPORTED):
+ *   0 <= T <= 8192, d_in and d_out multiples of 8,
+ *   r: multiple of 8 in [8, 128]; r_lora: multiple of 4 (f32) or 8 (bf16)
+ *   in [4, 128]; 1 <= n_adapters <= 65536; 1 <= n_clusters <= 65536;
+ *   dtype F32 with out_dtype F32, or dtype BF16 with out_dtype BF16 or F32.
+ * Arithmetic: fp32 inputs are multiplied in fp32; bf16 inputs are multiplied
+ * on bf16 matrix cores with fp32 accumulation; V^T x is kept in fp32, Sigma
+ * is applied in fp32, and the result is rounded to the input type before the
+ * U (or B) product.  Fields a call does not use are ignored (r, n_clusters
+ * for the uncompressed path; r_lora for the compressed one). */
+typedef struct {
+    int32_t T;            /* tokens in the batch */
+    int32_t d_in;         /* input features of the layer */
+    int32_t d_out;        /* output features of the layer */
+    int32_t r;            /* rank of the shared bases U_k, V_k */
+    int32_t n_adapters;   /* n: LoRAs in the collection */
+    int32_t n_clusters;   /* K: clusters */
+    int32_t r_lora;       /* rank of the uncompressed LoRAs (B_i, A_i) */
+    int32_t dtype;        /* cts_dtype of x, W, U, Vt, Sigma, A, B */
+    int32_t out_dtype;    /* cts_dtype of y */
+} cts_problem;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* cts_status_string(int status);
+
+/* Bytes of device workspace cts_apply needs for `p` (0 if p is invalid). */
+size_t cts_workspace_size(const cts_problem* p);
+
+/* Bytes of device workspace cts_apply_uncompressed needs for `p`. */
+size_t cts_workspace_size_uncompressed(const cts_problem* p);
+
+/* Token bucketing (the grouping of tokens by cluster that makes the shared-
+ * basis products contiguous GEMMs; Sec. 3.2 gives every LoRA of a cluster the
+ * same U_k, V_k).  Sorts the tokens by the key (cluster_of[adapter_id[t]],
+ * adapter_id[t], t), which is unique, so the result is exact and unique:
+ *   perm[j]            = token with the j-th smallest key        (int32 [T])
+ *   cluster_offsets[k] = number of tokens whose cluster is < k   (int32 [K+1])
+ * cluster_of == NULL means every adapter is its own cluster (then K == n).
+ * All arrays are device memory; T == 0 writes only cluster_offsets (zeros). */
+int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of,
+                        int32_t T, int32_t n, int32_t K,
+                        int32_t* perm, int32_t* cluster_offsets, void* stream);
+
+/* Compressed multi-adapter layer: overwrites y[t] with
+ * W x_t + U_k Sigma_i V_k^T x_t for every token (Sec. 3.1, 3.2, App. D).
+ * y must not overlap any input or the workspace. */
+int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
+              const int32_t* cluster_of, const void* W, const void* U,
+              const void* Vt, const void* Sigma, void* y,
+              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Uncompressed comparison path: overwrites y[t] with W x_t + B_i A_i x_t
+ * (Sec. 3, first paragraph), i = adapter_id[t], rank p->r_lora. */
+int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                           const void* W, const void* A, const void* B, void* y,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Synchronous id check for tests and debugging: copies the ids to the host
+ * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is
+ * outside [0, n) or any cluster_of outside [0, K) (cluster_of may be NULL). */
+int cts_validate_ids(const cts_problem* p, const int32_t* adapter_id,
+                     const int32_t* cluster_of, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CTS_H */

@@ -1,0 +1,215 @@
+"""ctypes binding of libcts.so (include/cts.h).
+
+Argument marshalling only: shapes, dtypes and devices are checked, raw
+device pointers and the current HIP stream are handed to the C library, and
+every step of the layer runs in the library's kernels.  There is no fallback:
+if libcts.so is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcts.so")
+_lib = None
+_lock = threading.Lock()
+
+CTS_OK, CTS_ERR_INVALID_ARG, CTS_ERR_UNSUPPORTED, CTS_ERR_WORKSPACE, CTS_ERR_HIP, CTS_ERR_BAD_IDS = range(6)
+CTS_F32, CTS_BF16 = 0, 1
+
+# every symbol include/cts.h declares
+EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
+            "cts_sort_by_cluster", "cts_apply", "cts_apply_uncompressed", "cts_validate_ids")
+
+
+class CtsError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__("%s: %s" % (where, status_string(code)))
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("d_in", ctypes.c_int32), ("d_out", ctypes.c_int32),
+                ("r", ctypes.c_int32), ("n_adapters", ctypes.c_int32),
+                ("n_clusters", ctypes.c_int32), ("r_lora", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        with _lock:
+            if _lib is None:
+                if not os.path.exists(_LIB_PATH):
+                    raise RuntimeError("libcts.so is not built (%s); run "
+                                       "`python -m paper_2407_00066_amd.build`" % _LIB_PATH)
+                L = ctypes.CDLL(_LIB_PATH)
+                vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+                pp = ctypes.POINTER(Problem)
+                L.cts_status_string.argtypes = [ctypes.c_int]
+                L.cts_status_string.restype = ctypes.c_char_p
+                L.cts_workspace_size.argtypes = [pp]
+                L.cts_workspace_size.restype = sz
+                L.cts_workspace_size_uncompressed.argtypes = [pp]
+                L.cts_workspace_size_uncompressed.restype = sz
+                L.cts_sort_by_cluster.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp]
+                L.cts_sort_by_cluster.restype = ctypes.c_int
+                L.cts_apply.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_apply.restype = ctypes.c_int
+                L.cts_apply_uncompressed.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_apply_uncompressed.restype = ctypes.c_int
+                L.cts_validate_ids.argtypes = [pp, vp, vp, vp]
+                L.cts_validate_ids.restype = ctypes.c_int
+                _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().cts_status_string(int(code)).decode()
+
+
+def _check(code: int, where: str):
+    if code != CTS_OK:
+        raise CtsError(code, where)
+
+
+_TORCH_DT = {torch.float32: CTS_F32, torch.bfloat16: CTS_BF16}
+
+
+def _dt(t: torch.Tensor, name: str) -> int:
+    if t.dtype not in _TORCH_DT:
+        raise TypeError("%s must be float32 or bfloat16, got %s" % (name, t.dtype))
+    return _TORCH_DT[t.dtype]
+
+
+def _dev(t: torch.Tensor, name: str, device: torch.device, dtype=None, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    return ctypes.c_void_p(t.data_ptr()) if t.numel() else None
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+_ws_cache: dict = {}
+
+
+def _workspace(device: torch.device, nbytes: int, workspace):
+    if workspace is not None:
+        if workspace.device != device or workspace.dtype != torch.uint8:
+            raise ValueError("workspace must be a uint8 tensor on %s" % device)
+        return workspace
+    ws = _ws_cache.get(device)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+        _ws_cache[device] = ws
+    return ws
+
+
+def make_problem(T, d_in, d_out, r=0, n_adapters=1, n_clusters=1, r_lora=0,
+                 dtype=CTS_BF16, out_dtype=None) -> Problem:
+    return Problem(T, d_in, d_out, r, n_adapters, n_clusters, r_lora, dtype,
+                   dtype if out_dtype is None else out_dtype)
+
+
+def workspace_size(p: Problem, compressed: bool = True) -> int:
+    f = lib().cts_workspace_size if compressed else lib().cts_workspace_size_uncompressed
+    return int(f(ctypes.byref(p)))
+
+
+def sort_by_cluster(adapter_id: torch.Tensor, cluster_of: torch.Tensor | None, n: int, K: int,
+                    perm: torch.Tensor | None = None, offsets: torch.Tensor | None = None):
+    """(perm, cluster_offsets): tokens sorted by (cluster, adapter, token)."""
+    dev = adapter_id.device
+    T = adapter_id.numel()
+    if perm is None:
+        perm = torch.empty(T, dtype=torch.int32, device=dev)
+    if offsets is None:
+        offsets = torch.empty(K + 1, dtype=torch.int32, device=dev)
+    a = _dev(adapter_id, "adapter_id", dev, torch.int32, (T,))
+    c = _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)) if cluster_of is not None else None
+    pp = _dev(perm, "perm", dev, torch.int32, (T,))
+    oo = _dev(offsets, "offsets", dev, torch.int32, (K + 1,))
+    _check(lib().cts_sort_by_cluster(a, c, T, n, K, pp, oo, _stream(dev)), "cts_sort_by_cluster")
+    return perm, offsets
+
+
+def apply(x, adapter_id, cluster_of, W, U, Vt, Sigma, out=None, out_dtype=None, workspace=None):
+    """y = W x_t + U_k Sigma_i V_k^T x_t per token (see include/cts.h)."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    K, _, r = U.shape
+    n = Sigma.shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=dt,
+                     out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(U, "U", dev, tdt, (K, d_out, r)),
+            _dev(Vt, "Vt", dev, tdt, (K, r, d_in)),
+            _dev(Sigma, "Sigma", dev, tdt, (n, r, r)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    nbytes = workspace_size(p, True)   # 0 for an invalid problem: cts_apply reports why
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                           _stream(dev)), "cts_apply")
+    return out
+
+
+def apply_uncompressed(x, adapter_id, W, A, B, out=None, out_dtype=None, workspace=None):
+    """y = W x_t + B_i A_i x_t per token (see include/cts.h)."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    n, r_l, _ = A.shape
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, n_adapters=n, r_lora=r_l, dtype=dt, out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(A, "A", dev, tdt, (n, r_l, d_in)),
+            _dev(B, "B", dev, tdt, (n, d_out, r_l)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    nbytes = workspace_size(p, False)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_uncompressed(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()),
+                                        ws.numel(), _stream(dev)), "cts_apply_uncompressed")
+    return out
+
+
+def validate_ids(adapter_id, cluster_of, n: int, K: int = 1) -> bool:
+    """True if every id is in range (synchronous; for tests and debugging)."""
+    dev = adapter_id.device
+    T = adapter_id.numel()
+    p = make_problem(T, 8, 8, n_adapters=n, n_clusters=K)
+    a = _dev(adapter_id, "adapter_id", dev, torch.int32, (T,))
+    c = _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)) if cluster_of is not None else None
+    code = lib().cts_validate_ids(ctypes.byref(p), a, c, _stream(dev))
+    if code == CTS_ERR_BAD_IDS:
+        return False
+    _check(code, "cts_validate_ids")
+    return True

@@ -1,0 +1,275 @@
+// C entry points of libcts: argument validation (pure host code, no HIP call
+// before every check has passed), workspace planning and the launch
+// sequence of the layer:
+//   1. bucketing          tokens sorted by (cluster, adapter)         sort.hip
+//   2. shrink             Z  = V_k^T X per cluster segment (fp32)     gemm.hip
+//   3. core               Z' = Sigma_i Z per token                     sigma.hip
+//   4. fused base + up    Y  = W X + U_k Z' scattered to token order   gemm.hip
+//   (5. split-K reduce    only when the fused GEMM is split along k)   sigma.hip
+// The uncompressed comparison path runs the same stages with one segment per
+// adapter, V_k^T -> A_i, U_k -> B_i and no core product.
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "cts.h"
+#include "cts_internal.h"
+
+namespace {
+
+using cts::Tile;
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+  int elt, out_elt;
+  int rank, nseg;
+  Tile main_tile, shrink_tile;
+  int main_split, shrink_split;
+  size_t off_perm, off_seg, off_aid, off_offs, off_zpart, off_zp, off_ypart, total;
+};
+
+int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
+
+// Validates the sizes of `p` for the compressed (compressed=true) or the
+// uncompressed path and fills the launch plan.  Pure host arithmetic.
+int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
+  if (!p) return CTS_ERR_INVALID_ARG;
+  if (p->T < 0 || p->d_in < 1 || p->d_out < 1 || p->n_adapters < 1) return CTS_ERR_INVALID_ARG;
+  if (compressed && (p->r < 1 || p->n_clusters < 1)) return CTS_ERR_INVALID_ARG;
+  if (!compressed && p->r_lora < 1) return CTS_ERR_INVALID_ARG;
+  if (p->dtype != CTS_F32 && p->dtype != CTS_BF16) return CTS_ERR_UNSUPPORTED;
+  if (p->out_dtype != CTS_F32 && p->out_dtype != CTS_BF16) return CTS_ERR_UNSUPPORTED;
+  if (p->dtype == CTS_F32 && p->out_dtype != CTS_F32) return CTS_ERR_UNSUPPORTED;
+  if (p->T > cts::kSortMaxT) return CTS_ERR_UNSUPPORTED;
+  if (p->d_in % 8 || p->d_out % 8) return CTS_ERR_UNSUPPORTED;
+  if (p->n_adapters > 65536) return CTS_ERR_UNSUPPORTED;
+  pl->elt = p->dtype == CTS_BF16 ? 2 : 4;
+  pl->out_elt = p->out_dtype == CTS_BF16 ? 2 : 4;
+  if (compressed) {
+    if (p->n_clusters > 65536) return CTS_ERR_UNSUPPORTED;
+    if (p->r % 8 || p->r > 128) return CTS_ERR_UNSUPPORTED;
+    pl->rank = p->r;
+    pl->nseg = p->n_clusters;
+  } else {
+    const int q = 16 / pl->elt;
+    if (p->r_lora % q || p->r_lora > 128) return CTS_ERR_UNSUPPORTED;
+    pl->rank = p->r_lora;
+    pl->nseg = p->n_adapters;
+  }
+
+  const int T = p->T;
+  int BM, BN, BK;
+  // fused GEMM: large MFMA tiles once the batch is prefill-sized, otherwise
+  // small tiles split along k so that the weight stream is spread over >= 256
+  // workgroups (one per compute unit).
+  if (p->dtype == CTS_F32) pl->main_tile = Tile::F32;
+  else pl->main_tile = (T >= 1024) ? Tile::Large : Tile::Small;
+  cts::tile_dims(pl->main_tile, &BM, &BN, &BK);
+  {
+    const int tiles = ceil_div(p->d_out, BM) * ceil_div(std::max(T, 1), BN);
+    const int nk = ceil_div(p->d_in, BK);
+    int s = (pl->main_tile == Tile::Large) ? 1 : ceil_div(256, tiles);
+    pl->main_split = std::max(1, std::min(std::min(s, nk), 16));
+  }
+  pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Small;
+  cts::tile_dims(pl->shrink_tile, &BM, &BN, &BK);
+  {
+    const int tiles = ceil_div(pl->rank, BM) * ceil_div(std::max(T, 1), BN);
+    const int nk = ceil_div(p->d_in, BK);
+    pl->shrink_split = std::max(1, std::min(ceil_div(256, tiles), nk));
+  }
+
+  size_t off = 0;
+  pl->off_perm = off;  off = align_up(off + 4ull * T);
+  pl->off_seg = off;   off = align_up(off + 4ull * T);
+  pl->off_aid = off;   off = align_up(off + 4ull * T);
+  pl->off_offs = off;  off = align_up(off + 4ull * (pl->nseg + 1));
+  pl->off_zpart = off; off = align_up(off + 4ull * pl->shrink_split * T * pl->rank);
+  pl->off_zp = off;    off = align_up(off + static_cast<size_t>(pl->elt) * T * pl->rank);
+  pl->off_ypart = off;
+  if (pl->main_split > 1) off = align_up(off + 4ull * pl->main_split * T * p->d_out);
+  pl->total = off;
+  return CTS_OK;
+}
+
+struct Range { const void* p; size_t bytes; };
+
+bool overlap(Range a, Range b) {
+  if (!a.p || !b.p || !a.bytes || !b.bytes) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// y must not overlap any input or the workspace; the workspace must not
+// overlap any input.
+bool any_overlap(Range y, Range ws, const Range* in, int n_in) {
+  if (overlap(y, ws)) return true;
+  for (int i = 0; i < n_in; ++i)
+    if (overlap(y, in[i]) || overlap(ws, in[i])) return true;
+  return false;
+}
+
+int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void* x,
+              const int32_t* adapter_id, const int32_t* cluster_of, const void* W,
+              const void* Ubasis, const void* Vbasis, const void* Sigma, void* y, void* workspace,
+              hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
+  int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
+  int32_t* said = reinterpret_cast<int32_t*>(ws + pl.off_aid);
+  int32_t* offs = reinterpret_cast<int32_t*>(ws + pl.off_offs);
+  float* zpart = reinterpret_cast<float*>(ws + pl.off_zpart);
+  void* zp = ws + pl.off_zp;
+  float* ypart = reinterpret_cast<float*>(ws + pl.off_ypart);
+  const int T = p->T, rank = pl.rank;
+
+  hipError_t e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
+                                  pl.nseg, perm, offs, sseg, said, stream);
+  if (e != hipSuccess) return CTS_ERR_HIP;
+
+  cts::GemmParams g{};
+  g.M = rank; g.N = T;
+  g.A0 = nullptr; g.K0 = 0;
+  g.A1 = Vbasis; g.seg_stride_a1 = static_cast<int64_t>(rank) * p->d_in; g.lda1 = p->d_in;
+  g.B1 = x; g.ldb1 = p->d_in; g.K1 = p->d_in; g.b1_gather = 1;
+  g.perm = perm; g.sorted_seg = sseg;
+  g.ksplit = pl.shrink_split; g.part = zpart;
+  e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
+  if (e != hipSuccess) return CTS_ERR_HIP;
+
+  e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters,
+                        compressed ? Sigma : nullptr, zp, p->dtype, stream);
+  if (e != hipSuccess) return CTS_ERR_HIP;
+
+  cts::GemmParams f{};
+  f.M = p->d_out; f.N = T;
+  f.A0 = W; f.lda0 = p->d_in; f.B0 = x; f.ldb0 = p->d_in; f.K0 = p->d_in;
+  f.A1 = Ubasis; f.seg_stride_a1 = static_cast<int64_t>(p->d_out) * rank; f.lda1 = rank;
+  f.B1 = zp; f.ldb1 = rank; f.K1 = rank; f.b1_gather = 0;
+  f.perm = perm; f.sorted_seg = sseg;
+  f.ksplit = pl.main_split;
+  f.part = pl.main_split > 1 ? ypart : nullptr;
+  f.out = y; f.ldo = p->d_out; f.out_perm = 1; f.out_dtype = p->out_dtype;
+  e = cts::launch_seg_gemm(f, p->dtype, pl.main_tile, stream);
+  if (e != hipSuccess) return CTS_ERR_HIP;
+
+  if (pl.main_split > 1) {
+    e = cts::launch_splitk_reduce(ypart, pl.main_split, T, p->d_out, perm, y, p->d_out,
+                                  p->out_dtype, stream);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+  }
+  return CTS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cts_status_string(int status) {
+  switch (status) {
+    case CTS_OK: return "CTS_OK";
+    case CTS_ERR_INVALID_ARG: return "CTS_ERR_INVALID_ARG: invalid argument";
+    case CTS_ERR_UNSUPPORTED: return "CTS_ERR_UNSUPPORTED: outside the supported limits";
+    case CTS_ERR_WORKSPACE: return "CTS_ERR_WORKSPACE: workspace too small";
+    case CTS_ERR_HIP: return "CTS_ERR_HIP: HIP runtime or launch failure";
+    case CTS_ERR_BAD_IDS: return "CTS_ERR_BAD_IDS: adapter or cluster id out of range";
+    default: return "CTS_ERR_UNKNOWN";
+  }
+}
+
+size_t cts_workspace_size(const cts_problem* p) {
+  Plan pl;
+  return make_plan(p, true, &pl) == CTS_OK ? pl.total : 0;
+}
+
+size_t cts_workspace_size_uncompressed(const cts_problem* p) {
+  Plan pl;
+  return make_plan(p, false, &pl) == CTS_OK ? pl.total : 0;
+}
+
+int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, int32_t T, int32_t n,
+                        int32_t K, int32_t* perm, int32_t* cluster_offsets, void* stream) {
+  if (T < 0 || n < 1 || K < 1 || !cluster_offsets) return CTS_ERR_INVALID_ARG;
+  if (!cluster_of && K != n) return CTS_ERR_INVALID_ARG;
+  if (T > 0 && (!adapter_id || !perm)) return CTS_ERR_INVALID_ARG;
+  if (T > cts::kSortMaxT || n > 65536 || K > 65536) return CTS_ERR_UNSUPPORTED;
+  const Range out[2] = {{perm, 4ull * T}, {cluster_offsets, 4ull * (K + 1)}};
+  const Range in[2] = {{adapter_id, 4ull * T}, {cluster_of, cluster_of ? 4ull * n : 0}};
+  if (overlap(out[0], out[1])) return CTS_ERR_INVALID_ARG;
+  for (const Range& o : out)
+    for (const Range& i : in)
+      if (overlap(o, i)) return CTS_ERR_INVALID_ARG;
+  const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets,
+                                        nullptr, nullptr, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
+}
+
+int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
+              const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+              const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  const int rc = make_plan(p, true, &pl);
+  if (rc != CTS_OK) return rc;
+  if (p->T == 0) return CTS_OK;
+  if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || !workspace)
+    return CTS_ERR_INVALID_ARG;
+  if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
+  const size_t e = pl.elt;
+  const size_t T = p->T, di = p->d_in, dout = p->d_out, r = p->r, n = p->n_adapters, K = p->n_clusters;
+  const Range in[7] = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
+                       {W, dout * di * e}, {U, K * dout * r * e}, {Vt, K * r * di * e},
+                       {Sigma, n * r * r * e}};
+  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 7))
+    return CTS_ERR_INVALID_ARG;
+  return run_layer(p, pl, true, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                           const void* W, const void* A, const void* B, void* y, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  Plan pl;
+  const int rc = make_plan(p, false, &pl);
+  if (rc != CTS_OK) return rc;
+  if (p->T == 0) return CTS_OK;
+  if (!x || !adapter_id || !W || !A || !B || !y || !workspace) return CTS_ERR_INVALID_ARG;
+  if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
+  const size_t e = pl.elt;
+  const size_t T = p->T, di = p->d_in, dout = p->d_out, rl = p->r_lora, n = p->n_adapters;
+  const Range in[5] = {{x, T * di * e}, {adapter_id, 4 * T}, {W, dout * di * e},
+                       {A, n * rl * di * e}, {B, n * dout * rl * e}};
+  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 5))
+    return CTS_ERR_INVALID_ARG;
+  return run_layer(p, pl, false, x, adapter_id, nullptr, W, B, A, nullptr, y, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+int cts_validate_ids(const cts_problem* p, const int32_t* adapter_id, const int32_t* cluster_of,
+                     void* stream) {
+  if (!p || p->T < 0 || p->n_adapters < 1) return CTS_ERR_INVALID_ARG;
+  if (cluster_of && p->n_clusters < 1) return CTS_ERR_INVALID_ARG;
+  if (p->T > 0 && !adapter_id) return CTS_ERR_INVALID_ARG;
+  const size_t T = p->T, n = p->n_adapters;
+  int32_t* h = static_cast<int32_t*>(malloc(4 * (T + (cluster_of ? n : 0) + 1)));
+  if (!h) return CTS_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int rc = CTS_OK;
+  if (T && hipMemcpyAsync(h, adapter_id, 4 * T, hipMemcpyDeviceToHost, s) != hipSuccess) rc = CTS_ERR_HIP;
+  if (rc == CTS_OK && cluster_of &&
+      hipMemcpyAsync(h + T, cluster_of, 4 * n, hipMemcpyDeviceToHost, s) != hipSuccess) rc = CTS_ERR_HIP;
+  if (rc == CTS_OK && hipStreamSynchronize(s) != hipSuccess) rc = CTS_ERR_HIP;
+  if (rc == CTS_OK) {
+    for (size_t t = 0; t < T; ++t)
+      if (h[t] < 0 || h[t] >= p->n_adapters) rc = CTS_ERR_BAD_IDS;
+    if (cluster_of)
+      for (size_t i = 0; i < n; ++i)
+        if (h[T + i] < 0 || h[T + i] >= p->n_clusters) rc = CTS_ERR_BAD_IDS;
+  }
+  free(h);
+  return rc;
+}
+
+}  // extern "C"

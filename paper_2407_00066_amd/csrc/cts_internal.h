@@ -1,0 +1,74 @@
+// Internal declarations shared by the HIP translation units of libcts.
+// Nothing here is part of the public ABI (see include/cts.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cts {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bfloat16 storage type: raw bits, converted explicitly.
+struct bf16_t { uint16_t bits; };
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// float -> bfloat16, round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// ---------------------------------------------------------------- bucketing
+constexpr int kSortThreads = 1024;
+constexpr int kSortMaxT = 8192;
+
+// Sorts tokens by (cluster, adapter, token).  Writes perm[T] and offs[K+1];
+// optionally sorted_seg[T] (cluster of each sorted position) and
+// sorted_aid[T] (adapter of each sorted position).  cluster_of may be null
+// (every adapter its own cluster, K == n).
+hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
+                       int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
+                       hipStream_t stream);
+
+// ----------------------------------------------------- segmented MFMA GEMM
+// out[j][m] (m < M rows of the weight operand, j < N sorted token positions) =
+//     sum_k A0[m][k] * B0[map(j)][k]                       (dense phase, K0)
+//   + sum_k A1_{seg(j)}[m][k] * B1[map1(j)][k]             (segment phase, K1)
+// where seg(j) = sorted_seg[j] and A1_s = A1 + s * seg_stride_a1.
+// map(j) = perm[j]; map1(j) = perm[j] if b1_gather else j.
+// Output: part != null -> fp32 partials part[ks][j][m] for split ks;
+//         else out[perm[j]][m] (out_perm) or out[j][m], element type out_dtype.
+struct GemmParams {
+  int M, N;
+  const void* A0; int64_t lda0; const void* B0; int64_t ldb0; int K0;
+  const void* A1; int64_t seg_stride_a1; int64_t lda1; const void* B1; int64_t ldb1; int K1;
+  int b1_gather;
+  const int32_t* perm;        // [N] sorted position -> token
+  const int32_t* sorted_seg;  // [N] sorted position -> segment (cluster / adapter)
+  int ksplit;
+  float* part;
+  void* out; int64_t ldo; int out_perm; int out_dtype;
+};
+
+enum class Tile { Large, Small, F32 };
+hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream);
+void tile_dims(Tile tile, int* BM, int* BN, int* BK);
+
+// ------------------------------------------------------------- Sigma stage
+// zp[j][c] = sum_{c'} Sigma_{aid(j)}[c][c'] * (sum_s zpart[s][j][c'])  (Sigma may be null:
+// then zp = sum_s zpart).  Rounded to the input type.
+hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
+                        const void* Sigma, void* zp, int in_dtype, hipStream_t stream);
+
+// y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
+hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,
+                                void* out, int64_t ldo, int out_dtype, hipStream_t stream);
+
+}  // namespace cts

@@ -1,0 +1,161 @@
+"""The C-ABI library loads, exports every symbol include/cts.h declares, and
+rejects every host-detectable argument error before touching HIP.  CPU only:
+no call here reaches a kernel launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2407_00066_amd as cts
+from paper_2407_00066_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cts.h")
+
+FAKE = ctypes.c_void_p(0x10000)   # never dereferenced: validation fails first
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(cts_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_binding_symbols():
+    assert _declared() == sorted(B.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = cts.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    for code in range(6):
+        assert cts.status_string(code).startswith("CTS_")
+    assert cts.status_string(99) == "CTS_ERR_UNKNOWN"
+
+
+def _p(**kw):
+    base = dict(T=64, d_in=4096, d_out=4096, r=64, n_adapters=100, n_clusters=1, r_lora=16)
+    base.update(kw)
+    return cts.make_problem(**base)
+
+
+def _apply(p, ptrs=None, ws_bytes=1 << 40, y=None, ws=None):
+    ptrs = ptrs or [FAKE] * 7
+    y = y if y is not None else ctypes.c_void_p(0x7000_0000_0000)
+    ws = ws if ws is not None else ctypes.c_void_p(0x6000_0000_0000)
+    return cts.lib().cts_apply(ctypes.byref(p), *ptrs[:7], y, ws, ws_bytes, None)
+
+
+def _apply_u(p, ws_bytes=1 << 40):
+    return cts.lib().cts_apply_uncompressed(ctypes.byref(p), *[FAKE] * 5,
+                                            ctypes.c_void_p(0x7000_0000_0000),
+                                            ctypes.c_void_p(0x6000_0000_0000), ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=-1), B.CTS_ERR_INVALID_ARG), (dict(d_in=0), B.CTS_ERR_INVALID_ARG),
+    (dict(d_out=-8), B.CTS_ERR_INVALID_ARG), (dict(r=0), B.CTS_ERR_INVALID_ARG),
+    (dict(n_adapters=0), B.CTS_ERR_INVALID_ARG), (dict(n_clusters=0), B.CTS_ERR_INVALID_ARG),
+    (dict(d_in=4100), B.CTS_ERR_UNSUPPORTED), (dict(d_out=12), B.CTS_ERR_UNSUPPORTED),
+    (dict(r=12), B.CTS_ERR_UNSUPPORTED), (dict(r=136), B.CTS_ERR_UNSUPPORTED),
+    (dict(T=8193), B.CTS_ERR_UNSUPPORTED), (dict(n_adapters=65537), B.CTS_ERR_UNSUPPORTED),
+    (dict(dtype=2), B.CTS_ERR_UNSUPPORTED), (dict(out_dtype=7), B.CTS_ERR_UNSUPPORTED),
+    (dict(dtype=B.CTS_F32, out_dtype=B.CTS_BF16), B.CTS_ERR_UNSUPPORTED),
+])
+def test_apply_rejects_bad_problem(kw, code):
+    assert _apply(_p(**kw)) == code
+    assert cts.workspace_size(_p(**kw)) == 0
+
+
+def test_apply_null_problem():
+    assert cts.lib().cts_apply(None, *[FAKE] * 9, 0, None) == B.CTS_ERR_INVALID_ARG
+
+
+def test_apply_null_pointers():
+    p = _p()
+    for i in range(7):
+        ptrs = [FAKE] * 7
+        ptrs[i] = None
+        assert _apply(p, ptrs) == B.CTS_ERR_INVALID_ARG, i
+    assert _apply(p, y=ctypes.c_void_p(0)) == B.CTS_ERR_INVALID_ARG
+
+
+def test_apply_t0_is_noop_without_pointers():
+    p = _p(T=0)
+    assert cts.lib().cts_apply(ctypes.byref(p), *[None] * 9, 0, None) == B.CTS_OK
+    assert cts.lib().cts_apply_uncompressed(ctypes.byref(p), *[None] * 7, 0, None) == B.CTS_OK
+
+
+def test_apply_workspace_too_small():
+    p = _p()
+    need = cts.workspace_size(p)
+    assert need > 0
+    assert _apply(p, ws_bytes=need - 1) == B.CTS_ERR_WORKSPACE
+
+
+def test_apply_rejects_overlaps():
+    p = _p(T=64, d_in=64, d_out=64, r=8, n_adapters=4)
+    base = 0x5000_0000_0000
+    # inputs far apart; y placed inside W
+    ptrs = [ctypes.c_void_p(base + i * (1 << 30)) for i in range(7)]
+    assert _apply(p, ptrs, y=ctypes.c_void_p(base + 3 * (1 << 30) + 64)) == B.CTS_ERR_INVALID_ARG
+    # workspace overlapping x
+    assert _apply(p, ptrs, ws=ctypes.c_void_p(base + 128)) == B.CTS_ERR_INVALID_ARG
+    # y overlapping the workspace
+    assert _apply(p, ptrs, y=ctypes.c_void_p(0x6000_0000_0000 + 256)) == B.CTS_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(r_lora=0), B.CTS_ERR_INVALID_ARG), (dict(r_lora=12), B.CTS_ERR_UNSUPPORTED),
+    (dict(r_lora=4, dtype=B.CTS_F32, out_dtype=B.CTS_F32, T=0), B.CTS_OK),
+    (dict(r_lora=136), B.CTS_ERR_UNSUPPORTED),
+])
+def test_uncompressed_validation(kw, code):
+    assert _apply_u(_p(**kw)) == code
+
+
+def test_uncompressed_ignores_compressed_fields():
+    p = _p(r=0, n_clusters=0, r_lora=16)
+    assert cts.workspace_size(p, compressed=False) > 0
+    assert _apply_u(p, ws_bytes=1) == B.CTS_ERR_WORKSPACE
+
+
+def test_workspace_grows_with_problem():
+    small = cts.workspace_size(_p(T=32))
+    big = cts.workspace_size(_p(T=4096, n_clusters=25, n_adapters=1000))
+    assert 0 < small < big
+    assert cts.workspace_size(_p(T=0)) >= 0
+
+
+def test_sort_validation():
+    L = cts.lib()
+    f = lambda *a: L.cts_sort_by_cluster(*a, None)
+    assert f(FAKE, FAKE, -1, 4, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 4, 0, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG
+    assert f(FAKE, None, 4, 4, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG   # K must equal n
+    assert f(None, FAKE, 4, 4, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 4, 4, 2, FAKE, None) == B.CTS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 9000, 4, 2, ctypes.c_void_p(0x9000_0000), ctypes.c_void_p(0xA000_0000)) \
+        == B.CTS_ERR_UNSUPPORTED
+    # perm overlapping cluster_offsets
+    assert f(ctypes.c_void_p(0x1000_0000), ctypes.c_void_p(0x2000_0000), 64, 4, 2,
+             ctypes.c_void_p(0x3000_0000), ctypes.c_void_p(0x3000_0000 + 8)) == B.CTS_ERR_INVALID_ARG
+
+
+def test_validate_ids_rejects_bad_problem():
+    L = cts.lib()
+    assert L.cts_validate_ids(None, FAKE, FAKE, None) == B.CTS_ERR_INVALID_ARG
+    p = _p(T=4, n_adapters=0)
+    assert L.cts_validate_ids(ctypes.byref(p), FAKE, FAKE, None) == B.CTS_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "_LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        B.lib()

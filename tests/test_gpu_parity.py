@@ -1,0 +1,249 @@
+"""GPU parity: the HIP library (through the C ABI) against the fp64 oracle.
+
+Bucketing is compared bit for bit.  Outputs are compared per token with the
+inf-norm relative error  max_o |y - y_ref| / max_o |y_ref|, which must stay
+<= 1e-5 for fp32 inputs and <= 2e-2 for bf16 inputs (fp32 accumulation).
+Small cases compare every output; the full-size workloads compare a sample
+of tokens chosen at tile and cluster-segment boundaries (the oracle forms a
+d_out x d_in update per sampled adapter).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2407_00066_amd as cts
+from paper_2407_00066_amd import workloads as wl
+
+from _gpu_helpers import TOL, dev, host, row_rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _sort_case(T, n, K, kind, seed):
+    rs = np.random.default_rng(seed)
+    aid = rs.integers(0, n, T).astype(np.int32)
+    if kind == "same":
+        aid[:] = n // 2
+    elif kind == "sorted":
+        aid = np.sort(aid)
+    elif kind == "reverse":
+        aid = np.sort(aid)[::-1].copy()
+    elif kind == "zipf":
+        aid = wl.zipf_ids(rs, n, T)
+    cof = None if kind == "identity" else rs.integers(0, K, n).astype(np.int32)
+    if kind == "empty":
+        cof = (np.arange(n) % 3 * (K // 3)).astype(np.int32)
+    return aid, cof
+
+
+SORT_CASES = [
+    (0, 5, 2, "uniform"), (1, 5, 2, "uniform"), (63, 8, 3, "uniform"), (64, 8, 3, "uniform"),
+    (65, 100, 1, "uniform"), (1, 1, 1, "uniform"), (500, 1, 1, "uniform"),
+    (4096, 1000, 25, "uniform"), (4096, 1000, 25, "zipf"), (8192, 65536, 4096, "uniform"),
+    (8192, 3, 2, "uniform"), (1000, 1000, 1000, "identity"), (777, 50, 10, "same"),
+    (777, 50, 10, "sorted"), (777, 50, 10, "reverse"), (600, 40, 30, "empty"),
+    (2049, 65536, 65536, "uniform"), (256, 1000, 50, "zipf"),
+]
+
+
+@pytest.mark.parametrize("T,n,K,kind", SORT_CASES)
+def test_sort_bit_exact(oracle_mod, T, n, K, kind):
+    aid, cof = _sort_case(T, n, K, kind, seed=T + 31 * n + K)
+    if kind == "identity":
+        K = n
+    say("sort T=%d n=%d K=%d %s" % (T, n, K, kind))
+    perm, offs = cts.sort_by_cluster(dev(aid), dev(cof) if cof is not None else None, n, K)
+    torch.cuda.synchronize()
+    rp, ro = oracle_mod.sort_by_cluster(aid, cof, n, K)
+    np.testing.assert_array_equal(perm.cpu().numpy(), rp)
+    np.testing.assert_array_equal(offs.cpu().numpy(), ro)
+
+
+# --------------------------------------------------------------------------
+# small and medium cases: every output compared
+
+SMALL = {
+    # name: (synthetic kwargs)
+    "tiny_fp32": dict(wl.CONFIGS["tiny_fp32"]),
+    "f32_ragged": dict(cfg=100, T=45, d_in=136, d_out=200, r=24, n=10, K=3, dtype="f32"),
+    "bf16_ragged": dict(cfg=101, T=203, d_in=392, d_out=328, r=32, n=37, K=5),
+    "bf16_large_tiles": dict(cfg=102, T=1100, d_in=520, d_out=264, r=64, n=50, K=7, ids="prefill",
+                             n_seq=9, seq_len=(40, 250)),
+    "bf16_r128_zipf": dict(cfg=103, T=77, d_in=256, d_out=512, r=128, n=300, K=3, ids="zipf"),
+    "bf16_T1": dict(cfg=104, T=1, d_in=64, d_out=64, r=16, n=3, K=2),
+    "bf16_one_adapter": dict(cfg=105, T=130, d_in=128, d_out=136, r=16, n=1, K=1),
+    "bf16_k_eq_n": dict(cfg=106, T=150, d_in=128, d_out=192, r=16, n=12, K=12),
+    "bf16_r8": dict(cfg=107, T=70, d_in=64, d_out=72, r=8, n=5, K=2),
+    "bf16_empty_clusters": dict(cfg=108, T=90, d_in=64, d_out=64, r=16, n=4, K=9),
+}
+
+
+def _inputs(w):
+    return (dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(w.U), dev(w.Vt),
+            dev(w.Sigma))
+
+
+@pytest.fixture(scope="module")
+def small_cases():
+    return {k: wl.synthetic(k, **v) for k, v in SMALL.items()}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_apply_small(oracle_mod, small_cases, name):
+    w = small_cases[name]
+    say("apply %s T=%d d_in=%d d_out=%d r=%d n=%d K=%d" % (name, w.T, w.d_in, w.d_out, w.r, w.n, w.K))
+    y = cts.apply(*_inputs(w))
+    torch.cuda.synchronize()
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, w.W, w.U, w.Vt, w.Sigma)
+    err = row_rel_err(host(y), ref)
+    assert err <= TOL[w.dtype], err
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "f32_ragged", "bf16_ragged", "bf16_large_tiles",
+                                  "bf16_T1", "bf16_one_adapter"])
+def test_uncompressed_small(oracle_mod, small_cases, name):
+    w = small_cases[name]
+    say("apply_uncompressed %s T=%d r_l=%d n=%d" % (name, w.T, w.r_l, w.n))
+    y = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
+    torch.cuda.synchronize()
+    ref = oracle_mod.apply_uncompressed(w.x, w.adapter_id, w.W, w.A, w.B)
+    err = row_rel_err(host(y), ref)
+    assert err <= TOL[w.dtype], err
+
+
+def test_tiny_exact_compressed_equals_uncompressed(oracle_mod):
+    """Prop. 1 on the GPU: the tiny collection compressed losslessly at r = 32
+    gives the uncompressed layer (both GPU paths and the oracle agree)."""
+    w = wl.make("tiny_fp32")
+    U, Vt, S = oracle_mod.exact_compress(w.A, w.B)
+    U32, V32, S32 = (a.astype(np.float32) for a in (U[None], Vt[None], S))
+    say("tiny-exact r=32")
+    cof = np.zeros(w.n, np.int32)
+    y_c = cts.apply(dev(w.x), dev(w.adapter_id), dev(cof), dev(w.W), dev(U32), dev(V32), dev(S32))
+    y_u = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
+    torch.cuda.synchronize()
+    ref = oracle_mod.apply_uncompressed(w.x, w.adapter_id, w.W, w.A, w.B)
+    assert row_rel_err(host(y_c), ref) <= 1e-5
+    assert row_rel_err(host(y_u), ref) <= 1e-5
+    assert row_rel_err(host(y_c), host(y_u)) <= 1e-5
+
+
+def test_zero_sigma_is_exactly_base_layer(small_cases):
+    """Sigma_i = 0 adds exactly nothing: bitwise equal to B_i = 0 on the
+    uncompressed path (same base GEMM, zero adapter term)."""
+    w = small_cases["bf16_ragged"]
+    say("zero-sigma bitwise")
+    S0 = np.zeros_like(w.Sigma)
+    y_c = cts.apply(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(w.U), dev(w.Vt), dev(S0))
+    y_u = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(np.zeros_like(w.B)))
+    torch.cuda.synchronize()
+    assert torch.equal(y_c, y_u)
+
+
+def test_fp32_output_from_bf16(oracle_mod, small_cases):
+    w = small_cases["bf16_ragged"]
+    say("bf16 in / f32 out")
+    y = cts.apply(*_inputs(w), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert y.dtype == torch.float32
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, w.W, w.U, w.Vt, w.Sigma)
+    assert row_rel_err(host(y), ref) <= TOL["bf16"]
+
+
+def test_deterministic(small_cases):
+    w = small_cases["bf16_large_tiles"]
+    say("determinism")
+    args = _inputs(w)
+    y1 = cts.apply(*args)
+    y2 = cts.apply(*args)
+    u1 = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
+    u2 = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2) and torch.equal(u1, u2)
+
+
+def test_token_permutation_equivariance(small_cases):
+    w = small_cases["bf16_ragged"]
+    say("permutation equivariance")
+    p = np.random.default_rng(5).permutation(w.T)
+    y = cts.apply(*_inputs(w))
+    yp = cts.apply(dev(w.x[p]), dev(w.adapter_id[p]), dev(w.cluster_of), dev(w.W), dev(w.U),
+                   dev(w.Vt), dev(w.Sigma))
+    torch.cuda.synchronize()
+    assert row_rel_err(host(yp), host(y)[p]) <= 1e-6
+
+
+def test_validate_ids():
+    say("validate_ids")
+    aid = torch.tensor([0, 3, 2], dtype=torch.int32, device="cuda")
+    cof = torch.tensor([0, 1, 1, 0], dtype=torch.int32, device="cuda")
+    assert cts.validate_ids(aid, cof, 4, 2)
+    assert not cts.validate_ids(aid, cof[:3], 3, 2)      # adapter id 3 >= n
+    assert not cts.validate_ids(aid, torch.tensor([0, 1, 2, 0], dtype=torch.int32, device="cuda"), 4, 2)
+
+
+def test_out_of_range_ids_do_not_fault(small_cases):
+    """Ids outside [0, n) are clamped inside the kernels; the call completes."""
+    w = small_cases["bf16_r8"]
+    say("out-of-range ids (clamped)")
+    aid = w.adapter_id.copy()
+    aid[0], aid[1] = -7, 1 << 20
+    y = cts.apply(dev(w.x), dev(aid), dev(w.cluster_of), dev(w.W), dev(w.U), dev(w.Vt), dev(w.Sigma))
+    torch.cuda.synchronize()
+    assert torch.isfinite(y.float()).all()
+
+
+# --------------------------------------------------------------------------
+# full-size workloads: sampled tokens
+
+def _sample_tokens(w, oracle_mod, extra=6, cap=14):
+    perm, offs = oracle_mod.sort_by_cluster(w.adapter_id, w.cluster_of, w.n, w.K)
+    pos = {0, w.T - 1}
+    for b in (63, 64, 127, 128):
+        if b < w.T:
+            pos.add(b)
+    for k in range(1, min(w.K, 4)):
+        if 0 < offs[k] < w.T:
+            pos.update({int(offs[k]) - 1, int(offs[k])})
+    rs = np.random.default_rng(w.T)
+    pos.update(rs.integers(0, w.T, extra).tolist())
+    toks = sorted({int(perm[j]) for j in pos})
+    return np.array(toks[:cap], np.int64)
+
+
+@pytest.fixture(scope="module")
+def full_cases():
+    return {}
+
+
+def _full(full_cases, name):
+    if name not in full_cases:
+        say("generating %s" % name)
+        full_cases[name] = wl.make(name)
+    return full_cases[name]
+
+
+@pytest.mark.parametrize("name", ["decode_q", "prefill_mix", "mlp_up"])
+def test_full_config_sampled(oracle_mod, full_cases, name):
+    w = _full(full_cases, name)
+    toks = _sample_tokens(w, oracle_mod, cap=14 if name != "mlp_up" else 8)
+    say("apply %s (full size), %d sampled tokens" % (name, len(toks)))
+    y = cts.apply(*_inputs(w))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, w.W, w.U, w.Vt, w.Sigma, tokens=toks)
+    err = row_rel_err(yh[toks], ref)
+    assert err <= TOL["bf16"], err
+
+
+@pytest.mark.parametrize("name", ["decode_q", "prefill_mix", "mlp_up"])
+def test_full_config_uncompressed_sampled(oracle_mod, full_cases, name):
+    w = _full(full_cases, name)
+    toks = _sample_tokens(w, oracle_mod, cap=10 if name != "mlp_up" else 6)
+    say("apply_uncompressed %s (full size), %d sampled tokens" % (name, len(toks)))
+    y = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
+    torch.cuda.synchronize()
+    ref = oracle_mod.apply_uncompressed(w.x, w.adapter_id, w.W, w.A, w.B, tokens=toks)
+    err = row_rel_err(host(y)[toks], ref)
+    assert err <= TOL["bf16"], err
