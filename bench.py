@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Throughput of the compressed multi-adapter layer (cts_apply) on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+
+A step is one call of the whole layer (bucketing, shrink, core product, fused
+base + up-projection GEMM) over one batch of seeded synthetic inputs that are
+already resident in HBM.  The timed region is K consecutive steps between two
+HIP events on the stream the library launches on.  Inputs are rotated over
+enough device copies (>= 512 MB in total) that the 256 MB last-level cache
+cannot hold them between steps.
+
+One JSON line is printed.  Besides the throughput it carries:
+  roofline      the dominant kernel (the fused GEMM): algorithmic flops or
+                bytes of one launch over its mean duration, measured here with
+                HIP events recorded around it, against MI355X's peak
+  cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
+                the same batch (about --cpu-seconds of work)
+  uncompressed  the same layer through the uncompressed gather path
+                (cts_apply_uncompressed, rank-16 B_i A_i) on the same batch
+  stages_us     mean duration of each stage of the layer
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/s and HBM GB/s (or MFMA util) of cts_apply at 1000 LoRAs, one MI355X"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix cores
+PEAK_F32_TFLOPS = 157.3        # MI355X dense fp32 matrix cores
+MALL_BYTES = 256 << 20
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def to_dev(a, device):
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(a).to(device)
+
+
+def main_kernel_model(w, touched_clusters):
+    """Algorithmic flops and bytes of one launch of the fused GEMM
+    Y = W X + U_k Z' (bytes: W, X, Y, each touched U_k once, Z')."""
+    e = 2 if w.dtype == "bf16" else 4
+    flops = 2.0 * w.T * w.d_in * w.d_out + 2.0 * w.T * w.r * w.d_out
+    nbytes = e * (w.d_out * w.d_in + w.T * w.d_in + w.T * w.d_out
+                  + touched_clusters * w.d_out * w.r + w.T * w.r)
+    return flops, nbytes
+
+
+def cpu_baseline(w, target_s):
+    """The oracle on a prefix of the batch (in batch order), grown until about
+    target_s seconds of oracle time; tokens/s = tokens / oracle seconds."""
+    import numpy as np
+    from oracle import oracle
+    f64 = [oracle.to_f64(a) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
+    spent, done, chunk = 0.0, 0, min(64, w.T)
+    while done < w.T and spent < target_s:
+        toks = np.arange(done, min(w.T, done + chunk))
+        tm = {}
+        oracle.apply(f64[0], w.adapter_id, w.cluster_of, f64[1], f64[2], f64[3], f64[4],
+                     tokens=toks, timing=tm)
+        spent += tm["s"]
+        done += len(toks)
+        per_tok = spent / done
+        chunk = int(max(1, min(w.T - done, (target_s - spent) / per_tok + 1)))
+    distinct = len(set(w.adapter_id[:done].tolist()))
+    return {"value": done / spent, "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "first %d of %d tokens of the batch (%d distinct adapters), %.1f s of "
+                      "fp64 oracle time" % (done, w.T, distinct, spent)}
+
+
+def time_steps(fn, sets, steps, warmup, torch):
+    for i in range(warmup):
+        fn(sets[i % len(sets)])
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for i in range(steps):
+        fn(sets[i % len(sets)])
+    ev1.record()
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / steps          # ms per step
+
+
+def stage_times(fn, sets, steps, torch, cts):
+    """Mean duration (us) of each stage, from events at its boundaries."""
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(cts.N_STAGE_EVENTS)]
+           for _ in range(steps)]
+    for i in range(steps):
+        cts.set_stage_events(evs[i])
+        fn(sets[i % len(sets)])
+    cts.set_stage_events(None)
+    torch.cuda.synchronize()
+    names = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
+    out = {}
+    for s, name in enumerate(names):
+        out[name] = 1e3 * sum(e[s].elapsed_time(e[s + 1]) for e in evs) / steps
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="prefill_mix",
+                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32"])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: the layer has no cross-GPU communication and this "
+              "build runs on a single GPU; run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2407_00066_amd as cts
+    from paper_2407_00066_amd import _binding as B
+    from paper_2407_00066_amd import workloads as wl
+
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    log("generating %s" % args.workload)
+    w = wl.make(args.workload)
+
+    set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
+    n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
+    base = [to_dev(a, device) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
+    sets = [base] + [[t.clone() for t in base] for _ in range(n_sets - 1)]
+    aid = to_dev(w.adapter_id, device)
+    cof = to_dev(w.cluster_of, device)
+    y = torch.empty((w.T, w.d_out), dtype=base[0].dtype, device=device)
+    p = cts.make_problem(w.T, w.d_in, w.d_out, r=w.r, n_adapters=w.n, n_clusters=w.K,
+                         dtype=B.CTS_BF16 if w.dtype == "bf16" else B.CTS_F32)
+    ws = torch.empty(max(1, cts.workspace_size(p)), dtype=torch.uint8, device=device)
+
+    def step(s):
+        x, W, U, Vt, S = s
+        cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+
+    log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
+        (n_sets, set_bytes / 1e6, args.warmup, args.steps))
+    ms = time_steps(step, sets, args.steps, args.warmup, torch)
+    stages = stage_times(step, sets, args.steps, torch, B)
+
+    # uncompressed comparison on the same batch
+    uA, uB = to_dev(w.A, device), to_dev(w.B, device)
+    pu = cts.make_problem(w.T, w.d_in, w.d_out, n_adapters=w.n, r_lora=w.r_l,
+                          dtype=B.CTS_BF16 if w.dtype == "bf16" else B.CTS_F32)
+    wsu = torch.empty(max(1, cts.workspace_size(pu, compressed=False)), dtype=torch.uint8, device=device)
+
+    def step_u(s):
+        x, W = s[0], s[1]
+        cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
+
+    log("timing cts_apply_uncompressed")
+    ms_u = time_steps(step_u, sets, args.steps, args.warmup, torch)
+    stages_u = stage_times(step_u, sets, args.steps, torch, B)
+    del uA, uB
+
+    touched = len(set(w.cluster_of[w.adapter_id].tolist()))
+    flops, nbytes = main_kernel_model(w, touched)
+    t_main = stages["fused_gemm"] * 1e-6
+    peak_fl = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    if flops / (peak_fl * 1e12) >= nbytes / (PEAK_HBM_GBS * 1e9):
+        achieved = flops / t_main / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_fl, "unit": "TFLOP/s",
+                "frac": round(achieved / peak_fl, 4), "traffic": None}
+    else:
+        achieved = nbytes / t_main / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    roof.update({"kernel": "seg_gemm_kernel (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
+                 "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    value = w.T / (ms * 1e-3)
+    rec = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
+        "config": {"workload": args.workload, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
+                   "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
+                   "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "uncompressed": {"value": round(w.T / (ms_u * 1e-3), 1), "unit": "tokens/s",
+                         "ms_per_step": round(ms_u, 5), "r_lora": w.r_l,
+                         "stages_us": {k: round(v, 2) for k, v in stages_u.items()}},
+        "stages_us": {k: round(v, 2) for k, v in stages.items()},
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -130,6 +130,20 @@ int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* a
 int cts_validate_ids(const cts_problem* p, const int32_t* adapter_id,
                      const int32_t* cluster_of, void* stream);
 
+/* Profiling aid; correct use of the library never needs it.
+ * events == NULL turns it off.  Otherwise `events` is a host array of
+ * CTS_N_STAGE_EVENTS hipEvent_t handles owned by the caller; the handles are
+ * copied, and every later cts_apply / cts_apply_uncompressed call records
+ * them on its stream at the stage boundaries of the layer:
+ *   [0] before the bucketing          [1] before the shrink V_k^T X
+ *   [2] before the core product       [3] before the fused W X + U_k Z' GEMM
+ *   [4] after the fused GEMM          [5] after the split-K reduction
+ *                                         (right after [4] when there is none)
+ * The setting is process-wide; changing it while another thread is inside a
+ * cts_apply call is a race. */
+#define CTS_N_STAGE_EVENTS 6
+int cts_set_stage_events(void* const* events);
+
 #ifdef __cplusplus
 }
 #endif

@@ -5,5 +5,5 @@ The kernels and the C ABI live in libcts.so (include/cts.h); this package
 binds it with ctypes.  torch is used only for device memory and streams.
 """
 from ._binding import (CtsError, Problem, apply, apply_uncompressed, lib, make_problem,  # noqa: F401
-                       sort_by_cluster, status_string, validate_ids, workspace_size,
+                       set_stage_events, sort_by_cluster, status_string, validate_ids, workspace_size,
                        CTS_F32, CTS_BF16)

@@ -22,7 +22,9 @@ CTS_F32, CTS_BF16 = 0, 1
 
 # every symbol include/cts.h declares
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
-            "cts_sort_by_cluster", "cts_apply", "cts_apply_uncompressed", "cts_validate_ids")
+            "cts_sort_by_cluster", "cts_apply", "cts_apply_uncompressed", "cts_validate_ids",
+            "cts_set_stage_events")
+N_STAGE_EVENTS = 6
 
 
 class CtsError(RuntimeError):
@@ -64,6 +66,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_apply_uncompressed.restype = ctypes.c_int
                 L.cts_validate_ids.argtypes = [pp, vp, vp, vp]
                 L.cts_validate_ids.restype = ctypes.c_int
+                L.cts_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+                L.cts_set_stage_events.restype = ctypes.c_int
                 _lib = L
     return _lib
 
@@ -213,3 +217,19 @@ def validate_ids(adapter_id, cluster_of, n: int, K: int = 1) -> bool:
         return False
     _check(code, "cts_validate_ids")
     return True
+
+
+def set_stage_events(events) -> None:
+    """Profiling aid: `events` is None (off) or N_STAGE_EVENTS torch.cuda.Event
+    objects (enable_timing=True) recorded at the layer's stage boundaries by
+    every later apply call (see cts_set_stage_events in include/cts.h)."""
+    if events is None:
+        _check(lib().cts_set_stage_events(None), "cts_set_stage_events")
+        return
+    if len(events) != N_STAGE_EVENTS:
+        raise ValueError("need %d events" % N_STAGE_EVENTS)
+    for e in events:
+        if e.cuda_event == 0:       # torch creates the HIP event at its first record
+            e.record()
+    arr = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.cuda_event for e in events])
+    _check(lib().cts_set_stage_events(arr), "cts_set_stage_events")

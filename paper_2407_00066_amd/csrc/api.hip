@@ -28,8 +28,12 @@ struct Plan {
   int rank, nseg;
   Tile main_tile, shrink_tile;
   int main_split, shrink_split;
-  size_t off_perm, off_seg, off_aid, off_offs, off_zpart, off_zp, off_ypart, total;
+  int max_items;
+  size_t off_perm, off_seg, off_aid, off_offs, off_items, off_nitems, off_zpart, off_zp, off_ypart,
+      total;
 };
+
+constexpr uint64_t kMaxOperandBytes = 0x7fffffffull;   // buffer-load offsets are 31-bit
 
 int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
 
@@ -79,20 +83,40 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   {
     const int tiles = ceil_div(pl->rank, BM) * ceil_div(std::max(T, 1), BN);
     const int nk = ceil_div(p->d_in, BK);
-    pl->shrink_split = std::max(1, std::min(ceil_div(256, tiles), nk));
+    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(256, tiles), nk), 16));
   }
+  pl->max_items = cts::max_sigma_items(T, p->n_adapters);
+
+  // every operand a kernel reads through a buffer resource must stay below 2^31 bytes
+  const uint64_t e = pl->elt;
+  const uint64_t seg_v = static_cast<uint64_t>(pl->rank) * p->d_in * e;
+  const uint64_t seg_u = static_cast<uint64_t>(p->d_out) * pl->rank * e;
+  if (static_cast<uint64_t>(T) * p->d_in * e > kMaxOperandBytes ||
+      static_cast<uint64_t>(p->d_out) * p->d_in * e > kMaxOperandBytes ||
+      seg_v > kMaxOperandBytes || seg_u > kMaxOperandBytes)
+    return CTS_ERR_UNSUPPORTED;
 
   size_t off = 0;
   pl->off_perm = off;  off = align_up(off + 4ull * T);
   pl->off_seg = off;   off = align_up(off + 4ull * T);
   pl->off_aid = off;   off = align_up(off + 4ull * T);
   pl->off_offs = off;  off = align_up(off + 4ull * (pl->nseg + 1));
+  pl->off_items = off; off = align_up(off + 4ull * (pl->max_items + 1));
+  pl->off_nitems = off; off = align_up(off + 4);
   pl->off_zpart = off; off = align_up(off + 4ull * pl->shrink_split * T * pl->rank);
   pl->off_zp = off;    off = align_up(off + static_cast<size_t>(pl->elt) * T * pl->rank);
   pl->off_ypart = off;
   if (pl->main_split > 1) off = align_up(off + 4ull * pl->main_split * T * p->d_out);
   pl->total = off;
   return CTS_OK;
+}
+
+// Stage-boundary events of the profiling aid (null when off).
+hipEvent_t g_stage_events[CTS_N_STAGE_EVENTS] = {};
+bool g_stage_on = false;
+
+hipError_t mark(int i, hipStream_t s) {
+  return g_stage_on ? hipEventRecord(g_stage_events[i], s) : hipSuccess;
 }
 
 struct Range { const void* p; size_t bytes; };
@@ -121,47 +145,58 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
   int32_t* said = reinterpret_cast<int32_t*>(ws + pl.off_aid);
   int32_t* offs = reinterpret_cast<int32_t*>(ws + pl.off_offs);
+  int32_t* items = reinterpret_cast<int32_t*>(ws + pl.off_items);
+  int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
   float* zpart = reinterpret_cast<float*>(ws + pl.off_zpart);
   void* zp = ws + pl.off_zp;
   float* ypart = reinterpret_cast<float*>(ws + pl.off_ypart);
   const int T = p->T, rank = pl.rank;
 
-  hipError_t e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
-                                  pl.nseg, perm, offs, sseg, said, stream);
+  hipError_t e = mark(0, stream);
   if (e != hipSuccess) return CTS_ERR_HIP;
+  e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
+                                  pl.nseg, perm, offs, sseg, said, items, n_items, stream);
+  if (e != hipSuccess || mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams g{};
   g.M = rank; g.N = T;
   g.A0 = nullptr; g.K0 = 0;
   g.A1 = Vbasis; g.seg_stride_a1 = static_cast<int64_t>(rank) * p->d_in; g.lda1 = p->d_in;
   g.B1 = x; g.ldb1 = p->d_in; g.K1 = p->d_in; g.b1_gather = 1;
+  g.a0_bytes = 0; g.b0_bytes = 0;
+  g.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(rank) * p->d_in * pl.elt);
+  g.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = pl.shrink_split; g.part = zpart;
   e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
-  if (e != hipSuccess) return CTS_ERR_HIP;
+  if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 
-  e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters,
-                        compressed ? Sigma : nullptr, zp, p->dtype, stream);
-  if (e != hipSuccess) return CTS_ERR_HIP;
+  e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
+                        pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream);
+  if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
   f.M = p->d_out; f.N = T;
   f.A0 = W; f.lda0 = p->d_in; f.B0 = x; f.ldb0 = p->d_in; f.K0 = p->d_in;
   f.A1 = Ubasis; f.seg_stride_a1 = static_cast<int64_t>(p->d_out) * rank; f.lda1 = rank;
   f.B1 = zp; f.ldb1 = rank; f.K1 = rank; f.b1_gather = 0;
+  f.a0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(p->d_out) * p->d_in * pl.elt);
+  f.b0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
+  f.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(p->d_out) * rank * pl.elt);
+  f.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * rank * pl.elt);
   f.perm = perm; f.sorted_seg = sseg;
   f.ksplit = pl.main_split;
   f.part = pl.main_split > 1 ? ypart : nullptr;
   f.out = y; f.ldo = p->d_out; f.out_perm = 1; f.out_dtype = p->out_dtype;
   e = cts::launch_seg_gemm(f, p->dtype, pl.main_tile, stream);
-  if (e != hipSuccess) return CTS_ERR_HIP;
+  if (e != hipSuccess || mark(4, stream) != hipSuccess) return CTS_ERR_HIP;
 
   if (pl.main_split > 1) {
     e = cts::launch_splitk_reduce(ypart, pl.main_split, T, p->d_out, perm, y, p->d_out,
                                   p->out_dtype, stream);
     if (e != hipSuccess) return CTS_ERR_HIP;
   }
-  return CTS_OK;
+  return mark(5, stream) == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
 
 }  // namespace
@@ -203,7 +238,8 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
     for (const Range& i : in)
       if (overlap(o, i)) return CTS_ERR_INVALID_ARG;
   const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets,
-                                        nullptr, nullptr, static_cast<hipStream_t>(stream));
+                                        nullptr, nullptr, nullptr, nullptr,
+                                        static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
 
@@ -245,6 +281,18 @@ int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* a
     return CTS_ERR_INVALID_ARG;
   return run_layer(p, pl, false, x, adapter_id, nullptr, W, B, A, nullptr, y, workspace,
                    static_cast<hipStream_t>(stream));
+}
+
+int cts_set_stage_events(void* const* events) {
+  if (!events) {
+    g_stage_on = false;
+    return CTS_OK;
+  }
+  for (int i = 0; i < CTS_N_STAGE_EVENTS; ++i)
+    if (!events[i]) return CTS_ERR_INVALID_ARG;
+  for (int i = 0; i < CTS_N_STAGE_EVENTS; ++i) g_stage_events[i] = static_cast<hipEvent_t>(events[i]);
+  g_stage_on = true;
+  return CTS_OK;
 }
 
 int cts_validate_ids(const cts_problem* p, const int32_t* adapter_id, const int32_t* cluster_of,

@@ -29,13 +29,23 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 constexpr int kSortThreads = 1024;
 constexpr int kSortMaxT = 8192;
 
+// Tokens of one adapter handled together by the core-product stage.
+constexpr int kSigmaChunk = 16;
+
+// Upper bound of the number of core-product items for T tokens and n adapters.
+inline int max_sigma_items(int T, int n) {
+  return (T + kSigmaChunk - 1) / kSigmaChunk + (n < T ? n : T);
+}
+
 // Sorts tokens by (cluster, adapter, token).  Writes perm[T] and offs[K+1];
-// optionally sorted_seg[T] (cluster of each sorted position) and
-// sorted_aid[T] (adapter of each sorted position).  cluster_of may be null
-// (every adapter its own cluster, K == n).
+// optionally sorted_seg[T] (cluster of each sorted position), sorted_aid[T]
+// (adapter of each sorted position) and the core-product items: items[0..c)
+// are the sorted positions where a run of one adapter starts or crosses a
+// multiple of kSigmaChunk, items[c] = T, and n_items[0] = c.  cluster_of may
+// be null (every adapter its own cluster, K == n).
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
-                       hipStream_t stream);
+                       int32_t* items, int32_t* n_items, hipStream_t stream);
 
 // ----------------------------------------------------- segmented MFMA GEMM
 // out[j][m] (m < M rows of the weight operand, j < N sorted token positions) =
@@ -45,10 +55,13 @@ hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int
 // map(j) = perm[j]; map1(j) = perm[j] if b1_gather else j.
 // Output: part != null -> fp32 partials part[ks][j][m] for split ks;
 //         else out[perm[j]][m] (out_perm) or out[j][m], element type out_dtype.
+// Every operand (and every segment of A1) must be smaller than 2^31 bytes:
+// a0_bytes, b0_bytes, a1_seg_bytes and b1_bytes bound the buffer loads.
 struct GemmParams {
   int M, N;
   const void* A0; int64_t lda0; const void* B0; int64_t ldb0; int K0;
   const void* A1; int64_t seg_stride_a1; int64_t lda1; const void* B1; int64_t ldb1; int K1;
+  uint32_t a0_bytes, b0_bytes, a1_seg_bytes, b1_bytes;
   int b1_gather;
   const int32_t* perm;        // [N] sorted position -> token
   const int32_t* sorted_seg;  // [N] sorted position -> segment (cluster / adapter)
@@ -63,8 +76,10 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK);
 
 // ------------------------------------------------------------- Sigma stage
 // zp[j][c] = sum_{c'} Sigma_{aid(j)}[c][c'] * (sum_s zpart[s][j][c'])  (Sigma may be null:
-// then zp = sum_s zpart).  Rounded to the input type.
+// then zp = sum_s zpart).  Rounded to the input type.  One workgroup per item
+// of the sort (max_items workgroups are launched; the extra ones exit).
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
+                        const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream);
 
 // y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.

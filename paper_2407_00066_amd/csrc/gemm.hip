@@ -6,37 +6,59 @@
 //                                fp32 accumulators   (App. D: base term once
 //                                for the batch, adapter term per token)
 // The operand with rows m is a weight (W, V_k^T, U_k: k-contiguous); the
-// operand with rows j is an activation gathered in cluster-sorted order
-// (x rows through perm, or Z' rows).  A workgroup owns a BM x BN output tile
+// operand with rows j is an activation in cluster-sorted order (x rows
+// gathered through perm, or Z' rows).  A workgroup owns a BM x BN output tile
 // and walks a flat list of BK-wide k-tiles: first the dense W tiles of its
-// split, then, for every cluster segment that intersects its token columns,
+// k-split, then, for every cluster segment that intersects its token columns,
 // the k-tiles of that segment's basis with the other columns masked to zero.
+//
+// Global loads are raw buffer loads of 16 bytes: a row or k chunk outside
+// the operand gets an out-of-range offset and reads as zero, so the loads
+// carry no branches and all of a k-tile's loads are in flight together while
+// the previous k-tile is multiplied out of LDS (register prefetch, two LDS
+// buffers, one barrier per k-tile).  LDS rows are padded by 16 bytes, which
+// makes the 16-byte fragment reads of one MFMA conflict-free.
 //
 // Matrix cores: v_mfma_f32_16x16x32_bf16 (bf16 in, fp32 acc) or
 // v_mfma_f32_16x16x4_f32.  Both operands of a product use the same per-lane
 // k assignment, so the hardware's internal k order does not matter; the
 // accumulator layout is lane l -> column l%16, rows 4*(l/16)+{0..3}.
-// Tiles are staged through LDS with one register-prefetched k-tile in flight
-// and rows padded by 16 bytes (conflict-free 16-byte fragment reads).
 #include "cts_internal.h"
 
 namespace cts {
 namespace {
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOob = 0x80000000u;   // every operand is < 2^31 bytes
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(nbytes), 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
 template <typename TI> struct MfmaTraits;
 template <> struct MfmaTraits<bf16_t> {
   static constexpr int EPC = 8;   // elements per 16-byte chunk
   static constexpr int KS = 32;   // k per MFMA
-  __device__ static __forceinline__ f32x4 mma(const bf16_t* a, const bf16_t* b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8*>(a),
-                                                   *reinterpret_cast<const bf16x8*>(b), c, 0, 0, 0);
+  static constexpr int KG = 8;    // k per lane per MFMA
+  typedef bf16x8 frag;
+  __device__ static __forceinline__ frag ld(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
 };
 template <> struct MfmaTraits<float> {
   static constexpr int EPC = 4;
   static constexpr int KS = 4;
-  __device__ static __forceinline__ f32x4 mma(const float* a, const float* b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(*a, *b, c, 0, 0, 0);
+  static constexpr int KG = 1;
+  typedef float frag;
+  __device__ static __forceinline__ frag ld(const float* p) { return *p; }
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
 };
 
@@ -45,18 +67,18 @@ struct Cfg {
   static constexpr int NT = WM * WN * 64;
   static constexpr int EPC = MfmaTraits<TI>::EPC;
   static constexpr int KS = MfmaTraits<TI>::KS;
-  static constexpr int KG = (KS == 32) ? 8 : 1;       // k elements per lane per MFMA
   static constexpr int CPR = BK / EPC;                // 16-byte chunks per tile row
+  static constexpr int RPP = NT / CPR;                // tile rows covered per pass
   static constexpr int LDS_ROW = BK + EPC;            // padded row, elements
-  static constexpr int CA = BM * CPR / NT;
-  static constexpr int CB = BN * CPR / NT;
+  static constexpr int CA = BM / RPP;                 // A chunks per thread
+  static constexpr int CB = BN / RPP;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int FM = WTM / 16, FN = WTN / 16;
   static constexpr int AB_BYTES = 2 * (BM + BN) * LDS_ROW * (int)sizeof(TI);
   static constexpr int ST_ROW = BM + 4;               // staged fp32 row (per token)
   static constexpr int ST_BYTES = BN * ST_ROW * 4;
   static constexpr int SMEM = AB_BYTES > ST_BYTES ? AB_BYTES : ST_BYTES;
-  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "chunk split");
+  static_assert(NT % CPR == 0 && BM % RPP == 0 && BN % RPP == 0, "chunk split");
   static_assert(WTM % 16 == 0 && WTN % 16 == 0 && BK % KS == 0, "tile shape");
 };
 
@@ -66,12 +88,14 @@ template <typename TI, int BM, int BN, int BK, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams p) {
   using C = Cfg<TI, BM, BN, BK, WM, WN>;
   using MT = MfmaTraits<TI>;
+  typedef typename MT::frag frag;
+  constexpr uint32_t ELT = sizeof(TI);
+
   __shared__ __attribute__((aligned(16))) char smem[C::SMEM];
   __shared__ int32_t t_perm[BN];
   __shared__ int32_t t_seg[BN];
   __shared__ int32_t run_start[BN + 1];
   __shared__ int32_t wave_runs[C::NT / 64];
-  __shared__ int32_t n_runs_s;
 
   TI* smA = reinterpret_cast<TI*>(smem);
   TI* smB = smA + 2 * BM * C::LDS_ROW;
@@ -89,29 +113,28 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
     t_seg[i] = (i < jn && p.sorted_seg) ? p.sorted_seg[j0 + i] : 0;
   }
   __syncthreads();
-  {
-    // run starts: positions where the segment changes (compaction by ballot)
-    bool any = false;
-    for (int base = 0; base < BN; base += C::NT) {
-      const int i = base + tid;
-      const bool st = (i < jn) && (i == 0 || t_seg[i] != t_seg[i - 1]);
-      const uint64_t bal = __ballot(st);
-      if (lane == 0) wave_runs[wave] = __popcll(bal);
-      __syncthreads();
-      int before = 0, total = 0;
-      for (int w = 0; w < C::NT / 64; ++w) { if (w < wave) before += wave_runs[w]; total += wave_runs[w]; }
-      const int prev = any ? n_runs_s : 0;
-      __syncthreads();
-      if (st) {
-        const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        run_start[prev + before + __popcll(bal & lt)] = i;
-      }
-      if (tid == 0) n_runs_s = prev + total;
-      any = true;
-      __syncthreads();
+  int n_runs = 0;
+  for (int base = 0; base < BN; base += C::NT) {
+    const int i = base + tid;
+    const bool st = (i < jn) && (i == 0 || t_seg[i] != t_seg[i - 1]);
+    const uint64_t bal = __ballot(st);
+    if (lane == 0) wave_runs[wave] = __popcll(bal);
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < C::NT / 64; ++w) {
+      const int c = wave_runs[w];
+      before += (w < wave) ? c : 0;
+      total += c;
     }
+    if (st) {
+      const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      run_start[n_runs + before + __popcll(bal & lt)] = i;
+    }
+    n_runs += total;
+    __syncthreads();
   }
-  const int n_runs = (p.sorted_seg && p.K1 > 0) ? n_runs_s : 0;
+  if (!(p.sorted_seg && p.K1 > 0)) n_runs = 0;
   if (tid == 0) run_start[n_runs] = jn;
   __syncthreads();
 
@@ -128,53 +151,68 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
   const int nd = d_hi - d_lo, ns = s_hi - s_lo;
   const int ntiles = nd + n_runs * ns;
 
-  // per-thread chunk coordinates (fixed across k-tiles)
-  int a_row[C::CA], a_kc[C::CA], b_row[C::CB], b_kc[C::CB];
-#pragma unroll
-  for (int i = 0; i < C::CA; ++i) { const int c = tid + i * C::NT; a_row[i] = c / C::CPR; a_kc[i] = c % C::CPR; }
-#pragma unroll
-  for (int i = 0; i < C::CB; ++i) { const int c = tid + i * C::NT; b_row[i] = c / C::CPR; b_kc[i] = c % C::CPR; }
+  // ---- per-thread load coordinates (fixed for the whole kernel) ------------
+  const int kc = tid % C::CPR;               // 16-byte chunk within a tile row
+  const int row0 = tid / C::CPR;             // first tile row, then + RPP each
 
-  uint4 ra[C::CA], rb[C::CB];
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(p.A0, p.a0_bytes);
+  const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
+  const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
 
-  auto load_tile = [&](int t) {
-    const TI* A; int64_t lda; const TI* B; int64_t ldb; int kbase, kend, lo, hi; bool gather;
+  uint32_t a0_row[C::CA], b0_row[C::CB];
+#pragma unroll
+  for (int i = 0; i < C::CA; ++i) {
+    const int m = m0 + row0 + i * C::RPP;
+    a0_row[i] = (m < p.M) ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT : kOob;
+  }
+#pragma unroll
+  for (int i = 0; i < C::CB; ++i) {
+    const int jl = row0 + i * C::RPP;
+    b0_row[i] = (jl < jn) ? static_cast<uint32_t>(t_perm[jl]) * static_cast<uint32_t>(p.ldb0) * ELT : kOob;
+  }
+
+  u32x4 ra[C::CA], rb[C::CB];
+
+  // issue the global loads of k-tile t into ra/rb
+  auto load_tile = [&](int t) __attribute__((always_inline)) {
     if (t < nd) {
-      const int kt = d_lo + t;
-      A = static_cast<const TI*>(p.A0); lda = p.lda0; B = static_cast<const TI*>(p.B0); ldb = p.ldb0;
-      kbase = kt * BK; kend = p.K0; lo = 0; hi = jn; gather = true;
+      const uint32_t k = static_cast<uint32_t>((d_lo + t) * BK) + kc * C::EPC;
+      const bool kok = k < static_cast<uint32_t>(p.K0);
+      const uint32_t kb = k * ELT;
+#pragma unroll
+      for (int i = 0; i < C::CA; ++i) ra[i] = load16(rA0, (kok && a0_row[i] != kOob) ? a0_row[i] + kb : kOob);
+#pragma unroll
+      for (int i = 0; i < C::CB; ++i) rb[i] = load16(rB0, (kok && b0_row[i] != kOob) ? b0_row[i] + kb : kOob);
     } else {
       const int q = (t - nd) / ns, kt = s_lo + (t - nd) % ns;
-      const int rs = run_start[q];
-      const int seg = t_seg[rs];
-      A = static_cast<const TI*>(p.A1) + static_cast<int64_t>(seg) * p.seg_stride_a1; lda = p.lda1;
-      B = static_cast<const TI*>(p.B1); ldb = p.ldb1;
-      kbase = kt * BK; kend = p.K1; lo = rs; hi = run_start[q + 1]; gather = p.b1_gather != 0;
-    }
+      const int lo = run_start[q], hi = run_start[q + 1];
+      const int seg = __builtin_amdgcn_readfirstlane(t_seg[lo]);
+      const __amdgpu_buffer_rsrc_t rA1 = make_rsrc(
+          static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes, p.a1_seg_bytes);
+      const uint32_t k = static_cast<uint32_t>(kt * BK) + kc * C::EPC;
+      const bool kok = k < static_cast<uint32_t>(p.K1);
+      const uint32_t kb = k * ELT;
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i) {
-      const int m = m0 + a_row[i], k = kbase + a_kc[i] * C::EPC;
-      ra[i] = (m < p.M && k < kend)
-                  ? *reinterpret_cast<const uint4*>(A + static_cast<int64_t>(m) * lda + k) : zero4;
-    }
+      for (int i = 0; i < C::CA; ++i) {
+        const int m = m0 + row0 + i * C::RPP;
+        ra[i] = load16(rA1, (kok && m < p.M) ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + kb : kOob);
+      }
 #pragma unroll
-    for (int i = 0; i < C::CB; ++i) {
-      const int jl = b_row[i], k = kbase + b_kc[i] * C::EPC;
-      const int64_t row = gather ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
-      rb[i] = (jl >= lo && jl < hi && k < kend)
-                  ? *reinterpret_cast<const uint4*>(B + row * ldb + k) : zero4;
+      for (int i = 0; i < C::CB; ++i) {
+        const int jl = row0 + i * C::RPP;
+        const bool ok = kok && jl >= lo && jl < hi;
+        const uint32_t row = p.b1_gather ? static_cast<uint32_t>(t_perm[jl]) : static_cast<uint32_t>(j0 + jl);
+        rb[i] = load16(rB1, ok ? row * static_cast<uint32_t>(p.ldb1) * ELT + kb : kOob);
+      }
     }
   };
-  auto store_tile = [&](int buf) {
-    TI* a = smA + buf * BM * C::LDS_ROW;
-    TI* b = smB + buf * BN * C::LDS_ROW;
+  auto store_tile = [&](int buf) __attribute__((always_inline)) {
+    TI* a = smA + buf * BM * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
+    TI* b = smB + buf * BN * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i)
-      *reinterpret_cast<uint4*>(a + a_row[i] * C::LDS_ROW + a_kc[i] * C::EPC) = ra[i];
+    for (int i = 0; i < C::CA; ++i) *reinterpret_cast<u32x4*>(a + i * C::RPP * C::LDS_ROW) = ra[i];
 #pragma unroll
-    for (int i = 0; i < C::CB; ++i)
-      *reinterpret_cast<uint4*>(b + b_row[i] * C::LDS_ROW + b_kc[i] * C::EPC) = rb[i];
+    for (int i = 0; i < C::CB; ++i) *reinterpret_cast<u32x4*>(b + i * C::RPP * C::LDS_ROW) = rb[i];
   };
 
   const int wm = wave / WN, wn = wave % WN;
@@ -184,26 +222,27 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int frow = lane & 15, fk = (lane >> 4) * C::KG;
-  auto compute = [&](int buf) {
-    const TI* a = smA + buf * BM * C::LDS_ROW + (wm * C::WTM + frow) * C::LDS_ROW + fk;
-    const TI* b = smB + buf * BN * C::LDS_ROW + (wn * C::WTN + frow) * C::LDS_ROW + fk;
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += C::KS) {
-#pragma unroll
-      for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j)
-          acc[i][j] = MT::mma(a + i * 16 * C::LDS_ROW + kk, b + j * 16 * C::LDS_ROW + kk, acc[i][j]);
-    }
-  };
+  const int frow = lane & 15, fk = (lane >> 4) * MT::KG;
 
   if (ntiles > 0) { load_tile(0); store_tile(0); }
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     const int cur = t & 1;
     if (t + 1 < ntiles) load_tile(t + 1);
-    compute(cur);
+    const TI* a = smA + cur * BM * C::LDS_ROW + (wm * C::WTM + frow) * C::LDS_ROW + fk;
+    const TI* b = smB + cur * BN * C::LDS_ROW + (wn * C::WTN + frow) * C::LDS_ROW + fk;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += C::KS) {
+      frag fa[C::FM], fb[C::FN];
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) fa[i] = MT::ld(a + i * 16 * C::LDS_ROW + kk);
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) fb[j] = MT::ld(b + j * 16 * C::LDS_ROW + kk);
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) acc[i][j] = MT::mma(fa[i], fb[j], acc[i][j]);
+    }
     if (t + 1 < ntiles) store_tile(cur ^ 1);
     __syncthreads();
   }
@@ -236,11 +275,13 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
       const int jl = c / CPRO, mc = (c % CPRO) * 8;
       if (jl < jn && m0 + mc < p.M) {
         const float* s = st + jl * C::ST_ROW + mc;
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(s);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(s + 4);
         uint4 v;
-        v.x = f32_to_bf16(s[0]) | (static_cast<uint32_t>(f32_to_bf16(s[1])) << 16);
-        v.y = f32_to_bf16(s[2]) | (static_cast<uint32_t>(f32_to_bf16(s[3])) << 16);
-        v.z = f32_to_bf16(s[4]) | (static_cast<uint32_t>(f32_to_bf16(s[5])) << 16);
-        v.w = f32_to_bf16(s[6]) | (static_cast<uint32_t>(f32_to_bf16(s[7])) << 16);
+        v.x = f32_to_bf16(lo[0]) | (static_cast<uint32_t>(f32_to_bf16(lo[1])) << 16);
+        v.y = f32_to_bf16(lo[2]) | (static_cast<uint32_t>(f32_to_bf16(lo[3])) << 16);
+        v.z = f32_to_bf16(hi[0]) | (static_cast<uint32_t>(f32_to_bf16(hi[1])) << 16);
+        v.w = f32_to_bf16(hi[2]) | (static_cast<uint32_t>(f32_to_bf16(hi[3])) << 16);
         const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
         *reinterpret_cast<uint4*>(out + row * p.ldo + m0 + mc) = v;
       }

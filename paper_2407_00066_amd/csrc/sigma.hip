@@ -2,14 +2,15 @@
 // Sec. 3.1: Sigma_i is the only per-LoRA matrix), and the split-K reduction
 // of the fused GEMM.
 //
-// Sigma stage.  Tokens arrive sorted by (cluster, adapter), so tokens of one
-// LoRA are contiguous: a workgroup walks its TB sorted positions run by run,
-// stages each run's Sigma_i in LDS once (fp32, rows padded to r+1 words so
-// that lanes reading one column hit distinct banks), and computes one output
-// element per thread with a fixed ascending-order fp32 dot product.  z_t is
-// first reduced over the shrink's k-splits in fixed order.  No atomics: the
-// result is bitwise reproducible.  With Sigma == null (uncompressed path) the
-// stage only reduces and converts.
+// Core product.  Tokens arrive sorted by (cluster, adapter), so tokens of one
+// LoRA are contiguous.  The sort cuts the sorted positions into items: runs
+// of one adapter, at most kSigmaChunk long.  A workgroup takes one item,
+// stages that adapter's Sigma_i in LDS once (fp32, rows padded to r+1 words
+// so that lanes reading one column hit distinct banks) and produces every
+// output of the item's tokens with a fixed ascending-order fp32 dot product.
+// z_t is first summed over the shrink's k-splits in fixed order.  No atomics:
+// the result is bitwise reproducible.  With Sigma == null (uncompressed path)
+// the stage only sums and converts.
 #include "cts_internal.h"
 
 namespace cts {
@@ -17,6 +18,7 @@ namespace {
 
 constexpr int kSigThreads = 256;
 constexpr int kSigMaxR = 128;
+constexpr int kPerThread = kSigmaChunk * kSigMaxR / kSigThreads;   // z elements per thread
 
 template <typename TI> __device__ __forceinline__ float ld(const TI* p, int64_t i);
 template <> __device__ __forceinline__ float ld<float>(const float* p, int64_t i) { return p[i]; }
@@ -26,58 +28,63 @@ template <typename TI> __device__ __forceinline__ void st(TI* p, int64_t i, floa
 template <> __device__ __forceinline__ void st<float>(float* p, int64_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st<bf16_t>(bf16_t* p, int64_t i, float v) { p[i].bits = f32_to_bf16(v); }
 
-template <typename TI, int TB>
+template <typename TI>
 __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restrict__ zpart, int S,
                                                             int T, int r,
                                                             const int32_t* __restrict__ sorted_aid,
-                                                            int n, const TI* __restrict__ Sigma,
+                                                            int n, const int32_t* __restrict__ items,
+                                                            const int32_t* __restrict__ n_items,
+                                                            const TI* __restrict__ Sigma,
                                                             TI* __restrict__ zp) {
-  __shared__ float z[TB * kSigMaxR];
+  __shared__ float z[kSigmaChunk * kSigMaxR];
   __shared__ float sig[kSigMaxR * (kSigMaxR + 1)];
-  __shared__ int32_t aid[TB];
 
+  const int item = blockIdx.x;
+  if (item >= n_items[0]) return;
   const int tid = threadIdx.x;
-  const int j0 = blockIdx.x * TB;
-  const int tb = min(TB, T - j0);
+  const int lo = items[item], hi = items[item + 1];
+  const int cnt = (hi - lo) * r;   // outputs of this item
 
-  for (int i = tid; i < tb; i += kSigThreads) {
-    int a = sorted_aid ? sorted_aid[j0 + i] : 0;
-    aid[i] = a < 0 ? 0 : (a >= n ? n - 1 : a);
+  // Sigma_a -> LDS (independent loads, issued before the partial sums)
+  const int ld_sig = r + 1;
+  if (Sigma != nullptr) {
+    int a = sorted_aid[lo];
+    a = a < 0 ? 0 : (a >= n ? n - 1 : a);
+    const TI* sa = Sigma + static_cast<int64_t>(a) * r * r;
+    for (int e = tid; e < r * r; e += kSigThreads) sig[(e / r) * ld_sig + (e % r)] = ld<TI>(sa, e);
   }
-  for (int e = tid; e < tb * r; e += kSigThreads) {
-    const int i = e / r, c = e % r;
-    const int64_t off = static_cast<int64_t>(j0 + i) * r + c;
-    float s = 0.f;
-    for (int q = 0; q < S; ++q) s += zpart[static_cast<int64_t>(q) * T * r + off];
-    z[i * r + c] = s;
+  // z = sum over k-splits, fixed order; the kPerThread loads of one split are independent
+  float acc[kPerThread];
+#pragma unroll
+  for (int u = 0; u < kPerThread; ++u) acc[u] = 0.f;
+  const int64_t split_stride = static_cast<int64_t>(T) * r;
+  const float* zbase = zpart + static_cast<int64_t>(lo) * r;
+  for (int q = 0; q < S; ++q) {
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+      const int e = tid + u * kSigThreads;
+      if (e < cnt) acc[u] += zbase[q * split_stride + e];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kPerThread; ++u) {
+    const int e = tid + u * kSigThreads;
+    if (e < cnt) z[e] = acc[u];
   }
   __syncthreads();
 
+  TI* out = zp + static_cast<int64_t>(lo) * r;
   if (Sigma == nullptr) {
-    for (int e = tid; e < tb * r; e += kSigThreads)
-      st<TI>(zp, static_cast<int64_t>(j0) * r + e, z[e]);
+    for (int e = tid; e < cnt; e += kSigThreads) st<TI>(out, e, z[e]);
     return;
   }
-
-  const int ld_sig = r + 1;
-  int cur = 0;
-  while (cur < tb) {
-    const int a = aid[cur];
-    int end = cur + 1;
-    while (end < tb && aid[end] == a) ++end;
-    const TI* sa = Sigma + static_cast<int64_t>(a) * r * r;
-    for (int e = tid; e < r * r; e += kSigThreads) sig[(e / r) * ld_sig + (e % r)] = ld<TI>(sa, e);
-    __syncthreads();
-    for (int e = tid; e < (end - cur) * r; e += kSigThreads) {
-      const int i = cur + e / r, c = e % r;
-      const float* srow = sig + c * ld_sig;
-      const float* zi = z + i * r;
-      float acc = 0.f;
-      for (int q = 0; q < r; ++q) acc = fmaf(srow[q], zi[q], acc);
-      st<TI>(zp, static_cast<int64_t>(j0 + i) * r + c, acc);
-    }
-    __syncthreads();
-    cur = end;
+  for (int e = tid; e < cnt; e += kSigThreads) {
+    const int i = e / r, c = e % r;
+    const float* srow = sig + c * ld_sig;
+    const float* zi = z + i * r;
+    float d = 0.f;
+    for (int q = 0; q < r; ++q) d = fmaf(srow[q], zi[q], d);
+    st<TI>(out, e, d);
   }
 }
 
@@ -119,15 +126,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }  // namespace
 
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
+                        const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream) {
-  constexpr int TB = 8;
-  dim3 grid((T + TB - 1) / TB);
+  dim3 grid(max_items);
   if (in_dtype == 0)
-    hipLaunchKernelGGL((sigma_kernel<float, TB>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, static_cast<const float*>(Sigma), static_cast<float*>(zp));
+    hipLaunchKernelGGL(sigma_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                       sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
+                       static_cast<float*>(zp));
   else
-    hipLaunchKernelGGL((sigma_kernel<bf16_t, TB>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, static_cast<const bf16_t*>(Sigma), static_cast<bf16_t*>(zp));
+    hipLaunchKernelGGL(sigma_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                       sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
+                       static_cast<bf16_t*>(zp));
   return hipGetLastError();
 }
 

@@ -34,7 +34,8 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int dbit
 __global__ __launch_bounds__(kSortThreads) void sort_kernel(
     const int32_t* __restrict__ adapter_id, const int32_t* __restrict__ cluster_of, int T, int n,
     int K, int bits_n, int bits_k, int32_t* __restrict__ perm, int32_t* __restrict__ offs,
-    int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid) {
+    int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid,
+    int32_t* __restrict__ items, int32_t* __restrict__ n_items) {
   __shared__ uint32_t key[kSortMaxT];
   __shared__ uint32_t buf0[kSortMaxT];
   __shared__ uint32_t buf1[kSortMaxT];
@@ -132,15 +133,44 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   }
 
   // outputs; out[] is free scratch now: sorted cluster values for the offsets
+  const uint32_t amask = (1u << bits_n) - 1u;
   for (int j = tid; j < T; j += kSortThreads) {
     const uint32_t t = in[j];
     const uint32_t k = key[t];
     perm[j] = static_cast<int32_t>(t);
     out[j] = k >> bits_n;
     if (sorted_seg) sorted_seg[j] = static_cast<int32_t>(k >> bits_n);
-    if (sorted_aid) sorted_aid[j] = static_cast<int32_t>(k & ((1u << bits_n) - 1u));
+    if (sorted_aid) sorted_aid[j] = static_cast<int32_t>(k & amask);
   }
   __syncthreads();
+
+  // core-product items: positions where the adapter changes or a
+  // kSigmaChunk window starts, compacted in order (ballot + wave prefix)
+  if (items) {
+    uint32_t done = 0;
+    for (int base = 0; base < T; base += kSortThreads) {
+      const int j = base + tid;
+      bool st = false;
+      if (j < T)
+        st = (j % kSigmaChunk == 0) || ((key[in[j]] & amask) != (key[in[j - 1]] & amask));
+      const uint64_t bal = __ballot(st);
+      if (lane == 0) hist[wave] = static_cast<uint32_t>(__popcll(bal));
+      __syncthreads();
+      uint32_t before = 0, total = 0;
+      for (int w = 0; w < kWaves; ++w) {
+        const uint32_t c = hist[w];
+        before += (w < wave) ? c : 0u;
+        total += c;
+      }
+      if (st) items[done + before + static_cast<uint32_t>(__popcll(bal & lt_mask))] = j;
+      done += total;
+      __syncthreads();
+    }
+    if (tid == 0) {
+      items[done] = T;
+      n_items[0] = static_cast<int32_t>(done);
+    }
+  }
   for (int k = tid; k <= K; k += kSortThreads) {
     int lo = 0, hi = T;
     while (lo < hi) {
@@ -161,11 +191,11 @@ int ceil_log2(int v) {
 
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
-                       hipStream_t stream) {
+                       int32_t* items, int32_t* n_items, hipStream_t stream) {
   const int bits_n = ceil_log2(n);
   const int bits_k = cluster_of ? ceil_log2(K) : 0;  // key is the adapter alone when K == n
   hipLaunchKernelGGL(sort_kernel, dim3(1), dim3(kSortThreads), 0, stream, adapter_id, cluster_of,
-                     T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid);
+                     T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items);
   return hipGetLastError();
 }
 
