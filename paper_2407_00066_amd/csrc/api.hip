@@ -70,12 +70,12 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   // small tiles split along k so that the weight stream is spread over >= 256
   // workgroups (one per compute unit).
   if (p->dtype == CTS_F32) pl->main_tile = Tile::F32;
-  else pl->main_tile = (T >= 1024) ? Tile::Large : Tile::Small;
+  else pl->main_tile = (T >= 1024) ? Tile::Large : (T >= 128 ? Tile::Mid : Tile::Small);
   cts::tile_dims(pl->main_tile, &BM, &BN, &BK);
   {
     const int tiles = ceil_div(p->d_out, BM) * ceil_div(std::max(T, 1), BN);
     const int nk = ceil_div(p->d_in, BK);
-    int s = (pl->main_tile == Tile::Large) ? 1 : ceil_div(256, tiles);
+    int s = (pl->main_tile == Tile::Small) ? ceil_div(256, tiles) : 1;
     pl->main_split = std::max(1, std::min(std::min(s, nk), 16));
   }
   pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Small;

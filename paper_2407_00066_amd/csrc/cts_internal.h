@@ -9,6 +9,7 @@ namespace cts {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // bfloat16 storage type: raw bits, converted explicitly.
 struct bf16_t { uint16_t bits; };
@@ -70,7 +71,7 @@ struct GemmParams {
   void* out; int64_t ldo; int out_perm; int out_dtype;
 };
 
-enum class Tile { Large, Small, F32 };
+enum class Tile { Large, Mid, Small, F32 };
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream);
 void tile_dims(Tile tile, int* BM, int* BN, int* BK);
 

@@ -15,14 +15,16 @@
 // Global loads are raw buffer loads of 16 bytes: a row or k chunk outside
 // the operand gets an out-of-range offset and reads as zero, so the loads
 // carry no branches and all of a k-tile's loads are in flight together while
-// the previous k-tile is multiplied out of LDS (register prefetch, two LDS
-// buffers, one barrier per k-tile).  LDS rows are padded by 16 bytes, which
+// earlier k-tiles are multiplied out of LDS (two register stages and two LDS
+// buffers: each load has two k-tiles of compute to arrive; one barrier per
+// k-tile).  LDS rows are padded by 16 bytes, which
 // makes the 16-byte fragment reads of one MFMA conflict-free.
 //
-// Matrix cores: v_mfma_f32_16x16x32_bf16 (bf16 in, fp32 acc) or
-// v_mfma_f32_16x16x4_f32.  Both operands of a product use the same per-lane
-// k assignment, so the hardware's internal k order does not matter; the
-// accumulator layout is lane l -> column l%16, rows 4*(l/16)+{0..3}.
+// Matrix cores: v_mfma_f32_32x32x16_bf16 or v_mfma_f32_16x16x32_bf16 (bf16
+// in, fp32 accumulate), v_mfma_f32_16x16x4_f32 for fp32 inputs.  Both
+// operands of a product use the same per-lane k assignment, so the hardware's
+// internal k order does not matter; only the accumulator layout (acc_row) is
+// fixed by the instruction.
 #include "cts_internal.h"
 
 namespace cts {
@@ -40,54 +42,73 @@ __device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) 
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
-template <typename TI> struct MfmaTraits;
-template <> struct MfmaTraits<bf16_t> {
-  static constexpr int EPC = 8;   // elements per 16-byte chunk
-  static constexpr int KS = 32;   // k per MFMA
-  static constexpr int KG = 8;    // k per lane per MFMA
+// MFMA shapes.  MB x MB output block per instruction; each lane holds KG
+// consecutive k of one row (A) or column (B): lane l -> row/column l % MB,
+// k group l / MB.
+template <typename TI, int MB> struct MfmaTraits;
+template <> struct MfmaTraits<bf16_t, 16> {      // v_mfma_f32_16x16x32_bf16
+  static constexpr int EPC = 8, KS = 32, KG = 8, NACC = 4;
   typedef bf16x8 frag;
+  typedef f32x4 accv;
   __device__ static __forceinline__ frag ld(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
-  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+  __device__ static __forceinline__ accv mma(frag a, frag b, accv c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
 };
-template <> struct MfmaTraits<float> {
-  static constexpr int EPC = 4;
-  static constexpr int KS = 4;
-  static constexpr int KG = 1;
+template <> struct MfmaTraits<bf16_t, 32> {      // v_mfma_f32_32x32x16_bf16
+  static constexpr int EPC = 8, KS = 16, KG = 8, NACC = 16;
+  typedef bf16x8 frag;
+  typedef f32x16 accv;
+  __device__ static __forceinline__ frag ld(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
+  __device__ static __forceinline__ accv mma(frag a, frag b, accv c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct MfmaTraits<float, 16> {       // v_mfma_f32_16x16x4_f32
+  static constexpr int EPC = 4, KS = 4, KG = 1, NACC = 4;
   typedef float frag;
+  typedef f32x4 accv;
   __device__ static __forceinline__ frag ld(const float* p) { return *p; }
-  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+  __device__ static __forceinline__ accv mma(frag a, frag b, accv c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
 };
 
-template <typename TI, int BM, int BN, int BK, int WM, int WN>
+// Row of accumulator element v of lane l inside an MB x MB block (the column
+// is l % MB): 16x16 -> 4*(l/16) + v; 32x32 -> 8*(v/4) + 4*(l/32) + v%4.
+template <int MB> __device__ __forceinline__ int acc_row(int lane, int v) {
+  return MB == 16 ? 4 * (lane >> 4) + v : 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+template <typename TI, int BM, int BN, int BK, int WM, int WN, int MB>
 struct Cfg {
   static constexpr int NT = WM * WN * 64;
-  static constexpr int EPC = MfmaTraits<TI>::EPC;
-  static constexpr int KS = MfmaTraits<TI>::KS;
+  static constexpr int EPC = MfmaTraits<TI, MB>::EPC;
+  static constexpr int KS = MfmaTraits<TI, MB>::KS;
   static constexpr int CPR = BK / EPC;                // 16-byte chunks per tile row
   static constexpr int RPP = NT / CPR;                // tile rows covered per pass
   static constexpr int LDS_ROW = BK + EPC;            // padded row, elements
   static constexpr int CA = BM / RPP;                 // A chunks per thread
   static constexpr int CB = BN / RPP;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
-  static constexpr int FM = WTM / 16, FN = WTN / 16;
+  static constexpr int FM = WTM / MB, FN = WTN / MB;
   static constexpr int AB_BYTES = 2 * (BM + BN) * LDS_ROW * (int)sizeof(TI);
   static constexpr int ST_ROW = BM + 4;               // staged fp32 row (per token)
   static constexpr int ST_BYTES = BN * ST_ROW * 4;
   static constexpr int SMEM = AB_BYTES > ST_BYTES ? AB_BYTES : ST_BYTES;
   static_assert(NT % CPR == 0 && BM % RPP == 0 && BN % RPP == 0, "chunk split");
-  static_assert(WTM % 16 == 0 && WTN % 16 == 0 && BK % KS == 0, "tile shape");
+  static_assert(WTM % MB == 0 && WTN % MB == 0 && BK % KS == 0, "tile shape");
 };
 
 __device__ __forceinline__ int split_lo(int n, int ks, int S) { return (int)((int64_t)n * ks / S); }
 
-template <typename TI, int BM, int BN, int BK, int WM, int WN>
-__global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams p) {
-  using C = Cfg<TI, BM, BN, BK, WM, WN>;
-  using MT = MfmaTraits<TI>;
+// STAGES: register stages of global loads in flight; OCC: waves per SIMD the
+// register allocation must allow; MB: MFMA block (16 or 32).
+template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB>
+__global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmParams p) {
+  using C = Cfg<TI, BM, BN, BK, WM, WN, MB>;
+  using MT = MfmaTraits<TI, MB>;
+  typedef typename MT::accv accv;
   typedef typename MT::frag frag;
   constexpr uint32_t ELT = sizeof(TI);
 
@@ -159,92 +180,123 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
   const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
   const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
 
-  uint32_t a0_row[C::CA], b0_row[C::CB];
+  // byte offsets of this thread's rows in each phase (kOob: outside the operand)
+  uint32_t a0_row[C::CA], a1_row[C::CA], b0_row[C::CB], b1_row[C::CB];
+  int b_jl[C::CB];
 #pragma unroll
   for (int i = 0; i < C::CA; ++i) {
     const int m = m0 + row0 + i * C::RPP;
-    a0_row[i] = (m < p.M) ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT : kOob;
+    const bool ok = m < p.M;
+    a0_row[i] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT : kOob;
+    a1_row[i] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT : kOob;
   }
 #pragma unroll
   for (int i = 0; i < C::CB; ++i) {
     const int jl = row0 + i * C::RPP;
-    b0_row[i] = (jl < jn) ? static_cast<uint32_t>(t_perm[jl]) * static_cast<uint32_t>(p.ldb0) * ELT : kOob;
+    const uint32_t tok = static_cast<uint32_t>(t_perm[jl]);
+    const uint32_t r1 = p.b1_gather ? tok : static_cast<uint32_t>(j0 + jl);
+    b_jl[i] = jl;
+    b0_row[i] = tok * static_cast<uint32_t>(p.ldb0) * ELT;
+    b1_row[i] = r1 * static_cast<uint32_t>(p.ldb1) * ELT;
   }
 
-  u32x4 ra[C::CA], rb[C::CB];
+  // register stages of global loads: with S stages the loads of k-tile t+S are
+  // issued while k-tile t is multiplied out of LDS
+  u32x4 ra[STAGES][C::CA], rb[STAGES][C::CB];
 
-  // issue the global loads of k-tile t into ra/rb
-  auto load_tile = [&](int t) __attribute__((always_inline)) {
-    if (t < nd) {
-      const uint32_t k = static_cast<uint32_t>((d_lo + t) * BK) + kc * C::EPC;
-      const bool kok = k < static_cast<uint32_t>(p.K0);
-      const uint32_t kb = k * ELT;
+  // load cursor: tiles are loaded strictly in order, so the position in the
+  // schedule advances incrementally (no division per tile)
+  int lt = 0;          // next k-tile to load
+  int lq = 0;          // its segment run (segment phase)
+  int lkt = s_lo;      // its k-tile within the segment phase
+
+  // issue the loads of the next k-tile; past the end every load is out of
+  // range and reads zeros, so the code has no data-dependent branches
+  auto load_next = [&](u32x4 (&a)[C::CA], u32x4 (&b)[C::CB]) __attribute__((always_inline)) {
+    const bool valid = lt < ntiles;
+    const bool dense = lt < nd;
+    const int q = min(lq, max(n_runs - 1, 0));
+    const int lo = dense ? 0 : run_start[q];
+    const int hi = dense ? jn : run_start[q + 1];
+    const int seg = __builtin_amdgcn_readfirstlane(t_seg[lo]);
+    const __amdgpu_buffer_rsrc_t rA =
+        dense ? rA0
+              : make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
+                          p.a1_seg_bytes);
+    const __amdgpu_buffer_rsrc_t rB = dense ? rB0 : rB1;
+    const int kt = dense ? d_lo + lt : lkt;
+    const uint32_t k = static_cast<uint32_t>(kt * BK) + kc * C::EPC;
+    // out-of-range chunks get bit 31 set (every operand is < 2^31 bytes)
+    const uint32_t kmask = (valid && k < static_cast<uint32_t>(dense ? p.K0 : p.K1)) ? 0u : kOob;
+    const uint32_t kb = k * ELT;
+    const uint32_t span = static_cast<uint32_t>(hi - lo);
 #pragma unroll
-      for (int i = 0; i < C::CA; ++i) ra[i] = load16(rA0, (kok && a0_row[i] != kOob) ? a0_row[i] + kb : kOob);
+    for (int i = 0; i < C::CA; ++i) a[i] = load16(rA, ((dense ? a0_row[i] : a1_row[i]) + kb) | kmask);
 #pragma unroll
-      for (int i = 0; i < C::CB; ++i) rb[i] = load16(rB0, (kok && b0_row[i] != kOob) ? b0_row[i] + kb : kOob);
-    } else {
-      const int q = (t - nd) / ns, kt = s_lo + (t - nd) % ns;
-      const int lo = run_start[q], hi = run_start[q + 1];
-      const int seg = __builtin_amdgcn_readfirstlane(t_seg[lo]);
-      const __amdgpu_buffer_rsrc_t rA1 = make_rsrc(
-          static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes, p.a1_seg_bytes);
-      const uint32_t k = static_cast<uint32_t>(kt * BK) + kc * C::EPC;
-      const bool kok = k < static_cast<uint32_t>(p.K1);
-      const uint32_t kb = k * ELT;
-#pragma unroll
-      for (int i = 0; i < C::CA; ++i) {
-        const int m = m0 + row0 + i * C::RPP;
-        ra[i] = load16(rA1, (kok && m < p.M) ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + kb : kOob);
-      }
-#pragma unroll
-      for (int i = 0; i < C::CB; ++i) {
-        const int jl = row0 + i * C::RPP;
-        const bool ok = kok && jl >= lo && jl < hi;
-        const uint32_t row = p.b1_gather ? static_cast<uint32_t>(t_perm[jl]) : static_cast<uint32_t>(j0 + jl);
-        rb[i] = load16(rB1, ok ? row * static_cast<uint32_t>(p.ldb1) * ELT + kb : kOob);
-      }
+    for (int i = 0; i < C::CB; ++i) {
+      const uint32_t jmask = (static_cast<uint32_t>(b_jl[i] - lo) < span) ? 0u : kOob;
+      b[i] = load16(rB, ((dense ? b0_row[i] : b1_row[i]) + kb) | kmask | jmask);
     }
+    if (!dense) {
+      ++lkt;
+      if (lkt >= s_hi) { lkt = s_lo; ++lq; }
+    }
+    ++lt;
   };
-  auto store_tile = [&](int buf) __attribute__((always_inline)) {
-    TI* a = smA + buf * BM * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
-    TI* b = smB + buf * BN * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
+  auto store_tile = [&](const u32x4 (&a)[C::CA], const u32x4 (&b)[C::CB], int buf) __attribute__((always_inline)) {
+    TI* da = smA + buf * BM * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
+    TI* db = smB + buf * BN * C::LDS_ROW + row0 * C::LDS_ROW + kc * C::EPC;
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i) *reinterpret_cast<u32x4*>(a + i * C::RPP * C::LDS_ROW) = ra[i];
+    for (int i = 0; i < C::CA; ++i) *reinterpret_cast<u32x4*>(da + i * C::RPP * C::LDS_ROW) = a[i];
 #pragma unroll
-    for (int i = 0; i < C::CB; ++i) *reinterpret_cast<u32x4*>(b + i * C::RPP * C::LDS_ROW) = rb[i];
+    for (int i = 0; i < C::CB; ++i) *reinterpret_cast<u32x4*>(db + i * C::RPP * C::LDS_ROW) = b[i];
   };
 
   const int wm = wave / WN, wn = wave % WN;
-  f32x4 acc[C::FM][C::FN];
+  accv acc[C::FM][C::FN];
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+      for (int v = 0; v < MT::NACC; ++v) acc[i][j][v] = 0.f;
 
-  const int frow = lane & 15, fk = (lane >> 4) * MT::KG;
-
-  if (ntiles > 0) { load_tile(0); store_tile(0); }
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ntiles) load_tile(t + 1);
-    const TI* a = smA + cur * BM * C::LDS_ROW + (wm * C::WTM + frow) * C::LDS_ROW + fk;
-    const TI* b = smB + cur * BN * C::LDS_ROW + (wn * C::WTN + frow) * C::LDS_ROW + fk;
+  const int frow = lane % MB, fk = (lane / MB) * MT::KG;
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const TI* a = smA + buf * BM * C::LDS_ROW + (wm * C::WTM + frow) * C::LDS_ROW + fk;
+    const TI* b = smB + buf * BN * C::LDS_ROW + (wn * C::WTN + frow) * C::LDS_ROW + fk;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += C::KS) {
       frag fa[C::FM], fb[C::FN];
 #pragma unroll
-      for (int i = 0; i < C::FM; ++i) fa[i] = MT::ld(a + i * 16 * C::LDS_ROW + kk);
+      for (int i = 0; i < C::FM; ++i) fa[i] = MT::ld(a + i * MB * C::LDS_ROW + kk);
 #pragma unroll
-      for (int j = 0; j < C::FN; ++j) fb[j] = MT::ld(b + j * 16 * C::LDS_ROW + kk);
+      for (int j = 0; j < C::FN; ++j) fb[j] = MT::ld(b + j * MB * C::LDS_ROW + kk);
 #pragma unroll
       for (int i = 0; i < C::FM; ++i)
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) acc[i][j] = MT::mma(fa[i], fb[j], acc[i][j]);
     }
-    if (t + 1 < ntiles) store_tile(cur ^ 1);
-    __syncthreads();
+  };
+
+  // prologue: k-tiles 0..STAGES-1 in flight, k-tile 0 staged in LDS buffer 0
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s) load_next(ra[s], rb[s]);
+  store_tile(ra[0], rb[0], 0);
+  __syncthreads();
+  // k-tile u sits in register stage u % STAGES until it is stored to LDS
+  // buffer u % 2 at the end of step u-1; the loop is unrolled so that both
+  // indices are compile-time constants
+  constexpr int U = (STAGES % 2 == 0) ? STAGES : 2 * STAGES;
+  for (int t = 0; t < ntiles; t += U) {
+#pragma unroll
+    for (int s = 0; s < U; ++s) {
+      if (t + s >= ntiles) break;
+      load_next(ra[s % STAGES], rb[s % STAGES]);                      // k-tile t+s+STAGES
+      compute(s % 2);                                                  // k-tile t+s
+      store_tile(ra[(s + 1) % STAGES], rb[(s + 1) % STAGES], (s + 1) % 2);  // k-tile t+s+1
+      __syncthreads();
+    }
   }
 
   // ---- epilogue: stage fp32 tile as [token][row], then 16-byte stores ------
@@ -253,9 +305,12 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
   for (int i = 0; i < C::FM; ++i)
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) {
-      const int col = wn * C::WTN + j * 16 + (lane & 15);
-      const int row = wm * C::WTM + i * 16 + (lane >> 4) * 4;
-      *reinterpret_cast<f32x4*>(st + col * C::ST_ROW + row) = acc[i][j];
+      const int col = wn * C::WTN + j * MB + lane % MB;
+      const int row = wm * C::WTM + i * MB;
+#pragma unroll
+      for (int v = 0; v < MT::NACC; v += 4)   // 4 consecutive rows per group
+        *reinterpret_cast<f32x4*>(st + col * C::ST_ROW + row + acc_row<MB>(lane, v)) =
+            f32x4{acc[i][j][v], acc[i][j][v + 1], acc[i][j][v + 2], acc[i][j][v + 3]};
     }
   __syncthreads();
 
@@ -300,27 +355,38 @@ __global__ __launch_bounds__(WM * WN * 64) void seg_gemm_kernel(const GemmParams
   }
 }
 
-template <typename TI, int BM, int BN, int BK, int WM, int WN>
+template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB = 16>
 hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
   dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_kernel<TI, BM, BN, BK, WM, WN>), grid, dim3(WM * WN * 64), 0, stream, p);
+  hipLaunchKernelGGL((seg_gemm_kernel<TI, BM, BN, BK, WM, WN, STAGES, OCC, MB>), grid,
+                     dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Tile shapes (measured on MI355X at the prefill, MLP and decode shapes of
+// the layer):
+//   Large  128 x 256 (d_out x tokens), 8 waves of 64 x 64, 32x32 MFMA    T >= 1024
+//   Mid    128 x 128, 8 waves of 32 x 64, 16x16 MFMA                    128 <= T < 1024
+//   Small   64 x  64, 4 waves of 32 x 32, 32x32 MFMA, split along k    T < 128, shrink
+//   F32     64 x  64, fp32 inputs
 void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
   switch (tile) {
-    case Tile::Large: *BM = 128; *BN = 128; *BK = 64; return;
+    case Tile::Large: *BM = 128; *BN = 256; *BK = 64; return;
+    case Tile::Mid: *BM = 128; *BN = 128; *BK = 64; return;
     case Tile::Small: *BM = 64; *BN = 64; *BK = 64; return;
     case Tile::F32: *BM = 64; *BN = 64; *BK = 32; return;
   }
 }
 
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream) {
-  if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2>(p, stream);
-  if (tile == Tile::Large) return launch_cfg<bf16_t, 128, 128, 64, 2, 2>(p, stream);
-  return launch_cfg<bf16_t, 64, 64, 64, 2, 2>(p, stream);
+  if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
+  switch (tile) {
+    case Tile::Large: return launch_cfg<bf16_t, 128, 256, 64, 2, 4, 2, 1, 32>(p, stream);
+    case Tile::Mid: return launch_cfg<bf16_t, 128, 128, 64, 4, 2, 2, 2, 16>(p, stream);
+    default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
+  }
 }
 
 }  // namespace cts
