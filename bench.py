@@ -85,6 +85,38 @@ def cpu_baseline(w, target_s):
                       "fp64 oracle time" % (done, w.T, distinct, spent)}
 
 
+def copy_calibration(torch, device, nbytes=256 << 20, reps=3):
+    """A plain device-to-device copy of known size (read nbytes, write nbytes),
+    run outside the timed region.  Under rocprofv3 --pmc its FETCH_SIZE and
+    WRITE_SIZE readings give the scale between the counters and real bytes."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device=device).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def traffic_from_profile(kernel_src):
+    """HBM bytes per launch of the fused GEMM measured with rocprofv3 --pmc
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the copy calibration), read from
+    the committed summary; None when there is none or the kernel source has
+    changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_seg_gemm_prefill_mix.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    digest = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
+    if fields.get("kernel_source_sha256") != digest or "hbm_bytes_per_launch" not in fields:
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
 def time_steps(fn, sets, steps, warmup, torch):
     for i in range(warmup):
         fn(sets[i % len(sets)])
@@ -140,6 +172,7 @@ def main():
 
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
+    copy_calibration(torch, device)
     log("generating %s" % args.workload)
     w = wl.make(args.workload)
 
@@ -190,6 +223,8 @@ def main():
         achieved = nbytes / t_main / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    if args.workload == "prefill_mix":
+        roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
     roof.update({"kernel": "seg_gemm_kernel (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
 

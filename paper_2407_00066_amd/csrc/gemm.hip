@@ -102,6 +102,31 @@ struct Cfg {
 
 __device__ __forceinline__ int split_lo(int n, int ks, int S) { return (int)((int64_t)n * ks / S); }
 
+// XCD-aware tile order.  The dispatcher hands workgroup b to XCD b % 8, and
+// each XCD has its own L2.  The linear block id is remapped so that XCD x
+// owns one contiguous range of a grouped tile order (GROUP m-tiles by all
+// n-tiles, column by column), i.e. a compact block of tiles whose weight rows
+// and token columns stay in that XCD's L2.  The map is a bijection for any
+// grid size.
+constexpr int kXcds = 8;
+constexpr int kGroupM = 8;
+__device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, int* ks) {
+  const int b = blockIdx.x;
+  const int nb_mn = gm * gn;
+  const int nb = static_cast<int>(gridDim.x);       // nb_mn * ksplit
+  const int q = nb / kXcds, rem = nb % kXcds;
+  const int x = b % kXcds, i = b / kXcds;
+  const int L = x * q + min(x, rem) + i;
+  *ks = L / nb_mn;
+  const int l = L % nb_mn;
+  const int per_group = kGroupM * gn;
+  const int g = l / per_group;
+  const int gsz = min(kGroupM, gm - g * kGroupM);   // m-tiles in this group
+  const int r = l % per_group;
+  *mt = g * kGroupM + r % gsz;
+  *nt = r / gsz;
+}
+
 // STAGES: register stages of global loads in flight; OCC: waves per SIMD the
 // register allocation must allow; MB: MFMA block (16 or 32).
 template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB>
@@ -122,9 +147,10 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
   TI* smB = smA + 2 * BM * C::LDS_ROW;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * BM;
-  const int j0 = blockIdx.y * BN;
-  const int ks = blockIdx.z;
+  int mt, nt, ks;
+  tile_of_block((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  const int m0 = mt * BM;
+  const int j0 = nt * BN;
   const int S = p.ksplit;
   const int jn = min(BN, p.N - j0);   // valid token columns in this tile
 
@@ -357,7 +383,8 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
 
 template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB = 16>
 hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
-  dim3 grid((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, p.ksplit);
+  // one linear dimension over (m-tile, n-tile, k-split), remapped in-kernel
+  dim3 grid(((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.ksplit);
   hipLaunchKernelGGL((seg_gemm_kernel<TI, BM, BN, BK, WM, WN, STAGES, OCC, MB>), grid,
                      dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
