@@ -70,7 +70,7 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   // small tiles split along k so that the weight stream is spread over >= 256
   // workgroups (one per compute unit).
   if (p->dtype == CTS_F32) pl->main_tile = Tile::F32;
-  else pl->main_tile = (T >= 1024) ? Tile::Large : (T >= 128 ? Tile::Mid : Tile::Small);
+  else pl->main_tile = (T >= 2048) ? Tile::Large : (T >= 128 ? Tile::Mid : Tile::Small);
   cts::tile_dims(pl->main_tile, &BM, &BN, &BK);
   {
     const int tiles = ceil_div(p->d_out, BM) * ceil_div(std::max(T, 1), BN);

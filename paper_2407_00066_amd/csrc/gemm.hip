@@ -256,12 +256,13 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
     const uint32_t kmask = (valid && k < static_cast<uint32_t>(dense ? p.K0 : p.K1)) ? 0u : kOob;
     const uint32_t kb = k * ELT;
     const uint32_t span = static_cast<uint32_t>(hi - lo);
+    const uint32_t dsel = dense ? 0xffffffffu : 0u;   // phase select by mask arithmetic
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i) a[i] = load16(rA, ((dense ? a0_row[i] : a1_row[i]) + kb) | kmask);
+    for (int i = 0; i < C::CA; ++i) a[i] = load16(rA, ((a1_row[i] ^ ((a0_row[i] ^ a1_row[i]) & dsel)) + kb) | kmask);
 #pragma unroll
     for (int i = 0; i < C::CB; ++i) {
       const uint32_t jmask = (static_cast<uint32_t>(b_jl[i] - lo) < span) ? 0u : kOob;
-      b[i] = load16(rB, ((dense ? b0_row[i] : b1_row[i]) + kb) | kmask | jmask);
+      b[i] = load16(rB, ((b1_row[i] ^ ((b0_row[i] ^ b1_row[i]) & dsel)) + kb) | kmask | jmask);
     }
     if (!dense) {
       ++lkt;
@@ -381,6 +382,411 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 variant with the k-tiles loaded straight into LDS.
+//
+// Each 16-byte buffer load writes its lane's chunk directly into LDS
+// (buffer_load_dwordx4 ... lds): one wave instruction fills 1 KB, i.e. 8 tile
+// rows of BK = 64 bf16 or 16 rows of BK = 32.  P LDS stages form a ring;
+// k-tile t+P-1 is loaded while k-tile t is multiplied, so P-1 k-tiles of
+// loads are in flight and no register holds staging data.  A lane stores
+// chunk c of its row in slot c ^ key(row) (XOR swizzle; key = row % 8 for
+// 128-byte rows, (row / 2) % 4 for 64-byte rows), which keeps the 16-byte
+// fragment reads of 8 consecutive rows on distinct LDS banks.  An
+// out-of-range lane (outside the operand, or a token column outside the
+// current cluster segment) writes zeros.
+//
+// The completion of the loads and of the fragment reads is waited for
+// explicitly (s_waitcnt with the exact count of loads still allowed in
+// flight), and the fragment reads are issued as ds_read_b128 in inline
+// assembly, so the compiler's blanket wait for LDS-writing loads before any
+// LDS read does not apply.
+template <int BK> __device__ __forceinline__ int swz_key(int row) {
+  return BK == 64 ? (row & 7) : ((row >> 1) & 3);
+}
+
+// The inline assembly below exists only in the device compilation pass (the
+// host pass of a HIP translation unit never executes kernel bodies).
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+#endif
+}
+
+template <int N> __device__ __forceinline__ void wait_lgkmcnt() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+#endif
+}
+
+// 16-byte LDS read issued as assembly: its completion is waited for with
+// wait_lgkmcnt, and pin() ties the fragment to that wait.
+__device__ __forceinline__ void lds_read16(bf16x8& dst, uint32_t addr) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("ds_read_b128 %0, %1" : "=v"(dst) : "v"(addr) : "memory");
+#endif
+}
+
+// 16-byte buffer load of each lane straight into LDS: lane l's chunk lands at
+// lds + 16*l (lds must be the same for the whole wave); out-of-range lanes
+// write zeros.
+__device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff,
+                                           0, 0, 0);
+#endif
+}
+
+__device__ __forceinline__ void pin(bf16x8& v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(v));
+#endif
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT>
+struct DmaCfg {
+  static constexpr int NT = WM * WN * 64, NW = WM * WN;
+  static constexpr int ROWB = BK * 2;                     // bytes per tile row
+  static constexpr int CH = BK / 8;                       // 16-byte chunks per row
+  static constexpr int RPI = 1024 / ROWB;                 // rows per 1 KB load
+  static constexpr int SB = (BM + BN) * ROWB;             // bytes per stage
+  static constexpr int QA = BM / RPI / NW, QB = BN / RPI / NW; // 1 KB loads per wave per k-tile
+  static constexpr int LPT = QA + QB;                     // loads per thread per k-tile
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int FM = WTM / MB, FN = WTN / MB;
+  static constexpr int KS = (MB == 32) ? 16 : 32;         // k per MFMA
+  static constexpr int NKS = BK / KS;
+  static constexpr int ST_ROW = BM + 4;
+  static constexpr int ST_BYTES = BN * ST_ROW * 4;
+  static constexpr int SMEM = (DIRECT || P * SB > ST_BYTES) ? P * SB : ST_BYTES;
+  static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "load split");
+  static_assert(WTM % MB == 0 && WTN % MB == 0 && BK % KS == 0, "wave tile");
+  static_assert(BK == 32 || BK == 64, "row width");
+  static_assert((P - 2) * LPT < 64, "vmcnt range");
+};
+
+// DIRECT: the epilogue writes straight from the accumulators (4 consecutive
+// output features of one token per lane) instead of staging the tile in LDS;
+// used when the fp32 tile does not fit in LDS.
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT>
+__global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const GemmParams p) {
+  using C = DmaCfg<BM, BN, BK, WM, WN, MB, P, DIRECT>;
+  using MT = MfmaTraits<bf16_t, MB>;
+  typedef typename MT::accv accv;
+  constexpr uint32_t ELT = 2;
+
+  __shared__ __attribute__((aligned(1024))) char smem[C::SMEM];
+  __shared__ int32_t t_perm[BN];
+  __shared__ int32_t t_seg[BN];
+  __shared__ int32_t run_start[BN + 1];
+  __shared__ int32_t wave_runs[C::NW];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int mt, nt, ks;
+  tile_of_block((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  const int m0 = mt * BM, j0 = nt * BN;
+  const int S = p.ksplit;
+  const int jn = min(BN, p.N - j0);
+
+  // ---- token columns of this tile: perm, segment, and segment runs -------
+  for (int i = tid; i < BN; i += C::NT) {
+    t_perm[i] = (i < jn) ? p.perm[j0 + i] : 0;
+    t_seg[i] = (i < jn && p.sorted_seg) ? p.sorted_seg[j0 + i] : 0;
+  }
+  __syncthreads();
+  int n_runs = 0;
+  for (int base = 0; base < BN; base += C::NT) {
+    const int i = base + tid;
+    const bool st = (i < jn) && (i == 0 || t_seg[i] != t_seg[i - 1]);
+    const uint64_t bal = __ballot(st);
+    if (lane == 0) wave_runs[wave] = __popcll(bal);
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < C::NW; ++w) {
+      const int c = wave_runs[w];
+      before += (w < wave) ? c : 0;
+      total += c;
+    }
+    if (st) {
+      const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      run_start[n_runs + before + __popcll(bal & lt)] = i;
+    }
+    n_runs += total;
+    __syncthreads();
+  }
+  if (!(p.sorted_seg && p.K1 > 0)) n_runs = 0;
+  if (tid == 0) run_start[n_runs] = jn;
+  __syncthreads();
+
+  // ---- k-tile schedule ----------------------------------------------------
+  const int nk0 = (p.K0 > 0) ? (p.K0 + BK - 1) / BK : 0;
+  const int nk1 = (p.K1 > 0) ? (p.K1 + BK - 1) / BK : 0;
+  int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0;
+  if (nk0 > 0) {
+    d_lo = split_lo(nk0, ks, S); d_hi = split_lo(nk0, ks + 1, S);
+    if (ks == 0) { s_lo = 0; s_hi = nk1; }
+  } else {
+    s_lo = split_lo(nk1, ks, S); s_hi = split_lo(nk1, ks + 1, S);
+  }
+  const int nd = d_hi - d_lo, ns = s_hi - s_lo;
+  const int ntiles = nd + n_runs * ns;
+
+  // ---- load mapping: this lane's row and chunk in each 1 KB load ------------
+  // load j of wave w covers tile rows [RPI*(w + NW*j), +RPI) of A (j < QA) or
+  // B; lane l takes row +l/CH and global chunk (l%CH) ^ key(row), stored at
+  // slot l%CH.
+  const int lrow = lane / C::CH;
+  const int lchunk = (lane % C::CH) ^ swz_key<BK>(lrow);
+  const uint32_t cbytes = static_cast<uint32_t>(lchunk * 16);
+  const uint32_t celem = static_cast<uint32_t>(lchunk * 8);
+  uint32_t a0_row[C::QA], a1_row[C::QA], b0_row[C::QB], b1_row[C::QB];
+  int b_jl[C::QB];
+#pragma unroll
+  for (int j = 0; j < C::QA; ++j) {
+    const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
+    const bool ok = m < p.M;
+    a0_row[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT : kOob;
+    a1_row[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT : kOob;
+  }
+#pragma unroll
+  for (int j = 0; j < C::QB; ++j) {
+    const int jl = C::RPI * (wave + C::NW * j) + lrow;
+    const uint32_t tok = static_cast<uint32_t>(t_perm[jl]);
+    const uint32_t r1 = p.b1_gather ? tok : static_cast<uint32_t>(j0 + jl);
+    b_jl[j] = jl;
+    b0_row[j] = tok * static_cast<uint32_t>(p.ldb0) * ELT;
+    b1_row[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT;
+  }
+  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(p.A0, p.a0_bytes);
+  const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
+  const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
+  char* const smem_a = smem + wave * 1024;                  // + stage*SB + j*NW*1024
+  char* const smem_b = smem + BM * C::ROWB + wave * 1024;
+
+  int lt = 0, lq = 0, lkt = s_lo;
+  // Per-k-tile load state, prepared once per k-tile (the loads themselves may
+  // be issued in several groups between the multiply steps).
+  struct TileLoad {
+    __amdgpu_buffer_rsrc_t rA, rB;
+    uint32_t kb, kmask, span, dsel;
+    int lo;
+  };
+  auto prep_next = [&, jn, n_runs, nd, ntiles, d_lo, s_lo, s_hi]() __attribute__((always_inline)) {
+    TileLoad L;
+    const bool valid = lt < ntiles;
+    const bool dense = lt < nd;
+    const int q = min(lq, max(n_runs - 1, 0));
+    L.lo = dense ? 0 : run_start[q];
+    const int hi = dense ? jn : run_start[q + 1];
+    const int seg = __builtin_amdgcn_readfirstlane(t_seg[L.lo]);
+    L.rA = dense ? rA0
+                 : make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
+                             p.a1_seg_bytes);
+    L.rB = dense ? rB0 : rB1;
+    const int kt = dense ? d_lo + lt : lkt;
+    const uint32_t k = static_cast<uint32_t>(kt * BK) + celem;
+    L.kmask = (valid && k < static_cast<uint32_t>(dense ? p.K0 : p.K1)) ? 0u : kOob;
+    L.kb = static_cast<uint32_t>(kt * BK) * ELT + cbytes;
+    L.span = static_cast<uint32_t>(hi - L.lo);
+    // phase select by mask arithmetic (a conditional pick between the two
+    // offset arrays would make the compiler keep them in scratch memory)
+    L.dsel = dense ? 0xffffffffu : 0u;
+    if (!dense) {
+      ++lkt;
+      if (lkt >= s_hi) { lkt = s_lo; ++lq; }
+    }
+    ++lt;
+    return L;
+  };
+  // issue loads [g0, g1) of the k-tile (A loads first, then B) into stage st
+  auto issue = [&](const TileLoad L, int st, int g0, int g1) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < C::QA; ++j)
+      if (j >= g0 && j < g1)
+        load16_lds(L.rA, smem_a + st * C::SB + j * C::NW * 1024,
+                   ((a1_row[j] ^ ((a0_row[j] ^ a1_row[j]) & L.dsel)) + L.kb) | L.kmask);
+#pragma unroll
+    for (int j = 0; j < C::QB; ++j) {
+      if (j + C::QA >= g0 && j + C::QA < g1) {
+        const uint32_t jmask = (static_cast<uint32_t>(b_jl[j] - L.lo) < L.span) ? 0u : kOob;
+        load16_lds(L.rB, smem_b + st * C::SB + j * C::NW * 1024,
+                   ((b1_row[j] ^ ((b0_row[j] ^ b1_row[j]) & L.dsel)) + L.kb) | L.kmask | jmask);
+      }
+    }
+  };
+  auto load_next = [&](int st) __attribute__((always_inline)) {
+    const TileLoad L = prep_next();
+    issue(L, st, 0, C::LPT);
+  };
+
+  // ---- fragment addresses ---------------------------------------------------
+  const int wm = wave / WN, wn = wave % WN;
+  const int fr = lane % MB, fg = lane / MB;                 // row in block, k group
+  const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+  const uint32_t a_row_addr = smem_base + static_cast<uint32_t>((wm * C::WTM + fr) * C::ROWB);
+  const uint32_t b_row_addr = smem_base + static_cast<uint32_t>(BM * C::ROWB + (wn * C::WTN + fr) * C::ROWB);
+  uint32_t slot[C::NKS];                                    // swizzled chunk slot per k-step
+#pragma unroll
+  for (int s2 = 0; s2 < C::NKS; ++s2) {
+    const int chunk = s2 * (C::KS / 8) + fg * (MT::KG / 8);
+    slot[s2] = static_cast<uint32_t>(((chunk ^ swz_key<BK>(fr)) * 16));
+  }
+
+  accv acc[C::FM][C::FN];
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+      for (int v = 0; v < MT::NACC; ++v) acc[i][j][v] = 0.f;
+
+  const int wphase = (C::NW >= 8 && wave >= C::NW / 2) ? C::NKS / 2 : 0;
+
+  // ---- main loop --------------------------------------------------------------
+#pragma unroll
+  for (int st = 0; st < P - 1; ++st) load_next(st);
+  int cur = 0;   // LDS stage of k-tile t
+  for (int t = 0; t < ntiles; ++t) {
+    wait_vmcnt<(P - 2) * C::LPT>();        // this thread's loads of k-tile t have landed
+    __builtin_amdgcn_s_barrier();          // ... and every wave's; stage of t-1 is free
+    int nst = cur + P - 1; if (nst >= P) nst -= P;
+    const TileLoad L = prep_next();        // k-tile t+P-1: its loads are issued in NKS
+    constexpr int GPS = (C::LPT + C::NKS - 1) / C::NKS;   // groups, one per multiply step;
+    // the two waves that share a SIMD (w and w + NW/2) issue their groups half a
+    // k-tile apart, so one multiplies while the other waits on load issue
+    const uint32_t sa = a_row_addr + cur * C::SB, sb = b_row_addr + cur * C::SB;
+    bf16x8 fa[2][C::FM], fb[2][C::FN];
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) lds_read16(fa[0][i], sa + slot[0] + i * MB * C::ROWB);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) lds_read16(fb[0][j], sb + slot[0] + j * MB * C::ROWB);
+#pragma unroll
+    for (int s2 = 0; s2 < C::NKS; ++s2) {
+      const int b = s2 & 1;
+      {
+        int g = s2 + wphase;
+        if (g >= C::NKS) g -= C::NKS;
+        issue(L, nst, g * GPS, (g + 1) * GPS);
+      }
+      if (s2 + 1 < C::NKS) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) lds_read16(fa[b ^ 1][i], sa + slot[s2 + 1] + i * MB * C::ROWB);
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) lds_read16(fb[b ^ 1][j], sb + slot[s2 + 1] + j * MB * C::ROWB);
+        // the fragments of step s2 are complete once only step s2+1's reads are pending
+        wait_lgkmcnt<(C::FM + C::FN < 15 ? C::FM + C::FN : 15)>();
+      } else {
+        wait_lgkmcnt<0>();
+      }
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) pin(fa[b][i]);
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) pin(fb[b][j]);
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) acc[i][j] = MT::mma(fa[b][i], fb[b][j], acc[i][j]);
+    }
+    cur = (cur + 1 == P) ? 0 : cur + 1;
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  if (DIRECT) {
+    // ---- epilogue from registers: lane holds rows acc_row(v..v+3) of column l%MB
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int jl = wn * C::WTN + j * MB + lane % MB;
+      const bool jok = jl < jn;
+      const int64_t orow = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+        for (int v = 0; v < MT::NACC; v += 4) {
+          const int m = m0 + wm * C::WTM + i * MB + acc_row<MB>(lane, v);
+          if (!jok || m >= p.M) continue;
+          const f32x4 val = f32x4{acc[i][j][v], acc[i][j][v + 1], acc[i][j][v + 2], acc[i][j][v + 3]};
+          if (p.part) {
+            *reinterpret_cast<f32x4*>(p.part + (static_cast<int64_t>(ks) * p.N + j0 + jl) * p.M + m) = val;
+          } else if (p.out_dtype == 1) {
+            uint2 w;
+            w.x = f32_to_bf16(val[0]) | (static_cast<uint32_t>(f32_to_bf16(val[1])) << 16);
+            w.y = f32_to_bf16(val[2]) | (static_cast<uint32_t>(f32_to_bf16(val[3])) << 16);
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + orow * p.ldo + m) = w;
+          } else {
+            *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + orow * p.ldo + m) = val;
+          }
+        }
+    }
+    return;
+  }
+
+  // ---- epilogue: stage fp32 tile as [token][row], then 16-byte stores ------
+  float* stg = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int col = wn * C::WTN + j * MB + lane % MB;
+      const int row = wm * C::WTM + i * MB;
+#pragma unroll
+      for (int v = 0; v < MT::NACC; v += 4)
+        *reinterpret_cast<f32x4*>(stg + col * C::ST_ROW + row + acc_row<MB>(lane, v)) =
+            f32x4{acc[i][j][v], acc[i][j][v + 1], acc[i][j][v + 2], acc[i][j][v + 3]};
+    }
+  __syncthreads();
+
+  if (p.part) {
+    float* part = p.part + static_cast<int64_t>(ks) * p.N * p.M;
+    constexpr int CPRO = BM / 4;
+    for (int c = tid; c < BN * CPRO; c += C::NT) {
+      const int jl = c / CPRO, mc = (c % CPRO) * 4;
+      if (jl < jn && m0 + mc < p.M)
+        *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(j0 + jl) * p.M + m0 + mc) =
+            *reinterpret_cast<const f32x4*>(stg + jl * C::ST_ROW + mc);
+    }
+  } else if (p.out_dtype == 1) {
+    constexpr int CPRO = BM / 8;
+    uint16_t* out = static_cast<uint16_t*>(p.out);
+    for (int c = tid; c < BN * CPRO; c += C::NT) {
+      const int jl = c / CPRO, mc = (c % CPRO) * 8;
+      if (jl < jn && m0 + mc < p.M) {
+        const float* s = stg + jl * C::ST_ROW + mc;
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(s);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(s + 4);
+        uint4 v;
+        v.x = f32_to_bf16(lo[0]) | (static_cast<uint32_t>(f32_to_bf16(lo[1])) << 16);
+        v.y = f32_to_bf16(lo[2]) | (static_cast<uint32_t>(f32_to_bf16(lo[3])) << 16);
+        v.z = f32_to_bf16(hi[0]) | (static_cast<uint32_t>(f32_to_bf16(hi[1])) << 16);
+        v.w = f32_to_bf16(hi[2]) | (static_cast<uint32_t>(f32_to_bf16(hi[3])) << 16);
+        const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
+        *reinterpret_cast<uint4*>(out + row * p.ldo + m0 + mc) = v;
+      }
+    }
+  } else {
+    constexpr int CPRO = BM / 4;
+    float* out = static_cast<float*>(p.out);
+    for (int c = tid; c < BN * CPRO; c += C::NT) {
+      const int jl = c / CPRO, mc = (c % CPRO) * 4;
+      if (jl < jn && m0 + mc < p.M) {
+        const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
+        *reinterpret_cast<f32x4*>(out + row * p.ldo + m0 + mc) =
+            *reinterpret_cast<const f32x4*>(stg + jl * C::ST_ROW + mc);
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0>
+hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
+  dim3 grid(((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.ksplit);
+  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT>), grid,
+                     dim3(WM * WN * 64), 0, stream, p);
+  return hipGetLastError();
+}
+
 template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB = 16>
 hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
   // one linear dimension over (m-tile, n-tile, k-split), remapped in-kernel
@@ -394,13 +800,14 @@ hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
 
 // Tile shapes (measured on MI355X at the prefill, MLP and decode shapes of
 // the layer):
-//   Large  128 x 256 (d_out x tokens), 8 waves of 64 x 64, 32x32 MFMA    T >= 1024
-//   Mid    128 x 128, 8 waves of 32 x 64, 16x16 MFMA                    128 <= T < 1024
+//   Large  256 x 256 (d_out x tokens), 8 waves of 64 x 128, 32x32 MFMA,
+//          k-tiles loaded straight into a 2-stage LDS ring            T >= 2048
+//   Mid    128 x 128, 8 waves of 32 x 64, 16x16 MFMA, register-staged  128 <= T < 2048
 //   Small   64 x  64, 4 waves of 32 x 32, 32x32 MFMA, split along k    T < 128, shrink
 //   F32     64 x  64, fp32 inputs
 void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
   switch (tile) {
-    case Tile::Large: *BM = 128; *BN = 256; *BK = 64; return;
+    case Tile::Large: *BM = 256; *BN = 256; *BK = 64; return;
     case Tile::Mid: *BM = 128; *BN = 128; *BK = 64; return;
     case Tile::Small: *BM = 64; *BN = 64; *BK = 64; return;
     case Tile::F32: *BM = 64; *BN = 64; *BK = 32; return;
@@ -410,7 +817,7 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream) {
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
-    case Tile::Large: return launch_cfg<bf16_t, 128, 256, 64, 2, 4, 2, 1, 32>(p, stream);
+    case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 32, 2, 1>(p, stream);
     case Tile::Mid: return launch_cfg<bf16_t, 128, 128, 64, 4, 2, 2, 2, 16>(p, stream);
     default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
   }

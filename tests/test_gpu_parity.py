@@ -74,6 +74,9 @@ SMALL = {
     "bf16_one_adapter": dict(cfg=105, T=130, d_in=128, d_out=136, r=16, n=1, K=1),
     "bf16_k_eq_n": dict(cfg=106, T=150, d_in=128, d_out=192, r=16, n=12, K=12),
     "bf16_r8": dict(cfg=107, T=70, d_in=64, d_out=72, r=8, n=5, K=2),
+    # T >= 2048 takes the LDS-ring GEMM: ragged in every dimension, many segments
+    "bf16_ring_ragged": dict(cfg=109, T=2300, d_in=328, d_out=280, r=24, n=90, K=11, ids="prefill",
+                             n_seq=20, seq_len=(40, 200)),
     "bf16_empty_clusters": dict(cfg=108, T=90, d_in=64, d_out=64, r=16, n=4, K=9),
 }
 
@@ -100,7 +103,7 @@ def test_apply_small(oracle_mod, small_cases, name):
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "f32_ragged", "bf16_ragged", "bf16_large_tiles",
-                                  "bf16_T1", "bf16_one_adapter"])
+                                  "bf16_T1", "bf16_one_adapter", "bf16_ring_ragged"])
 def test_uncompressed_small(oracle_mod, small_cases, name):
     w = small_cases[name]
     say("apply_uncompressed %s T=%d r_l=%d n=%d" % (name, w.T, w.r_l, w.n))
