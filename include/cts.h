@@ -27,7 +27,9 @@
  * Sigma_i (or B_i) by the caller.
  *
  * Memory and ownership.  Every array pointer is DEVICE memory owned by the
- * caller; `p` is HOST memory, read during the call only.  The library never
+ * caller; `p` is HOST memory, read during the call only.  Float arrays and
+ * the workspace must be 16-byte aligned, id arrays 4-byte aligned (device
+ * allocations are); a misaligned pointer is CTS_ERR_INVALID_ARG.  The library never
  * allocates, frees or synchronises in these calls: the caller provides a
  * device workspace of at least cts_workspace_size(p) (resp.
  * cts_workspace_size_uncompressed(p)) bytes, which may be reused between

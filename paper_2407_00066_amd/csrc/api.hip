@@ -28,9 +28,9 @@ struct Plan {
   int rank, nseg;
   Tile main_tile, shrink_tile;
   int main_split, shrink_split;
-  int max_items;
-  size_t off_perm, off_seg, off_aid, off_offs, off_items, off_nitems, off_zpart, off_zp, off_ypart,
-      total;
+  int max_items, max_ctiles;
+  size_t off_perm, off_seg, off_aid, off_offs, off_items, off_nitems, off_ctiles, off_nctiles,
+      off_zpart, off_zp, off_ypart, total;
 };
 
 constexpr uint64_t kMaxOperandBytes = 0x7fffffffull;   // buffer-load offsets are 31-bit
@@ -78,10 +78,14 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
     int s = (pl->main_tile == Tile::Small) ? ceil_div(256, tiles) : 1;
     pl->main_split = std::max(1, std::min(std::min(s, nk), 16));
   }
+  // shrink: one workgroup per (cluster segment tile of <= kSegTile tokens,
+  // 64 rank rows), split along d_in so that the grid covers the 256 CUs
   pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Small;
   cts::tile_dims(pl->shrink_tile, &BM, &BN, &BK);
+  pl->max_ctiles = cts::max_seg_tiles(T, pl->nseg);
   {
-    const int tiles = ceil_div(pl->rank, BM) * ceil_div(std::max(T, 1), BN);
+    const int expect = ceil_div(std::max(T, 1), BN) + std::min(pl->nseg, std::max(T, 1)) / 2;
+    const int tiles = ceil_div(pl->rank, BM) * std::max(expect, 1);
     const int nk = ceil_div(p->d_in, BK);
     pl->shrink_split = std::max(1, std::min(std::min(ceil_div(256, tiles), nk), 16));
   }
@@ -103,6 +107,8 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   pl->off_offs = off;  off = align_up(off + 4ull * (pl->nseg + 1));
   pl->off_items = off; off = align_up(off + 4ull * (pl->max_items + 1));
   pl->off_nitems = off; off = align_up(off + 4);
+  pl->off_ctiles = off; off = align_up(off + 4ull * (pl->max_ctiles + 1));
+  pl->off_nctiles = off; off = align_up(off + 4);
   pl->off_zpart = off; off = align_up(off + 4ull * pl->shrink_split * T * pl->rank);
   pl->off_zp = off;    off = align_up(off + static_cast<size_t>(pl->elt) * T * pl->rank);
   pl->off_ypart = off;
@@ -120,6 +126,12 @@ hipError_t mark(int i, hipStream_t s) {
 }
 
 struct Range { const void* p; size_t bytes; };
+
+// Every float array is read or written in 16-byte vectors: its address must be
+// a multiple of 16 (ids: of 4).
+bool misaligned(const void* ptr, uintptr_t a) {
+  return (reinterpret_cast<uintptr_t>(ptr) & (a - 1)) != 0;
+}
 
 bool overlap(Range a, Range b) {
   if (!a.p || !b.p || !a.bytes || !b.bytes) return false;
@@ -147,6 +159,8 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   int32_t* offs = reinterpret_cast<int32_t*>(ws + pl.off_offs);
   int32_t* items = reinterpret_cast<int32_t*>(ws + pl.off_items);
   int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
+  int32_t* ctiles = reinterpret_cast<int32_t*>(ws + pl.off_ctiles);
+  int32_t* n_ctiles = reinterpret_cast<int32_t*>(ws + pl.off_nctiles);
   float* zpart = reinterpret_cast<float*>(ws + pl.off_zpart);
   void* zp = ws + pl.off_zp;
   float* ypart = reinterpret_cast<float*>(ws + pl.off_ypart);
@@ -155,7 +169,8 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   hipError_t e = mark(0, stream);
   if (e != hipSuccess) return CTS_ERR_HIP;
   e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
-                                  pl.nseg, perm, offs, sseg, said, items, n_items, stream);
+                                  pl.nseg, perm, offs, sseg, said, items, n_items, ctiles,
+                                  n_ctiles, stream);
   if (e != hipSuccess || mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams g{};
@@ -168,6 +183,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   g.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = pl.shrink_split; g.part = zpart;
+  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
   e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
   if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 
@@ -230,6 +246,9 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
   if (T < 0 || n < 1 || K < 1 || !cluster_offsets) return CTS_ERR_INVALID_ARG;
   if (!cluster_of && K != n) return CTS_ERR_INVALID_ARG;
   if (T > 0 && (!adapter_id || !perm)) return CTS_ERR_INVALID_ARG;
+  if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4) || misaligned(perm, 4) ||
+      misaligned(cluster_offsets, 4))
+    return CTS_ERR_INVALID_ARG;
   if (T > cts::kSortMaxT || n > 65536 || K > 65536) return CTS_ERR_UNSUPPORTED;
   const Range out[2] = {{perm, 4ull * T}, {cluster_offsets, 4ull * (K + 1)}};
   const Range in[2] = {{adapter_id, 4ull * T}, {cluster_of, cluster_of ? 4ull * n : 0}};
@@ -238,7 +257,7 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
     for (const Range& i : in)
       if (overlap(o, i)) return CTS_ERR_INVALID_ARG;
   const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets,
-                                        nullptr, nullptr, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
@@ -252,6 +271,9 @@ int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
   if (p->T == 0) return CTS_OK;
   if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || !workspace)
     return CTS_ERR_INVALID_ARG;
+  for (const void* q : {x, W, U, Vt, Sigma, static_cast<const void*>(y), static_cast<const void*>(workspace)})
+    if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
+  if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4)) return CTS_ERR_INVALID_ARG;
   if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
   const size_t e = pl.elt;
   const size_t T = p->T, di = p->d_in, dout = p->d_out, r = p->r, n = p->n_adapters, K = p->n_clusters;
@@ -272,6 +294,9 @@ int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* a
   if (rc != CTS_OK) return rc;
   if (p->T == 0) return CTS_OK;
   if (!x || !adapter_id || !W || !A || !B || !y || !workspace) return CTS_ERR_INVALID_ARG;
+  for (const void* q : {x, W, A, B, static_cast<const void*>(y), static_cast<const void*>(workspace)})
+    if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
+  if (misaligned(adapter_id, 4)) return CTS_ERR_INVALID_ARG;
   if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
   const size_t e = pl.elt;
   const size_t T = p->T, di = p->d_in, dout = p->d_out, rl = p->r_lora, n = p->n_adapters;

@@ -38,15 +38,24 @@ inline int max_sigma_items(int T, int n) {
   return (T + kSigmaChunk - 1) / kSigmaChunk + (n < T ? n : T);
 }
 
+// Token columns of one shrink tile: a run of one cluster inside a kSegTile
+// window of sorted positions.
+constexpr int kSegTile = 64;
+inline int max_seg_tiles(int T, int nseg) {
+  return (T + kSegTile - 1) / kSegTile + (nseg < T ? nseg : T);
+}
+
 // Sorts tokens by (cluster, adapter, token).  Writes perm[T] and offs[K+1];
 // optionally sorted_seg[T] (cluster of each sorted position), sorted_aid[T]
 // (adapter of each sorted position) and the core-product items: items[0..c)
 // are the sorted positions where a run of one adapter starts or crosses a
-// multiple of kSigmaChunk, items[c] = T, and n_items[0] = c.  cluster_of may
-// be null (every adapter its own cluster, K == n).
+// multiple of kSigmaChunk, items[c] = T, and n_items[0] = c; likewise the
+// segment tiles ctiles/n_ctiles for runs of one cluster and kSegTile.
+// cluster_of may be null (every adapter its own cluster, K == n).
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
-                       int32_t* items, int32_t* n_items, hipStream_t stream);
+                       int32_t* items, int32_t* n_items, int32_t* ctiles, int32_t* n_ctiles,
+                       hipStream_t stream);
 
 // ----------------------------------------------------- segmented MFMA GEMM
 // out[j][m] (m < M rows of the weight operand, j < N sorted token positions) =
@@ -69,6 +78,10 @@ struct GemmParams {
   int ksplit;
   float* part;
   void* out; int64_t ldo; int out_perm; int out_dtype;
+  // optional explicit token tiles: tile t covers sorted positions
+  // [tile_start[t], tile_start[t+1]) (at most the tile width); n_tiles[0]
+  // tiles exist and the grid is sized for max_tiles (the rest exit at once)
+  const int32_t* tile_start; const int32_t* n_tiles; int max_tiles;
 };
 
 enum class Tile { Large, Mid, Small, F32 };

@@ -136,6 +136,7 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
   typedef typename MT::accv accv;
   typedef typename MT::frag frag;
   constexpr uint32_t ELT = sizeof(TI);
+  const int gn = p.tile_start ? p.max_tiles : (p.N + BN - 1) / BN;
 
   __shared__ __attribute__((aligned(16))) char smem[C::SMEM];
   __shared__ int32_t t_perm[BN];
@@ -148,11 +149,12 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int mt, nt, ks;
-  tile_of_block((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  tile_of_block((p.M + BM - 1) / BM, gn, &mt, &nt, &ks);
+  if (p.tile_start && nt >= p.n_tiles[0]) return;    // whole workgroup: no tile
   const int m0 = mt * BM;
-  const int j0 = nt * BN;
+  const int j0 = p.tile_start ? p.tile_start[nt] : nt * BN;
   const int S = p.ksplit;
-  const int jn = min(BN, p.N - j0);   // valid token columns in this tile
+  const int jn = p.tile_start ? (p.tile_start[nt + 1] - j0) : min(BN, p.N - j0);   // valid columns
 
   // ---- token columns of this tile: perm, segment, and segment runs -------
   for (int i = tid; i < BN; i += C::NT) {
@@ -790,7 +792,8 @@ hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
 template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB = 16>
 hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
   // one linear dimension over (m-tile, n-tile, k-split), remapped in-kernel
-  dim3 grid(((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.ksplit);
+  const int gn = p.tile_start ? p.max_tiles : (p.N + BN - 1) / BN;
+  dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
   hipLaunchKernelGGL((seg_gemm_kernel<TI, BM, BN, BK, WM, WN, STAGES, OCC, MB>), grid,
                      dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
@@ -815,6 +818,8 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
 }
 
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream) {
+  // explicit token tiles (at most kSegTile columns) only with the 64-wide tiles
+  if (p.tile_start && !(tile == Tile::Small || tile == Tile::F32)) return hipErrorInvalidValue;
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
     case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 32, 2, 1>(p, stream);

@@ -18,11 +18,27 @@ namespace {
 
 constexpr int kSigThreads = 256;
 constexpr int kSigMaxR = 128;
-constexpr int kPerThread = kSigmaChunk * kSigMaxR / kSigThreads;   // z elements per thread
+constexpr int kSigLd = kSigMaxR + 4;      // LDS row stride (floats): 16-byte aligned, conflict-free
 
-template <typename TI> __device__ __forceinline__ float ld(const TI* p, int64_t i);
-template <> __device__ __forceinline__ float ld<float>(const float* p, int64_t i) { return p[i]; }
-template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i].bits); }
+template <typename TI> struct Vec16;
+template <> struct Vec16<float> {          // 4 floats per 16 bytes
+  static constexpr int N = 4;
+  __device__ static __forceinline__ void widen(const uint4& v, float* o) {
+    o[0] = __uint_as_float(v.x); o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z); o[3] = __uint_as_float(v.w);
+  }
+};
+template <> struct Vec16<bf16_t> {         // 8 bf16 per 16 bytes
+  static constexpr int N = 8;
+  __device__ static __forceinline__ void widen(const uint4& v, float* o) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = bf16_to_f32(static_cast<uint16_t>(w[i] & 0xffffu));
+      o[2 * i + 1] = bf16_to_f32(static_cast<uint16_t>(w[i] >> 16));
+    }
+  }
+};
 
 template <typename TI> __device__ __forceinline__ void st(TI* p, int64_t i, float v);
 template <> __device__ __forceinline__ void st<float>(float* p, int64_t i, float v) { p[i] = v; }
@@ -36,54 +52,71 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             const int32_t* __restrict__ n_items,
                                                             const TI* __restrict__ Sigma,
                                                             TI* __restrict__ zp) {
-  __shared__ float z[kSigmaChunk * kSigMaxR];
-  __shared__ float sig[kSigMaxR * (kSigMaxR + 1)];
+  __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
+  __shared__ __attribute__((aligned(16))) float sig[kSigMaxR * kSigLd];
 
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
   const int tid = threadIdx.x;
   const int lo = items[item], hi = items[item + 1];
-  const int cnt = (hi - lo) * r;   // outputs of this item
+  const int nt = hi - lo;                 // tokens of this item (<= kSigmaChunk), one adapter
+  const int cnt = nt * r;                 // outputs of this item
 
-  // Sigma_a -> LDS (independent loads, issued before the partial sums)
-  const int ld_sig = r + 1;
+  // Sigma_a -> LDS as fp32, 16-byte loads (issued before the partial sums)
   if (Sigma != nullptr) {
     int a = sorted_aid[lo];
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
-    const TI* sa = Sigma + static_cast<int64_t>(a) * r * r;
-    for (int e = tid; e < r * r; e += kSigThreads) sig[(e / r) * ld_sig + (e % r)] = ld<TI>(sa, e);
-  }
-  // z = sum over k-splits, fixed order; the kPerThread loads of one split are independent
-  float acc[kPerThread];
+    constexpr int V = Vec16<TI>::N;
+    const uint4* sa = reinterpret_cast<const uint4*>(Sigma + static_cast<int64_t>(a) * r * r);
+    const int nv = r * r / V;
+    for (int e = tid; e < nv; e += kSigThreads) {
+      float w[V];
+      Vec16<TI>::widen(sa[e], w);
+      const int row = (e * V) / r, col = (e * V) % r;
 #pragma unroll
-  for (int u = 0; u < kPerThread; ++u) acc[u] = 0.f;
-  const int64_t split_stride = static_cast<int64_t>(T) * r;
-  const float* zbase = zpart + static_cast<int64_t>(lo) * r;
-  for (int q = 0; q < S; ++q) {
-#pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-      const int e = tid + u * kSigThreads;
-      if (e < cnt) acc[u] += zbase[q * split_stride + e];
+      for (int u = 0; u < V; ++u) sig[row * kSigLd + col + u] = w[u];
     }
   }
+  // z = sum over the shrink's k-splits in fixed order; 4 consecutive values
+  // per thread, 8 splits' loads in flight at a time
+  const int64_t split_stride = static_cast<int64_t>(T) * r;
+  const float* zbase = zpart + static_cast<int64_t>(lo) * r;
+  for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    int q = 0;
+    for (; q + 8 <= S; q += 8) {
+      f32x4 v[8];
 #pragma unroll
-  for (int u = 0; u < kPerThread; ++u) {
-    const int e = tid + u * kSigThreads;
-    if (e < cnt) z[e] = acc[u];
+      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; q < S; ++q) acc += *reinterpret_cast<const f32x4*>(zbase + q * split_stride + e4);
+    const int i = e4 / r, c = e4 % r;
+    *reinterpret_cast<f32x4*>(z + i * kSigLd + c) = acc;
   }
   __syncthreads();
 
   TI* out = zp + static_cast<int64_t>(lo) * r;
   if (Sigma == nullptr) {
-    for (int e = tid; e < cnt; e += kSigThreads) st<TI>(out, e, z[e]);
+    for (int e = tid; e < cnt; e += kSigThreads) st<TI>(out, e, z[(e / r) * kSigLd + e % r]);
     return;
   }
+  // z'[i][c] = sum_q Sigma[c][q] z[i][q]: one output per thread and pass,
+  // 16-byte LDS reads, fixed ascending q order
   for (int e = tid; e < cnt; e += kSigThreads) {
     const int i = e / r, c = e % r;
-    const float* srow = sig + c * ld_sig;
-    const float* zi = z + i * r;
+    const float* srow = sig + c * kSigLd;
+    const float* zi = z + i * kSigLd;
     float d = 0.f;
-    for (int q = 0; q < r; ++q) d = fmaf(srow[q], zi[q], d);
+    for (int q = 0; q < r; q += 4) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(srow + q);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(zi + q);
+      d = fmaf(a[0], b[0], d);
+      d = fmaf(a[1], b[1], d);
+      d = fmaf(a[2], b[2], d);
+      d = fmaf(a[3], b[3], d);
+    }
     st<TI>(out, e, d);
   }
 }

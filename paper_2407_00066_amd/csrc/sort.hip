@@ -35,7 +35,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
     const int32_t* __restrict__ adapter_id, const int32_t* __restrict__ cluster_of, int T, int n,
     int K, int bits_n, int bits_k, int32_t* __restrict__ perm, int32_t* __restrict__ offs,
     int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid,
-    int32_t* __restrict__ items, int32_t* __restrict__ n_items) {
+    int32_t* __restrict__ items, int32_t* __restrict__ n_items, int32_t* __restrict__ ctiles,
+    int32_t* __restrict__ n_ctiles) {
   __shared__ uint32_t key[kSortMaxT];
   __shared__ uint32_t buf0[kSortMaxT];
   __shared__ uint32_t buf1[kSortMaxT];
@@ -144,15 +145,15 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   }
   __syncthreads();
 
-  // core-product items: positions where the adapter changes or a
-  // kSigmaChunk window starts, compacted in order (ballot + wave prefix)
-  if (items) {
+  // Compaction of run starts, in order (ballot + wave prefix): a sorted
+  // position starts an entry when it starts a kChunk-aligned window or its
+  // key (masked by kmask) differs from the previous position's.
+  auto compact_starts = [&](uint32_t kmask, int chunk, int32_t* outp, int32_t* outn) {
     uint32_t done = 0;
     for (int base = 0; base < T; base += kSortThreads) {
       const int j = base + tid;
       bool st = false;
-      if (j < T)
-        st = (j % kSigmaChunk == 0) || ((key[in[j]] & amask) != (key[in[j - 1]] & amask));
+      if (j < T) st = (j % chunk == 0) || ((key[in[j]] & kmask) != (key[in[j - 1]] & kmask));
       const uint64_t bal = __ballot(st);
       if (lane == 0) hist[wave] = static_cast<uint32_t>(__popcll(bal));
       __syncthreads();
@@ -162,15 +163,19 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
         before += (w < wave) ? c : 0u;
         total += c;
       }
-      if (st) items[done + before + static_cast<uint32_t>(__popcll(bal & lt_mask))] = j;
+      if (st) outp[done + before + static_cast<uint32_t>(__popcll(bal & lt_mask))] = j;
       done += total;
       __syncthreads();
     }
     if (tid == 0) {
-      items[done] = T;
-      n_items[0] = static_cast<int32_t>(done);
+      outp[done] = T;
+      outn[0] = static_cast<int32_t>(done);
     }
-  }
+  };
+  // core-product items: runs of one adapter, cut at kSigmaChunk windows
+  if (items) compact_starts(amask, kSigmaChunk, items, n_items);
+  // segment tiles: runs of one cluster, cut at kSegTile windows
+  if (ctiles) compact_starts(~amask, kSegTile, ctiles, n_ctiles);
   for (int k = tid; k <= K; k += kSortThreads) {
     int lo = 0, hi = T;
     while (lo < hi) {
@@ -191,11 +196,13 @@ int ceil_log2(int v) {
 
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
-                       int32_t* items, int32_t* n_items, hipStream_t stream) {
+                       int32_t* items, int32_t* n_items, int32_t* ctiles, int32_t* n_ctiles,
+                       hipStream_t stream) {
   const int bits_n = ceil_log2(n);
   const int bits_k = cluster_of ? ceil_log2(K) : 0;  // key is the adapter alone when K == n
   hipLaunchKernelGGL(sort_kernel, dim3(1), dim3(kSortThreads), 0, stream, adapter_id, cluster_of,
-                     T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items);
+                     T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
+                     ctiles, n_ctiles);
   return hipGetLastError();
 }
 

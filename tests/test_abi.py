@@ -13,7 +13,7 @@ from paper_2407_00066_amd import _binding as B
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "cts.h")
 
-FAKE = ctypes.c_void_p(0x10000)   # never dereferenced: validation fails first
+FAKE = ctypes.c_void_p(0x10000)   # never dereferenced: validation fails first (16-byte aligned)
 
 
 def _declared():
@@ -83,6 +83,16 @@ def test_apply_null_pointers():
         ptrs[i] = None
         assert _apply(p, ptrs) == B.CTS_ERR_INVALID_ARG, i
     assert _apply(p, y=ctypes.c_void_p(0)) == B.CTS_ERR_INVALID_ARG
+
+
+def test_apply_rejects_misaligned_pointers():
+    p = _p()
+    for i in range(7):
+        ptrs = [ctypes.c_void_p(0x5000_0000_0000 + k * (1 << 32)) for k in range(7)]
+        ptrs[i] = ctypes.c_void_p(ptrs[i].value + (2 if i in (1, 2) else 8))
+        assert _apply(p, ptrs) == B.CTS_ERR_INVALID_ARG, i
+    assert _apply(p, y=ctypes.c_void_p(0x7000_0000_0000 + 8)) == B.CTS_ERR_INVALID_ARG
+    assert _apply(p, ws=ctypes.c_void_p(0x6000_0000_0000 + 4)) == B.CTS_ERR_INVALID_ARG
 
 
 def test_apply_t0_is_noop_without_pointers():
