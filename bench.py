@@ -225,7 +225,8 @@ def main():
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
     if args.workload == "prefill_mix":
         roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
-    roof.update({"kernel": "seg_gemm_kernel (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
+    gemm_kernel = ("seg_gemm_dma_kernel" if w.dtype == "bf16" and w.T >= 2048 else "seg_gemm_kernel")
+    roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
 
     cpu = None
