@@ -392,9 +392,11 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
 // rows of BK = 64 bf16 or 16 rows of BK = 32.  P LDS stages form a ring;
 // k-tile t+P-1 is loaded while k-tile t is multiplied, so P-1 k-tiles of
 // loads are in flight and no register holds staging data.  A lane stores
-// chunk c of its row in slot c ^ key(row) (XOR swizzle; key = row % 8 for
-// 128-byte rows, (row / 2) % 4 for 64-byte rows), which keeps the 16-byte
-// fragment reads of 8 consecutive rows on distinct LDS banks.  An
+// chunk c of its row in slot c ^ key(row) (XOR swizzle; key = (row / 2) % 8
+// for 128-byte rows, (row / 4) % 4 for 64-byte rows).  The LDS serves a
+// 16-byte read for 16 lanes (256 bytes, all 64 banks) per cycle, and a
+// fragment read covers 16 consecutive rows at one logical chunk: with this
+// key those 16 requests fall on 16 distinct bank groups.  An
 // out-of-range lane (outside the operand, or a token column outside the
 // current cluster segment) writes zeros.
 //
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
 // assembly, so the compiler's blanket wait for LDS-writing loads before any
 // LDS read does not apply.
 template <int BK> __device__ __forceinline__ int swz_key(int row) {
-  return BK == 64 ? (row & 7) : ((row >> 1) & 3);
+  return BK == 64 ? ((row >> 1) & 7) : ((row >> 2) & 3);
 }
 
 // The inline assembly below exists only in the device compilation pass (the
@@ -433,10 +435,11 @@ __device__ __forceinline__ void lds_read16(bf16x8& dst, uint32_t addr) {
 // 16-byte buffer load of each lane straight into LDS: lane l's chunk lands at
 // lds + 16*l (lds must be the same for the whole wave); out-of-range lanes
 // write zeros.
-__device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff) {
+__device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff,
+                                           uint32_t soff = 0) {
 #if defined(__HIP_DEVICE_COMPILE__)
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff,
-                                           0, 0, 0);
+                                           soff, 0, 0);
 #endif
 }
 
@@ -540,17 +543,25 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // B; lane l takes row +l/CH and global chunk (l%CH) ^ key(row), stored at
   // slot l%CH.
   const int lrow = lane / C::CH;
-  const int lchunk = (lane % C::CH) ^ swz_key<BK>(lrow);
+  // the key depends on the tile row modulo 16 only, and every wave's rows
+  // start at a multiple of 16 plus RPI * wave
+  static_assert((C::RPI * C::NW) % 16 == 0, "swizzle period");
+  const int lchunk = (lane % C::CH) ^ swz_key<BK>(C::RPI * wave + lrow);
   const uint32_t cbytes = static_cast<uint32_t>(lchunk * 16);
   const uint32_t celem = static_cast<uint32_t>(lchunk * 8);
-  uint32_t a0_row[C::QA], a1_row[C::QA], b0_row[C::QB], b1_row[C::QB];
+  // Per-lane byte offsets of this lane's chunk at k = 0, for the dense (0)
+  // and adapter (1) operands; kOob marks a row outside the operand (and, for
+  // the dense token operand, a column outside the tile).  A k-tile adds its
+  // uniform k byte offset: in the dense phase as the load's scalar offset, so
+  // a full dense k-tile needs no per-lane arithmetic at all.
+  uint32_t a0_v[C::QA], a1_v[C::QA], b0_v[C::QB], b1_v[C::QB];
   int b_jl[C::QB];
 #pragma unroll
   for (int j = 0; j < C::QA; ++j) {
     const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
     const bool ok = m < p.M;
-    a0_row[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT : kOob;
-    a1_row[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT : kOob;
+    a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT + cbytes : kOob;
+    a1_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + cbytes : kOob;
   }
 #pragma unroll
   for (int j = 0; j < C::QB; ++j) {
@@ -558,8 +569,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     const uint32_t tok = static_cast<uint32_t>(t_perm[jl]);
     const uint32_t r1 = p.b1_gather ? tok : static_cast<uint32_t>(j0 + jl);
     b_jl[j] = jl;
-    b0_row[j] = tok * static_cast<uint32_t>(p.ldb0) * ELT;
-    b1_row[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT;
+    b0_v[j] = (jl < jn) ? tok * static_cast<uint32_t>(p.ldb0) * ELT + cbytes : kOob;
+    b1_v[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT + cbytes;
   }
   const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(p.A0, p.a0_bytes);
   const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
@@ -572,51 +583,73 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // be issued in several groups between the multiply steps).
   struct TileLoad {
     __amdgpu_buffer_rsrc_t rA, rB;
-    uint32_t kb, kmask, span, dsel;
+    uint32_t kk, kmask, span, dsel;   // kk: uniform k byte offset of the k-tile
     int lo;
   };
   auto prep_next = [&, jn, n_runs, nd, ntiles, d_lo, s_lo, s_hi]() __attribute__((always_inline)) {
     TileLoad L;
     const bool valid = lt < ntiles;
-    const bool dense = lt < nd;
-    const int q = min(lq, max(n_runs - 1, 0));
-    L.lo = dense ? 0 : run_start[q];
-    const int hi = dense ? jn : run_start[q + 1];
-    const int seg = __builtin_amdgcn_readfirstlane(t_seg[L.lo]);
-    L.rA = dense ? rA0
-                 : make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
-                             p.a1_seg_bytes);
-    L.rB = dense ? rB0 : rB1;
-    const int kt = dense ? d_lo + lt : lkt;
-    const uint32_t k = static_cast<uint32_t>(kt * BK) + celem;
-    L.kmask = (valid && k < static_cast<uint32_t>(dense ? p.K0 : p.K1)) ? 0u : kOob;
-    L.kb = static_cast<uint32_t>(kt * BK) * ELT + cbytes;
-    L.span = static_cast<uint32_t>(hi - L.lo);
-    // phase select by mask arithmetic (a conditional pick between the two
-    // offset arrays would make the compiler keep them in scratch memory)
-    L.dsel = dense ? 0xffffffffu : 0u;
-    if (!dense) {
+    uint32_t k0, klim;
+    if (lt < nd) {
+      // dense phase (W X): a wave-uniform branch that touches no LDS, so the
+      // steady state pays no lookup latency between barrier and multiply
+      L.lo = 0;
+      L.span = static_cast<uint32_t>(jn);
+      L.rA = rA0;
+      L.rB = rB0;
+      L.dsel = 0xffffffffu;
+      k0 = static_cast<uint32_t>((d_lo + lt) * BK);
+      klim = static_cast<uint32_t>(p.K0);
+    } else {
+      // adapter phase (U_k Z'): one cluster run of the tile per k-tile group
+      const int q = min(lq, max(n_runs - 1, 0));
+      L.lo = run_start[q];
+      const int hi = run_start[q + 1];
+      const int seg = __builtin_amdgcn_readfirstlane(t_seg[L.lo]);
+      L.rA = make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
+                       p.a1_seg_bytes);
+      L.rB = rB1;
+      L.span = static_cast<uint32_t>(hi - L.lo);
+      // phase select by mask arithmetic (a conditional pick between the two
+      // offset arrays would make the compiler keep them in scratch memory)
+      L.dsel = 0u;
+      k0 = static_cast<uint32_t>(lkt * BK);
+      klim = static_cast<uint32_t>(p.K1);
       ++lkt;
       if (lkt >= s_hi) { lkt = s_lo; ++lq; }
     }
+    L.kmask = (valid && k0 + celem < klim) ? 0u : kOob;
+    L.kk = k0 * ELT;
     ++lt;
     return L;
   };
-  // issue loads [g0, g1) of the k-tile (A loads first, then B) into stage st
+  // issue loads [g0, g1) of the k-tile (A loads first, then B) into stage st;
+  // general form: any phase, per-lane k and column masks
   auto issue = [&](const TileLoad L, int st, int g0, int g1) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < C::QA; ++j)
       if (j >= g0 && j < g1)
         load16_lds(L.rA, smem_a + st * C::SB + j * C::NW * 1024,
-                   ((a1_row[j] ^ ((a0_row[j] ^ a1_row[j]) & L.dsel)) + L.kb) | L.kmask);
+                   ((a1_v[j] ^ ((a0_v[j] ^ a1_v[j]) & L.dsel)) + L.kk) | L.kmask);
 #pragma unroll
     for (int j = 0; j < C::QB; ++j) {
       if (j + C::QA >= g0 && j + C::QA < g1) {
         const uint32_t jmask = (static_cast<uint32_t>(b_jl[j] - L.lo) < L.span) ? 0u : kOob;
         load16_lds(L.rB, smem_b + st * C::SB + j * C::NW * 1024,
-                   ((b1_row[j] ^ ((b0_row[j] ^ b1_row[j]) & L.dsel)) + L.kb) | L.kmask | jmask);
+                   ((b1_v[j] ^ ((b0_v[j] ^ b1_v[j]) & L.dsel)) + L.kk) | L.kmask | jmask);
       }
     }
+  };
+  // fast form: dense phase, whole k-tile; an out-of-range row stays at kOob
+  // (plus a k offset below 2^31, still past the end of the operand)
+  auto issue_fast = [&](const TileLoad L, int st, int g0, int g1) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < C::QA; ++j)
+      if (j >= g0 && j < g1) load16_lds(rA0, smem_a + st * C::SB + j * C::NW * 1024, a0_v[j], L.kk);
+#pragma unroll
+    for (int j = 0; j < C::QB; ++j)
+      if (j + C::QA >= g0 && j + C::QA < g1)
+        load16_lds(rB0, smem_b + st * C::SB + j * C::NW * 1024, b0_v[j], L.kk);
   };
   auto load_next = [&](int st) __attribute__((always_inline)) {
     const TileLoad L = prep_next();
@@ -644,55 +677,100 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 #pragma unroll
       for (int v = 0; v < MT::NACC; ++v) acc[i][j][v] = 0.f;
 
-  const int wphase = (C::NW >= 8 && wave >= C::NW / 2) ? C::NKS / 2 : 0;
-
   // ---- main loop --------------------------------------------------------------
+  // Per k-tile t (LDS stage cur), multiply step s uses fragment buffer s % 2:
+  //  * steps before the last: the MFMAs of step s are interleaved one by one
+  //    with the fragment reads of step s+1 and, in the first half of the
+  //    k-tile, with the loads of k-tile t+P-1;
+  //  * last step: half of its MFMAs, then the wait for this lane's loads of
+  //    k-tile t+1 and the workgroup barrier (after it every wave's loads of
+  //    t+1 are in LDS and every wave has finished reading k-tile t-1's stage,
+  //    which the next iteration overwrites), then the fragment reads of
+  //    k-tile t+1's first step interleaved with the remaining MFMAs.
+  // So no multiply step waits on fragment-read latency, and the barrier sits
+  // behind MFMAs already issued.
+  static_assert(C::NKS % 2 == 0, "fragment buffers alternate across k-tiles");
+  constexpr int NM = C::FM * C::FN;                          // MFMAs per step
+  constexpr int NR = C::FM + C::FN;                          // fragment reads per step
+  constexpr int NLG = C::NKS > 2 ? C::NKS / 2 : 1;           // steps that issue loads
+  constexpr int GPS = (C::LPT + NLG - 1) / NLG;              // loads per such step
+  static_assert(GPS <= (NM > NR ? NM : NR), "every load gets an issue slot");
+  bf16x8 fa[2][C::FM], fb[2][C::FN];
+  auto read_frag = [&](int buf, int r, uint32_t sa, uint32_t sb, uint32_t sl) __attribute__((always_inline)) {
+    if (r < C::FM) lds_read16(fa[buf][r], sa + sl + r * MB * C::ROWB);
+    else lds_read16(fb[buf][r - C::FM], sb + sl + (r - C::FM) * MB * C::ROWB);
+  };
+  auto mma = [&](int buf, int m) __attribute__((always_inline)) {
+    const int i = m / C::FN, j = m % C::FN;
+    acc[i][j] = MT::mma(fa[buf][i], fb[buf][j], acc[i][j]);
+  };
+
 #pragma unroll
   for (int st = 0; st < P - 1; ++st) load_next(st);
+  wait_vmcnt<(P - 2) * C::LPT>();
+  __builtin_amdgcn_s_barrier();
+#pragma unroll
+  for (int r = 0; r < NR; ++r) read_frag(0, r, a_row_addr, b_row_addr, slot[0]);
+
+  // Dense k-tiles that cover a whole BK slice are a prefix of the schedule;
+  // while the k-tile being loaded is one of them the loop runs the fast load
+  // form (uniform k offset only), then the general form to the end.
+  const int nd_full = nd - ((nd > 0 && d_hi * BK > p.K0) ? 1 : 0);
+  const int nfast = max(0, min(ntiles, nd_full - (P - 1)));
   int cur = 0;   // LDS stage of k-tile t
-  for (int t = 0; t < ntiles; ++t) {
-    wait_vmcnt<(P - 2) * C::LPT>();        // this thread's loads of k-tile t have landed
-    __builtin_amdgcn_s_barrier();          // ... and every wave's; stage of t-1 is free
-    int nst = cur + P - 1; if (nst >= P) nst -= P;
-    const TileLoad L = prep_next();        // k-tile t+P-1: its loads are issued in NKS
-    constexpr int GPS = (C::LPT + C::NKS - 1) / C::NKS;   // groups, one per multiply step;
-    // the two waves that share a SIMD (w and w + NW/2) issue their groups half a
-    // k-tile apart, so one multiplies while the other waits on load issue
+  auto ktile = [&](const TileLoad L, const bool fast) __attribute__((always_inline)) {
+    int nst = cur + P - 1; if (nst >= P) nst -= P;         // stage of k-tile t+P-1
+    int ncur = cur + 1; if (ncur >= P) ncur -= P;          // stage of k-tile t+1
     const uint32_t sa = a_row_addr + cur * C::SB, sb = b_row_addr + cur * C::SB;
-    bf16x8 fa[2][C::FM], fb[2][C::FN];
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) lds_read16(fa[0][i], sa + slot[0] + i * MB * C::ROWB);
-#pragma unroll
-    for (int j = 0; j < C::FN; ++j) lds_read16(fb[0][j], sb + slot[0] + j * MB * C::ROWB);
+    const uint32_t na = a_row_addr + ncur * C::SB, nb = b_row_addr + ncur * C::SB;
+    auto iss = [&](int g0, int g1) __attribute__((always_inline)) {
+      if (fast) issue_fast(L, nst, g0, g1);
+      else issue(L, nst, g0, g1);
+    };
 #pragma unroll
     for (int s2 = 0; s2 < C::NKS; ++s2) {
       const int b = s2 & 1;
-      {
-        int g = s2 + wphase;
-        if (g >= C::NKS) g -= C::NKS;
-        issue(L, nst, g * GPS, (g + 1) * GPS);
-      }
-      if (s2 + 1 < C::NKS) {
-#pragma unroll
-        for (int i = 0; i < C::FM; ++i) lds_read16(fa[b ^ 1][i], sa + slot[s2 + 1] + i * MB * C::ROWB);
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j) lds_read16(fb[b ^ 1][j], sb + slot[s2 + 1] + j * MB * C::ROWB);
-        // the fragments of step s2 are complete once only step s2+1's reads are pending
-        wait_lgkmcnt<(C::FM + C::FN < 15 ? C::FM + C::FN : 15)>();
-      } else {
-        wait_lgkmcnt<0>();
-      }
+      wait_lgkmcnt<0>();                                   // step s2's fragments are in
 #pragma unroll
       for (int i = 0; i < C::FM; ++i) pin(fa[b][i]);
 #pragma unroll
       for (int j = 0; j < C::FN; ++j) pin(fb[b][j]);
+      if (s2 + 1 < C::NKS) {
 #pragma unroll
-      for (int i = 0; i < C::FM; ++i)
+        for (int m = 0; m < (NM > NR ? NM : NR); ++m) {
+          if (m < NM) mma(b, m);
+          if (m < NR) read_frag(b ^ 1, m, sa, sb, slot[s2 + 1]);
+          if (s2 < NLG && m < GPS) iss(s2 * GPS + m, s2 * GPS + m + 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) acc[i][j] = MT::mma(fa[b][i], fb[b][j], acc[i][j]);
+        for (int m = 0; m < NM / 2; ++m) {
+          mma(b, m);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        wait_vmcnt<(P - 2) * C::LPT>();                    // this lane's loads of k-tile t+1
+        __builtin_amdgcn_s_barrier();                      // ... and every wave's
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int m = 0; m < (NM - NM / 2 > NR ? NM - NM / 2 : NR); ++m) {
+          if (NM / 2 + m < NM) mma(b, NM / 2 + m);
+          if (m < NR) read_frag(b ^ 1, m, na, nb, slot[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
     }
-    cur = (cur + 1 == P) ? 0 : cur + 1;
+    cur = ncur;
+  };
+  int t = 0;
+  for (; t < nfast; ++t) {
+    TileLoad L;                                            // dense k-tile lt, whole
+    L.kk = static_cast<uint32_t>((d_lo + lt) * BK) * ELT;
+    ++lt;
+    ktile(L, true);
   }
+  for (; t < ntiles; ++t) ktile(prep_next(), false);
+  wait_lgkmcnt<0>();
   wait_vmcnt<0>();
   __syncthreads();
 
