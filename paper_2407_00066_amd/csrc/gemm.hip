@@ -900,7 +900,7 @@ hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStre
   if (p.tile_start && !(tile == Tile::Small || tile == Tile::F32)) return hipErrorInvalidValue;
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
-    case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 32, 2, 1>(p, stream);
+    case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 16, 2, 1>(p, stream);
     case Tile::Mid: return launch_cfg<bf16_t, 128, 128, 64, 4, 2, 2, 2, 16>(p, stream);
     default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
   }

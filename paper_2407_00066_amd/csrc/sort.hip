@@ -1,34 +1,81 @@
 // Token bucketing: a stable LSD radix sort of the token indices by the
 // composite key (cluster << bits_n | adapter), done by one 1024-thread
-// workgroup entirely in LDS.  The token index is the implicit last key
-// (stability), so the order is the unique (cluster, adapter, token) order.
+// workgroup entirely in LDS.  (key, token) pairs move together and the token
+// index is the implicit last key (stability), so the order is the unique
+// (cluster, adapter, token) order.
 //
 // Grouping tokens by cluster is what turns the shared-basis products into
 // contiguous GEMM segments: every LoRA of cluster k uses U_k, V_k (Sec. 3.2).
 //
-// Per radix pass (digit of <= 8 bits), each of the 16 waves owns a contiguous
-// run of tokens.  A wave ranks equal digits inside each 64-token chunk with
-// one ballot per digit bit (lanes with identical digits get identical
-// ballot-and masks), so ranking needs no atomics and is deterministic:
-//   1) count walk:   per-wave digit histogram in LDS,
-//   2) scan:         exclusive scan over (digit, wave) in digit-major order,
-//   3) scatter walk: position = running base + rank among equal digits.
+// Per 8-bit radix pass, each of the 16 waves owns a contiguous run of
+// 64-token chunks.  Inside a chunk, a lane finds the lanes holding the same
+// digit with ballots (deterministic, no atomics): first one ballot per
+// distinct digit of the chunk (tokens of one request share an adapter, so a
+// chunk usually holds one to three digits), then, if more than eight distinct
+// digits remain, one ballot per digit bit.  The count walk records each
+// token's offset inside its (wave, digit) group; an exclusive scan in
+// (digit, wave) order turns the group sizes into bases; the scatter walk
+// writes every pair to base + offset.
+//
+// After the last pass one blocked scan compacts, in sorted order, the starts
+// of the Sigma-stage items (runs of one adapter cut at kSigmaChunk) and of
+// the shrink's segment tiles (runs of one cluster cut at kSegTile).
 #include "cts_internal.h"
 
 namespace cts {
 namespace {
 
 constexpr int kWaves = kSortThreads / 64;
-constexpr int kRadix = 256;
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int kMaxCpw = kSortMaxT / 64 / kWaves;   // chunks per wave, at most
+static_assert(kWaves * kRadix == 4 * kSortThreads, "scan: four counters per thread");
 
-__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int dbits) {
-  uint64_t m = __ballot(valid);
-  for (int b = 0; b < dbits; ++b) {
-    const bool bit = (d >> b) & 1u;
-    const uint64_t bb = __ballot(bit);
-    m &= bit ? bb : ~bb;
+// Lanes of this wave whose digit equals this lane's (only lanes in `valid`).
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t valid, int lane) {
+  uint64_t rem = valid, peers = 0;
+  for (int it = 0; it < 8 && rem; ++it) {
+    const int leader = __ffsll(static_cast<unsigned long long>(rem)) - 1;
+    const uint32_t dl = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(d), leader));
+    const uint64_t eq = __ballot(d == dl) & valid;
+    if (d == dl) peers = eq;
+    rem &= ~eq;
   }
-  return m;
+  if (rem) {
+    uint64_t m = valid;
+#pragma unroll
+    for (int b = 0; b < kRadixBits; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      m &= bit ? bb : ~bb;
+    }
+    if ((rem >> lane) & 1ull) peers = m;
+  }
+  return peers;
+}
+
+// Exclusive scan of one value per thread over the workgroup; also returns the
+// total.  Uses wsum[kWaves]; contains two barriers.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, int lane, int wave,
+                                                         uint32_t* total) {
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t u = __shfl_up(x, off);
+    if (lane >= off) x += u;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t s = wsum[w];
+    before += (w < wave) ? s : 0u;
+    all += s;
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
 }
 
 __global__ __launch_bounds__(kSortThreads) void sort_kernel(
@@ -37,150 +84,146 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
     int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid,
     int32_t* __restrict__ items, int32_t* __restrict__ n_items, int32_t* __restrict__ ctiles,
     int32_t* __restrict__ n_ctiles) {
-  __shared__ uint32_t key[kSortMaxT];
-  __shared__ uint32_t buf0[kSortMaxT];
-  __shared__ uint32_t buf1[kSortMaxT];
-  __shared__ uint32_t hist[kWaves * kRadix];
-  __shared__ uint32_t tot[kRadix];
-  __shared__ uint32_t incl[kRadix];
-  __shared__ uint32_t wsum[4];
+  __shared__ uint32_t kbuf[2][kSortMaxT];
+  __shared__ uint16_t vbuf[2][kSortMaxT];
+  __shared__ uint32_t hist[kWaves * kRadix];   // [wave][digit]
+  __shared__ uint32_t wsum[kWaves];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // key layout: cluster << bits_n | adapter; without a cluster map (K == n)
+  // the key is the adapter, which is also its cluster
+  const int cshift = cluster_of ? bits_n : 0;
 
   for (int t = tid; t < T; t += kSortThreads) {
     int a = adapter_id[t];
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
-    int c = cluster_of ? cluster_of[a] : a;
-    c = c < 0 ? 0 : (c >= K ? K - 1 : c);
-    key[t] = (static_cast<uint32_t>(c) << bits_n) | static_cast<uint32_t>(a);
-    buf0[t] = static_cast<uint32_t>(t);
+    uint32_t key = static_cast<uint32_t>(a);
+    if (cluster_of) {
+      int c = cluster_of[a];
+      c = c < 0 ? 0 : (c >= K ? K - 1 : c);
+      key |= static_cast<uint32_t>(c) << bits_n;
+    }
+    kbuf[0][t] = key;
+    vbuf[0][t] = static_cast<uint16_t>(t);
   }
-  __syncthreads();
 
-  const int total_bits = bits_n + bits_k;
-  const int passes = (total_bits + 7) / 8;
-  const int dbits = passes ? (total_bits + passes - 1) / passes : 0;
-  const uint32_t dmask = (1u << dbits) - 1u;
-  const int R = 1 << dbits;
+  const int passes = (bits_n + bits_k + kRadixBits - 1) / kRadixBits;
   const int chunks = (T + 63) / 64;
   const int cpw = (chunks + kWaves - 1) / kWaves;
   const int seg_lo = wave * cpw * 64;
   const int seg_hi = min(T, seg_lo + cpw * 64);
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 
-  uint32_t* in = buf0;
-  uint32_t* out = buf1;
+  int in = 0;
   for (int p = 0; p < passes; ++p) {
-    const int shift = p * dbits;
-    for (int i = tid; i < kWaves * kRadix; i += kSortThreads) hist[i] = 0;
+    const int shift = p * kRadixBits;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hist[tid + i * kSortThreads] = 0;
     __syncthreads();
 
-    // 1) count walk (wave-private histogram rows; leaders have distinct digits)
-    for (int b = seg_lo; b < seg_hi; b += 64) {
-      const int idx = b + lane;
-      const bool valid = idx < seg_hi;
-      const uint32_t item = valid ? in[idx] : 0u;
-      const uint32_t d = valid ? ((key[item] >> shift) & dmask) : 0u;
-      const uint64_t peers = match_digit(d, valid, dbits);
-      if (valid && lane == __ffsll(static_cast<unsigned long long>(peers)) - 1)
-        hist[wave * kRadix + d] += static_cast<uint32_t>(__popcll(peers));
-    }
-    __syncthreads();
-
-    // 2) exclusive scan in (digit, wave) order
-    if (tid < R) {
-      uint32_t s = 0;
-      for (int w = 0; w < kWaves; ++w) s += hist[w * kRadix + tid];
-      tot[tid] = s;
-    }
-    __syncthreads();
-    if (tid < kRadix) {
-      uint32_t v = (tid < R) ? tot[tid] : 0u;
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t u = __shfl_up(v, off);
-        if (lane >= off) v += u;
-      }
-      incl[tid] = v;
-      if (lane == 63) wsum[wave] = v;
-    }
-    __syncthreads();
-    if (tid < R) {
-      uint32_t run = incl[tid] - tot[tid];
-      for (int w = 0; w < wave; ++w) run += wsum[w];
-      for (int w = 0; w < kWaves; ++w) {
-        const uint32_t h = hist[w * kRadix + tid];
-        hist[w * kRadix + tid] = run;
-        run += h;
+    // count walk: offset of each token inside its (wave, digit) group
+    uint32_t kr[kMaxCpw], dr[kMaxCpw], pos[kMaxCpw];
+    uint16_t vr[kMaxCpw];
+#pragma unroll
+    for (int c = 0; c < kMaxCpw; ++c) {
+      kr[c] = 0; dr[c] = 0; pos[c] = 0; vr[c] = 0;
+      if (c < cpw) {
+        const int idx = seg_lo + c * 64 + lane;
+        const bool valid = idx < seg_hi;
+        const uint32_t k = valid ? kbuf[in][idx] : 0u;
+        const uint16_t v = valid ? vbuf[in][idx] : static_cast<uint16_t>(0);
+        const uint32_t d = (k >> shift) & (kRadix - 1);
+        const uint64_t peers = match_digit(d, __ballot(valid), lane);
+        const uint32_t rank = static_cast<uint32_t>(__popcll(peers & lt_mask));
+        // every lane of a digit group reads the count before the group's
+        // lowest lane adds the group size (same wave: in order)
+        const uint32_t old = valid ? hist[wave * kRadix + d] : 0u;
+        if (valid && rank == 0) hist[wave * kRadix + d] = old + static_cast<uint32_t>(__popcll(peers));
+        kr[c] = k; vr[c] = v; dr[c] = d; pos[c] = old + rank;
       }
     }
     __syncthreads();
 
-    // 3) scatter walk
-    for (int b = seg_lo; b < seg_hi; b += 64) {
-      const int idx = b + lane;
-      const bool valid = idx < seg_hi;
-      const uint32_t item = valid ? in[idx] : 0u;
-      const uint32_t d = valid ? ((key[item] >> shift) & dmask) : 0u;
-      const uint64_t peers = match_digit(d, valid, dbits);
-      if (valid) {
-        const uint32_t base = hist[wave * kRadix + d];
-        out[base + static_cast<uint32_t>(__popcll(peers & lt_mask))] = item;
-        if (lane == __ffsll(static_cast<unsigned long long>(peers)) - 1)
-          hist[wave * kRadix + d] = base + static_cast<uint32_t>(__popcll(peers));
+    // exclusive scan in (digit, wave) order: thread owns digit tid/4, waves
+    // 4*(tid%4) .. +3
+    {
+      const int d = tid >> 2, w0 = (tid & 3) * 4;
+      uint32_t x[4], s = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { x[j] = hist[(w0 + j) * kRadix + d]; s += x[j]; }
+      uint32_t total;
+      uint32_t base = block_exclusive_scan(s, wsum, lane, wave, &total);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { hist[(w0 + j) * kRadix + d] = base; base += x[j]; }
+    }
+    __syncthreads();
+
+    // scatter walk
+#pragma unroll
+    for (int c = 0; c < kMaxCpw; ++c) {
+      if (c < cpw) {
+        const int idx = seg_lo + c * 64 + lane;
+        if (idx < seg_hi) {
+          const uint32_t dst = hist[wave * kRadix + dr[c]] + pos[c];
+          kbuf[in ^ 1][dst] = kr[c];
+          vbuf[in ^ 1][dst] = vr[c];
+        }
       }
     }
     __syncthreads();
-    uint32_t* tmp = in; in = out; out = tmp;
+    in ^= 1;
   }
 
-  // outputs; out[] is free scratch now: sorted cluster values for the offsets
+  // outputs (coalesced)
   const uint32_t amask = (1u << bits_n) - 1u;
   for (int j = tid; j < T; j += kSortThreads) {
-    const uint32_t t = in[j];
-    const uint32_t k = key[t];
-    perm[j] = static_cast<int32_t>(t);
-    out[j] = k >> bits_n;
-    if (sorted_seg) sorted_seg[j] = static_cast<int32_t>(k >> bits_n);
+    const uint32_t k = kbuf[in][j];
+    perm[j] = static_cast<int32_t>(vbuf[in][j]);
+    if (sorted_seg) sorted_seg[j] = static_cast<int32_t>(k >> cshift);
     if (sorted_aid) sorted_aid[j] = static_cast<int32_t>(k & amask);
   }
-  __syncthreads();
 
-  // Compaction of run starts, in order (ballot + wave prefix): a sorted
-  // position starts an entry when it starts a kChunk-aligned window or its
-  // key (masked by kmask) differs from the previous position's.
-  auto compact_starts = [&](uint32_t kmask, int chunk, int32_t* outp, int32_t* outn) {
-    uint32_t done = 0;
-    for (int base = 0; base < T; base += kSortThreads) {
-      const int j = base + tid;
-      bool st = false;
-      if (j < T) st = (j % chunk == 0) || ((key[in[j]] & kmask) != (key[in[j - 1]] & kmask));
-      const uint64_t bal = __ballot(st);
-      if (lane == 0) hist[wave] = static_cast<uint32_t>(__popcll(bal));
-      __syncthreads();
-      uint32_t before = 0, total = 0;
-      for (int w = 0; w < kWaves; ++w) {
-        const uint32_t c = hist[w];
-        before += (w < wave) ? c : 0u;
-        total += c;
-      }
-      if (st) outp[done + before + static_cast<uint32_t>(__popcll(bal & lt_mask))] = j;
-      done += total;
-      __syncthreads();
+  // run starts, both lists in one blocked scan: thread tid owns positions
+  // [tid*ipt, tid*ipt + ipt); counts packed as items | tiles << 16 (each
+  // total is at most T + 1 <= 8193)
+  if (items || ctiles) {
+    const int ipt = (T + kSortThreads - 1) / kSortThreads;
+    const int j0 = tid * ipt, j1 = min(T, j0 + ipt);
+    uint32_t cnt = 0;
+    uint32_t kp = (j0 > 0 && j0 < T) ? kbuf[in][j0 - 1] : 0u;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t k = kbuf[in][j];
+      const bool si = (j % kSigmaChunk == 0) || k != kp;
+      const bool sc = (j % kSegTile == 0) || (k >> cshift) != (kp >> cshift);
+      cnt += (si ? 1u : 0u) + (sc ? 0x10000u : 0u);
+      kp = k;
+    }
+    uint32_t total;
+    uint32_t base = block_exclusive_scan(cnt, wsum, lane, wave, &total);
+    uint32_t bi = base & 0xffffu, bc = base >> 16;
+    kp = (j0 > 0 && j0 < T) ? kbuf[in][j0 - 1] : 0u;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t k = kbuf[in][j];
+      const bool si = (j % kSigmaChunk == 0) || k != kp;
+      const bool sc = (j % kSegTile == 0) || (k >> cshift) != (kp >> cshift);
+      if (si && items) items[bi] = j;
+      if (sc && ctiles) ctiles[bc] = j;
+      bi += si ? 1u : 0u;
+      bc += sc ? 1u : 0u;
+      kp = k;
     }
     if (tid == 0) {
-      outp[done] = T;
-      outn[0] = static_cast<int32_t>(done);
+      if (items) { items[total & 0xffffu] = T; n_items[0] = static_cast<int32_t>(total & 0xffffu); }
+      if (ctiles) { ctiles[total >> 16] = T; n_ctiles[0] = static_cast<int32_t>(total >> 16); }
     }
-  };
-  // core-product items: runs of one adapter, cut at kSigmaChunk windows
-  if (items) compact_starts(amask, kSigmaChunk, items, n_items);
-  // segment tiles: runs of one cluster, cut at kSegTile windows
-  if (ctiles) compact_starts(~amask, kSegTile, ctiles, n_ctiles);
+  }
+
+  // cluster offsets: first sorted position whose cluster is >= k
   for (int k = tid; k <= K; k += kSortThreads) {
     int lo = 0, hi = T;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
-      if (out[mid] < static_cast<uint32_t>(k)) lo = mid + 1; else hi = mid;
+      if ((kbuf[in][mid] >> cshift) < static_cast<uint32_t>(k)) lo = mid + 1; else hi = mid;
     }
     offs[k] = lo;
   }
