@@ -5,20 +5,26 @@
 
 A step is one call of the whole layer (bucketing, shrink, core product, fused
 base + up-projection GEMM) over one batch of seeded synthetic inputs that are
-already resident in HBM.  The timed region is K consecutive steps between two
-HIP events on the stream the library launches on.  Inputs are rotated over
-enough device copies (>= 512 MB in total) that the 256 MB last-level cache
-cannot hold them between steps.
+already resident in HBM; for the workload stack32 it is one pass over all 224
+linear projections of a 32-layer 7B-shaped decoder (q, k, v, o, gate, up,
+down), each its own cts_apply call with its own weights.  The timed region is
+K consecutive steps between two HIP events on the stream the library launches
+on.  Single-layer inputs are rotated over enough device copies (>= 512 MB in
+total) that the 256 MB last-level cache cannot hold them between steps; the
+stack's weights (about 32 GB) are distinct per projection anyway.
 
 One JSON line is printed.  Besides the throughput it carries:
-  roofline      the dominant kernel (the fused GEMM): algorithmic flops or
-                bytes of one launch over its mean duration, measured here with
-                HIP events recorded around it, against MI355X's peak
-  cpu_baseline  the fp64 CPU oracle timed on this host on a bounded sample of
-                the same batch (about --cpu-seconds of work)
-  uncompressed  the same layer through the uncompressed gather path
-                (cts_apply_uncompressed, rank-16 B_i A_i) on the same batch
-  stages_us     mean duration of each stage of the layer
+  roofline        the dominant kernel (the fused GEMM): algorithmic flops or
+                  bytes of one launch over its mean duration, measured here
+                  with HIP events recorded around it, against MI355X's peak
+                  (stack32: all GEMM launches of a step over their summed time)
+  cpu_baseline    the fp64 CPU oracle timed on this host on a bounded sample
+                  of the same batch (about --cpu-seconds of work)
+  uncompressed    the same layer through the uncompressed gather path
+                  (cts_apply_uncompressed, rank-16 B_i A_i) on the same batch
+  single_adapter  the same batch with every token on one LoRA (n = K = 1);
+                  ratio = this throughput / that one
+  stages_us       mean duration of each stage of the layer (per step)
 """
 from __future__ import annotations
 
@@ -28,6 +34,7 @@ import math
 import os
 import sys
 import time
+import types
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -146,13 +153,240 @@ def stage_times(fn, sets, steps, torch, cts):
     return out
 
 
+def roofline_of(flops, nbytes, t_s, dtype):
+    peak_fl = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_F32_TFLOPS
+    if flops / (peak_fl * 1e12) >= nbytes / (PEAK_HBM_GBS * 1e9):
+        achieved = flops / t_s / 1e12
+        return {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_fl, "unit": "TFLOP/s",
+                "frac": round(achieved / peak_fl, 4), "traffic": None}
+    achieved = nbytes / t_s / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+
+
+def bench_layer(args, torch, np, cts, B, wl, device):
+    log("generating %s" % args.workload)
+    w = wl.make(args.workload)
+
+    set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
+    n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
+    base = [to_dev(a, device) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
+    sets = [base] + [[t.clone() for t in base] for _ in range(n_sets - 1)]
+    aid = to_dev(w.adapter_id, device)
+    cof = to_dev(w.cluster_of, device)
+    y = torch.empty((w.T, w.d_out), dtype=base[0].dtype, device=device)
+    dt = B.CTS_BF16 if w.dtype == "bf16" else B.CTS_F32
+    p = cts.make_problem(w.T, w.d_in, w.d_out, r=w.r, n_adapters=w.n, n_clusters=w.K, dtype=dt)
+    ws = torch.empty(max(1, cts.workspace_size(p)), dtype=torch.uint8, device=device)
+
+    def step(s):
+        x, W, U, Vt, S = s
+        cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+
+    log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
+        (n_sets, set_bytes / 1e6, args.warmup, args.steps))
+    ms = time_steps(step, sets, args.steps, args.warmup, torch)
+    stages = stage_times(step, sets, args.steps, torch, B)
+
+    # one adapter: the same batch, every token on LoRA 0 of cluster 0
+    aid1 = torch.zeros_like(aid)
+    cof1 = torch.zeros(1, dtype=torch.int32, device=device)
+    p1 = cts.make_problem(w.T, w.d_in, w.d_out, r=w.r, n_adapters=1, n_clusters=1, dtype=dt)
+    ws1 = torch.empty(max(1, cts.workspace_size(p1)), dtype=torch.uint8, device=device)
+
+    def step1(s):
+        x, W, U, Vt, S = s
+        cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
+
+    log("timing cts_apply with one adapter")
+    ms1 = time_steps(step1, sets, args.steps, args.warmup, torch)
+
+    # uncompressed comparison on the same batch
+    uA, uB = to_dev(w.A, device), to_dev(w.B, device)
+    pu = cts.make_problem(w.T, w.d_in, w.d_out, n_adapters=w.n, r_lora=w.r_l, dtype=dt)
+    wsu = torch.empty(max(1, cts.workspace_size(pu, compressed=False)), dtype=torch.uint8, device=device)
+
+    def step_u(s):
+        x, W = s[0], s[1]
+        cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
+
+    log("timing cts_apply_uncompressed")
+    ms_u = time_steps(step_u, sets, args.steps, args.warmup, torch)
+    stages_u = stage_times(step_u, sets, args.steps, torch, B)
+    del uA, uB
+
+    touched = len(set(w.cluster_of[w.adapter_id].tolist()))
+    flops, nbytes = main_kernel_model(w, touched)
+    roof = roofline_of(flops, nbytes, stages["fused_gemm"] * 1e-6, w.dtype)
+    if args.workload == "prefill_mix":
+        roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
+    gemm_kernel = ("seg_gemm_dma_kernel" if w.dtype == "bf16" and w.T >= 2048 else "seg_gemm_kernel")
+    roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
+                 "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_seconds)
+
+    value = w.T / (ms * 1e-3)
+    value1 = w.T / (ms1 * 1e-3)
+    return {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
+        "config": {"workload": args.workload, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
+                   "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
+                   "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "uncompressed": {"value": round(w.T / (ms_u * 1e-3), 1), "unit": "tokens/s",
+                         "ms_per_step": round(ms_u, 5), "r_lora": w.r_l,
+                         "stages_us": {k: round(v, 2) for k, v in stages_u.items()}},
+        "single_adapter": {"value": round(value1, 1), "unit": "tokens/s", "ms_per_step": round(ms1, 5),
+                           "ratio": round(value / value1, 4)},
+        "stages_us": {k: round(v, 2) for k, v in stages.items()},
+    }
+
+
+def stack_cpu_baseline(projs, aid_h, cof_h, target_s, torch, np):
+    """The oracle on the first layer's projections, one of each shape, for a
+    prefix of the batch; the stack's tokens/s is extrapolated as tokens over
+    the summed per-token oracle time of all 224 projections."""
+    from oracle import oracle
+    from paper_2407_00066_amd import workloads as wl
+    per_tok, cores, detail = {}, oracle.num_threads(), []
+    budget = target_s / 4
+    for name, d_in, d_out in wl.STACK_PROJ:
+        shape = (d_in, d_out)
+        if shape in per_tok:
+            continue
+        x, W, U, Vt, S = projs[0][name][:5]
+        host = [t.view(torch.int16).cpu().numpy().view(np.uint16) for t in (x, W, U, Vt, S)]
+        f64 = [oracle.to_f64(a) for a in host]
+        spent, done, chunk = 0.0, 0, 2
+        while done < len(aid_h) and spent < budget:
+            toks = np.arange(done, min(len(aid_h), done + chunk))
+            tm = {}
+            oracle.apply(f64[0], aid_h, cof_h, f64[1], f64[2], f64[3], f64[4], tokens=toks, timing=tm)
+            spent += tm["s"]
+            done += len(toks)
+            chunk = max(1, min(len(aid_h) - done, int((budget - spent) / (spent / done)) + 1))
+        per_tok[shape] = spent / done
+        detail.append("%dx%d: %d tokens in %.1f s" % (d_in, d_out, done, spent))
+    t_tok = wl.STACK_LAYERS * sum(per_tok[(d_in, d_out)] for _, d_in, d_out in wl.STACK_PROJ)
+    return {"value": 1.0 / t_tok, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "layer-0 projections, one per shape (%s), per-token time x 32 layers x 7 "
+                      "projections" % "; ".join(detail)}
+
+
+def bench_stack(args, torch, np, cts, B, wl, device):
+    T, r, n, K = wl.STACK["T"], wl.STACK["r"], wl.STACK["n"], wl.STACK["K"]
+    g = torch.Generator(device=device)
+    g.manual_seed(wl.SEED_BASE + 500)
+    rs = np.random.default_rng(wl.SEED_BASE + 501)
+    aid_h = rs.integers(0, n, T).astype(np.int32)
+    cof_h = wl.balanced_clusters(rs, n, K)
+    aid, cof = to_dev(aid_h, device), to_dev(cof_h, device)
+
+    def gauss(shape, var):
+        return (torch.randn(shape, generator=g, device=device) * math.sqrt(var)).to(torch.bfloat16)
+
+    log("generating the 32-layer stack on the device")
+    xs = {4096: gauss((T, 4096), 1.0), 14336: gauss((T, 14336), 1.0)}
+    ys = {d: torch.empty((T, d), dtype=torch.bfloat16, device=device) for d in (1024, 4096, 14336)}
+    projs, wsz, wsz1 = [], 1, 1
+    for _ in range(wl.STACK_LAYERS):
+        layer = {}
+        for name, d_in, d_out in wl.STACK_PROJ:
+            layer[name] = (xs[d_in], gauss((d_out, d_in), 1.0 / d_in), gauss((K, d_out, r), 1.0 / d_out),
+                           gauss((K, r, d_in), 1.0 / d_in), gauss((n, r, r), 1.0 / r), ys[d_out])
+            pb = cts.make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=B.CTS_BF16)
+            p1 = cts.make_problem(T, d_in, d_out, r=r, n_adapters=1, n_clusters=1, dtype=B.CTS_BF16)
+            wsz, wsz1 = max(wsz, cts.workspace_size(pb)), max(wsz1, cts.workspace_size(p1))
+        projs.append(layer)
+    torch.cuda.synchronize()
+    ws = torch.empty(wsz, dtype=torch.uint8, device=device)
+    ws1 = torch.empty(wsz1, dtype=torch.uint8, device=device)
+    aid1 = torch.zeros_like(aid)
+    cof1 = torch.zeros(1, dtype=torch.int32, device=device)
+    resident = sum(t.numel() * t.element_size() for L in projs for v in L.values() for t in v[1:5])
+
+    def step(_):
+        for L in projs:
+            for name, _, _ in wl.STACK_PROJ:
+                x, W, U, Vt, S, y = L[name]
+                cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+
+    def step1(_):
+        for L in projs:
+            for name, _, _ in wl.STACK_PROJ:
+                x, W, U, Vt, S, y = L[name]
+                cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
+
+    log("timing the stack: %.1f GB of weights, %d warmup + %d steps" % (resident / 1e9, args.warmup, args.steps))
+    ms = time_steps(step, [None], args.steps, args.warmup, torch)
+    log("timing the stack with one adapter")
+    ms1 = time_steps(step1, [None], args.steps, args.warmup, torch)
+
+    # per-call stage events over a few steps: the GEMM time of a step
+    n_ev = min(args.steps, 3)
+    calls = wl.STACK_LAYERS * len(wl.STACK_PROJ)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.N_STAGE_EVENTS)] for _ in range(calls * n_ev)]
+    c = 0
+    for _ in range(n_ev):
+        for L in projs:
+            for name, _, _ in wl.STACK_PROJ:
+                x, W, U, Vt, S, y = L[name]
+                B.set_stage_events(evs[c])
+                cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+                c += 1
+    B.set_stage_events(None)
+    torch.cuda.synchronize()
+    names = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
+    stages = {nm: 1e3 * sum(e[i].elapsed_time(e[i + 1]) for e in evs) / n_ev for i, nm in enumerate(names)}
+
+    touched = len(set(cof_h[aid_h].tolist()))
+    flops = nbytes = 0.0
+    for name, d_in, d_out in wl.STACK_PROJ:
+        f, b = main_kernel_model(types.SimpleNamespace(T=T, d_in=d_in, d_out=d_out, r=r, dtype="bf16"),
+                                 touched)
+        flops += f * wl.STACK_LAYERS
+        nbytes += b * wl.STACK_LAYERS
+    roof = roofline_of(flops, nbytes, stages["fused_gemm"] * 1e-6, "bf16")
+    roof.update({"kernel": "seg_gemm_kernel (fused W X + U_k Z'), all %d launches of a step" % calls,
+                 "mean_us": round(stages["fused_gemm"] / calls, 2),
+                 "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
+        cpu = stack_cpu_baseline(projs, aid_h, cof_h, args.cpu_seconds, torch, np)
+    value, value1 = T / (ms * 1e-3), T / (ms1 * 1e-3)
+    return {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded, generated on the device; %.1f GB of weights resident in HBM)" % (resident / 1e9),
+        "config": {"workload": "stack32", "T": T, "layers": wl.STACK_LAYERS,
+                   "projections": [list(pr) for pr in wl.STACK_PROJ], "r": r, "n_adapters": n,
+                   "n_clusters": K, "touched_clusters": touched,
+                   "distinct_adapters": len(set(aid_h.tolist())), "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "single_adapter": {"value": round(value1, 1), "unit": "tokens/s", "ms_per_step": round(ms1, 5),
+                           "ratio": round(value / value1, 4)},
+        "stages_us": {k: round(v, 2) for k, v in stages.items()},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill_mix",
-                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32"])
+                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -173,83 +407,10 @@ def main():
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     copy_calibration(torch, device)
-    log("generating %s" % args.workload)
-    w = wl.make(args.workload)
-
-    set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
-    n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
-    base = [to_dev(a, device) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
-    sets = [base] + [[t.clone() for t in base] for _ in range(n_sets - 1)]
-    aid = to_dev(w.adapter_id, device)
-    cof = to_dev(w.cluster_of, device)
-    y = torch.empty((w.T, w.d_out), dtype=base[0].dtype, device=device)
-    p = cts.make_problem(w.T, w.d_in, w.d_out, r=w.r, n_adapters=w.n, n_clusters=w.K,
-                         dtype=B.CTS_BF16 if w.dtype == "bf16" else B.CTS_F32)
-    ws = torch.empty(max(1, cts.workspace_size(p)), dtype=torch.uint8, device=device)
-
-    def step(s):
-        x, W, U, Vt, S = s
-        cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
-
-    log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
-        (n_sets, set_bytes / 1e6, args.warmup, args.steps))
-    ms = time_steps(step, sets, args.steps, args.warmup, torch)
-    stages = stage_times(step, sets, args.steps, torch, B)
-
-    # uncompressed comparison on the same batch
-    uA, uB = to_dev(w.A, device), to_dev(w.B, device)
-    pu = cts.make_problem(w.T, w.d_in, w.d_out, n_adapters=w.n, r_lora=w.r_l,
-                          dtype=B.CTS_BF16 if w.dtype == "bf16" else B.CTS_F32)
-    wsu = torch.empty(max(1, cts.workspace_size(pu, compressed=False)), dtype=torch.uint8, device=device)
-
-    def step_u(s):
-        x, W = s[0], s[1]
-        cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
-
-    log("timing cts_apply_uncompressed")
-    ms_u = time_steps(step_u, sets, args.steps, args.warmup, torch)
-    stages_u = stage_times(step_u, sets, args.steps, torch, B)
-    del uA, uB
-
-    touched = len(set(w.cluster_of[w.adapter_id].tolist()))
-    flops, nbytes = main_kernel_model(w, touched)
-    t_main = stages["fused_gemm"] * 1e-6
-    peak_fl = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    if flops / (peak_fl * 1e12) >= nbytes / (PEAK_HBM_GBS * 1e9):
-        achieved = flops / t_main / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_fl, "unit": "TFLOP/s",
-                "frac": round(achieved / peak_fl, 4), "traffic": None}
+    if args.workload == "stack32":
+        rec = bench_stack(args, torch, np, cts, B, wl, device)
     else:
-        achieved = nbytes / t_main / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
-    if args.workload == "prefill_mix":
-        roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
-    gemm_kernel = ("seg_gemm_dma_kernel" if w.dtype == "bf16" and w.T >= 2048 else "seg_gemm_kernel")
-    roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
-                 "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
-        cpu = cpu_baseline(w, args.cpu_seconds)
-
-    value = w.T / (ms * 1e-3)
-    rec = {
-        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
-        "config": {"workload": args.workload, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
-                   "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
-                   "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
-        "roofline": roof,
-        "cpu_baseline": cpu,
-        "uncompressed": {"value": round(w.T / (ms_u * 1e-3), 1), "unit": "tokens/s",
-                         "ms_per_step": round(ms_u, 5), "r_lora": w.r_l,
-                         "stages_us": {k: round(v, 2) for k, v in stages_u.items()}},
-        "stages_us": {k: round(v, 2) for k, v in stages.items()},
-    }
+        rec = bench_layer(args, torch, np, cts, B, wl, device)
     print(json.dumps(rec), flush=True)
 
 

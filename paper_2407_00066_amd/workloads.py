@@ -188,6 +188,17 @@ CONFIGS = {
     "mlp_up": dict(cfg=3, T=256, d_in=4096, d_out=14336, r=128, n=1000, K=50, ids="zipf"),
 }
 
+# The 32-layer 7B-shaped decoder stack: every linear projection of a layer,
+# 1000 LoRAs in 50 clusters (r=64) per projection, 512 uniform decode tokens.
+STACK_LAYERS = 32
+STACK_PROJ = (("q", 4096, 4096), ("k", 4096, 1024), ("v", 4096, 1024), ("o", 4096, 4096),
+              ("gate", 4096, 14336), ("up", 4096, 14336), ("down", 14336, 4096))
+STACK = dict(T=512, r=64, n=1000, K=50, ids="uniform")
+# one parity workload per distinct projection shape of the stack
+for _i, (_name, _din, _dout) in enumerate((("q", 4096, 4096), ("kv", 4096, 1024),
+                                            ("gate", 4096, 14336), ("down", 14336, 4096))):
+    CONFIGS["stack_" + _name] = dict(cfg=10 + _i, d_in=_din, d_out=_dout, with_lora=False, **STACK)
+
 
 def make(name: str, **overrides) -> Workload:
     spec = dict(CONFIGS[name])

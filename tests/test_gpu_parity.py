@@ -240,6 +240,22 @@ def test_full_config_sampled(oracle_mod, full_cases, name):
     assert err <= TOL["bf16"], err
 
 
+@pytest.mark.parametrize("name", ["stack_q", "stack_kv", "stack_gate", "stack_down"])
+def test_stack_projection_sampled(oracle_mod, full_cases, name):
+    """Each distinct projection shape of the 32-layer decoder stack at full size."""
+    w = _full(full_cases, name)
+    toks = _sample_tokens(w, oracle_mod, cap=8)
+    say("apply %s (full size), %d sampled tokens" % (name, len(toks)))
+    y = cts.apply(*_inputs(w))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, w.W, w.U, w.Vt, w.Sigma, tokens=toks)
+    err = row_rel_err(yh[toks], ref)
+    assert err <= TOL["bf16"], err
+    full_cases.pop(name)
+
+
 @pytest.mark.parametrize("name", ["decode_q", "prefill_mix", "mlp_up"])
 def test_full_config_uncompressed_sampled(oracle_mod, full_cases, name):
     w = _full(full_cases, name)
