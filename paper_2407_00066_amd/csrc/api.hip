@@ -66,17 +66,38 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
 
   const int T = p->T;
   int BM, BN, BK;
-  // fused GEMM: large MFMA tiles once the batch is prefill-sized, otherwise
-  // small tiles split along k so that the weight stream is spread over >= 256
-  // workgroups (one per compute unit).
-  if (p->dtype == CTS_F32) pl->main_tile = Tile::F32;
-  else pl->main_tile = (T >= 2048) ? Tile::Large : (T >= 128 ? Tile::Mid : Tile::Small);
+  // fused GEMM tile and k split.  Prefill-sized batches: 256x256 tiles.
+  // Smaller batches are bound by the weight stream and by how often each
+  // compute unit re-reads its operands from L2: 256x128 tiles when they alone
+  // give most compute units work or the reduction is long (then split along
+  // k up to 256 workgroups), else 128x64 tiles, and 64x64 for decode
+  // batches, split along k up to 256 workgroups (partials summed afterwards).
+  auto tiles_of = [&](Tile t) {
+    int bm, bn, bk;
+    cts::tile_dims(t, &bm, &bn, &bk);
+    return ceil_div(p->d_out, bm) * ceil_div(std::max(T, 1), bn);
+  };
+  int max_split = 1;
+  if (p->dtype == CTS_F32) {
+    pl->main_tile = Tile::F32;
+  } else if (T >= 2048) {
+    pl->main_tile = Tile::Large;
+  } else if (T > 64 && (tiles_of(Tile::Wide) >= 192 || p->d_in >= 8192)) {
+    pl->main_tile = Tile::Wide;
+    max_split = 8;
+  } else if (T > 64) {
+    pl->main_tile = Tile::Narrow;
+    max_split = 4;
+  } else {
+    pl->main_tile = Tile::Decode;
+    max_split = 4;
+  }
   cts::tile_dims(pl->main_tile, &BM, &BN, &BK);
   {
-    const int tiles = ceil_div(p->d_out, BM) * ceil_div(std::max(T, 1), BN);
+    const int tiles = tiles_of(pl->main_tile);
     const int nk = ceil_div(p->d_in, BK);
-    int s = (pl->main_tile == Tile::Small) ? ceil_div(256, tiles) : 1;
-    pl->main_split = std::max(1, std::min(std::min(s, nk), 16));
+    const int s = std::min(std::min(ceil_div(256, tiles), max_split), std::max(1, nk / 4));
+    pl->main_split = std::max(1, s);
   }
   // shrink: one workgroup per (cluster segment tile of <= kSegTile tokens,
   // 64 rank rows), split along d_in so that about two workgroups run on each
