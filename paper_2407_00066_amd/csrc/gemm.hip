@@ -861,211 +861,6 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   }
 }
 
-// ---------------------------------------------------------------------------
-// Streaming variant for short token tiles (decode batches): the weight rows
-// are read once from HBM and nothing needs sharing inside the workgroup
-// except the final sum, so the main loop has no LDS traffic and no barrier.
-//
-// A workgroup owns a 64 x 64 output tile (64 rows of W, 64 sorted token
-// columns) and one k range of the split.  Its k-steps (32 deep: dense steps
-// over W X, then, in split 0, r/32 steps per cluster run of U_k Z') are dealt
-// to the 4 waves in contiguous ranges.  A wave loads its 4 A fragments (16
-// rows x 32 k each) and 4 B fragments (16 tokens x 32 k) per step straight
-// into registers in the MFMA operand layout, D-1 steps ahead of the multiply
-// (the compiler waits for each load exactly where its registers are used).
-// A token column outside the current run, a row past M or a k past the
-// operand reads as zero.  At the end the four partial tiles are summed in
-// fixed wave order through LDS and written out (bf16/fp32 rows scattered to
-// token order, or fp32 split partials).
-constexpr int kSkBM = 64, kSkBN = 64, kSkW = 4, kSkFM = 4, kSkFN = 4, kSkKS = 32;
-
-template <int D>
-__global__ __launch_bounds__(kSkW * 64, 1) void seg_gemm_stream_kernel(const GemmParams p) {
-  using MT = MfmaTraits<bf16_t, 16>;
-  __shared__ int32_t t_perm[kSkBN];
-  __shared__ int32_t run_start[kSkBN + 1];
-  __shared__ int32_t run_seg[kSkBN];
-  __shared__ int32_t n_runs_s;
-  __shared__ __attribute__((aligned(16))) float red[kSkW][kSkBN][kSkBM + 4];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int mt, nt, ks;
-  tile_of_block((p.M + kSkBM - 1) / kSkBM, (p.N + kSkBN - 1) / kSkBN, &mt, &nt, &ks);
-  const int m0 = mt * kSkBM, j0 = nt * kSkBN;
-  const int jn = min(kSkBN, p.N - j0);
-  const int S = p.ksplit;
-
-  // token columns and cluster runs of the tile (one wave: 64 columns)
-  if (wave == 0) {
-    const bool ok = lane < jn;
-    t_perm[lane] = ok ? p.perm[j0 + lane] : 0;
-    const int seg = (ok && p.sorted_seg) ? p.sorted_seg[j0 + lane] : 0;
-    const int prev = __shfl_up(seg, 1);
-    const bool st = ok && (lane == 0 || seg != prev);
-    const uint64_t bal = __ballot(st);
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    if (st) {
-      const int q = __popcll(bal & lt);
-      run_start[q] = lane;
-      run_seg[q] = seg;
-    }
-    if (lane == 0) {
-      const int nr = (p.sorted_seg && p.K1 > 0 && ks == 0) ? __popcll(bal) : 0;
-      n_runs_s = nr;
-      run_start[__popcll(bal)] = jn;
-    }
-  }
-  __syncthreads();
-  const int n_runs = n_runs_s;
-
-  // step list of this workgroup and this wave's share
-  const int nk0 = (p.K0 > 0) ? (p.K0 + kSkKS - 1) / kSkKS : 0;
-  const int nk1 = (p.K1 > 0) ? (p.K1 + kSkKS - 1) / kSkKS : 0;
-  const int d_lo = split_lo(nk0, ks, S), d_hi = split_lo(nk0, ks + 1, S);
-  const int nd = d_hi - d_lo;
-  const int total = nd + n_runs * nk1;
-  const int lo = split_lo(total, wave, kSkW), hi = split_lo(total, wave + 1, kSkW);
-
-  // per-lane operand offsets (bytes, k = 0): row fr of each A fragment, token
-  // column fr of each B fragment, k group fg
-  const int fr = lane & 15, fg = lane >> 4;
-  uint32_t a0o[kSkFM], a1o[kSkFM], b0o[kSkFN], b1o[kSkFN];
-  int bjl[kSkFN];
-#pragma unroll
-  for (int i = 0; i < kSkFM; ++i) {
-    const int m = m0 + 16 * i + fr;
-    const bool ok = m < p.M;
-    a0o[i] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * 2u + fg * 16u : kOob;
-    a1o[i] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * 2u + fg * 16u : kOob;
-  }
-#pragma unroll
-  for (int j = 0; j < kSkFN; ++j) {
-    const int jl = 16 * j + fr;
-    bjl[j] = jl;
-    b0o[j] = (jl < jn) ? static_cast<uint32_t>(t_perm[jl]) * static_cast<uint32_t>(p.ldb0) * 2u + fg * 16u
-                       : kOob;
-    const uint32_t r1 = p.b1_gather ? static_cast<uint32_t>(t_perm[jl]) : static_cast<uint32_t>(j0 + jl);
-    b1o[j] = r1 * static_cast<uint32_t>(p.ldb1) * 2u + fg * 16u;
-  }
-  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(p.A0, p.a0_bytes);
-  const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
-  const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
-
-  bf16x8 fa[D][kSkFM], fb[D][kSkFN];
-  f32x4 acc[kSkFM][kSkFN];
-#pragma unroll
-  for (int i = 0; i < kSkFM; ++i)
-#pragma unroll
-    for (int j = 0; j < kSkFN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // loads of step i into slot sl; an invalid step (past the wave's range)
-  // loads zeros, so the pipeline multiplies unconditionally and has no branch
-  auto load_dense = [&](int i, int sl, bool valid) __attribute__((always_inline)) {
-    const uint32_t kk = static_cast<uint32_t>((d_lo + i) * kSkKS);
-    const uint32_t km = (valid && kk + fg * 8u < static_cast<uint32_t>(p.K0)) ? 0u : kOob;
-#pragma unroll
-    for (int f = 0; f < kSkFM; ++f)
-      fa[sl][f] = __builtin_bit_cast(bf16x8, load16(rA0, (a0o[f] + kk * 2u) | km));
-#pragma unroll
-    for (int f = 0; f < kSkFN; ++f)
-      fb[sl][f] = __builtin_bit_cast(bf16x8, load16(rB0, (b0o[f] + kk * 2u) | km));
-  };
-  auto load_adapter = [&](int i, int sl, bool valid) __attribute__((always_inline)) {
-    const int u = i - nd;
-    const int q = min(u / max(nk1, 1), max(n_runs - 1, 0));
-    const uint32_t kk = static_cast<uint32_t>((u - q * nk1) * kSkKS);
-    const int rlo = run_start[q], rhi = run_start[q + 1];
-    const int seg = __builtin_amdgcn_readfirstlane(run_seg[q]);
-    const __amdgpu_buffer_rsrc_t rA =
-        make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
-                  p.a1_seg_bytes);
-    const uint32_t km = (valid && kk + fg * 8u < static_cast<uint32_t>(p.K1)) ? 0u : kOob;
-#pragma unroll
-    for (int f = 0; f < kSkFM; ++f)
-      fa[sl][f] = __builtin_bit_cast(bf16x8, load16(rA, (a1o[f] + kk * 2u) | km));
-#pragma unroll
-    for (int f = 0; f < kSkFN; ++f) {
-      const uint32_t jm = (bjl[f] >= rlo && bjl[f] < rhi) ? 0u : kOob;
-      fb[sl][f] = __builtin_bit_cast(bf16x8, load16(rB1, (b1o[f] + kk * 2u) | km | jm));
-    }
-  };
-  auto multiply = [&](int sl) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < kSkFM; ++i)
-#pragma unroll
-      for (int j = 0; j < kSkFN; ++j) acc[i][j] = MT::mma(fa[sl][i], fb[sl][j], acc[i][j]);
-  };
-
-  // dense steps of this wave, then its adapter steps (only split 0 has
-  // any); each range is pipelined D-1 steps deep.  Steps are taken in groups
-  // of D so that every slot index is a constant.
-  auto run_range = [&](int a, int b, auto load) __attribute__((always_inline)) {
-    if (a >= b) return;
-#pragma unroll
-    for (int d = 0; d < D - 1; ++d) load(a + d, d, a + d < b);
-    for (int i = a; i < b; i += D) {
-#pragma unroll
-      for (int d = 0; d < D; ++d) {
-        const int nx = i + d + D - 1;
-        load(nx, (d + D - 1) % D, nx < b);
-        multiply(d);
-      }
-    }
-  };
-  run_range(lo, min(hi, nd), load_dense);
-  run_range(max(lo, nd), hi, load_adapter);
-
-  // sum of the four waves' tiles in wave order, then the store
-#pragma unroll
-  for (int i = 0; i < kSkFM; ++i)
-#pragma unroll
-    for (int j = 0; j < kSkFN; ++j)
-      *reinterpret_cast<f32x4*>(&red[wave][16 * j + fr][16 * i + 4 * fg]) = acc[i][j];
-  __syncthreads();
-  const int jl = tid >> 2, mq = (tid & 3) * 16;
-  if (jl < jn) {
-    f32x4 sum[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) sum[c] = *reinterpret_cast<const f32x4*>(&red[0][jl][mq + 4 * c]);
-#pragma unroll
-    for (int w = 1; w < kSkW; ++w)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) sum[c] += *reinterpret_cast<const f32x4*>(&red[w][jl][mq + 4 * c]);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {                 // two groups of 8 rows (M % 8 == 0)
-      const int m = m0 + mq + 8 * h;
-      if (m >= p.M) continue;
-      const f32x4 lo4 = sum[2 * h], hi4 = sum[2 * h + 1];
-      if (p.part) {
-        float* dst = p.part + (static_cast<int64_t>(ks) * p.N + j0 + jl) * p.M + m;
-        *reinterpret_cast<f32x4*>(dst) = lo4;
-        *reinterpret_cast<f32x4*>(dst + 4) = hi4;
-      } else {
-        const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
-        if (p.out_dtype == 1) {
-          uint4 v;
-          v.x = f32_to_bf16(lo4[0]) | (static_cast<uint32_t>(f32_to_bf16(lo4[1])) << 16);
-          v.y = f32_to_bf16(lo4[2]) | (static_cast<uint32_t>(f32_to_bf16(lo4[3])) << 16);
-          v.z = f32_to_bf16(hi4[0]) | (static_cast<uint32_t>(f32_to_bf16(hi4[1])) << 16);
-          v.w = f32_to_bf16(hi4[2]) | (static_cast<uint32_t>(f32_to_bf16(hi4[3])) << 16);
-          *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.out) + row * p.ldo + m) = v;
-        } else {
-          float* dst = static_cast<float*>(p.out) + row * p.ldo + m;
-          *reinterpret_cast<f32x4*>(dst) = lo4;
-          *reinterpret_cast<f32x4*>(dst + 4) = hi4;
-        }
-      }
-    }
-  }
-}
-
-template <int D>
-hipError_t launch_stream(const GemmParams& p, hipStream_t stream) {
-  dim3 grid(((p.M + kSkBM - 1) / kSkBM) * ((p.N + kSkBN - 1) / kSkBN) * p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_stream_kernel<D>), grid, dim3(kSkW * 64), 0, stream, p);
-  return hipGetLastError();
-}
-
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0>
 hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   dim3 grid(((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.ksplit);
