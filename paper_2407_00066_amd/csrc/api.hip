@@ -100,16 +100,17 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
     pl->main_split = std::max(1, s);
   }
   // shrink: one workgroup per (cluster segment tile of <= kSegTile tokens,
-  // 64 rank rows), split along d_in so that about two workgroups run on each
-  // of the 256 CUs (the split partials are summed by the Sigma stage)
-  pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Small;
+  // 64 rank rows), split along d_in so that about 256 (bf16) or 512 (fp32)
+  // workgroups run; the Sigma stage sums the split partials
+  pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Shrink;
   cts::tile_dims(pl->shrink_tile, &BM, &BN, &BK);
   pl->max_ctiles = cts::max_seg_tiles(T, pl->nseg);
   {
     const int expect = ceil_div(std::max(T, 1), BN) + std::min(pl->nseg, std::max(T, 1)) / 2;
     const int tiles = ceil_div(pl->rank, BM) * std::max(expect, 1);
     const int nk = ceil_div(p->d_in, BK);
-    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(512, tiles), nk), 16));
+    const int target = (p->dtype == CTS_F32) ? 512 : 256;
+    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 16));
   }
   pl->max_items = cts::max_sigma_items(T, p->n_adapters);
 

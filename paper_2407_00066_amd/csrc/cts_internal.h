@@ -85,10 +85,11 @@ struct GemmParams {
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide
-// 256x128x64, Narrow 128x64x128 and Decode 64x64x128 load their k-tiles
-// straight into LDS; Mid 128x128x64 and Small 64x64x64 (the only one that
-// takes explicit token tiles) stage them in registers; F32 is the fp32 path.
-enum class Tile { Large, Wide, Narrow, Decode, Mid, Small, F32 };
+// 256x128x64, Narrow 128x64x128, Decode 64x64x128 and Shrink 64x64x64 load
+// their k-tiles straight into LDS; Mid 128x128x64 and Small 64x64x64 stage
+// them in registers; F32 is the fp32 path.  Explicit token tiles are taken by
+// the 64-wide ones (Decode, Shrink, Small, F32).
+enum class Tile { Large, Wide, Narrow, Decode, Shrink, Mid, Small, F32 };
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream);
 void tile_dims(Tile tile, int* BM, int* BN, int* BK);
 

@@ -490,11 +490,36 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __shared__ int32_t wave_runs[C::NW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Token-tile mode (explicit tiles, each inside one segment): the tile's
+  // segment operand becomes the dense operand (A = A1 of that segment, B = B1),
+  // so the whole k loop takes the dense load path and there is no second phase.
+  const bool tlist = p.tile_start != nullptr;
   int mt, nt, ks;
-  tile_of_block((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, &mt, &nt, &ks);
-  const int m0 = mt * BM, j0 = nt * BN;
+  tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  int j0, jn;
+  if (tlist) {
+    if (nt >= p.n_tiles[0]) return;                         // whole workgroup, before any barrier
+    j0 = p.tile_start[nt];
+    jn = p.tile_start[nt + 1] - j0;
+  } else {
+    j0 = nt * BN;
+    jn = min(BN, p.N - j0);
+  }
+  const void* A0 = p.A0;
+  const void* B0 = p.B0;
+  uint32_t a0_bytes = p.a0_bytes, b0_bytes = p.b0_bytes;
+  int64_t lda0 = p.lda0, ldb0 = p.ldb0;
+  int K0 = p.K0, K1 = p.K1;
+  bool b0_gather = true;
+  if (tlist) {
+    const int seg = p.sorted_seg[j0];
+    A0 = static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes;
+    a0_bytes = p.a1_seg_bytes; lda0 = p.lda1; K0 = p.K1;
+    B0 = p.B1; b0_bytes = p.b1_bytes; ldb0 = p.ldb1; b0_gather = p.b1_gather != 0;
+    K1 = 0;
+  }
+  const int m0 = mt * BM;
   const int S = p.ksplit;
-  const int jn = min(BN, p.N - j0);
 
   // ---- token columns of this tile: perm, segment, and segment runs -------
   for (int i = tid; i < BN; i += C::NT) {
@@ -523,13 +548,13 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     n_runs += total;
     __syncthreads();
   }
-  if (!(p.sorted_seg && p.K1 > 0)) n_runs = 0;
+  if (!(p.sorted_seg && K1 > 0)) n_runs = 0;
   if (tid == 0) run_start[n_runs] = jn;
   __syncthreads();
 
   // ---- k-tile schedule ----------------------------------------------------
-  const int nk0 = (p.K0 > 0) ? (p.K0 + BK - 1) / BK : 0;
-  const int nk1 = (p.K1 > 0) ? (p.K1 + BK - 1) / BK : 0;
+  const int nk0 = (K0 > 0) ? (K0 + BK - 1) / BK : 0;
+  const int nk1 = (K1 > 0) ? (K1 + BK - 1) / BK : 0;
   int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0;
   if (nk0 > 0) {
     d_lo = split_lo(nk0, ks, S); d_hi = split_lo(nk0, ks + 1, S);
@@ -562,7 +587,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   for (int j = 0; j < C::QA; ++j) {
     const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
     const bool ok = m < p.M;
-    a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda0) * ELT + cbytes : kOob;
+    a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT + cbytes : kOob;
     a1_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + cbytes : kOob;
   }
 #pragma unroll
@@ -571,11 +596,12 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     const uint32_t tok = static_cast<uint32_t>(t_perm[jl]);
     const uint32_t r1 = p.b1_gather ? tok : static_cast<uint32_t>(j0 + jl);
     b_jl[j] = jl;
-    b0_v[j] = (jl < jn) ? tok * static_cast<uint32_t>(p.ldb0) * ELT + cbytes : kOob;
+    const uint32_t r0 = b0_gather ? tok : static_cast<uint32_t>(j0 + jl);
+    b0_v[j] = (jl < jn) ? r0 * static_cast<uint32_t>(ldb0) * ELT + cbytes : kOob;
     b1_v[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT + cbytes;
   }
-  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(p.A0, p.a0_bytes);
-  const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(p.B0, p.b0_bytes);
+  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(A0, a0_bytes);
+  const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(B0, b0_bytes);
   const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
   char* const smem_a = smem + wave * 1024;                  // + stage*SB + j*NW*1024
   char* const smem_b = smem + BM * C::ROWB + wave * 1024;
@@ -601,7 +627,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       L.rB = rB0;
       L.dsel = 0xffffffffu;
       k0 = static_cast<uint32_t>((d_lo + lt) * BK);
-      klim = static_cast<uint32_t>(p.K0);
+      klim = static_cast<uint32_t>(K0);
     } else {
       // adapter phase (U_k Z'): one cluster run of the tile per k-tile group
       const int q = min(lq, max(n_runs - 1, 0));
@@ -616,7 +642,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       // offset arrays would make the compiler keep them in scratch memory)
       L.dsel = 0u;
       k0 = static_cast<uint32_t>(lkt * BK);
-      klim = static_cast<uint32_t>(p.K1);
+      klim = static_cast<uint32_t>(K1);
       ++lkt;
       if (lkt >= s_hi) { lkt = s_lo; ++lq; }
     }
@@ -717,7 +743,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // Dense k-tiles that cover a whole BK slice are a prefix of the schedule;
   // while the k-tile being loaded is one of them the loop runs the fast load
   // form (uniform k offset only), then the general form to the end.
-  const int nd_full = nd - ((nd > 0 && d_hi * BK > p.K0) ? 1 : 0);
+  const int nd_full = nd - ((nd > 0 && d_hi * BK > K0) ? 1 : 0);
   const int nfast = max(0, min(ntiles, nd_full - (P - 1)));
   int cur = 0;   // LDS stage of k-tile t
   auto ktile = [&](const TileLoad L, const bool fast) __attribute__((always_inline)) {
@@ -863,7 +889,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0>
 hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
-  dim3 grid(((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.ksplit);
+  const int gn = p.tile_start ? p.max_tiles : (p.N + BN - 1) / BN;
+  dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
   hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT>), grid,
                      dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
@@ -894,6 +921,7 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
     case Tile::Wide: *BM = 256; *BN = 128; *BK = 64; return;
     case Tile::Narrow: *BM = 128; *BN = 64; *BK = 128; return;
     case Tile::Decode: *BM = 64; *BN = 64; *BK = 128; return;
+    case Tile::Shrink: *BM = 64; *BN = 64; *BK = 64; return;
     case Tile::Mid: *BM = 128; *BN = 128; *BK = 64; return;
     case Tile::Small: *BM = 64; *BN = 64; *BK = 64; return;
     case Tile::F32: *BM = 64; *BN = 64; *BK = 32; return;
@@ -902,13 +930,16 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
 
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream) {
   // explicit token tiles (at most kSegTile columns) only with the 64-wide tiles
-  if (p.tile_start && !(tile == Tile::Small || tile == Tile::F32)) return hipErrorInvalidValue;
+  if (p.tile_start &&
+      !(tile == Tile::Decode || tile == Tile::Shrink || tile == Tile::Small || tile == Tile::F32))
+    return hipErrorInvalidValue;
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
     case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 16, 2, 1>(p, stream);
     case Tile::Wide: return launch_dma<256, 128, 64, 4, 2, 16, 3, 1>(p, stream);
     case Tile::Narrow: return launch_dma<128, 64, 128, 4, 1, 16, 3, 1>(p, stream);
     case Tile::Decode: return launch_dma<64, 64, 128, 2, 2, 16, 4, 1>(p, stream);
+    case Tile::Shrink: return launch_dma<64, 64, 64, 2, 2, 16, 3, 1>(p, stream);
     case Tile::Mid: return launch_cfg<bf16_t, 128, 128, 64, 4, 2, 2, 2, 16>(p, stream);
     default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
   }
