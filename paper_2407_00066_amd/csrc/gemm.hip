@@ -520,11 +520,75 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   }
   const int m0 = mt * BM;
   const int S = p.ksplit;
+  static_assert(BN <= C::NT, "one token column per thread");
 
-  // ---- token columns of this tile: perm, segment, and segment runs -------
-  for (int i = tid; i < BN; i += C::NT) {
-    t_perm[i] = (i < jn) ? p.perm[j0 + i] : 0;
-    t_seg[i] = (i < jn && p.sorted_seg) ? p.sorted_seg[j0 + i] : 0;
+  // ---- token columns of this tile (loads only; stored to LDS below) -------
+  int v_perm = 0, v_seg = 0;
+  if (tid < jn) {
+    v_perm = p.perm[j0 + tid];
+    v_seg = p.sorted_seg ? p.sorted_seg[j0 + tid] : 0;
+  }
+
+  // ---- load mapping: this lane's row and chunk in each 1 KB load ------------
+  // load j of wave w covers tile rows [RPI*(w + NW*j), +RPI) of A (j < QA) or
+  // B; lane l takes row +l/CH and global chunk (l%CH) ^ key(row), stored at
+  // slot l%CH.
+  const int lrow = lane / C::CH;
+  // the key depends on the tile row modulo 16 only, and every wave's rows
+  // start at a multiple of 16 plus RPI * wave
+  static_assert((C::RPI * C::NW) % 16 == 0, "swizzle period");
+  const int lchunk = (lane % C::CH) ^ swz_key<BK>(C::RPI * wave + lrow);
+  const uint32_t cbytes = static_cast<uint32_t>(lchunk * 16);
+  const uint32_t celem = static_cast<uint32_t>(lchunk * 8);
+  // Per-lane byte offsets of this lane's chunk at k = 0, for the dense (0)
+  // and adapter (1) operands; kOob marks a row outside the operand (and, for
+  // the dense token operand, a column outside the tile).  A k-tile adds its
+  // uniform k byte offset: in the dense phase as the load's scalar offset, so
+  // a full dense k-tile needs no per-lane arithmetic at all.
+  uint32_t a0_v[C::QA], a1_v[C::QA], b0_v[C::QB], b1_v[C::QB];
+  int b_jl[C::QB];
+#pragma unroll
+  for (int j = 0; j < C::QA; ++j) {
+    const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
+    const bool ok = m < p.M;
+    a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT + cbytes : kOob;
+    a1_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + cbytes : kOob;
+  }
+  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(A0, a0_bytes);
+  char* const smem_a = smem + wave * 1024;                  // + stage*SB + j*NW*1024
+  char* const smem_b = smem + BM * C::ROWB + wave * 1024;
+
+  // ---- dense k range of this split ----------------------------------------
+  const int nk0 = (K0 > 0) ? (K0 + BK - 1) / BK : 0;
+  const int nk1 = (K1 > 0) ? (K1 + BK - 1) / BK : 0;
+  int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0;
+  if (nk0 > 0) {
+    d_lo = split_lo(nk0, ks, S); d_hi = split_lo(nk0, ks + 1, S);
+    if (ks == 0) { s_lo = 0; s_hi = nk1; }
+  } else {
+    s_lo = split_lo(nk1, ks, S); s_hi = split_lo(nk1, ks + 1, S);
+  }
+  const int nd = d_hi - d_lo, ns = s_hi - s_lo;
+
+  // The weight rows do not depend on the token order: when the first P-1
+  // k-tiles are whole dense tiles, their weight loads go out now, in flight
+  // while the token columns and cluster runs are set up (the token operand's
+  // loads follow once its rows are known).  Rings deeper than three stages
+  // keep the plain order (their wait counts assume it).
+  const bool early = (P <= 3) && nd >= P - 1 && (d_lo + P - 1) * BK <= K0;
+  if (early) {
+#pragma unroll
+    for (int st = 0; st < P - 1; ++st)
+#pragma unroll
+      for (int j = 0; j < C::QA; ++j)
+        load16_lds(rA0, smem_a + st * C::SB + j * C::NW * 1024, a0_v[j],
+                   static_cast<uint32_t>((d_lo + st) * BK) * ELT);
+  }
+
+  // ---- token columns: perm, segment, and segment runs ----------------------
+  if (tid < BN) {
+    t_perm[tid] = v_perm;
+    t_seg[tid] = v_seg;
   }
   __syncthreads();
   int n_runs = 0;
@@ -552,44 +616,10 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   if (tid == 0) run_start[n_runs] = jn;
   __syncthreads();
 
-  // ---- k-tile schedule ----------------------------------------------------
-  const int nk0 = (K0 > 0) ? (K0 + BK - 1) / BK : 0;
-  const int nk1 = (K1 > 0) ? (K1 + BK - 1) / BK : 0;
-  int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0;
-  if (nk0 > 0) {
-    d_lo = split_lo(nk0, ks, S); d_hi = split_lo(nk0, ks + 1, S);
-    if (ks == 0) { s_lo = 0; s_hi = nk1; }
-  } else {
-    s_lo = split_lo(nk1, ks, S); s_hi = split_lo(nk1, ks + 1, S);
-  }
-  const int nd = d_hi - d_lo, ns = s_hi - s_lo;
+  // ---- k-tile schedule: the dense tiles, then each cluster run's tiles ------
   const int ntiles = nd + n_runs * ns;
 
-  // ---- load mapping: this lane's row and chunk in each 1 KB load ------------
-  // load j of wave w covers tile rows [RPI*(w + NW*j), +RPI) of A (j < QA) or
-  // B; lane l takes row +l/CH and global chunk (l%CH) ^ key(row), stored at
-  // slot l%CH.
-  const int lrow = lane / C::CH;
-  // the key depends on the tile row modulo 16 only, and every wave's rows
-  // start at a multiple of 16 plus RPI * wave
-  static_assert((C::RPI * C::NW) % 16 == 0, "swizzle period");
-  const int lchunk = (lane % C::CH) ^ swz_key<BK>(C::RPI * wave + lrow);
-  const uint32_t cbytes = static_cast<uint32_t>(lchunk * 16);
-  const uint32_t celem = static_cast<uint32_t>(lchunk * 8);
-  // Per-lane byte offsets of this lane's chunk at k = 0, for the dense (0)
-  // and adapter (1) operands; kOob marks a row outside the operand (and, for
-  // the dense token operand, a column outside the tile).  A k-tile adds its
-  // uniform k byte offset: in the dense phase as the load's scalar offset, so
-  // a full dense k-tile needs no per-lane arithmetic at all.
-  uint32_t a0_v[C::QA], a1_v[C::QA], b0_v[C::QB], b1_v[C::QB];
-  int b_jl[C::QB];
-#pragma unroll
-  for (int j = 0; j < C::QA; ++j) {
-    const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
-    const bool ok = m < p.M;
-    a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT + cbytes : kOob;
-    a1_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + cbytes : kOob;
-  }
+  // ---- token operand rows -------------------------------------------------
 #pragma unroll
   for (int j = 0; j < C::QB; ++j) {
     const int jl = C::RPI * (wave + C::NW * j) + lrow;
@@ -600,12 +630,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     b0_v[j] = (jl < jn) ? r0 * static_cast<uint32_t>(ldb0) * ELT + cbytes : kOob;
     b1_v[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT + cbytes;
   }
-  const __amdgpu_buffer_rsrc_t rA0 = make_rsrc(A0, a0_bytes);
   const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(B0, b0_bytes);
   const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
-  char* const smem_a = smem + wave * 1024;                  // + stage*SB + j*NW*1024
-  char* const smem_b = smem + BM * C::ROWB + wave * 1024;
-
   int lt = 0, lq = 0, lkt = s_lo;
   // Per-k-tile load state, prepared once per k-tile (the loads themselves may
   // be issued in several groups between the multiply steps).
@@ -733,9 +759,21 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     acc[i][j] = MT::mma(fa[buf][i], fb[buf][j], acc[i][j]);
   };
 
+  if (early) {
+    // weight loads of k-tiles 0..P-2 are out; add their token loads
 #pragma unroll
-  for (int st = 0; st < P - 1; ++st) load_next(st);
-  wait_vmcnt<(P - 2) * C::LPT>();
+    for (int st = 0; st < P - 1; ++st) {
+      TileLoad L;
+      L.kk = static_cast<uint32_t>((d_lo + st) * BK) * ELT;
+      issue_fast(L, st, C::QA, C::LPT);
+    }
+    lt = P - 1;
+    wait_vmcnt<(P - 2) * C::QB>();       // k-tile 0's token loads, and all weight loads
+  } else {
+#pragma unroll
+    for (int st = 0; st < P - 1; ++st) load_next(st);
+    wait_vmcnt<(P - 2) * C::LPT>();
+  }
   __builtin_amdgcn_s_barrier();
 #pragma unroll
   for (int r = 0; r < NR; ++r) read_frag(0, r, a_row_addr, b_row_addr, slot[0]);

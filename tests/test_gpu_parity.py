@@ -78,6 +78,8 @@ SMALL = {
     "bf16_ring_ragged": dict(cfg=109, T=2300, d_in=328, d_out=280, r=24, n=90, K=11, ids="prefill",
                              n_seq=20, seq_len=(40, 200)),
     "bf16_empty_clusters": dict(cfg=108, T=90, d_in=64, d_out=64, r=16, n=4, K=9),
+    # d_in >= 8192 takes the 256x128 ring tiles with an 8-way split along d_in
+    "bf16_wide_split": dict(cfg=110, T=300, d_in=8200, d_out=264, r=32, n=40, K=6, ids="zipf"),
 }
 
 
