@@ -110,7 +110,7 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
     const int tiles = ceil_div(pl->rank, BM) * std::max(expect, 1);
     const int nk = ceil_div(p->d_in, BK);
     const int target = (p->dtype == CTS_F32) ? 512 : 256;
-    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 16));
+    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 64));
   }
   pl->max_items = cts::max_sigma_items(T, p->n_adapters);
 
