@@ -62,19 +62,32 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const int nt = hi - lo;                 // tokens of this item (<= kSigmaChunk), one adapter
   const int cnt = nt * r;                 // outputs of this item
 
-  // Sigma_a -> LDS as fp32, 16-byte loads (issued before the partial sums)
+  // Sigma_a -> LDS as fp32: every 16-byte load of this thread is issued
+  // before the first is widened and stored (one round trip, not a chain)
   if (Sigma != nullptr) {
     int a = sorted_aid[lo];
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
     constexpr int V = Vec16<TI>::N;
+    constexpr int PER = (kSigMaxR * kSigMaxR / V + kSigThreads - 1) / kSigThreads;
     const uint4* sa = reinterpret_cast<const uint4*>(Sigma + static_cast<int64_t>(a) * r * r);
     const int nv = r * r / V;
-    for (int e = tid; e < nv; e += kSigThreads) {
-      float w[V];
-      Vec16<TI>::widen(sa[e], w);
-      const int row = (e * V) / r, col = (e * V) % r;
+    uint4 raw[PER];
 #pragma unroll
-      for (int u = 0; u < V; ++u) sig[row * kSigLd + col + u] = w[u];
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + u * kSigThreads;
+      raw[u] = (e < nv) ? sa[e] : uint4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + u * kSigThreads;
+      if (e < nv) {
+        float w[V];
+        Vec16<TI>::widen(raw[u], w);
+        const int row = (e * V) / r, col = (e * V) % r;     // V consecutive columns, col % V == 0
+#pragma unroll
+        for (int q = 0; q < V; q += 4)
+          *reinterpret_cast<f32x4*>(sig + row * kSigLd + col + q) = f32x4{w[q], w[q + 1], w[q + 2], w[q + 3]};
+      }
     }
   }
   // z = sum over the shrink's k-splits in fixed order; 4 consecutive values
@@ -102,22 +115,27 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     for (int e = tid; e < cnt; e += kSigThreads) st<TI>(out, e, z[(e / r) * kSigLd + e % r]);
     return;
   }
-  // z'[i][c] = sum_q Sigma[c][q] z[i][q]: one output per thread and pass,
-  // 16-byte LDS reads, fixed ascending q order
-  for (int e = tid; e < cnt; e += kSigThreads) {
-    const int i = e / r, c = e % r;
-    const float* srow = sig + c * kSigLd;
-    const float* zi = z + i * kSigLd;
-    float d = 0.f;
-    for (int q = 0; q < r; q += 4) {
-      const f32x4 a = *reinterpret_cast<const f32x4*>(srow + q);
-      const f32x4 b = *reinterpret_cast<const f32x4*>(zi + q);
-      d = fmaf(a[0], b[0], d);
-      d = fmaf(a[1], b[1], d);
-      d = fmaf(a[2], b[2], d);
-      d = fmaf(a[3], b[3], d);
+  // z'[i][c] = sum_q Sigma[c][q] z[i][q] on the fp32 matrix cores: one
+  // 16x16x4 MFMA step multiplies the item's (up to 16) token rows by 16
+  // columns of Sigma^T over 4 k; wave w takes column blocks w, w+4, ...
+  // A lane reads one z value (row l%16, k l/16) and one Sigma value (row =
+  // output column l%16, k l/16) per step.  Rows past the item's tokens and
+  // columns past r read stale LDS and are never stored (an output depends
+  // only on its own row of z and its own row of Sigma).
+  const int lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fk = lane >> 4;
+  for (int cb = wave; cb * 16 < r; cb += kSigThreads / 64) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const float* zr = z + fr * kSigLd + fk;
+    const float* sr = sig + (cb * 16 + fr) * kSigLd + fk;
+    for (int q = 0; q < r; q += 4)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(zr[q], sr[q], acc, 0, 0, 0);
+    const int c = cb * 16 + fr;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = 4 * fk + v;
+      if (i < nt && c < r) st<TI>(out, static_cast<int64_t>(i) * r + c, acc[v]);
     }
-    st<TI>(out, e, d);
   }
 }
 
