@@ -29,6 +29,7 @@ constexpr int kWaves = kSortThreads / 64;
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int kMaxCpw = kSortMaxT / 64 / kWaves;   // chunks per wave, at most
+constexpr int kMaxRuns = kSortThreads;             // run path: at most one run per thread
 static_assert(kWaves * kRadix == 4 * kSortThreads, "scan: four counters per thread");
 
 // Lanes of this wave whose digit equals this lane's (only lanes in `valid`).
@@ -88,6 +89,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   __shared__ uint16_t vbuf[2][kSortMaxT];
   __shared__ uint32_t hist[kWaves * kRadix];   // [wave][digit]
   __shared__ uint32_t wsum[kWaves];
+  __shared__ uint32_t run_key[kMaxRuns], run_start[kMaxRuns + 1], run_order[kMaxRuns], run_off[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -114,8 +116,74 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   const int seg_lo = wave * cpw * 64;
   const int seg_hi = min(T, seg_lo + cpw * 64);
 
+  __syncthreads();
   int in = 0;
-  for (int p = 0; p < passes; ++p) {
+
+  // ---- run path -------------------------------------------------------------
+  // Tokens of one request share an adapter, so the keys usually come in long
+  // runs.  When there are at most kMaxRuns maximal runs of equal keys, the
+  // runs themselves are ranked by (key, first token) with an all-pairs count,
+  // their lengths are summed in rank order, and every token goes to its run's
+  // offset plus its place in the run: the same stable order as the radix
+  // passes, which run otherwise.
+  {
+    const int ipt = (T + kSortThreads - 1) / kSortThreads;
+    const int j0 = tid * ipt, j1 = min(T, j0 + ipt);
+    uint32_t cnt = 0;
+    uint32_t kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t k = kbuf[0][j];
+      cnt += (j == 0 || k != kp) ? 1u : 0u;
+      kp = k;
+    }
+    uint32_t R;
+    const uint32_t base = block_exclusive_scan(cnt, wsum, lane, wave, &R);
+    if (R <= static_cast<uint32_t>(kMaxRuns)) {                  // uniform
+      uint32_t r = base;
+      kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
+      for (int j = j0; j < j1; ++j) {
+        const uint32_t k = kbuf[0][j];
+        if (j == 0 || k != kp) { run_start[r] = j; run_key[r] = k; ++r; }
+        kp = k;
+      }
+      if (tid == 0) run_start[R] = T;
+      __syncthreads();
+      if (static_cast<uint32_t>(tid) < R) {
+        const uint32_t kr = run_key[tid];
+        uint32_t rank = 0;
+        for (uint32_t q = 0; q < R; ++q) {
+          const uint32_t kq = run_key[q];
+          rank += (kq < kr || (kq == kr && q < static_cast<uint32_t>(tid))) ? 1u : 0u;
+        }
+        run_order[rank] = tid;
+      }
+      __syncthreads();
+      uint32_t len = 0;
+      if (static_cast<uint32_t>(tid) < R) {
+        const uint32_t rr = run_order[tid];
+        len = run_start[rr + 1] - run_start[rr];
+      }
+      uint32_t tot;
+      const uint32_t off = block_exclusive_scan(len, wsum, lane, wave, &tot);
+      if (static_cast<uint32_t>(tid) < R) run_off[run_order[tid]] = off;
+      __syncthreads();
+      int rid = static_cast<int>(base) - 1;                      // run holding j0 - 1
+      kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
+      for (int j = j0; j < j1; ++j) {
+        const uint32_t k = kbuf[0][j];
+        if (j == 0 || k != kp) ++rid;
+        kp = k;
+        const uint32_t pos = run_off[rid] + static_cast<uint32_t>(j) - run_start[rid];
+        kbuf[1][pos] = k;
+        vbuf[1][pos] = static_cast<uint16_t>(j);
+      }
+      __syncthreads();
+      in = 1;
+    }
+  }
+
+  const bool radix = (in == 0);
+  for (int p = 0; radix && p < passes; ++p) {
     const int shift = p * kRadixBits;
 #pragma unroll
     for (int i = 0; i < 4; ++i) hist[tid + i * kSortThreads] = 0;

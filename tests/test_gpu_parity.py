@@ -30,6 +30,17 @@ def _sort_case(T, n, K, kind, seed):
         aid = np.sort(aid)[::-1].copy()
     elif kind == "zipf":
         aid = wl.zipf_ids(rs, n, T)
+    elif kind.startswith("runs"):
+        # kind "runsR": R maximal runs of equal ids (neighbouring runs differ;
+        # an id may come back in a later run), run lengths random >= 1
+        R = int(kind[4:])
+        cuts = np.sort(rs.choice(np.arange(1, T), R - 1, replace=False))
+        lens = np.diff(np.concatenate([[0], cuts, [T]]))
+        ids = [int(rs.integers(0, n))]
+        for _ in range(R - 1):
+            nxt = int(rs.integers(0, n - 1))
+            ids.append(nxt + (nxt >= ids[-1]))
+        aid = np.repeat(np.array(ids, dtype=np.int32), lens)
     cof = None if kind == "identity" else rs.integers(0, K, n).astype(np.int32)
     if kind == "empty":
         cof = (np.arange(n) % 3 * (K // 3)).astype(np.int32)
@@ -43,6 +54,10 @@ SORT_CASES = [
     (8192, 3, 2, "uniform"), (1000, 1000, 1000, "identity"), (777, 50, 10, "same"),
     (777, 50, 10, "sorted"), (777, 50, 10, "reverse"), (600, 40, 30, "empty"),
     (2049, 65536, 65536, "uniform"), (256, 1000, 50, "zipf"),
+    # request runs: at most 1024 runs are ranked as whole runs, more take the
+    # token-level passes
+    (4096, 1000, 25, "runs32"), (8192, 20, 4, "runs1024"), (8192, 20, 4, "runs1025"),
+    (3000, 2, 2, "runs1000"), (1024, 5000, 300, "runs1024"), (8192, 65536, 4096, "runs700"),
 ]
 
 
