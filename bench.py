@@ -137,18 +137,24 @@ def time_steps(fn, sets, steps, warmup, torch):
     return ev0.elapsed_time(ev1) / steps          # ms per step
 
 
+STAGES = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
+
+
 def stage_times(fn, sets, steps, torch, cts):
-    """Mean duration (us) of each stage, from events at its boundaries."""
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(cts.N_STAGE_EVENTS)]
+    """Mean duration (us) of each stage, from events at its boundaries, and
+    the marker cost: the interval between the last boundary event and one
+    more event recorded right after it with no work between (every stage
+    interval holds one such marker interval besides its kernel)."""
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(cts.N_STAGE_EVENTS + 1)]
            for _ in range(steps)]
     for i in range(steps):
-        cts.set_stage_events(evs[i])
+        cts.set_stage_events(evs[i][:-1])
         fn(sets[i % len(sets)])
+        evs[i][-1].record()
     cts.set_stage_events(None)
     torch.cuda.synchronize()
-    names = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
     out = {}
-    for s, name in enumerate(names):
+    for s, name in enumerate(STAGES + ["marker"]):
         out[name] = 1e3 * sum(e[s].elapsed_time(e[s + 1]) for e in evs) / steps
     return out
 
@@ -217,11 +223,14 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     touched = len(set(w.cluster_of[w.adapter_id].tolist()))
     flops, nbytes = main_kernel_model(w, touched)
-    roof = roofline_of(flops, nbytes, stages["fused_gemm"] * 1e-6, w.dtype)
+    # the GEMM's duration: its stage interval less the marker interval
+    gemm_us = stages["fused_gemm"] - stages["marker"]
+    roof = roofline_of(flops, nbytes, gemm_us * 1e-6, w.dtype)
     if args.workload == "prefill_mix":
         roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
-    gemm_kernel = ("seg_gemm_dma_kernel" if w.dtype == "bf16" and w.T >= 2048 else "seg_gemm_kernel")
-    roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(stages["fused_gemm"], 2),
+    gemm_kernel = "seg_gemm_dma_kernel" if w.dtype == "bf16" else "seg_gemm_kernel"
+    roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(gemm_us, 2),
+                 "stage_us": round(stages["fused_gemm"], 2), "marker_us": round(stages["marker"], 2),
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
 
     cpu = None
@@ -333,19 +342,21 @@ def bench_stack(args, torch, np, cts, B, wl, device):
     # per-call stage events over a few steps: the GEMM time of a step
     n_ev = min(args.steps, 3)
     calls = wl.STACK_LAYERS * len(wl.STACK_PROJ)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.N_STAGE_EVENTS)] for _ in range(calls * n_ev)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(B.N_STAGE_EVENTS + 1)]
+           for _ in range(calls * n_ev)]
     c = 0
     for _ in range(n_ev):
         for L in projs:
             for name, _, _ in wl.STACK_PROJ:
                 x, W, U, Vt, S, y = L[name]
-                B.set_stage_events(evs[c])
+                B.set_stage_events(evs[c][:-1])
                 cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+                evs[c][-1].record()
                 c += 1
     B.set_stage_events(None)
     torch.cuda.synchronize()
-    names = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
-    stages = {nm: 1e3 * sum(e[i].elapsed_time(e[i + 1]) for e in evs) / n_ev for i, nm in enumerate(names)}
+    stages = {nm: 1e3 * sum(e[i].elapsed_time(e[i + 1]) for e in evs) / n_ev
+              for i, nm in enumerate(STAGES + ["marker"])}
 
     touched = len(set(cof_h[aid_h].tolist()))
     flops = nbytes = 0.0
@@ -354,9 +365,11 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                                  touched)
         flops += f * wl.STACK_LAYERS
         nbytes += b * wl.STACK_LAYERS
-    roof = roofline_of(flops, nbytes, stages["fused_gemm"] * 1e-6, "bf16")
-    roof.update({"kernel": "seg_gemm_kernel (fused W X + U_k Z'), all %d launches of a step" % calls,
-                 "mean_us": round(stages["fused_gemm"] / calls, 2),
+    gemm_us = stages["fused_gemm"] - stages["marker"]          # per step: calls x (stage - marker)
+    roof = roofline_of(flops, nbytes, gemm_us * 1e-6, "bf16")
+    roof.update({"kernel": "seg_gemm_dma_kernel (fused W X + U_k Z'), all %d launches of a step" % calls,
+                 "mean_us": round(gemm_us / calls, 2), "stage_us": round(stages["fused_gemm"] / calls, 2),
+                 "marker_us": round(stages["marker"] / calls, 2),
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
     cpu = None
     if not args.no_cpu_baseline:

@@ -96,7 +96,8 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   {
     const int tiles = tiles_of(pl->main_tile);
     const int nk = ceil_div(p->d_in, BK);
-    const int s = std::min(std::min(ceil_div(256, tiles), max_split), std::max(1, nk / 4));
+    // no more workgroups than one round over the compute units
+    const int s = std::min(std::min(std::max(1, 256 / tiles), max_split), std::max(1, nk / 4));
     pl->main_split = std::max(1, s);
   }
   // shrink: one workgroup per (cluster segment tile of <= kSegTile tokens,

@@ -445,6 +445,16 @@ __device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, char* lds, 
 #endif
 }
 
+// 4-byte buffer load of each lane into LDS, used as an L2 prefetch: the data
+// lands in a scratch LDS slot nobody reads, only the cache fill matters.
+__device__ __forceinline__ void load4_lds(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff,
+                                          uint32_t soff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 4, voff,
+                                           soff, 0, 0);
+#endif
+}
+
 __device__ __forceinline__ void pin(bf16x8& v) {
 #if defined(__HIP_DEVICE_COMPILE__)
   asm volatile("" : "+v"(v));
@@ -476,9 +486,19 @@ struct DmaCfg {
 // DIRECT: the epilogue writes straight from the accumulators (4 consecutive
 // output features of one token per lane) instead of staging the tile in LDS;
 // used when the fp32 tile does not fit in LDS.
-template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT>
+// PFD > 0 (rings of two or three stages): during k-tile t the workgroup also
+// touches, one 4-byte load per cache line, its share of the weight rows and
+// token rows of dense k-tile t + P - 1 + PFD, so that the LDS loads of that
+// k-tile find them in L2.  Tiles of one XCD come in blocks of 8 row tiles
+// (tile_of_block), so the 8 workgroups on one column tile each take every
+// 8th token row; the WSPL workgroups on one row tile (4 with 256 tiles of
+// 256x256) each take every WSPL-th weight row.
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT, int PFD = 0, int WSPL = 1>
 __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const GemmParams p) {
   using C = DmaCfg<BM, BN, BK, WM, WN, MB, P, DIRECT>;
+  static_assert(PFD == 0 || P <= 3, "prefetch wait counts cover rings of two or three stages");
+  constexpr int NPF = PFD > 0 ? 1 : 0;                     // prefetch loads per wave per k-tile
+  constexpr int PFW = C::NW / 2;                           // waves prefetching weight rows
   using MT = MfmaTraits<bf16_t, MB>;
   typedef typename MT::accv accv;
   constexpr uint32_t ELT = 2;
@@ -488,6 +508,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __shared__ int32_t t_seg[BN];
   __shared__ int32_t run_start[BN + 1];
   __shared__ int32_t wave_runs[C::NW];
+  __shared__ uint32_t pf_sink[PFD > 0 ? 64 : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // Token-tile mode (explicit tiles, each inside one segment): the tile's
@@ -573,9 +594,9 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // The weight rows do not depend on the token order: when the first P-1
   // k-tiles are whole dense tiles, their weight loads go out now, in flight
   // while the token columns and cluster runs are set up (the token operand's
-  // loads follow once its rows are known).  Rings deeper than three stages
-  // keep the plain order (their wait counts assume it).
-  const bool early = (P <= 3) && nd >= P - 1 && (d_lo + P - 1) * BK <= K0;
+  // loads follow once its rows are known).  With four stages the first
+  // k-tile's wait below is adjusted for this order.
+  const bool early = (P <= 4) && nd >= P - 1 && (d_lo + P - 1) * BK <= K0;
   if (early) {
 #pragma unroll
     for (int st = 0; st < P - 1; ++st)
@@ -633,6 +654,33 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(B0, b0_bytes);
   const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
   int lt = 0, lq = 0, lkt = s_lo;
+
+  // dense k-tiles that cover a whole BK slice (a prefix of the schedule)
+  const int nd_full = nd - ((nd > 0 && d_hi * BK > K0) ? 1 : 0);
+  // L2 prefetch: this lane's weight row or token row (kOob when none)
+  uint32_t pf_v = kOob;
+  const bool pf_w = __builtin_amdgcn_readfirstlane(wave) < PFW;
+  if (PFD > 0) {
+    static_assert(BM % (WSPL * PFW) == 0 && BM / WSPL / PFW <= 64 && BN % (8 * PFW) == 0 &&
+                  BN / 8 / PFW <= 64, "prefetch lanes");
+    if (pf_w) {
+      const int m = m0 + WSPL * (wave * (BM / WSPL / PFW) + lane) + (nt % WSPL);
+      if (lane < BM / WSPL / PFW && m < p.M) pf_v = static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT;
+    } else {
+      const int jl = 8 * ((wave - PFW) * (BN / 8 / PFW) + lane) + (mt & 7);
+      if (lane < BN / 8 / PFW && jl < jn) {
+        const uint32_t r0 = b0_gather ? static_cast<uint32_t>(t_perm[jl]) : static_cast<uint32_t>(j0 + jl);
+        pf_v = r0 * static_cast<uint32_t>(ldb0) * ELT;
+      }
+    }
+  }
+  // dense k-tile ti of this split (ti counted from d_lo; past the whole
+  // dense tiles the load touches nothing)
+  auto prefetch = [&](int ti) __attribute__((always_inline)) {
+    if (PFD > 0)
+      load4_lds(pf_w ? rA0 : rB0, pf_sink, (ti < nd_full) ? pf_v : kOob,
+                static_cast<uint32_t>((d_lo + ti) * BK) * ELT);
+  };
   // Per-k-tile load state, prepared once per k-tile (the loads themselves may
   // be issued in several groups between the multiply steps).
   struct TileLoad {
@@ -749,6 +797,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   constexpr int NLG = C::NKS > 2 ? C::NKS / 2 : 1;           // steps that issue loads
   constexpr int GPS = (C::LPT + NLG - 1) / NLG;              // loads per such step
   static_assert(GPS <= (NM > NR ? NM : NR), "every load gets an issue slot");
+  static_assert(NPF == 0 || GPS < (NM > NR ? NM : NR), "a slot for the prefetch");
   bf16x8 fa[2][C::FM], fb[2][C::FN];
   auto read_frag = [&](int buf, int r, uint32_t sa, uint32_t sb, uint32_t sl) __attribute__((always_inline)) {
     if (r < C::FM) lds_read16(fa[buf][r], sa + sl + r * MB * C::ROWB);
@@ -759,6 +808,9 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     acc[i][j] = MT::mma(fa[buf][i], fb[buf][j], acc[i][j]);
   };
 
+  // prefetch of the first PFD k-tiles after the ring's (waited for with them)
+#pragma unroll
+  for (int i = 0; i < PFD; ++i) prefetch(P - 1 + i);
   if (early) {
     // weight loads of k-tiles 0..P-2 are out; add their token loads
 #pragma unroll
@@ -781,9 +833,9 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // Dense k-tiles that cover a whole BK slice are a prefix of the schedule;
   // while the k-tile being loaded is one of them the loop runs the fast load
   // form (uniform k offset only), then the general form to the end.
-  const int nd_full = nd - ((nd > 0 && d_hi * BK > K0) ? 1 : 0);
   const int nfast = max(0, min(ntiles, nd_full - (P - 1)));
   int cur = 0;   // LDS stage of k-tile t
+  int t = 0;
   auto ktile = [&](const TileLoad L, const bool fast) __attribute__((always_inline)) {
     int nst = cur + P - 1; if (nst >= P) nst -= P;         // stage of k-tile t+P-1
     int ncur = cur + 1; if (ncur >= P) ncur -= P;          // stage of k-tile t+1
@@ -807,6 +859,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
           if (m < NM) mma(b, m);
           if (m < NR) read_frag(b ^ 1, m, sa, sb, slot[s2 + 1]);
           if (s2 < NLG && m < GPS) iss(s2 * GPS + m, s2 * GPS + m + 1);
+          if (NPF && s2 == NLG - 1 && m == GPS) prefetch(t + P - 1 + PFD);   // after every load
           __builtin_amdgcn_sched_barrier(0);
         }
       } else {
@@ -815,7 +868,14 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
           mma(b, m);
           __builtin_amdgcn_sched_barrier(0);
         }
-        wait_vmcnt<(P - 2) * C::LPT>();                    // this lane's loads of k-tile t+1
+        // this lane's loads of k-tile t+1.  In the early order (weight loads
+        // of k-tiles 0..2, then their token loads) k-tile 1's token loads
+        // are followed by k-tile 2's token loads and k-tile 3's loads only.
+        // With prefetches each k-tile's loads are followed by one prefetch
+        // load; the prologue's go out before its ring loads.
+        if (P == 4 && early && t == 0) wait_vmcnt<(P == 4 ? 2 * C::LPT - C::QA : 0)>();
+        else if (P == 3 && NPF && t == 0) wait_vmcnt<(P - 2) * C::LPT + NPF>();
+        else wait_vmcnt<(P - 2) * C::LPT + (P - 1) * NPF>();
         __builtin_amdgcn_s_barrier();                      // ... and every wave's
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -828,7 +888,6 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     }
     cur = ncur;
   };
-  int t = 0;
   for (; t < nfast; ++t) {
     TileLoad L;                                            // dense k-tile lt, whole
     L.kk = static_cast<uint32_t>((d_lo + lt) * BK) * ELT;
@@ -925,11 +984,12 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0>
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0, int PFD = 0,
+          int WSPL = 1>
 hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const int gn = p.tile_start ? p.max_tiles : (p.N + BN - 1) / BN;
   dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT>), grid,
+  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL>), grid,
                      dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
 }
@@ -973,7 +1033,7 @@ hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStre
     return hipErrorInvalidValue;
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
-    case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 16, 2, 1>(p, stream);
+    case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 16, 2, 1, 6, 4>(p, stream);
     case Tile::Wide: return launch_dma<256, 128, 64, 4, 2, 16, 3, 1>(p, stream);
     case Tile::Narrow: return launch_dma<128, 64, 128, 4, 1, 16, 3, 1>(p, stream);
     case Tile::Decode: return launch_dma<64, 64, 128, 2, 2, 16, 4, 1>(p, stream);

@@ -95,6 +95,10 @@ SMALL = {
     "bf16_empty_clusters": dict(cfg=108, T=90, d_in=64, d_out=64, r=16, n=4, K=9),
     # d_in >= 8192 takes the 256x128 ring tiles with an 8-way split along d_in
     "bf16_wide_split": dict(cfg=110, T=300, d_in=8200, d_out=264, r=32, n=40, K=6, ids="zipf"),
+    # T <= 64 takes the 64x64 decode tiles (four-stage ring, weight loads issued
+    # before the token setup): ragged d_in over two splits, and a whole-tile case
+    "bf16_decode_ragged": dict(cfg=111, T=50, d_in=1000, d_out=200, r=32, n=20, K=3),
+    "bf16_decode_split4": dict(cfg=112, T=64, d_in=2048, d_out=320, r=16, n=30, K=2),
 }
 
 
