@@ -9,7 +9,9 @@ already resident in HBM; for the workload stack32 it is one pass over all 224
 linear projections of a 32-layer 7B-shaped decoder (q, k, v, o, gate, up,
 down), each its own cts_apply call with its own weights.  The timed region is
 K consecutive steps between two HIP events on the stream the library launches
-on.  Single-layer inputs are rotated over enough device copies (>= 512 MB in
+on; the steps are launched call by call.  The same steps replayed from HIP
+graphs captured from their cts_apply calls (as a serving loop replays a decode
+step) are reported under "graph_replay".  Single-layer inputs are rotated over enough device copies (>= 512 MB in
 total) that the 256 MB last-level cache cannot hold them between steps; the
 stack's weights (about 32 GB) are distinct per projection anyway.
 
@@ -137,6 +139,32 @@ def time_steps(fn, sets, steps, warmup, torch):
     return ev0.elapsed_time(ev1) / steps          # ms per step
 
 
+def captured(fn, sets, torch):
+    """One HIP graph per input set holding the launches of fn(set) (the
+    library allocates, copies and clears nothing inside a call, so a whole
+    step is captured); a replay runs the same kernels on the same buffers
+    without the host-side work of the calls."""
+    torch.cuda.synchronize()
+    graphs = []
+    for st in sets:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(st)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    return graphs
+
+
+def time_launches(fn, sets, args, torch):
+    """(eager ms, graph-replay ms) per step: the step launched call by call,
+    then from its captured graph."""
+    eager = time_steps(fn, sets, args.steps, args.warmup, torch)
+    graphs = captured(fn, sets, torch)
+    graph = time_steps(lambda g: g.replay(), graphs, args.steps, args.warmup, torch)
+    del graphs
+    return eager, graph
+
+
 STAGES = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
 
 
@@ -191,7 +219,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
         (n_sets, set_bytes / 1e6, args.warmup, args.steps))
-    ms = time_steps(step, sets, args.steps, args.warmup, torch)
+    ms, ms_g = time_launches(step, sets, args, torch)
     stages = stage_times(step, sets, args.steps, torch, B)
 
     # one adapter: the same batch, every token on LoRA 0 of cluster 0
@@ -205,7 +233,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
 
     log("timing cts_apply with one adapter")
-    ms1 = time_steps(step1, sets, args.steps, args.warmup, torch)
+    ms1, ms1_g = time_launches(step1, sets, args, torch)
 
     # uncompressed comparison on the same batch
     uA, uB = to_dev(w.A, device), to_dev(w.B, device)
@@ -217,7 +245,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
 
     log("timing cts_apply_uncompressed")
-    ms_u = time_steps(step_u, sets, args.steps, args.warmup, torch)
+    ms_u, ms_u_g = time_launches(step_u, sets, args, torch)
     stages_u = stage_times(step_u, sets, args.steps, torch, B)
     del uA, uB
 
@@ -244,6 +272,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "graph_replay": {"value": round(w.T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5)},
         "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
         "config": {"workload": args.workload, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
                    "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
@@ -251,10 +280,11 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         "roofline": roof,
         "cpu_baseline": cpu,
         "uncompressed": {"value": round(w.T / (ms_u * 1e-3), 1), "unit": "tokens/s",
-                         "ms_per_step": round(ms_u, 5), "r_lora": w.r_l,
+                         "ms_per_step": round(ms_u, 5), "graph_replay_ms_per_step": round(ms_u_g, 5),
+                         "r_lora": w.r_l,
                          "stages_us": {k: round(v, 2) for k, v in stages_u.items()}},
         "single_adapter": {"value": round(value1, 1), "unit": "tokens/s", "ms_per_step": round(ms1, 5),
-                           "ratio": round(value / value1, 4)},
+                           "graph_replay_ms_per_step": round(ms1_g, 5), "ratio": round(value / value1, 4)},
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
     }
 
@@ -335,9 +365,9 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                 cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
 
     log("timing the stack: %.1f GB of weights, %d warmup + %d steps" % (resident / 1e9, args.warmup, args.steps))
-    ms = time_steps(step, [None], args.steps, args.warmup, torch)
+    ms, ms_g = time_launches(step, [None], args, torch)
     log("timing the stack with one adapter")
-    ms1 = time_steps(step1, [None], args.steps, args.warmup, torch)
+    ms1, ms1_g = time_launches(step1, [None], args, torch)
 
     # per-call stage events over a few steps: the GEMM time of a step
     n_ev = min(args.steps, 3)
@@ -379,7 +409,9 @@ def bench_stack(args, torch, np, cts, B, wl, device):
     return {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "graph_replay": {"value": round(T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5)},
+        "dtype": "bf16",
         "data": "synthetic (seeded, generated on the device; %.1f GB of weights resident in HBM)" % (resident / 1e9),
         "config": {"workload": "stack32", "T": T, "layers": wl.STACK_LAYERS,
                    "projections": [list(pr) for pr in wl.STACK_PROJ], "r": r, "n_adapters": n,
@@ -388,7 +420,7 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         "roofline": roof,
         "cpu_baseline": cpu,
         "single_adapter": {"value": round(value1, 1), "unit": "tokens/s", "ms_per_step": round(ms1, 5),
-                           "ratio": round(value / value1, 4)},
+                           "graph_replay_ms_per_step": round(ms1_g, 5), "ratio": round(value / value1, 4)},
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
     }
 

@@ -69,9 +69,10 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   // fused GEMM tile and k split.  Prefill-sized batches: 256x256 tiles.
   // Smaller batches are bound by the weight stream and by how often each
   // compute unit re-reads its operands from L2: 256x128 tiles when they alone
-  // give most compute units work or the reduction is long (then split along
-  // k up to 256 workgroups), else 128x64 tiles, and 64x64 for decode
-  // batches, split along k up to 256 workgroups (partials summed afterwards).
+  // give most compute units work or the reduction is long, else 128x128
+  // tiles while they still give at least 128 tiles, else 128x64 tiles, and
+  // 64x64 for decode batches; each split along k up to one round of 256
+  // workgroups (partials summed afterwards).
   auto tiles_of = [&](Tile t) {
     int bm, bn, bk;
     cts::tile_dims(t, &bm, &bn, &bk);
@@ -85,6 +86,9 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   } else if (T > 64 && (tiles_of(Tile::Wide) >= 192 || p->d_in >= 8192)) {
     pl->main_tile = Tile::Wide;
     max_split = 8;
+  } else if (T > 64 && tiles_of(Tile::Mid) >= 128) {
+    pl->main_tile = Tile::Mid;
+    max_split = 4;
   } else if (T > 64) {
     pl->main_tile = Tile::Narrow;
     max_split = 4;

@@ -85,9 +85,9 @@ struct GemmParams {
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide
-// 256x128x64, Narrow 128x64x128, Decode 64x64x128 and Shrink 64x64x64 load
-// their k-tiles straight into LDS; Mid 128x128x64 and Small 64x64x64 stage
-// them in registers; F32 is the fp32 path.  Explicit token tiles are taken by
+// 256x128x64, Mid 128x128x64, Narrow 128x64x128, Decode 64x64x128 and Shrink
+// 64x64x64 load their k-tiles straight into LDS; Small 64x64x64 stages them
+// in registers; F32 is the fp32 path.  Explicit token tiles are taken by
 // the 64-wide ones (Decode, Shrink, Small, F32).
 enum class Tile { Large, Wide, Narrow, Decode, Shrink, Mid, Small, F32 };
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream);

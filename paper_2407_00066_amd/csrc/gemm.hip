@@ -590,20 +590,23 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     s_lo = split_lo(nk1, ks, S); s_hi = split_lo(nk1, ks + 1, S);
   }
   const int nd = d_hi - d_lo, ns = s_hi - s_lo;
+  // dense k-tiles that cover a whole BK slice: d_lo .. d_lo + nd_full - 1
+  const int nd_full = nd - ((nd > 0 && d_hi * BK > K0) ? 1 : 0);
+  auto dk = [&](int i) __attribute__((always_inline)) { return d_lo + i; };   // dense k-tile at position i
 
   // The weight rows do not depend on the token order: when the first P-1
   // k-tiles are whole dense tiles, their weight loads go out now, in flight
   // while the token columns and cluster runs are set up (the token operand's
   // loads follow once its rows are known).  With four stages the first
   // k-tile's wait below is adjusted for this order.
-  const bool early = (P <= 4) && nd >= P - 1 && (d_lo + P - 1) * BK <= K0;
+  const bool early = (P <= 4) && nd_full >= P - 1;
   if (early) {
 #pragma unroll
     for (int st = 0; st < P - 1; ++st)
 #pragma unroll
       for (int j = 0; j < C::QA; ++j)
         load16_lds(rA0, smem_a + st * C::SB + j * C::NW * 1024, a0_v[j],
-                   static_cast<uint32_t>((d_lo + st) * BK) * ELT);
+                   static_cast<uint32_t>(dk(st) * BK) * ELT);
   }
 
   // ---- token columns: perm, segment, and segment runs ----------------------
@@ -655,14 +658,12 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
   int lt = 0, lq = 0, lkt = s_lo;
 
-  // dense k-tiles that cover a whole BK slice (a prefix of the schedule)
-  const int nd_full = nd - ((nd > 0 && d_hi * BK > K0) ? 1 : 0);
   // L2 prefetch: this lane's weight row or token row (kOob when none)
   uint32_t pf_v = kOob;
   const bool pf_w = __builtin_amdgcn_readfirstlane(wave) < PFW;
   if (PFD > 0) {
-    static_assert(BM % (WSPL * PFW) == 0 && BM / WSPL / PFW <= 64 && BN % (8 * PFW) == 0 &&
-                  BN / 8 / PFW <= 64, "prefetch lanes");
+    static_assert(PFD == 0 || (BM % (WSPL * PFW) == 0 && BM / WSPL / PFW <= 64 &&
+                               BN % (8 * PFW) == 0 && BN / 8 / PFW <= 64), "prefetch lanes");
     if (pf_w) {
       const int m = m0 + WSPL * (wave * (BM / WSPL / PFW) + lane) + (nt % WSPL);
       if (lane < BM / WSPL / PFW && m < p.M) pf_v = static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT;
@@ -679,7 +680,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   auto prefetch = [&](int ti) __attribute__((always_inline)) {
     if (PFD > 0)
       load4_lds(pf_w ? rA0 : rB0, pf_sink, (ti < nd_full) ? pf_v : kOob,
-                static_cast<uint32_t>((d_lo + ti) * BK) * ELT);
+                static_cast<uint32_t>(dk(ti) * BK) * ELT);
   };
   // Per-k-tile load state, prepared once per k-tile (the loads themselves may
   // be issued in several groups between the multiply steps).
@@ -700,7 +701,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       L.rA = rA0;
       L.rB = rB0;
       L.dsel = 0xffffffffu;
-      k0 = static_cast<uint32_t>((d_lo + lt) * BK);
+      k0 = static_cast<uint32_t>(dk(lt) * BK);
       klim = static_cast<uint32_t>(K0);
     } else {
       // adapter phase (U_k Z'): one cluster run of the tile per k-tile group
@@ -816,7 +817,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 #pragma unroll
     for (int st = 0; st < P - 1; ++st) {
       TileLoad L;
-      L.kk = static_cast<uint32_t>((d_lo + st) * BK) * ELT;
+      L.kk = static_cast<uint32_t>(dk(st) * BK) * ELT;
       issue_fast(L, st, C::QA, C::LPT);
     }
     lt = P - 1;
@@ -890,7 +891,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   };
   for (; t < nfast; ++t) {
     TileLoad L;                                            // dense k-tile lt, whole
-    L.kk = static_cast<uint32_t>((d_lo + lt) * BK) * ELT;
+    L.kk = static_cast<uint32_t>(dk(lt) * BK) * ELT;
     ++lt;
     ktile(L, true);
   }
@@ -1038,7 +1039,7 @@ hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStre
     case Tile::Narrow: return launch_dma<128, 64, 128, 4, 1, 16, 3, 1>(p, stream);
     case Tile::Decode: return launch_dma<64, 64, 128, 2, 2, 16, 4, 1>(p, stream);
     case Tile::Shrink: return launch_dma<64, 64, 64, 2, 2, 16, 3, 1>(p, stream);
-    case Tile::Mid: return launch_cfg<bf16_t, 128, 128, 64, 4, 2, 2, 2, 16>(p, stream);
+    case Tile::Mid: return launch_dma<128, 128, 64, 4, 2, 16, 4, 1>(p, stream);
     default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
   }
 }

@@ -29,7 +29,9 @@ constexpr int kWaves = kSortThreads / 64;
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int kMaxCpw = kSortMaxT / 64 / kWaves;   // chunks per wave, at most
-constexpr int kMaxRuns = kSortThreads;             // run path: at most one run per thread
+// run path: at most this many runs (its all-pairs ranking costs R^2 / 1024
+// compares per thread; past a few hundred runs the radix passes are cheaper)
+constexpr int kMaxRuns = 256;
 static_assert(kWaves * kRadix == 4 * kSortThreads, "scan: four counters per thread");
 
 // Lanes of this wave whose digit equals this lane's (only lanes in `valid`).
@@ -89,7 +91,9 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   __shared__ uint16_t vbuf[2][kSortMaxT];
   __shared__ uint32_t hist[kWaves * kRadix];   // [wave][digit]
   __shared__ uint32_t wsum[kWaves];
-  __shared__ uint32_t run_key[kMaxRuns], run_start[kMaxRuns + 1], run_order[kMaxRuns], run_off[kMaxRuns];
+  // run keys padded with 16 entries that rank below nothing (all ones)
+  __shared__ __attribute__((aligned(16))) uint32_t run_key[kMaxRuns + 16];
+  __shared__ uint32_t run_start[kMaxRuns + 1], run_order[kMaxRuns], run_off[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -147,13 +151,26 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
         kp = k;
       }
       if (tid == 0) run_start[R] = T;
+      if (tid < 16) run_key[R + tid] = 0xffffffffu;            // keys use at most 31 bits
       __syncthreads();
       if (static_cast<uint32_t>(tid) < R) {
         const uint32_t kr = run_key[tid];
         uint32_t rank = 0;
-        for (uint32_t q = 0; q < R; ++q) {
-          const uint32_t kq = run_key[q];
-          rank += (kq < kr || (kq == kr && q < static_cast<uint32_t>(tid))) ? 1u : 0u;
+        const uint4* rk = reinterpret_cast<const uint4*>(run_key);
+        // 16 keys per step, four 16-byte reads in flight
+        for (uint32_t q = 0; q < R; q += 16) {
+          uint4 v[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = rk[q / 4 + i];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t kq[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t qi = q + 4 * i + j;
+              rank += (kq[j] < kr || (kq[j] == kr && qi < static_cast<uint32_t>(tid))) ? 1u : 0u;
+            }
+          }
         }
         run_order[rank] = tid;
       }

@@ -54,9 +54,10 @@ SORT_CASES = [
     (8192, 3, 2, "uniform"), (1000, 1000, 1000, "identity"), (777, 50, 10, "same"),
     (777, 50, 10, "sorted"), (777, 50, 10, "reverse"), (600, 40, 30, "empty"),
     (2049, 65536, 65536, "uniform"), (256, 1000, 50, "zipf"),
-    # request runs: at most 1024 runs are ranked as whole runs, more take the
+    # request runs: at most 256 runs are ranked as whole runs, more take the
     # token-level passes
-    (4096, 1000, 25, "runs32"), (8192, 20, 4, "runs1024"), (8192, 20, 4, "runs1025"),
+    (4096, 1000, 25, "runs32"), (8192, 20, 4, "runs256"), (8192, 20, 4, "runs257"),
+    (300, 1000, 50, "runs256"), (8192, 20, 4, "runs1024"),
     (3000, 2, 2, "runs1000"), (1024, 5000, 300, "runs1024"), (8192, 65536, 4096, "runs700"),
 ]
 
@@ -99,6 +100,9 @@ SMALL = {
     # before the token setup): ragged d_in over two splits, and a whole-tile case
     "bf16_decode_ragged": dict(cfg=111, T=50, d_in=1000, d_out=200, r=32, n=20, K=3),
     "bf16_decode_split4": dict(cfg=112, T=64, d_in=2048, d_out=320, r=16, n=30, K=2),
+    # 128x128 ring tiles (at least 128 of them, too few 256x128 tiles): ragged
+    # token tail and d_in
+    "bf16_mid_tiles": dict(cfg=113, T=200, d_in=200, d_out=8192, r=24, n=30, K=4, ids="zipf"),
 }
 
 
