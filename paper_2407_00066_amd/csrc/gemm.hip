@@ -1007,13 +1007,16 @@ hipError_t launch_cfg(const GemmParams& p, hipStream_t stream) {
 
 }  // namespace
 
-// Tile shapes (measured on MI355X at the prefill, MLP and decode shapes of
-// the layer):
-//   Large  256 x 256 (d_out x tokens), 8 waves of 64 x 128, 32x32 MFMA,
-//          k-tiles loaded straight into a 2-stage LDS ring            T >= 2048
-//   Mid    128 x 128, 8 waves of 32 x 64, 16x16 MFMA, register-staged  128 <= T < 2048
-//   Small   64 x  64, 4 waves of 32 x 32, 32x32 MFMA, split along k    T < 128, shrink
-//   F32     64 x  64, fp32 inputs
+// Tile shapes (BM x BN x BK: d_out rows x tokens x k; chosen by the plan from
+// measurements on MI355X).  The ring tiles use 16x16x32 MFMA:
+//   Large   256 x 256 x  64, 8 waves, 2-stage ring + L2 prefetch      T >= 2048
+//   Wide    256 x 128 x  64, 8 waves, 3 stages     many row tiles or d_in >= 8192
+//   Mid     128 x 128 x  64, 8 waves, 4 stages     >= 128 tiles
+//   Narrow  128 x  64 x 128, 4 waves, 3 stages     other T > 64
+//   Decode   64 x  64 x 128, 4 waves, 4 stages     T <= 64
+//   Shrink   64 x  64 x  64, 4 waves, 3 stages     the V_k^T X products
+//   Small    64 x  64 x  64, register-staged (bf16)
+//   F32      64 x  64 x  32, register-staged, fp32 inputs
 void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
   switch (tile) {
     case Tile::Large: *BM = 256; *BN = 256; *BK = 64; return;

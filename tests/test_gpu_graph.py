@@ -21,9 +21,10 @@ def _layer(name, **kw):
 
 
 def test_graph_replay_matches_eager():
-    # two layers of different shapes in one graph (the ring GEMM with a k
-    # split and the 256x256 tiles), as a decoder stack would capture them
-    w1, a1 = _layer("graph_a", cfg=120, T=64, d_in=512, d_out=320, r=32, n=40, K=5)
+    # two layers of different shapes in one graph (the decode tiles with a
+    # 4-way k split summed in the GEMM, and the 256x256 tiles), as a decoder
+    # stack would capture them
+    w1, a1 = _layer("graph_a", cfg=120, T=64, d_in=2048, d_out=320, r=32, n=40, K=5)
     w2, a2 = _layer("graph_b", cfg=121, T=2100, d_in=256, d_out=296, r=16, n=30, K=4, ids="prefill",
                     n_seq=12, seq_len=(60, 300))
     y1 = torch.empty((w1.T, w1.d_out), dtype=torch.bfloat16, device="cuda")

@@ -156,6 +156,22 @@ def test_tiny_exact_compressed_equals_uncompressed(oracle_mod):
     assert row_rel_err(host(y_c), host(y_u)) <= 1e-5
 
 
+def test_split_sum_repeatable(oracle_mod, small_cases):
+    """The decode tiles split d_in four ways (fp32 partials summed in split
+    order): repeated calls on one workspace give identical bits and match
+    the oracle."""
+    w = small_cases["bf16_decode_split4"]
+    say("split-sum repeat")
+    p = cts.make_problem(w.T, w.d_in, w.d_out, r=w.r, n_adapters=w.n, n_clusters=w.K)
+    ws = torch.empty(cts.workspace_size(p), dtype=torch.uint8, device="cuda")
+    ys = [cts.apply(*_inputs(w), workspace=ws) for _ in range(3)]
+    torch.cuda.synchronize()
+    for y in ys[1:]:
+        assert torch.equal(y, ys[0])
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, w.W, w.U, w.Vt, w.Sigma)
+    assert row_rel_err(host(ys[0]), ref) <= TOL[w.dtype]
+
+
 def test_zero_sigma_is_exactly_base_layer(small_cases):
     """Sigma_i = 0 adds exactly nothing: bitwise equal to B_i = 0 on the
     uncompressed path (same base GEMM, zero adapter term)."""
