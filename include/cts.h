@@ -134,9 +134,10 @@ int cts_validate_ids(const cts_problem* p, const int32_t* adapter_id,
 
 /* Profiling aid; correct use of the library never needs it.
  * events == NULL turns it off.  Otherwise `events` is a host array of
- * CTS_N_STAGE_EVENTS hipEvent_t handles owned by the caller; the handles are
- * copied, and every later cts_apply / cts_apply_uncompressed call records
- * them on its stream at the stage boundaries of the layer:
+ * CTS_N_STAGE_EVENTS hipEvent_t handles owned by the caller (a NULL entry is
+ * skipped); the handles are copied, and every later cts_apply /
+ * cts_apply_uncompressed call records them on its stream at the stage
+ * boundaries of the layer:
  *   [0] before the bucketing          [1] before the shrink V_k^T X
  *   [2] before the core product       [3] before the fused W X + U_k Z' GEMM
  *   [4] after the fused GEMM          [5] after the split-K reduction

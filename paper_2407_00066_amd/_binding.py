@@ -220,16 +220,17 @@ def validate_ids(adapter_id, cluster_of, n: int, K: int = 1) -> bool:
 
 
 def set_stage_events(events) -> None:
-    """Profiling aid: `events` is None (off) or N_STAGE_EVENTS torch.cuda.Event
-    objects (enable_timing=True) recorded at the layer's stage boundaries by
-    every later apply call (see cts_set_stage_events in include/cts.h)."""
+    """Profiling aid: `events` is None (off) or N_STAGE_EVENTS entries, each a
+    torch.cuda.Event (enable_timing=True) or None (not recorded), recorded at
+    the layer's stage boundaries by every later apply call (see
+    cts_set_stage_events in include/cts.h)."""
     if events is None:
         _check(lib().cts_set_stage_events(None), "cts_set_stage_events")
         return
     if len(events) != N_STAGE_EVENTS:
         raise ValueError("need %d events" % N_STAGE_EVENTS)
     for e in events:
-        if e.cuda_event == 0:       # torch creates the HIP event at its first record
+        if e is not None and e.cuda_event == 0:   # torch creates the HIP event at its first record
             e.record()
-    arr = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.cuda_event for e in events])
+    arr = (ctypes.c_void_p * N_STAGE_EVENTS)(*[e.cuda_event if e is not None else None for e in events])
     _check(lib().cts_set_stage_events(arr), "cts_set_stage_events")
