@@ -196,10 +196,14 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
 
   hipError_t e = mark(0, stream);
   if (e != hipSuccess) return CTS_ERR_HIP;
-  e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
-                                  pl.nseg, perm, offs, sseg, said, items, n_items, ctiles,
-                                  n_ctiles, stream);
-  if (e != hipSuccess || mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
+  // small bf16 batches are bucketed inside the shrink kernel (one launch less)
+  const bool fuse_sort = T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
+  if (!fuse_sort) {
+    e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
+                         pl.nseg, perm, offs, sseg, said, items, n_items, ctiles, n_ctiles, stream);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+  }
+  if (mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams g{};
   g.M = rank; g.N = T;
@@ -212,6 +216,15 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = pl.shrink_split; g.part = zpart;
   g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  if (fuse_sort) {
+    g.tile_start = nullptr; g.n_tiles = nullptr;
+    g.fs_adapter = adapter_id; g.fs_cluster = compressed ? cluster_of : nullptr;
+    g.fs_n = p->n_adapters; g.fs_K = pl.nseg;
+    int bits_n = 0;
+    while ((1 << bits_n) < p->n_adapters) ++bits_n;
+    g.fs_bits_n = bits_n;
+    g.fs_perm = perm; g.fs_seg = sseg; g.fs_aid = said; g.fs_items = items; g.fs_nitems = n_items;
+  }
   e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
   if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 

@@ -41,6 +41,9 @@ inline int max_sigma_items(int T, int n) {
 // Token columns of one shrink tile: a run of one cluster inside a kSegTile
 // window of sorted positions.
 constexpr int kSegTile = 64;
+// Batches of at most this many tokens are bucketed inside the shrink kernel
+// (no separate sort launch).
+constexpr int kFuseSortMaxT = 2 * 64;
 inline int max_seg_tiles(int T, int nseg) {
   return (T + kSegTile - 1) / kSegTile + (nseg < T ? nseg : T);
 }
@@ -82,6 +85,15 @@ struct GemmParams {
   // [tile_start[t], tile_start[t+1]) (at most the tile width); n_tiles[0]
   // tiles exist and the grid is sized for max_tiles (the rest exit at once)
   const int32_t* tile_start; const int32_t* n_tiles; int max_tiles;
+  // optional bucketing inside the kernel (token-tile mode, N <= kFuseSortMaxT;
+  // fs_adapter != null): every workgroup sorts the N tokens by (cluster,
+  // adapter, token) in LDS and takes its tile, perm and segments from there;
+  // workgroup 0 also writes perm, sorted_seg, sorted_aid and the core-product
+  // items exactly as launch_sort would (ids clamped the same way).  perm,
+  // sorted_seg, tile_start and n_tiles are then unused.
+  const int32_t* fs_adapter; const int32_t* fs_cluster;   // fs_cluster null: key = adapter
+  int fs_n, fs_K, fs_bits_n;
+  int32_t* fs_perm; int32_t* fs_seg; int32_t* fs_aid; int32_t* fs_items; int32_t* fs_nitems;
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide

@@ -493,7 +493,8 @@ struct DmaCfg {
 // (tile_of_block), so the 8 workgroups on one column tile each take every
 // 8th token row; the WSPL workgroups on one row tile (4 with 256 tiles of
 // 256x256) each take every WSPL-th weight row.
-template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT, int PFD = 0, int WSPL = 1>
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT, int PFD = 0, int WSPL = 1,
+          int FSORT = 0>
 __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const GemmParams p) {
   using C = DmaCfg<BM, BN, BK, WM, WN, MB, P, DIRECT>;
   static_assert(PFD == 0 || P <= 3, "prefetch wait counts cover rings of two or three stages");
@@ -509,19 +510,88 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __shared__ int32_t run_start[BN + 1];
   __shared__ int32_t wave_runs[C::NW];
   __shared__ uint32_t pf_sink[PFD > 0 ? 64 : 1];
+  constexpr int FS = FSORT ? kFuseSortMaxT : 1;
+  __shared__ uint32_t fs_raw[FS], fs_key[FS];                // keys in token order, sorted
+  __shared__ int32_t fs_perm[FS], fs_tile[FS + 1];
+  __shared__ int32_t fs_cnt[2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  // FSORT: bucketing of the (at most kFuseSortMaxT) tokens in LDS.  The key
+  // is cluster << bits_n | adapter (the adapter alone without a cluster
+  // map); the rank of token t is the number of smaller keys plus equal keys
+  // of earlier tokens, the stable order of the separate sort.
+  const int fs_cshift = p.fs_cluster ? p.fs_bits_n : 0;
+  if (FSORT) {
+    static_assert(!FSORT || (C::NT >= kFuseSortMaxT && BN >= 64), "one token per thread; 64-token tiles");
+    const int T = p.N;
+    if (tid < T) {
+      int a = p.fs_adapter[tid];
+      a = a < 0 ? 0 : (a >= p.fs_n ? p.fs_n - 1 : a);
+      uint32_t key = static_cast<uint32_t>(a);
+      if (p.fs_cluster) {
+        int c = p.fs_cluster[a];
+        c = c < 0 ? 0 : (c >= p.fs_K ? p.fs_K - 1 : c);
+        key |= static_cast<uint32_t>(c) << p.fs_bits_n;
+      }
+      fs_raw[tid] = key;
+    }
+    __syncthreads();
+    if (tid < T) {
+      const uint32_t key = fs_raw[tid];
+      int rank = 0;
+      for (int j = 0; j < T; ++j) {
+        const uint32_t kj = fs_raw[j];
+        rank += (kj < key || (kj == key && j < tid)) ? 1 : 0;
+      }
+      fs_perm[rank] = tid;
+      fs_key[rank] = key;
+    }
+    __syncthreads();
+    // wave 0: tile starts (a multiple of kSegTile or a new cluster) and, for
+    // workgroup 0, core-product item starts (a multiple of kSigmaChunk or a
+    // new key)
+    if (wave == 0) {
+      int nt_ = 0, ni_ = 0;
+      for (int base = 0; base < T; base += 64) {
+        const int j = base + lane;
+        const bool valid = j < T;
+        const uint32_t k = valid ? fs_key[j] : 0u;
+        const uint32_t kp = (valid && j > 0) ? fs_key[j - 1] : 0u;
+        const bool st = valid && (j % kSegTile == 0 || (k >> fs_cshift) != (kp >> fs_cshift));
+        const bool si = valid && (j % kSigmaChunk == 0 || k != kp);
+        const uint64_t bt = __ballot(st), bi = __ballot(si);
+        if (st) fs_tile[nt_ + __popcll(bt & lt_mask)] = j;
+        if (si && blockIdx.x == 0) p.fs_items[ni_ + __popcll(bi & lt_mask)] = j;
+        nt_ += __popcll(bt);
+        ni_ += __popcll(bi);
+      }
+      if (lane == 0) {
+        fs_tile[nt_] = T;
+        fs_cnt[0] = nt_;
+        if (blockIdx.x == 0) { p.fs_items[ni_] = T; p.fs_nitems[0] = ni_; }
+      }
+    }
+    if (blockIdx.x == 0 && tid < T) {
+      const uint32_t k = fs_key[tid];
+      p.fs_perm[tid] = fs_perm[tid];
+      p.fs_seg[tid] = static_cast<int32_t>(k >> fs_cshift);
+      p.fs_aid[tid] = static_cast<int32_t>(k & ((1u << p.fs_bits_n) - 1u));
+    }
+    __syncthreads();
+  }
   // Token-tile mode (explicit tiles, each inside one segment): the tile's
   // segment operand becomes the dense operand (A = A1 of that segment, B = B1),
   // so the whole k loop takes the dense load path and there is no second phase.
-  const bool tlist = p.tile_start != nullptr;
+  const bool tlist = FSORT || p.tile_start != nullptr;
   int mt, nt, ks;
   tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks);
   int j0, jn;
   if (tlist) {
-    if (nt >= p.n_tiles[0]) return;                         // whole workgroup, before any barrier
-    j0 = p.tile_start[nt];
-    jn = p.tile_start[nt + 1] - j0;
+    // whole workgroup, after every barrier above
+    if (nt >= (FSORT ? fs_cnt[0] : p.n_tiles[0])) return;
+    j0 = FSORT ? fs_tile[nt] : p.tile_start[nt];
+    jn = (FSORT ? fs_tile[nt + 1] : p.tile_start[nt + 1]) - j0;
   } else {
     j0 = nt * BN;
     jn = min(BN, p.N - j0);
@@ -533,7 +603,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   int K0 = p.K0, K1 = p.K1;
   bool b0_gather = true;
   if (tlist) {
-    const int seg = p.sorted_seg[j0];
+    const int seg = FSORT ? static_cast<int>(fs_key[j0] >> fs_cshift) : p.sorted_seg[j0];
     A0 = static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes;
     a0_bytes = p.a1_seg_bytes; lda0 = p.lda1; K0 = p.K1;
     B0 = p.B1; b0_bytes = p.b1_bytes; ldb0 = p.ldb1; b0_gather = p.b1_gather != 0;
@@ -546,8 +616,13 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // ---- token columns of this tile (loads only; stored to LDS below) -------
   int v_perm = 0, v_seg = 0;
   if (tid < jn) {
-    v_perm = p.perm[j0 + tid];
-    v_seg = p.sorted_seg ? p.sorted_seg[j0 + tid] : 0;
+    if (FSORT) {
+      v_perm = fs_perm[j0 + tid];
+      v_seg = static_cast<int>(fs_key[j0 + tid] >> fs_cshift);
+    } else {
+      v_perm = p.perm[j0 + tid];
+      v_seg = p.sorted_seg ? p.sorted_seg[j0 + tid] : 0;
+    }
   }
 
   // ---- load mapping: this lane's row and chunk in each 1 KB load ------------
@@ -986,11 +1061,11 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0, int PFD = 0,
-          int WSPL = 1>
+          int WSPL = 1, int FSORT = 0>
 hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
-  const int gn = p.tile_start ? p.max_tiles : (p.N + BN - 1) / BN;
+  const int gn = (p.tile_start || FSORT) ? p.max_tiles : (p.N + BN - 1) / BN;
   dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL>), grid,
+  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT>), grid,
                      dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
 }
@@ -1035,13 +1110,18 @@ hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStre
   if (p.tile_start &&
       !(tile == Tile::Decode || tile == Tile::Shrink || tile == Tile::Small || tile == Tile::F32))
     return hipErrorInvalidValue;
+  // in-kernel bucketing exists in the bf16 shrink tile only
+  if (p.fs_adapter && (in_dtype == 0 || tile != Tile::Shrink || p.N > kFuseSortMaxT || p.tile_start))
+    return hipErrorInvalidValue;
   if (in_dtype == 0) return launch_cfg<float, 64, 64, 32, 2, 2, 1, 2, 16>(p, stream);
   switch (tile) {
     case Tile::Large: return launch_dma<256, 256, 64, 4, 2, 16, 2, 1, 6, 4>(p, stream);
     case Tile::Wide: return launch_dma<256, 128, 64, 4, 2, 16, 3, 1>(p, stream);
     case Tile::Narrow: return launch_dma<128, 64, 128, 4, 1, 16, 3, 1>(p, stream);
     case Tile::Decode: return launch_dma<64, 64, 128, 2, 2, 16, 4, 1>(p, stream);
-    case Tile::Shrink: return launch_dma<64, 64, 64, 2, 2, 16, 3, 1>(p, stream);
+    case Tile::Shrink:
+      if (p.fs_adapter) return launch_dma<64, 64, 64, 2, 2, 16, 3, 1, 0, 1, 1>(p, stream);
+      return launch_dma<64, 64, 64, 2, 2, 16, 3, 1>(p, stream);
     case Tile::Mid: return launch_dma<128, 128, 64, 4, 2, 16, 4, 1>(p, stream);
     default: return launch_cfg<bf16_t, 64, 64, 64, 2, 2, 2, 2, 32>(p, stream);
   }
