@@ -17,8 +17,9 @@ namespace cts {
 namespace {
 
 constexpr int kSigThreads = 256;
-constexpr int kSigMaxR = 128;
-constexpr int kSigLd = kSigMaxR + 4;      // LDS row stride (floats): 16-byte aligned, conflict-free
+// MAXR: the largest rank a kernel instance takes (64 or 128).  LDS rows are
+// MAXR + 4 floats: 16-byte aligned, and lanes reading one column of 16 rows
+// (4 consecutive k each) land on distinct banks.
 
 template <typename TI> struct Vec16;
 template <> struct Vec16<float> {          // 4 floats per 16 bytes
@@ -44,7 +45,7 @@ template <typename TI> __device__ __forceinline__ void st(TI* p, int64_t i, floa
 template <> __device__ __forceinline__ void st<float>(float* p, int64_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st<bf16_t>(bf16_t* p, int64_t i, float v) { p[i].bits = f32_to_bf16(v); }
 
-template <typename TI>
+template <typename TI, int MAXR>
 __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restrict__ zpart, int S,
                                                             int T, int r,
                                                             const int32_t* __restrict__ sorted_aid,
@@ -52,8 +53,9 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             const int32_t* __restrict__ n_items,
                                                             const TI* __restrict__ Sigma,
                                                             TI* __restrict__ zp) {
+  constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
-  __shared__ __attribute__((aligned(16))) float sig[kSigMaxR * kSigLd];
+  __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
 
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
@@ -68,7 +70,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     int a = sorted_aid[lo];
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
     constexpr int V = Vec16<TI>::N;
-    constexpr int PER = (kSigMaxR * kSigMaxR / V + kSigThreads - 1) / kSigThreads;
+    constexpr int PER = (MAXR * MAXR / V + kSigThreads - 1) / kSigThreads;
     const uint4* sa = reinterpret_cast<const uint4*>(Sigma + static_cast<int64_t>(a) * r * r);
     const int nv = r * r / V;
     uint4 raw[PER];
@@ -91,18 +93,18 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     }
   }
   // z = sum over the shrink's k-splits in fixed order; 4 consecutive values
-  // per thread, 8 splits' loads in flight at a time
+  // per thread, 16 splits' loads in flight at a time
   const int64_t split_stride = static_cast<int64_t>(T) * r;
   const float* zbase = zpart + static_cast<int64_t>(lo) * r;
   for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     int q = 0;
-    for (; q + 8 <= S; q += 8) {
-      f32x4 v[8];
+    for (; q + 16 <= S; q += 16) {
+      f32x4 v[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
+      for (int u = 0; u < 16; ++u) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc += v[u];
+      for (int u = 0; u < 16; ++u) acc += v[u];
     }
     for (; q < S; ++q) acc += *reinterpret_cast<const f32x4*>(zbase + q * split_stride + e4);
     const int i = e4 / r, c = e4 % r;
@@ -180,12 +182,21 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream) {
   dim3 grid(max_items);
-  if (in_dtype == 0)
-    hipLaunchKernelGGL(sigma_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+  if (r > 128) return hipErrorInvalidValue;
+  if (in_dtype == 0 && r <= 64)
+    hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
                        static_cast<float*>(zp));
+  else if (in_dtype == 0)
+    hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                       sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
+                       static_cast<float*>(zp));
+  else if (r <= 64)
+    hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                       sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
+                       static_cast<bf16_t*>(zp));
   else
-    hipLaunchKernelGGL(sigma_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+    hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
                        static_cast<bf16_t*>(zp));
   return hipGetLastError();
