@@ -98,15 +98,15 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const float* zbase = zpart + static_cast<int64_t>(lo) * r;
   for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    int q = 0;
-    for (; q + 16 <= S; q += 16) {
+    for (int q = 0; q < S; q += 16) {
       f32x4 v[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
+      for (int u = 0; u < 16; ++u)
+        if (q + u < S) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
 #pragma unroll
-      for (int u = 0; u < 16; ++u) acc += v[u];
+      for (int u = 0; u < 16; ++u)
+        if (q + u < S) acc += v[u];
     }
-    for (; q < S; ++q) acc += *reinterpret_cast<const f32x4*>(zbase + q * split_stride + e4);
     const int i = e4 / r, c = e4 % r;
     *reinterpret_cast<f32x4*>(z + i * kSigLd + c) = acc;
   }

@@ -29,6 +29,8 @@ constexpr int kWaves = kSortThreads / 64;
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int kMaxCpw = kSortMaxT / 64 / kWaves;   // chunks per wave, at most
+// cluster maps up to this size are staged in LDS (in the radix histogram)
+constexpr int kLdsMap = kWaves * kRadix;
 // run path: at most this many runs (its all-pairs ranking costs R^2 / 1024
 // compares per thread; past a few hundred runs the radix passes are cheaper)
 constexpr int kMaxRuns = 256;
@@ -101,17 +103,38 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   // the key is the adapter, which is also its cluster
   const int cshift = cluster_of ? bits_n : 0;
 
-  for (int t = tid; t < T; t += kSortThreads) {
-    int a = adapter_id[t];
-    a = a < 0 ? 0 : (a >= n ? n - 1 : a);
-    uint32_t key = static_cast<uint32_t>(a);
-    if (cluster_of) {
+  // A cluster map of at most kLdsMap entries is staged in LDS (its loads go
+  // out with the adapter ids', one round trip instead of a dependent second
+  // one); the run arrays' space is free until the run path below.
+  const bool map_lds = cluster_of && n <= kLdsMap;
+  int32_t* const cmap = reinterpret_cast<int32_t*>(hist);
+  if (map_lds)
+    for (int i = tid; i < n; i += kSortThreads) cmap[i] = cluster_of[i];
+  if (cluster_of && !map_lds) {
+    for (int t = tid; t < T; t += kSortThreads) {
+      int a = adapter_id[t];
+      a = a < 0 ? 0 : (a >= n ? n - 1 : a);
       int c = cluster_of[a];
       c = c < 0 ? 0 : (c >= K ? K - 1 : c);
-      key |= static_cast<uint32_t>(c) << bits_n;
+      kbuf[0][t] = static_cast<uint32_t>(a) | (static_cast<uint32_t>(c) << bits_n);
+      vbuf[0][t] = static_cast<uint16_t>(t);
     }
-    kbuf[0][t] = key;
-    vbuf[0][t] = static_cast<uint16_t>(t);
+  } else {
+    for (int t = tid; t < T; t += kSortThreads) {
+      int a = adapter_id[t];
+      a = a < 0 ? 0 : (a >= n ? n - 1 : a);
+      kbuf[0][t] = static_cast<uint32_t>(a);
+      vbuf[0][t] = static_cast<uint16_t>(t);
+    }
+    if (map_lds) {
+      __syncthreads();
+      for (int t = tid; t < T; t += kSortThreads) {
+        const uint32_t a = kbuf[0][t];
+        int c = cmap[a];
+        c = c < 0 ? 0 : (c >= K ? K - 1 : c);
+        kbuf[0][t] = a | (static_cast<uint32_t>(c) << bits_n);
+      }
+    }
   }
 
   const int passes = (bits_n + bits_k + kRadixBits - 1) / kRadixBits;
