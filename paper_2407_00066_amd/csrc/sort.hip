@@ -25,16 +25,25 @@
 namespace cts {
 namespace {
 
-constexpr int kWaves = kSortThreads / 64;
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
-constexpr int kMaxCpw = kSortMaxT / 64 / kWaves;   // chunks per wave, at most
-// cluster maps up to this size are staged in LDS (in the radix histogram)
-constexpr int kLdsMap = kWaves * kRadix;
 // run path: at most this many runs (its all-pairs ranking costs R^2 / 1024
 // compares per thread; past a few hundred runs the radix passes are cheaper)
 constexpr int kMaxRuns = 256;
-static_assert(kWaves * kRadix == 4 * kSortThreads, "scan: four counters per thread");
+
+// One workgroup of NT threads sorts at most MAXT tokens: 1024 threads for up
+// to kSortMaxT, 256 threads (cheaper barriers) for up to 2048.
+template <int NT> struct SortCfg {
+  static constexpr int W = NT / 64;                          // waves
+  static constexpr int MAXT = NT == 1024 ? kSortMaxT : 2048;
+  static constexpr int MC = MAXT / 64 / W;                   // chunks per wave, at most
+  static constexpr int TPD = NT / kRadix;                    // scan threads per digit
+  // cluster maps up to this size are staged in LDS (in the radix histogram)
+  static constexpr int LDS_MAP = W * kRadix;
+  static_assert(W * kRadix == 4 * NT, "scan: four counters per thread");
+  static_assert(kMaxRuns <= NT, "run path: one run per thread");
+};
+constexpr int kSortSmallT = 2048;
 
 // Lanes of this wave whose digit equals this lane's (only lanes in `valid`).
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t valid, int lane) {
@@ -60,7 +69,8 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t valid, int 
 }
 
 // Exclusive scan of one value per thread over the workgroup; also returns the
-// total.  Uses wsum[kWaves]; contains two barriers.
+// total.  Uses wsum[NW]; contains two barriers.
+template <int NW>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, int lane, int wave,
                                                          uint32_t* total) {
   uint32_t x = v;
@@ -73,7 +83,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   __syncthreads();
   uint32_t before = 0, all = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     const uint32_t s = wsum[w];
     before += (w < wave) ? s : 0u;
     all += s;
@@ -83,14 +93,17 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return before + x - v;
 }
 
-__global__ __launch_bounds__(kSortThreads) void sort_kernel(
+template <int NT>
+__global__ __launch_bounds__(NT) void sort_kernel(
     const int32_t* __restrict__ adapter_id, const int32_t* __restrict__ cluster_of, int T, int n,
     int K, int bits_n, int bits_k, int32_t* __restrict__ perm, int32_t* __restrict__ offs,
     int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid,
     int32_t* __restrict__ items, int32_t* __restrict__ n_items, int32_t* __restrict__ ctiles,
     int32_t* __restrict__ n_ctiles) {
-  __shared__ uint32_t kbuf[2][kSortMaxT];
-  __shared__ uint16_t vbuf[2][kSortMaxT];
+  using C = SortCfg<NT>;
+  constexpr int kWaves = C::W;
+  __shared__ uint32_t kbuf[2][C::MAXT];
+  __shared__ uint16_t vbuf[2][C::MAXT];
   __shared__ uint32_t hist[kWaves * kRadix];   // [wave][digit]
   __shared__ uint32_t wsum[kWaves];
   // run keys padded with 16 entries that rank below nothing (all ones)
@@ -103,15 +116,15 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   // the key is the adapter, which is also its cluster
   const int cshift = cluster_of ? bits_n : 0;
 
-  // A cluster map of at most kLdsMap entries is staged in LDS (its loads go
+  // A cluster map of at most C::LDS_MAP entries is staged in LDS (its loads go
   // out with the adapter ids', one round trip instead of a dependent second
   // one); the run arrays' space is free until the run path below.
-  const bool map_lds = cluster_of && n <= kLdsMap;
+  const bool map_lds = cluster_of && n <= C::LDS_MAP;
   int32_t* const cmap = reinterpret_cast<int32_t*>(hist);
   if (map_lds)
-    for (int i = tid; i < n; i += kSortThreads) cmap[i] = cluster_of[i];
+    for (int i = tid; i < n; i += NT) cmap[i] = cluster_of[i];
   if (cluster_of && !map_lds) {
-    for (int t = tid; t < T; t += kSortThreads) {
+    for (int t = tid; t < T; t += NT) {
       int a = adapter_id[t];
       a = a < 0 ? 0 : (a >= n ? n - 1 : a);
       int c = cluster_of[a];
@@ -120,7 +133,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
       vbuf[0][t] = static_cast<uint16_t>(t);
     }
   } else {
-    for (int t = tid; t < T; t += kSortThreads) {
+    for (int t = tid; t < T; t += NT) {
       int a = adapter_id[t];
       a = a < 0 ? 0 : (a >= n ? n - 1 : a);
       kbuf[0][t] = static_cast<uint32_t>(a);
@@ -128,7 +141,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
     }
     if (map_lds) {
       __syncthreads();
-      for (int t = tid; t < T; t += kSortThreads) {
+      for (int t = tid; t < T; t += NT) {
         const uint32_t a = kbuf[0][t];
         int c = cmap[a];
         c = c < 0 ? 0 : (c >= K ? K - 1 : c);
@@ -154,7 +167,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   // offset plus its place in the run: the same stable order as the radix
   // passes, which run otherwise.
   {
-    const int ipt = (T + kSortThreads - 1) / kSortThreads;
+    const int ipt = (T + NT - 1) / NT;
     const int j0 = tid * ipt, j1 = min(T, j0 + ipt);
     uint32_t cnt = 0;
     uint32_t kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
@@ -164,7 +177,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
       kp = k;
     }
     uint32_t R;
-    const uint32_t base = block_exclusive_scan(cnt, wsum, lane, wave, &R);
+    const uint32_t base = block_exclusive_scan<kWaves>(cnt, wsum, lane, wave, &R);
     if (R <= static_cast<uint32_t>(kMaxRuns)) {                  // uniform
       uint32_t r = base;
       kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
@@ -204,7 +217,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
         len = run_start[rr + 1] - run_start[rr];
       }
       uint32_t tot;
-      const uint32_t off = block_exclusive_scan(len, wsum, lane, wave, &tot);
+      const uint32_t off = block_exclusive_scan<kWaves>(len, wsum, lane, wave, &tot);
       if (static_cast<uint32_t>(tid) < R) run_off[run_order[tid]] = off;
       __syncthreads();
       int rid = static_cast<int>(base) - 1;                      // run holding j0 - 1
@@ -226,14 +239,14 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   for (int p = 0; radix && p < passes; ++p) {
     const int shift = p * kRadixBits;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) hist[tid + i * kSortThreads] = 0;
+    for (int i = 0; i < 4; ++i) hist[tid + i * NT] = 0;
     __syncthreads();
 
     // count walk: offset of each token inside its (wave, digit) group
-    uint32_t kr[kMaxCpw], dr[kMaxCpw], pos[kMaxCpw];
-    uint16_t vr[kMaxCpw];
+    uint32_t kr[C::MC], dr[C::MC], pos[C::MC];
+    uint16_t vr[C::MC];
 #pragma unroll
-    for (int c = 0; c < kMaxCpw; ++c) {
+    for (int c = 0; c < C::MC; ++c) {
       kr[c] = 0; dr[c] = 0; pos[c] = 0; vr[c] = 0;
       if (c < cpw) {
         const int idx = seg_lo + c * 64 + lane;
@@ -252,15 +265,15 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
     }
     __syncthreads();
 
-    // exclusive scan in (digit, wave) order: thread owns digit tid/4, waves
-    // 4*(tid%4) .. +3
+    // exclusive scan in (digit, wave) order: thread owns digit tid/TPD and
+    // four consecutive waves of it
     {
-      const int d = tid >> 2, w0 = (tid & 3) * 4;
+      const int d = tid / C::TPD, w0 = (tid % C::TPD) * 4;
       uint32_t x[4], s = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) { x[j] = hist[(w0 + j) * kRadix + d]; s += x[j]; }
       uint32_t total;
-      uint32_t base = block_exclusive_scan(s, wsum, lane, wave, &total);
+      uint32_t base = block_exclusive_scan<kWaves>(s, wsum, lane, wave, &total);
 #pragma unroll
       for (int j = 0; j < 4; ++j) { hist[(w0 + j) * kRadix + d] = base; base += x[j]; }
     }
@@ -268,7 +281,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
 
     // scatter walk
 #pragma unroll
-    for (int c = 0; c < kMaxCpw; ++c) {
+    for (int c = 0; c < C::MC; ++c) {
       if (c < cpw) {
         const int idx = seg_lo + c * 64 + lane;
         if (idx < seg_hi) {
@@ -284,7 +297,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
 
   // outputs (coalesced)
   const uint32_t amask = (1u << bits_n) - 1u;
-  for (int j = tid; j < T; j += kSortThreads) {
+  for (int j = tid; j < T; j += NT) {
     const uint32_t k = kbuf[in][j];
     perm[j] = static_cast<int32_t>(vbuf[in][j]);
     if (sorted_seg) sorted_seg[j] = static_cast<int32_t>(k >> cshift);
@@ -295,7 +308,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   // [tid*ipt, tid*ipt + ipt); counts packed as items | tiles << 16 (each
   // total is at most T + 1 <= 8193)
   if (items || ctiles) {
-    const int ipt = (T + kSortThreads - 1) / kSortThreads;
+    const int ipt = (T + NT - 1) / NT;
     const int j0 = tid * ipt, j1 = min(T, j0 + ipt);
     uint32_t cnt = 0;
     uint32_t kp = (j0 > 0 && j0 < T) ? kbuf[in][j0 - 1] : 0u;
@@ -307,7 +320,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
       kp = k;
     }
     uint32_t total;
-    uint32_t base = block_exclusive_scan(cnt, wsum, lane, wave, &total);
+    uint32_t base = block_exclusive_scan<kWaves>(cnt, wsum, lane, wave, &total);
     uint32_t bi = base & 0xffffu, bc = base >> 16;
     kp = (j0 > 0 && j0 < T) ? kbuf[in][j0 - 1] : 0u;
     for (int j = j0; j < j1; ++j) {
@@ -327,7 +340,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(
   }
 
   // cluster offsets: first sorted position whose cluster is >= k
-  for (int k = tid; k <= K; k += kSortThreads) {
+  for (int k = tid; k <= K; k += NT) {
     int lo = 0, hi = T;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
@@ -351,9 +364,14 @@ hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int
                        hipStream_t stream) {
   const int bits_n = ceil_log2(n);
   const int bits_k = cluster_of ? ceil_log2(K) : 0;  // key is the adapter alone when K == n
-  hipLaunchKernelGGL(sort_kernel, dim3(1), dim3(kSortThreads), 0, stream, adapter_id, cluster_of,
-                     T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
-                     ctiles, n_ctiles);
+  if (T <= kSortSmallT)
+    hipLaunchKernelGGL(sort_kernel<256>, dim3(1), dim3(256), 0, stream, adapter_id, cluster_of,
+                       T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
+                       ctiles, n_ctiles);
+  else
+    hipLaunchKernelGGL(sort_kernel<1024>, dim3(1), dim3(1024), 0, stream, adapter_id, cluster_of,
+                       T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
+                       ctiles, n_ctiles);
   return hipGetLastError();
 }
 
