@@ -21,11 +21,14 @@
  *     Delta_i = U_k Sigma_i V_k^T            (formed explicitly, d_out x d_in)
  *     y_t     = (W + Delta_i) x_t
  * and, for the uncompressed comparison path, Delta_i = B_i A_i.
+ * Sec. 3.1, the diagonal variant (eq. JD-Diag): Sigma_i is diagonal, given as
+ * its r diagonal entries sigma_i, and Delta_i = U_k diag(sigma_i) V_k^T.
  *
  * Array layouts (row-major, all host memory, all double):
  *   x      [T][d_in]            W      [d_out][d_in]
  *   U      [K][d_out][r]        Vt     [K][r][d_in]   (V_k^T, same as a LoRA A)
  *   Sigma  [n][r][r]            (applied as z' = Sigma_i z)
+ *   sigma  [n][r]               (diagonal variant: z'_q = sigma_i[q] z_q)
  *   A      [n][r_l][d_in]       B      [n][d_out][r_l]
  *   y      [n_tok][d_out]       rows follow the order of `tokens`
  *
@@ -179,6 +182,47 @@ int cts_oracle_apply(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
             const int64_t k = cluster_of[a];
             /* M = Sigma_a V_k^T  (r x d_in) */
             matmul(Sigma + a * r * r, Vt + k * r * d_in, M, r, r, d_in);
+            /* D = U_k M  (d_out x d_in) */
+            matmul(U + k * d_out * r, M, D, d_out, r, d_in);
+            cur = a;
+        }
+        apply_rows(W, D, x + t * d_in, y + s * d_out, d_out, d_in);
+    }
+    free(M); free(D); free(order);
+    return 0;
+}
+
+/* Diagonal variant (Sec. 3.1, eq. JD-Diag): Delta_i = U_k diag(sigma_i) V_k^T,
+ * with diag(sigma_i) V_k^T formed as V_k^T with row q scaled by sigma_i[q]. */
+int cts_oracle_apply_diag(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                          int64_t n, int64_t K,
+                          const double* x, const int32_t* adapter_id,
+                          const int32_t* cluster_of, const double* W,
+                          const double* U, const double* Vt, const double* sigma,
+                          const int64_t* tokens, int64_t n_tok, double* y) {
+    if (T < 0 || d_in < 1 || d_out < 1 || r < 1 || n < 1 || K < 1 || n_tok < 0) return -1;
+    int rc = check_tokens(adapter_id, T, tokens, n_tok, n);
+    if (rc) return rc;
+    for (int64_t i = 0; i < n; ++i)
+        if (cluster_of[i] < 0 || cluster_of[i] >= K) return -2;
+    if (n_tok == 0) return 0;
+
+    double* M = (double*)malloc(sizeof(double) * (size_t)(r * d_in));
+    double* D = (double*)malloc(sizeof(double) * (size_t)(d_out * d_in));
+    int64_t* order = visit_order(adapter_id, tokens, n_tok, n);
+    if (!M || !D || !order) { free(M); free(D); free(order); return -1; }
+
+    int64_t cur = -1;
+    for (int64_t v = 0; v < n_tok; ++v) {
+        const int64_t s = order[v];
+        const int64_t t = tokens[s];
+        const int64_t a = adapter_id[t];
+        if (a != cur) {
+            const int64_t k = cluster_of[a];
+            /* M = diag(sigma_a) V_k^T  (r x d_in) */
+            for (int64_t q = 0; q < r; ++q)
+                for (int64_t c = 0; c < d_in; ++c)
+                    M[q * d_in + c] = sigma[a * r + q] * Vt[k * r * d_in + q * d_in + c];
             /* D = U_k M  (d_out x d_in) */
             matmul(U + k * d_out * r, M, D, d_out, r, d_in);
             cur = a;

@@ -13,6 +13,9 @@ Conventions
   ``U[K][d_out][r]``, ``Vt[K][r][d_in]`` (= V_k transposed), ``Sigma[n][r][r]``,
   ``A[n][r_l][d_in]``, ``B[n][d_out][r_l]``.
 
+``apply_diag`` is the diagonal-Sigma variant of Sec. 3.1 (eq. JD-Diag) with
+``sigma[n][r]`` holding the diagonals.
+
 Besides the apply/sort oracles this module holds ``exact_compress``: the
 lossless JD-Full construction of Proposition 1 with Sigma_i taken from the
 stationarity condition of App. A.1 (Sigma_i = U^T B_i A_i V).  It builds the
@@ -58,6 +61,8 @@ def _load():
         lib.cts_oracle_apply.argtypes = [i64, i64, i64, i64, i64, i64, f64p, i32p, i32p,
                                          f64p, f64p, f64p, f64p, i64p, i64, f64p]
         lib.cts_oracle_apply.restype = ctypes.c_int
+        lib.cts_oracle_apply_diag.argtypes = lib.cts_oracle_apply.argtypes
+        lib.cts_oracle_apply_diag.restype = ctypes.c_int
         lib.cts_oracle_apply_uncompressed.argtypes = [i64, i64, i64, i64, i64, f64p, i32p,
                                                       f64p, f64p, f64p, i64p, i64, f64p]
         lib.cts_oracle_apply_uncompressed.restype = ctypes.c_int
@@ -133,6 +138,32 @@ def apply(x, adapter_id, cluster_of, W, U, Vt, Sigma, tokens=None, timing=None):
         timing["s"] = time.perf_counter() - t0
     if rc != 0:
         raise ValueError("oracle apply rejected its input (code %d)" % rc)
+    return y[:len(tok)]
+
+
+def apply_diag(x, adapter_id, cluster_of, W, U, Vt, sigma, tokens=None, timing=None):
+    """Diagonal variant (Sec. 3.1, eq. JD-Diag): y[s] = (W + U_k diag(sigma_i)
+    V_k^T) x_t for t = tokens[s], sigma [n][r] holding the diagonals; float64
+    [len(tokens)][d_out]."""
+    x64, W64, U64, V64, s64 = (np.ascontiguousarray(to_f64(a)) for a in (x, W, U, Vt, sigma))
+    aid, cof = _ids(adapter_id), _ids(cluster_of)
+    T, d_in = x64.shape
+    d_out = W64.shape[0]
+    K, _, r = U64.shape
+    n = s64.shape[0]
+    assert W64.shape == (d_out, d_in) and V64.shape == (K, r, d_in) and s64.shape == (n, r)
+    assert aid.shape == (T,) and cof.shape == (n,)
+    tok = _tokens(tokens, T)
+    y = np.zeros((max(len(tok), 1), d_out), np.float64)
+    f = ctypes.c_double
+    t0 = time.perf_counter()
+    rc = _load().cts_oracle_apply_diag(T, d_in, d_out, r, n, K, _c(x64, f), _c(aid, ctypes.c_int32),
+                                       _c(cof, ctypes.c_int32), _c(W64, f), _c(U64, f), _c(V64, f),
+                                       _c(s64, f), _c(tok, ctypes.c_int64), len(tok), _c(y, f))
+    if timing is not None:
+        timing["s"] = time.perf_counter() - t0
+    if rc != 0:
+        raise ValueError("oracle apply_diag rejected its input (code %d)" % rc)
     return y[:len(tok)]
 
 
