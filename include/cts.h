@@ -120,6 +120,17 @@ int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
               const void* Vt, const void* Sigma, void* y,
               void* workspace, size_t workspace_bytes, void* stream);
 
+/* Diagonal-Sigma variant (Sec. 3.1, eq. JD-Diag; App. F): overwrites y[t]
+ * with W x_t + U_k diag(sigma_i) V_k^T x_t.  Same arguments, layouts, limits,
+ * workspace (cts_workspace_size) and errors as cts_apply, except that `sigma`
+ * holds the diagonals only: sigma[n][r] in p->dtype (16-byte aligned), and
+ * the core product is the elementwise scale z'_q = sigma_i[q] z_q (fp32,
+ * rounded to the input type before the U_k product). */
+int cts_apply_diag(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                   const int32_t* cluster_of, const void* W, const void* U,
+                   const void* Vt, const void* sigma, void* y,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
 /* Uncompressed comparison path: overwrites y[t] with W x_t + B_i A_i x_t
  * (Sec. 3, first paragraph), i = adapter_id[t], rank p->r_lora. */
 int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,

@@ -22,8 +22,8 @@ CTS_F32, CTS_BF16 = 0, 1
 
 # every symbol include/cts.h declares
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
-            "cts_sort_by_cluster", "cts_apply", "cts_apply_uncompressed", "cts_validate_ids",
-            "cts_set_stage_events")
+            "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_uncompressed",
+            "cts_validate_ids", "cts_set_stage_events")
 N_STAGE_EVENTS = 6
 
 
@@ -62,6 +62,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_sort_by_cluster.restype = ctypes.c_int
                 L.cts_apply.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply.restype = ctypes.c_int
+                L.cts_apply_diag.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_apply_diag.restype = ctypes.c_int
                 L.cts_apply_uncompressed.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply_uncompressed.restype = ctypes.c_int
                 L.cts_validate_ids.argtypes = [pp, vp, vp, vp]
@@ -177,6 +179,36 @@ def apply(x, adapter_id, cluster_of, W, U, Vt, Sigma, out=None, out_dtype=None, 
     ws = _workspace(dev, nbytes, workspace)
     _check(lib().cts_apply(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                            _stream(dev)), "cts_apply")
+    return out
+
+
+def apply_diag(x, adapter_id, cluster_of, W, U, Vt, sigma, out=None, out_dtype=None, workspace=None):
+    """y = W x_t + U_k diag(sigma_i) V_k^T x_t per token, sigma [n][r] (see
+    cts_apply_diag in include/cts.h)."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    K, _, r = U.shape
+    n = sigma.shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=dt,
+                     out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(U, "U", dev, tdt, (K, d_out, r)),
+            _dev(Vt, "Vt", dev, tdt, (K, r, d_in)),
+            _dev(sigma, "sigma", dev, tdt, (n, r)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    nbytes = workspace_size(p, True)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_diag(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                _stream(dev)), "cts_apply_diag")
     return out
 
 

@@ -179,7 +179,7 @@ bool any_overlap(Range y, Range ws, const Range* in, int n_in) {
 int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void* x,
               const int32_t* adapter_id, const int32_t* cluster_of, const void* W,
               const void* Ubasis, const void* Vbasis, const void* Sigma, void* y, void* workspace,
-              hipStream_t stream) {
+              hipStream_t stream, bool sigma_diag = false) {
   char* ws = static_cast<char*>(workspace);
   int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
   int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
@@ -229,7 +229,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 
   e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
-                        pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream);
+                        pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag);
   if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
@@ -303,9 +303,12 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
   return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
 
-int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
-              const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
-              const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+int apply_compressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                     const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+                     const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream,
+                     bool sigma_diag) {
   Plan pl;
   const int rc = make_plan(p, true, &pl);
   if (rc != CTS_OK) return rc;
@@ -320,11 +323,28 @@ int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
   const size_t T = p->T, di = p->d_in, dout = p->d_out, r = p->r, n = p->n_adapters, K = p->n_clusters;
   const Range in[7] = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
                        {W, dout * di * e}, {U, K * dout * r * e}, {Vt, K * r * di * e},
-                       {Sigma, n * r * r * e}};
+                       {Sigma, n * (sigma_diag ? 1 : r) * r * e}};
   if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 7))
     return CTS_ERR_INVALID_ARG;
   return run_layer(p, pl, true, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
-                   static_cast<hipStream_t>(stream));
+                   static_cast<hipStream_t>(stream), sigma_diag);
+}
+
+}  // namespace
+
+int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
+              const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+              const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream) {
+  return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
+                          workspace_bytes, stream, false);
+}
+
+int cts_apply_diag(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                   const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+                   const void* sigma, void* y, void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, sigma, y, workspace,
+                          workspace_bytes, stream, true);
 }
 
 int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,

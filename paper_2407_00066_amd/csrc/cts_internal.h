@@ -107,11 +107,14 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK);
 
 // ------------------------------------------------------------- Sigma stage
 // zp[j][c] = sum_{c'} Sigma_{aid(j)}[c][c'] * (sum_s zpart[s][j][c'])  (Sigma may be null:
-// then zp = sum_s zpart).  Rounded to the input type.  One workgroup per item
-// of the sort (max_items workgroups are launched; the extra ones exit).
+// then zp = sum_s zpart).  With diag, Sigma is [n][r] (the diagonals) and
+// zp[j][c] = Sigma_{aid(j)}[c] * (sum_s zpart[s][j][c]).  Rounded to the input
+// type.  One workgroup per item of the sort (max_items workgroups are
+// launched; the extra ones exit).
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
-                        const void* Sigma, void* zp, int in_dtype, hipStream_t stream);
+                        const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
+                        bool diag = false);
 
 // y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,

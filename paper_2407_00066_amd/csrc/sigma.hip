@@ -45,6 +45,52 @@ template <typename TI> __device__ __forceinline__ void st(TI* p, int64_t i, floa
 template <> __device__ __forceinline__ void st<float>(float* p, int64_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st<bf16_t>(bf16_t* p, int64_t i, float v) { p[i].bits = f32_to_bf16(v); }
 
+template <typename TI> __device__ __forceinline__ float ld(const TI* p, int64_t i);
+template <> __device__ __forceinline__ float ld<float>(const float* p, int64_t i) { return p[i]; }
+template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i].bits); }
+
+// Diagonal Sigma_i (Sec. 3.1, eq. JD-Diag; App. F: no batched product is
+// needed): z'_t[c] = sigma_i[c] z_t[c], an elementwise scale.  Same items and
+// the same fixed-order split sum as sigma_kernel; no LDS.
+template <typename TI>
+__global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __restrict__ zpart, int S,
+                                                                 int T, int r,
+                                                                 const int32_t* __restrict__ sorted_aid,
+                                                                 int n, const int32_t* __restrict__ items,
+                                                                 const int32_t* __restrict__ n_items,
+                                                                 const TI* __restrict__ sigma,
+                                                                 TI* __restrict__ zp) {
+  const int item = blockIdx.x;
+  if (item >= n_items[0]) return;
+  const int tid = threadIdx.x;
+  const int lo = items[item], hi = items[item + 1];
+  const int cnt = (hi - lo) * r;
+  int a = sorted_aid[lo];
+  a = a < 0 ? 0 : (a >= n ? n - 1 : a);
+  const TI* sa = sigma + static_cast<int64_t>(a) * r;
+  const int64_t split_stride = static_cast<int64_t>(T) * r;
+  const float* zbase = zpart + static_cast<int64_t>(lo) * r;
+  TI* out = zp + static_cast<int64_t>(lo) * r;
+  for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
+    const int c = e4 % r;                                  // r % 8 == 0: c..c+3 in one row
+    float s[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) s[v] = ld<TI>(sa, c + v);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < S; q += 16) {
+      f32x4 w[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (q + u < S) w[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (q + u < S) acc += w[u];
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) st<TI>(out, e4 + v, s[v] * acc[v]);
+  }
+}
+
 template <typename TI, int MAXR>
 __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restrict__ zpart, int S,
                                                             int T, int r,
@@ -180,8 +226,20 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
-                        const void* Sigma, void* zp, int in_dtype, hipStream_t stream) {
+                        const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
+                        bool diag) {
   dim3 grid(max_items);
+  if (diag && Sigma) {
+    if (in_dtype == 0)
+      hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                         sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
+                         static_cast<float*>(zp));
+    else
+      hipLaunchKernelGGL(sigma_diag_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
+                         sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
+                         static_cast<bf16_t*>(zp));
+    return hipGetLastError();
+  }
   if (r > 128) return hipErrorInvalidValue;
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,

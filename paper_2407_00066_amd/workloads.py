@@ -27,7 +27,7 @@ import numpy as np
 SEED_BASE = 240700066
 
 # stream ids
-_S_W, _S_U, _S_V, _S_SIG, _S_X, _S_IDS, _S_CLU, _S_A, _S_B, _S_LEN, _S_SEQ = range(1, 12)
+_S_W, _S_U, _S_V, _S_SIG, _S_X, _S_IDS, _S_CLU, _S_A, _S_B, _S_LEN, _S_SEQ, _S_SDIAG = range(1, 13)
 
 
 def _rng(cfg: int, stream: int) -> np.random.Generator:
@@ -198,6 +198,13 @@ STACK = dict(T=512, r=64, n=1000, K=50, ids="uniform")
 for _i, (_name, _din, _dout) in enumerate((("q", 4096, 4096), ("kv", 4096, 1024),
                                             ("gate", 4096, 14336), ("down", 14336, 4096))):
     CONFIGS["stack_" + _name] = dict(cfg=10 + _i, d_in=_din, d_out=_dout, with_lora=False, **STACK)
+
+
+def sigma_diagonals(cfg: int, n: int, r: int, dtype: str, var: float = 1.0) -> np.ndarray:
+    """Diagonal Sigma_i (Sec. 3.1, JD-Diag) as [n][r], entries ~N(0, var): with
+    var = 1 the scaled z'_q = sigma_i[q] z_q keeps the magnitude of z, as the
+    full Sigma_i ~N(0, 1/r) does."""
+    return _gauss(_rng(cfg, _S_SDIAG), (n, r), var, dtype)
 
 
 def make(name: str, **overrides) -> Workload:

@@ -169,3 +169,44 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "_LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         B.lib()
+
+
+# the diagonal-Sigma entry point validates exactly as cts_apply does
+
+def _apply_d(p, ptrs=None, ws_bytes=1 << 40, y=None, ws=None):
+    ptrs = ptrs or [FAKE] * 7
+    y = y if y is not None else ctypes.c_void_p(0x7000_0000_0000)
+    ws = ws if ws is not None else ctypes.c_void_p(0x6000_0000_0000)
+    return cts.lib().cts_apply_diag(ctypes.byref(p), *ptrs[:7], y, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=-1), B.CTS_ERR_INVALID_ARG), (dict(r=0), B.CTS_ERR_INVALID_ARG),
+    (dict(n_clusters=0), B.CTS_ERR_INVALID_ARG), (dict(r=12), B.CTS_ERR_UNSUPPORTED),
+    (dict(T=8193), B.CTS_ERR_UNSUPPORTED), (dict(dtype=2), B.CTS_ERR_UNSUPPORTED),
+])
+def test_apply_diag_rejects_bad_problem(kw, code):
+    assert _apply_d(_p(**kw)) == code
+
+
+def test_apply_diag_null_and_misaligned_pointers():
+    p = _p()
+    assert cts.lib().cts_apply_diag(None, *[FAKE] * 9, 0, None) == B.CTS_ERR_INVALID_ARG
+    for i in range(7):
+        ptrs = [FAKE] * 7
+        ptrs[i] = None
+        assert _apply_d(p, ptrs) == B.CTS_ERR_INVALID_ARG, i
+    ptrs = [ctypes.c_void_p(0x5000_0000_0000 + k * (1 << 32)) for k in range(7)]
+    ptrs[6] = ctypes.c_void_p(ptrs[6].value + 8)          # sigma not 16-byte aligned
+    assert _apply_d(p, ptrs) == B.CTS_ERR_INVALID_ARG
+    assert _apply_d(p, ws_bytes=cts.workspace_size(p) - 1) == B.CTS_ERR_WORKSPACE
+    assert cts.lib().cts_apply_diag(ctypes.byref(_p(T=0)), *[None] * 9, 0, None) == B.CTS_OK
+
+
+def test_apply_diag_rejects_overlap_with_sigma():
+    # y overlapping sigma: sigma is n x r here (not n x r x r)
+    p = _p(n_adapters=4, r=64)
+    base = 0x5000_0000_0000
+    ptrs = [ctypes.c_void_p(base + k * (1 << 32)) for k in range(7)]
+    y = ctypes.c_void_p(ptrs[6].value + 256)               # inside sigma's 4 * 64 * 2 bytes
+    assert _apply_d(p, ptrs, y=y) == B.CTS_ERR_INVALID_ARG
