@@ -71,18 +71,19 @@ def main_kernel_model(w, touched_clusters):
     return flops, nbytes
 
 
-def cpu_baseline(w, target_s):
+def cpu_baseline(w, target_s, sigma=None):
     """The oracle on a prefix of the batch (in batch order), grown until about
-    target_s seconds of oracle time; tokens/s = tokens / oracle seconds."""
+    target_s seconds of oracle time; tokens/s = tokens / oracle seconds.  With
+    `sigma` ([n][r] diagonals) the diagonal-Sigma oracle is timed."""
     import numpy as np
     from oracle import oracle
-    f64 = [oracle.to_f64(a) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
+    f64 = [oracle.to_f64(a) for a in (w.x, w.W, w.U, w.Vt, w.Sigma if sigma is None else sigma)]
+    fn = oracle.apply if sigma is None else oracle.apply_diag
     spent, done, chunk = 0.0, 0, min(64, w.T)
     while done < w.T and spent < target_s:
         toks = np.arange(done, min(w.T, done + chunk))
         tm = {}
-        oracle.apply(f64[0], w.adapter_id, w.cluster_of, f64[1], f64[2], f64[3], f64[4],
-                     tokens=toks, timing=tm)
+        fn(f64[0], w.adapter_id, w.cluster_of, f64[1], f64[2], f64[3], f64[4], tokens=toks, timing=tm)
         spent += tm["s"]
         done += len(toks)
         per_tok = spent / done
@@ -222,6 +223,10 @@ def roofline_of(flops, nbytes, t_s, dtype):
 def bench_layer(args, torch, np, cts, B, wl, device):
     log("generating %s" % args.workload)
     w = wl.make(args.workload)
+    diag = args.sigma == "diag"
+    if diag:   # the diagonal-Sigma variant (Sec. 3.1, JD-Diag): Sigma holds [n][r] diagonals
+        w.Sigma = wl.sigma_diagonals(wl.CONFIGS[args.workload]["cfg"], w.n, w.r, w.dtype)
+    layer = cts.apply_diag if diag else cts.apply
 
     set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
     n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
@@ -236,7 +241,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     def step(s):
         x, W, U, Vt, S = s
-        cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+        layer(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
 
     log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
         (n_sets, set_bytes / 1e6, args.warmup, args.steps))
@@ -252,7 +257,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     def step1(s):
         x, W, U, Vt, S = s
-        cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
+        layer(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
 
     log("timing cts_apply with one adapter")
     ms1, ms1_g = time_launches(step1, sets, args, torch)
@@ -286,7 +291,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
-        cpu = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_seconds, sigma=w.Sigma if diag else None)
 
     value = w.T / (ms * 1e-3)
     value1 = w.T / (ms1 * 1e-3)
@@ -296,7 +301,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "graph_replay": {"value": round(w.T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5)},
         "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
-        "config": {"workload": args.workload, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
+        "config": {"workload": args.workload, "sigma": args.sigma, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
                    "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
                    "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
         "roofline": roof,
@@ -474,6 +479,9 @@ def main():
                     choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sigma", default="full", choices=["full", "diag"],
+                    help="full r x r Sigma_i (JD-Full, the default) or diagonal Sigma_i "
+                         "(JD-Diag, cts_apply_diag); single-layer workloads only")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -493,6 +501,9 @@ def main():
     torch.cuda.set_device(device)
     copy_calibration(torch, device)
     if args.workload == "stack32":
+        if args.sigma != "full":
+            print("--sigma diag applies to the single-layer workloads", file=sys.stderr)
+            sys.exit(2)
         rec = bench_stack(args, torch, np, cts, B, wl, device)
     else:
         rec = bench_layer(args, torch, np, cts, B, wl, device)
