@@ -23,6 +23,11 @@
  * and, for the uncompressed comparison path, Delta_i = B_i A_i.
  * Sec. 3.1, the diagonal variant (eq. JD-Diag): Sigma_i is diagonal, given as
  * its r diagonal entries sigma_i, and Delta_i = U_k diag(sigma_i) V_k^T.
+ * Mixed ranks (Sec. 3.2: each cluster is given its own rank; App. G: LoRAs of
+ * different ranks): arrays are stored at the largest rank, cluster k uses its
+ * first r_k columns of U_k, rows of V_k^T and the leading r_k x r_k block of
+ * Sigma_i, and uncompressed adapter i its first r_i columns of B_i and rows
+ * of A_i; the stored entries past those ranks are never read.
  *
  * Array layouts (row-major, all host memory, all double):
  *   x      [T][d_in]            W      [d_out][d_in]
@@ -230,6 +235,103 @@ int cts_oracle_apply_diag(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
         apply_rows(W, D, x + t * d_in, y + s * d_out, d_out, d_in);
     }
     free(M); free(D); free(order);
+    return 0;
+}
+
+/* Mixed ranks, compressed path: Delta_i = U_k[:, :r_k] Sigma_i[:r_k, :r_k]
+ * V_k^T[:r_k, :] with r_k = rank_of_cluster[k] (0 <= r_k <= r). */
+int cts_oracle_apply_ranked(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                            int64_t n, int64_t K,
+                            const double* x, const int32_t* adapter_id,
+                            const int32_t* cluster_of, const double* W,
+                            const double* U, const double* Vt, const double* Sigma,
+                            const int32_t* rank_of_cluster,
+                            const int64_t* tokens, int64_t n_tok, double* y) {
+    if (T < 0 || d_in < 1 || d_out < 1 || r < 1 || n < 1 || K < 1 || n_tok < 0) return -1;
+    int rc = check_tokens(adapter_id, T, tokens, n_tok, n);
+    if (rc) return rc;
+    for (int64_t i = 0; i < n; ++i)
+        if (cluster_of[i] < 0 || cluster_of[i] >= K) return -2;
+    for (int64_t k = 0; k < K; ++k)
+        if (rank_of_cluster[k] < 0 || rank_of_cluster[k] > r) return -3;
+    if (n_tok == 0) return 0;
+
+    double* M = (double*)malloc(sizeof(double) * (size_t)(r * d_in));
+    double* D = (double*)malloc(sizeof(double) * (size_t)(d_out * d_in));
+    int64_t* order = visit_order(adapter_id, tokens, n_tok, n);
+    if (!M || !D || !order) { free(M); free(D); free(order); return -1; }
+
+    int64_t cur = -1;
+    for (int64_t v = 0; v < n_tok; ++v) {
+        const int64_t s = order[v];
+        const int64_t t = tokens[s];
+        const int64_t a = adapter_id[t];
+        if (a != cur) {
+            const int64_t k = cluster_of[a];
+            const int64_t rk = rank_of_cluster[k];
+            const double* Sa = Sigma + a * r * r;
+            const double* Vk = Vt + k * r * d_in;
+            const double* Uk = U + k * d_out * r;
+            /* M = Sigma_a[:rk, :rk] V_k^T[:rk, :]  (rk x d_in) */
+            for (int64_t q = 0; q < rk; ++q)
+                for (int64_t c = 0; c < d_in; ++c) {
+                    double acc = 0.0;
+                    for (int64_t p = 0; p < rk; ++p) acc += Sa[q * r + p] * Vk[p * d_in + c];
+                    M[q * d_in + c] = acc;
+                }
+            /* D = U_k[:, :rk] M  (d_out x d_in) */
+            for (int64_t o = 0; o < d_out; ++o)
+                for (int64_t c = 0; c < d_in; ++c) {
+                    double acc = 0.0;
+                    for (int64_t q = 0; q < rk; ++q) acc += Uk[o * r + q] * M[q * d_in + c];
+                    D[o * d_in + c] = acc;
+                }
+            cur = a;
+        }
+        apply_rows(W, D, x + t * d_in, y + s * d_out, d_out, d_in);
+    }
+    free(M); free(D); free(order);
+    return 0;
+}
+
+/* Mixed ranks, uncompressed path: Delta_i = B_i[:, :r_i] A_i[:r_i, :] with
+ * r_i = rank_of_adapter[i] (0 <= r_i <= r_l). */
+int cts_oracle_apply_uncompressed_ranked(int64_t T, int64_t d_in, int64_t d_out, int64_t r_l,
+                                         int64_t n, const double* x, const int32_t* adapter_id,
+                                         const double* W, const double* A, const double* B,
+                                         const int32_t* rank_of_adapter,
+                                         const int64_t* tokens, int64_t n_tok, double* y) {
+    if (T < 0 || d_in < 1 || d_out < 1 || r_l < 1 || n < 1 || n_tok < 0) return -1;
+    int rc = check_tokens(adapter_id, T, tokens, n_tok, n);
+    if (rc) return rc;
+    for (int64_t i = 0; i < n; ++i)
+        if (rank_of_adapter[i] < 0 || rank_of_adapter[i] > r_l) return -3;
+    if (n_tok == 0) return 0;
+
+    double* D = (double*)malloc(sizeof(double) * (size_t)(d_out * d_in));
+    int64_t* order = visit_order(adapter_id, tokens, n_tok, n);
+    if (!D || !order) { free(D); free(order); return -1; }
+
+    int64_t cur = -1;
+    for (int64_t v = 0; v < n_tok; ++v) {
+        const int64_t s = order[v];
+        const int64_t t = tokens[s];
+        const int64_t a = adapter_id[t];
+        if (a != cur) {
+            const int64_t ra = rank_of_adapter[a];
+            const double* Ba = B + a * d_out * r_l;
+            const double* Aa = A + a * r_l * d_in;
+            for (int64_t o = 0; o < d_out; ++o)
+                for (int64_t c = 0; c < d_in; ++c) {
+                    double acc = 0.0;
+                    for (int64_t q = 0; q < ra; ++q) acc += Ba[o * r_l + q] * Aa[q * d_in + c];
+                    D[o * d_in + c] = acc;
+                }
+            cur = a;
+        }
+        apply_rows(W, D, x + t * d_in, y + s * d_out, d_out, d_in);
+    }
+    free(D); free(order);
     return 0;
 }
 

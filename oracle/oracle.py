@@ -14,7 +14,9 @@ Conventions
   ``A[n][r_l][d_in]``, ``B[n][d_out][r_l]``.
 
 ``apply_diag`` is the diagonal-Sigma variant of Sec. 3.1 (eq. JD-Diag) with
-``sigma[n][r]`` holding the diagonals.
+``sigma[n][r]`` holding the diagonals.  ``apply_ranked`` and
+``apply_uncompressed_ranked`` take mixed ranks (a rank per cluster, Sec. 3.2;
+a rank per uncompressed LoRA, App. G) over arrays stored at the largest rank.
 
 Besides the apply/sort oracles this module holds ``exact_compress``: the
 lossless JD-Full construction of Proposition 1 with Sigma_i taken from the
@@ -63,6 +65,12 @@ def _load():
         lib.cts_oracle_apply.restype = ctypes.c_int
         lib.cts_oracle_apply_diag.argtypes = lib.cts_oracle_apply.argtypes
         lib.cts_oracle_apply_diag.restype = ctypes.c_int
+        lib.cts_oracle_apply_ranked.argtypes = [i64, i64, i64, i64, i64, i64, f64p, i32p, i32p,
+                                                f64p, f64p, f64p, f64p, i32p, i64p, i64, f64p]
+        lib.cts_oracle_apply_ranked.restype = ctypes.c_int
+        lib.cts_oracle_apply_uncompressed_ranked.argtypes = [i64, i64, i64, i64, i64, f64p, i32p,
+                                                             f64p, f64p, f64p, i32p, i64p, i64, f64p]
+        lib.cts_oracle_apply_uncompressed_ranked.restype = ctypes.c_int
         lib.cts_oracle_apply_uncompressed.argtypes = [i64, i64, i64, i64, i64, f64p, i32p,
                                                       f64p, f64p, f64p, i64p, i64, f64p]
         lib.cts_oracle_apply_uncompressed.restype = ctypes.c_int
@@ -164,6 +172,59 @@ def apply_diag(x, adapter_id, cluster_of, W, U, Vt, sigma, tokens=None, timing=N
         timing["s"] = time.perf_counter() - t0
     if rc != 0:
         raise ValueError("oracle apply_diag rejected its input (code %d)" % rc)
+    return y[:len(tok)]
+
+
+def apply_ranked(x, adapter_id, cluster_of, W, U, Vt, Sigma, rank_of_cluster, tokens=None, timing=None):
+    """Mixed ranks (Sec. 3.2: each cluster its own rank): y[s] = (W + U_k[:, :r_k]
+    Sigma_i[:r_k, :r_k] V_k^T[:r_k, :]) x_t with r_k = rank_of_cluster[k]; U,
+    Vt and Sigma are stored at the largest rank and the rest is never read."""
+    x64, W64, U64, V64, S64 = (np.ascontiguousarray(to_f64(a)) for a in (x, W, U, Vt, Sigma))
+    aid, cof, rk = _ids(adapter_id), _ids(cluster_of), _ids(rank_of_cluster)
+    T, d_in = x64.shape
+    d_out = W64.shape[0]
+    K, _, r = U64.shape
+    n = S64.shape[0]
+    assert W64.shape == (d_out, d_in) and V64.shape == (K, r, d_in) and S64.shape == (n, r, r)
+    assert aid.shape == (T,) and cof.shape == (n,) and rk.shape == (K,)
+    tok = _tokens(tokens, T)
+    y = np.zeros((max(len(tok), 1), d_out), np.float64)
+    f = ctypes.c_double
+    t0 = time.perf_counter()
+    rc = _load().cts_oracle_apply_ranked(T, d_in, d_out, r, n, K, _c(x64, f), _c(aid, ctypes.c_int32),
+                                         _c(cof, ctypes.c_int32), _c(W64, f), _c(U64, f), _c(V64, f),
+                                         _c(S64, f), _c(rk, ctypes.c_int32), _c(tok, ctypes.c_int64),
+                                         len(tok), _c(y, f))
+    if timing is not None:
+        timing["s"] = time.perf_counter() - t0
+    if rc != 0:
+        raise ValueError("oracle apply_ranked rejected its input (code %d)" % rc)
+    return y[:len(tok)]
+
+
+def apply_uncompressed_ranked(x, adapter_id, W, A, B, rank_of_adapter, tokens=None, timing=None):
+    """Uncompressed LoRAs of different ranks (App. G): y[s] = (W + B_i[:, :r_i]
+    A_i[:r_i, :]) x_t with r_i = rank_of_adapter[i]; A, B stored at the
+    largest rank."""
+    x64, W64, A64, B64 = (np.ascontiguousarray(to_f64(a)) for a in (x, W, A, B))
+    aid, ra = _ids(adapter_id), _ids(rank_of_adapter)
+    T, d_in = x64.shape
+    d_out = W64.shape[0]
+    n, r_l, _ = A64.shape
+    assert W64.shape == (d_out, d_in) and A64.shape == (n, r_l, d_in) and B64.shape == (n, d_out, r_l)
+    assert aid.shape == (T,) and ra.shape == (n,)
+    tok = _tokens(tokens, T)
+    y = np.zeros((max(len(tok), 1), d_out), np.float64)
+    f = ctypes.c_double
+    t0 = time.perf_counter()
+    rc = _load().cts_oracle_apply_uncompressed_ranked(T, d_in, d_out, r_l, n, _c(x64, f),
+                                                      _c(aid, ctypes.c_int32), _c(W64, f), _c(A64, f),
+                                                      _c(B64, f), _c(ra, ctypes.c_int32),
+                                                      _c(tok, ctypes.c_int64), len(tok), _c(y, f))
+    if timing is not None:
+        timing["s"] = time.perf_counter() - t0
+    if rc != 0:
+        raise ValueError("oracle apply_uncompressed_ranked rejected its input (code %d)" % rc)
     return y[:len(tok)]
 
 
