@@ -131,11 +131,35 @@ int cts_apply_diag(const cts_problem* p, const void* x, const int32_t* adapter_i
                    const void* Vt, const void* sigma, void* y,
                    void* workspace, size_t workspace_bytes, void* stream);
 
+/* Mixed ranks (Sec. 3.2: each cluster is given its own rank).  As cts_apply,
+ * with U, Vt and Sigma stored at the largest rank p->r, and rank_of_cluster
+ * (device int32 [K], 4-byte aligned) giving r_k: the layer uses
+ * U_k[:, :r_k] Sigma_i[:r_k, :r_k] V_k^T[:r_k, :], and the stored entries past
+ * r_k are never read into the result (they may hold anything, NaN included).
+ * Each r_k must be a multiple of 8 in [0, p->r]; a value outside is clamped
+ * into [0, p->r] and rounded down to a multiple of 8 (device contents are not
+ * checked on the host).  Same workspace as cts_apply. */
+int cts_apply_ranked(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                     const int32_t* cluster_of, const void* W, const void* U,
+                     const void* Vt, const void* Sigma, const int32_t* rank_of_cluster,
+                     void* y, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Uncompressed comparison path: overwrites y[t] with W x_t + B_i A_i x_t
  * (Sec. 3, first paragraph), i = adapter_id[t], rank p->r_lora. */
 int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
                            const void* W, const void* A, const void* B, void* y,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* Uncompressed LoRAs of different ranks (App. G): as cts_apply_uncompressed,
+ * with A, B stored at the largest rank p->r_lora and rank_of_adapter (device
+ * int32 [n], 4-byte aligned) giving r_i: the layer uses B_i[:, :r_i]
+ * A_i[:r_i, :]; entries past r_i are never read into the result.  Each r_i
+ * must be a multiple of 8 in [0, p->r_lora] (else clamped and rounded down,
+ * as in cts_apply_ranked).  Same workspace as cts_apply_uncompressed. */
+int cts_apply_uncompressed_ranked(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                                  const void* W, const void* A, const void* B,
+                                  const int32_t* rank_of_adapter, void* y,
+                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* Synchronous id check for tests and debugging: copies the ids to the host
  * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is

@@ -273,6 +273,7 @@ int cts_oracle_apply_ranked(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
             const double* Vk = Vt + k * r * d_in;
             const double* Uk = U + k * d_out * r;
             /* M = Sigma_a[:rk, :rk] V_k^T[:rk, :]  (rk x d_in) */
+            #pragma omp parallel for schedule(static)
             for (int64_t q = 0; q < rk; ++q)
                 for (int64_t c = 0; c < d_in; ++c) {
                     double acc = 0.0;
@@ -280,6 +281,7 @@ int cts_oracle_apply_ranked(int64_t T, int64_t d_in, int64_t d_out, int64_t r,
                     M[q * d_in + c] = acc;
                 }
             /* D = U_k[:, :rk] M  (d_out x d_in) */
+            #pragma omp parallel for schedule(static)
             for (int64_t o = 0; o < d_out; ++o)
                 for (int64_t c = 0; c < d_in; ++c) {
                     double acc = 0.0;
@@ -321,6 +323,7 @@ int cts_oracle_apply_uncompressed_ranked(int64_t T, int64_t d_in, int64_t d_out,
             const int64_t ra = rank_of_adapter[a];
             const double* Ba = B + a * d_out * r_l;
             const double* Aa = A + a * r_l * d_in;
+            #pragma omp parallel for schedule(static)
             for (int64_t o = 0; o < d_out; ++o)
                 for (int64_t c = 0; c < d_in; ++c) {
                     double acc = 0.0;

@@ -22,8 +22,9 @@ CTS_F32, CTS_BF16 = 0, 1
 
 # every symbol include/cts.h declares
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
-            "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_uncompressed",
-            "cts_validate_ids", "cts_set_stage_events")
+            "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
+            "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
+            "cts_set_stage_events")
 N_STAGE_EVENTS = 6
 
 
@@ -64,6 +65,10 @@ def lib() -> ctypes.CDLL:
                 L.cts_apply.restype = ctypes.c_int
                 L.cts_apply_diag.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply_diag.restype = ctypes.c_int
+                L.cts_apply_ranked.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_apply_ranked.restype = ctypes.c_int
+                L.cts_apply_uncompressed_ranked.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_apply_uncompressed_ranked.restype = ctypes.c_int
                 L.cts_apply_uncompressed.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply_uncompressed.restype = ctypes.c_int
                 L.cts_validate_ids.argtypes = [pp, vp, vp, vp]
@@ -209,6 +214,66 @@ def apply_diag(x, adapter_id, cluster_of, W, U, Vt, sigma, out=None, out_dtype=N
     ws = _workspace(dev, nbytes, workspace)
     _check(lib().cts_apply_diag(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                                 _stream(dev)), "cts_apply_diag")
+    return out
+
+
+def apply_ranked(x, adapter_id, cluster_of, W, U, Vt, Sigma, rank_of_cluster, out=None, out_dtype=None,
+                 workspace=None):
+    """Mixed ranks: as apply, cluster k using U_k[:, :r_k], Sigma_i[:r_k, :r_k],
+    V_k^T[:r_k] with r_k = rank_of_cluster[k] (see cts_apply_ranked)."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    K, _, r = U.shape
+    n = Sigma.shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=dt,
+                     out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(U, "U", dev, tdt, (K, d_out, r)),
+            _dev(Vt, "Vt", dev, tdt, (K, r, d_in)),
+            _dev(Sigma, "Sigma", dev, tdt, (n, r, r)),
+            _dev(rank_of_cluster, "rank_of_cluster", dev, torch.int32, (K,)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    nbytes = workspace_size(p, True)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_ranked(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                  _stream(dev)), "cts_apply_ranked")
+    return out
+
+
+def apply_uncompressed_ranked(x, adapter_id, W, A, B, rank_of_adapter, out=None, out_dtype=None,
+                              workspace=None):
+    """LoRAs of different ranks: as apply_uncompressed, adapter i using
+    B_i[:, :r_i] A_i[:r_i] (see cts_apply_uncompressed_ranked)."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    n, r_l, _ = A.shape
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, n_adapters=n, r_lora=r_l, dtype=dt, out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(A, "A", dev, tdt, (n, r_l, d_in)),
+            _dev(B, "B", dev, tdt, (n, d_out, r_l)),
+            _dev(rank_of_adapter, "rank_of_adapter", dev, torch.int32, (n,)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    nbytes = workspace_size(p, False)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_uncompressed_ranked(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()),
+                                               ws.numel(), _stream(dev)), "cts_apply_uncompressed_ranked")
     return out
 
 

@@ -179,7 +179,7 @@ bool any_overlap(Range y, Range ws, const Range* in, int n_in) {
 int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void* x,
               const int32_t* adapter_id, const int32_t* cluster_of, const void* W,
               const void* Ubasis, const void* Vbasis, const void* Sigma, void* y, void* workspace,
-              hipStream_t stream, bool sigma_diag = false) {
+              hipStream_t stream, bool sigma_diag = false, const int32_t* seg_rank = nullptr) {
   char* ws = static_cast<char*>(workspace);
   int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
   int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
@@ -229,7 +229,8 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 
   e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
-                        pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag);
+                        pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag,
+                        sseg, seg_rank);
   if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
@@ -241,7 +242,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   f.b0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
   f.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(p->d_out) * rank * pl.elt);
   f.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * rank * pl.elt);
-  f.perm = perm; f.sorted_seg = sseg;
+  f.perm = perm; f.sorted_seg = sseg; f.seg_rank = seg_rank;
   f.ksplit = pl.main_split;
   f.part = pl.main_split > 1 ? ypart : nullptr;
   f.out = y; f.ldo = p->d_out; f.out_perm = 1; f.out_dtype = p->out_dtype;
@@ -308,7 +309,7 @@ namespace {
 int apply_compressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
                      const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
                      const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream,
-                     bool sigma_diag) {
+                     bool sigma_diag, const int32_t* rank_of_cluster = nullptr, bool ranked = false) {
   Plan pl;
   const int rc = make_plan(p, true, &pl);
   if (rc != CTS_OK) return rc;
@@ -318,16 +319,18 @@ int apply_compressed(const cts_problem* p, const void* x, const int32_t* adapter
   for (const void* q : {x, W, U, Vt, Sigma, static_cast<const void*>(y), static_cast<const void*>(workspace)})
     if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
   if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4)) return CTS_ERR_INVALID_ARG;
+  if (ranked && (!rank_of_cluster || misaligned(rank_of_cluster, 4))) return CTS_ERR_INVALID_ARG;
   if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
   const size_t e = pl.elt;
   const size_t T = p->T, di = p->d_in, dout = p->d_out, r = p->r, n = p->n_adapters, K = p->n_clusters;
-  const Range in[7] = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
+  const Range in[8] = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
                        {W, dout * di * e}, {U, K * dout * r * e}, {Vt, K * r * di * e},
-                       {Sigma, n * (sigma_diag ? 1 : r) * r * e}};
-  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 7))
+                       {Sigma, n * (sigma_diag ? 1 : r) * r * e},
+                       {rank_of_cluster, ranked ? 4 * K : 0}};
+  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 8))
     return CTS_ERR_INVALID_ARG;
   return run_layer(p, pl, true, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
-                   static_cast<hipStream_t>(stream), sigma_diag);
+                   static_cast<hipStream_t>(stream), sigma_diag, ranked ? rank_of_cluster : nullptr);
 }
 
 }  // namespace
@@ -347,9 +350,20 @@ int cts_apply_diag(const cts_problem* p, const void* x, const int32_t* adapter_i
                           workspace_bytes, stream, true);
 }
 
-int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
-                           const void* W, const void* A, const void* B, void* y, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+int cts_apply_ranked(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                     const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+                     const void* Sigma, const int32_t* rank_of_cluster, void* y, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
+                          workspace_bytes, stream, false, rank_of_cluster, true);
+}
+
+namespace {
+
+int apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                       const void* W, const void* A, const void* B, void* y, void* workspace,
+                       size_t workspace_bytes, void* stream, const int32_t* rank_of_adapter,
+                       bool ranked) {
   Plan pl;
   const int rc = make_plan(p, false, &pl);
   if (rc != CTS_OK) return rc;
@@ -358,15 +372,34 @@ int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* a
   for (const void* q : {x, W, A, B, static_cast<const void*>(y), static_cast<const void*>(workspace)})
     if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
   if (misaligned(adapter_id, 4)) return CTS_ERR_INVALID_ARG;
+  if (ranked && (!rank_of_adapter || misaligned(rank_of_adapter, 4))) return CTS_ERR_INVALID_ARG;
   if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
   const size_t e = pl.elt;
   const size_t T = p->T, di = p->d_in, dout = p->d_out, rl = p->r_lora, n = p->n_adapters;
-  const Range in[5] = {{x, T * di * e}, {adapter_id, 4 * T}, {W, dout * di * e},
-                       {A, n * rl * di * e}, {B, n * dout * rl * e}};
-  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 5))
+  const Range in[6] = {{x, T * di * e}, {adapter_id, 4 * T}, {W, dout * di * e},
+                       {A, n * rl * di * e}, {B, n * dout * rl * e},
+                       {rank_of_adapter, ranked ? 4 * n : 0}};
+  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 6))
     return CTS_ERR_INVALID_ARG;
   return run_layer(p, pl, false, x, adapter_id, nullptr, W, B, A, nullptr, y, workspace,
-                   static_cast<hipStream_t>(stream));
+                   static_cast<hipStream_t>(stream), false, ranked ? rank_of_adapter : nullptr);
+}
+
+}  // namespace
+
+int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                           const void* W, const void* A, const void* B, void* y, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  return apply_uncompressed(p, x, adapter_id, W, A, B, y, workspace, workspace_bytes, stream,
+                            nullptr, false);
+}
+
+int cts_apply_uncompressed_ranked(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                                  const void* W, const void* A, const void* B,
+                                  const int32_t* rank_of_adapter, void* y, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  return apply_uncompressed(p, x, adapter_id, W, A, B, y, workspace, workspace_bytes, stream,
+                            rank_of_adapter, true);
 }
 
 int cts_set_stage_events(void* const* events) {

@@ -78,6 +78,9 @@ struct GemmParams {
   int b1_gather;
   const int32_t* perm;        // [N] sorted position -> token
   const int32_t* sorted_seg;  // [N] sorted position -> segment (cluster / adapter)
+  // optional rank of each segment: the segment phase of segment s reads only
+  // its first rank_of(s) elements of the reduction (rank_of: see seg_rank_of)
+  const int32_t* seg_rank;
   int ksplit;
   float* part;
   void* out; int64_t ldo; int out_perm; int out_dtype;
@@ -105,16 +108,27 @@ enum class Tile { Large, Wide, Narrow, Decode, Shrink, Mid, Small, F32 };
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream);
 void tile_dims(Tile tile, int* BM, int* BN, int* BK);
 
+// Rank of segment s from a caller's rank table: clamped to [0, kmax] and
+// rounded down to a multiple of 8 (16-byte chunks never straddle it).
+__device__ __forceinline__ int seg_rank_of(const int32_t* seg_rank, int s, int kmax) {
+  int v = seg_rank[s];
+  v = v < 0 ? 0 : (v > kmax ? kmax : v);
+  return v & ~7;
+}
+
 // ------------------------------------------------------------- Sigma stage
 // zp[j][c] = sum_{c'} Sigma_{aid(j)}[c][c'] * (sum_s zpart[s][j][c'])  (Sigma may be null:
 // then zp = sum_s zpart).  With diag, Sigma is [n][r] (the diagonals) and
-// zp[j][c] = Sigma_{aid(j)}[c] * (sum_s zpart[s][j][c]).  Rounded to the input
-// type.  One workgroup per item of the sort (max_items workgroups are
-// launched; the extra ones exit).
+// zp[j][c] = Sigma_{aid(j)}[c] * (sum_s zpart[s][j][c]).  With seg_rank, the
+// position's segment sorted_seg[j] has rank rk = seg_rank_of(seg_rank, .., r):
+// only c, c' < rk are read (Sigma's leading block, z's first rk entries) and
+// zp[j][c >= rk] = 0.  Rounded to the input type.  One workgroup per item of
+// the sort (max_items workgroups are launched; the extra ones exit).
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
-                        bool diag = false);
+                        bool diag = false, const int32_t* sorted_seg = nullptr,
+                        const int32_t* seg_rank = nullptr);
 
 // y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,

@@ -254,8 +254,9 @@ __global__ __launch_bounds__(WM * WN * 64, OCC) void seg_gemm_kernel(const GemmP
     const __amdgpu_buffer_rsrc_t rB = dense ? rB0 : rB1;
     const int kt = dense ? d_lo + lt : lkt;
     const uint32_t k = static_cast<uint32_t>(kt * BK) + kc * C::EPC;
+    const int klim = dense ? p.K0 : (p.seg_rank ? seg_rank_of(p.seg_rank, seg, p.K1) : p.K1);
     // out-of-range chunks get bit 31 set (every operand is < 2^31 bytes)
-    const uint32_t kmask = (valid && k < static_cast<uint32_t>(dense ? p.K0 : p.K1)) ? 0u : kOob;
+    const uint32_t kmask = (valid && k < static_cast<uint32_t>(klim)) ? 0u : kOob;
     const uint32_t kb = k * ELT;
     const uint32_t span = static_cast<uint32_t>(hi - lo);
     const uint32_t dsel = dense ? 0xffffffffu : 0u;   // phase select by mask arithmetic
@@ -792,7 +793,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       // offset arrays would make the compiler keep them in scratch memory)
       L.dsel = 0u;
       k0 = static_cast<uint32_t>(lkt * BK);
-      klim = static_cast<uint32_t>(K1);
+      klim = static_cast<uint32_t>(p.seg_rank ? seg_rank_of(p.seg_rank, seg, K1) : K1);
       ++lkt;
       if (lkt >= s_hi) { lkt = s_lo; ++lq; }
     }

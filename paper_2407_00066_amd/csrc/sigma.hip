@@ -59,12 +59,15 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
                                                                  int n, const int32_t* __restrict__ items,
                                                                  const int32_t* __restrict__ n_items,
                                                                  const TI* __restrict__ sigma,
-                                                                 TI* __restrict__ zp) {
+                                                                 TI* __restrict__ zp,
+                                                                 const int32_t* __restrict__ sorted_seg,
+                                                                 const int32_t* __restrict__ seg_rank) {
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
   const int tid = threadIdx.x;
   const int lo = items[item], hi = items[item + 1];
   const int cnt = (hi - lo) * r;
+  const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;   // a multiple of 8
   int a = sorted_aid[lo];
   a = a < 0 ? 0 : (a >= n ? n - 1 : a);
   const TI* sa = sigma + static_cast<int64_t>(a) * r;
@@ -73,11 +76,12 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
   TI* out = zp + static_cast<int64_t>(lo) * r;
   for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
     const int c = e4 % r;                                  // r % 8 == 0: c..c+3 in one row
+    const bool in_rank = c < rk;                           // and all four, or none, below rk
     float s[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) s[v] = ld<TI>(sa, c + v);
+    for (int v = 0; v < 4; ++v) s[v] = in_rank ? ld<TI>(sa, c + v) : 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < S; q += 16) {
+    for (int q = 0; in_rank && q < S; q += 16) {
       f32x4 w[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u)
@@ -98,7 +102,9 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             int n, const int32_t* __restrict__ items,
                                                             const int32_t* __restrict__ n_items,
                                                             const TI* __restrict__ Sigma,
-                                                            TI* __restrict__ zp) {
+                                                            TI* __restrict__ zp,
+                                                            const int32_t* __restrict__ sorted_seg,
+                                                            const int32_t* __restrict__ seg_rank) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
@@ -109,6 +115,9 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const int lo = items[item], hi = items[item + 1];
   const int nt = hi - lo;                 // tokens of this item (<= kSigmaChunk), one adapter
   const int cnt = nt * r;                 // outputs of this item
+  // rank of the item's segment (a multiple of 8): Sigma's entries past it and
+  // z's are neither read nor used; they stage as zeros
+  const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;
 
   // Sigma_a -> LDS as fp32: every 16-byte load of this thread is issued
   // before the first is widened and stored (one round trip, not a chain)
@@ -123,7 +132,8 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = tid + u * kSigThreads;
-      raw[u] = (e < nv) ? sa[e] : uint4{0u, 0u, 0u, 0u};
+      const int row = (e * V) / r, col = (e * V) % r;
+      raw[u] = (e < nv && row < rk && col < rk) ? sa[e] : uint4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
@@ -144,7 +154,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const float* zbase = zpart + static_cast<int64_t>(lo) * r;
   for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int q = 0; q < S; q += 16) {
+    for (int q = 0; e4 % r < rk && q < S; q += 16) {
       f32x4 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u)
@@ -227,36 +237,37 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
-                        bool diag) {
+                        bool diag, const int32_t* sorted_seg, const int32_t* seg_rank) {
+  if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
   dim3 grid(max_items);
   if (diag && Sigma) {
     if (in_dtype == 0)
       hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                         static_cast<float*>(zp));
+                         static_cast<float*>(zp), sorted_seg, seg_rank);
     else
       hipLaunchKernelGGL(sigma_diag_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                         static_cast<bf16_t*>(zp));
+                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
     return hipGetLastError();
   }
   if (r > 128) return hipErrorInvalidValue;
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp));
+                       static_cast<float*>(zp), sorted_seg, seg_rank);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp));
+                       static_cast<float*>(zp), sorted_seg, seg_rank);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp));
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp));
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
   return hipGetLastError();
 }
 

@@ -27,7 +27,7 @@ import numpy as np
 SEED_BASE = 240700066
 
 # stream ids
-_S_W, _S_U, _S_V, _S_SIG, _S_X, _S_IDS, _S_CLU, _S_A, _S_B, _S_LEN, _S_SEQ, _S_SDIAG = range(1, 13)
+_S_W, _S_U, _S_V, _S_SIG, _S_X, _S_IDS, _S_CLU, _S_A, _S_B, _S_LEN, _S_SEQ, _S_SDIAG, _S_RANK = range(1, 14)
 
 
 def _rng(cfg: int, stream: int) -> np.random.Generator:
@@ -205,6 +205,13 @@ def sigma_diagonals(cfg: int, n: int, r: int, dtype: str, var: float = 1.0) -> n
     var = 1 the scaled z'_q = sigma_i[q] z_q keeps the magnitude of z, as the
     full Sigma_i ~N(0, 1/r) does."""
     return _gauss(_rng(cfg, _S_SDIAG), (n, r), var, dtype)
+
+
+def mixed_ranks(cfg: int, count: int, r_max: int, lo: int = 16) -> np.ndarray:
+    """A rank per cluster (Sec. 3.2) or per uncompressed LoRA (App. G: ranks
+    drawn uniformly between 16 and 64): multiples of 8, uniform in [lo, r_max]."""
+    lo = min(lo, r_max)
+    return (8 * _rng(cfg, _S_RANK).integers(lo // 8, r_max // 8 + 1, size=count)).astype(np.int32)
 
 
 def make(name: str, **overrides) -> Workload:

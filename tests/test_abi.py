@@ -210,3 +210,39 @@ def test_apply_diag_rejects_overlap_with_sigma():
     ptrs = [ctypes.c_void_p(base + k * (1 << 32)) for k in range(7)]
     y = ctypes.c_void_p(ptrs[6].value + 256)               # inside sigma's 4 * 64 * 2 bytes
     assert _apply_d(p, ptrs, y=y) == B.CTS_ERR_INVALID_ARG
+
+
+# mixed-rank entry points: the rank table is one more checked pointer
+
+def test_apply_ranked_validation():
+    p = _p(n_clusters=4)
+    L = cts.lib()
+    ptr = lambda k: ctypes.c_void_p(0x5000_0000_0000 + k * (1 << 32))
+    y, ws = ctypes.c_void_p(0x7000_0000_0000), ctypes.c_void_p(0x6000_0000_0000)
+    ins = [ptr(k) for k in range(7)]
+    assert L.cts_apply_ranked(None, *ins, ptr(7), y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    assert L.cts_apply_ranked(ctypes.byref(p), *ins, None, y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    bad = ctypes.c_void_p(ptr(7).value + 2)                # rank table not 4-byte aligned
+    assert L.cts_apply_ranked(ctypes.byref(p), *ins, bad, y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    on_y = ctypes.c_void_p(y.value + 64)                   # rank table inside y
+    assert L.cts_apply_ranked(ctypes.byref(p), *ins, on_y, y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    need = cts.workspace_size(p)
+    assert L.cts_apply_ranked(ctypes.byref(p), *ins, ptr(7), y, ws, need - 1, None) == B.CTS_ERR_WORKSPACE
+    assert L.cts_apply_ranked(ctypes.byref(_p(T=0)), *[None] * 8, None, None, 0, None) == B.CTS_OK
+    assert L.cts_apply_ranked(ctypes.byref(_p(r=12)), *ins, ptr(7), y, ws, 1 << 40, None) == B.CTS_ERR_UNSUPPORTED
+
+
+def test_apply_uncompressed_ranked_validation():
+    p = _p()
+    L = cts.lib()
+    ptr = lambda k: ctypes.c_void_p(0x5000_0000_0000 + k * (1 << 32))
+    y, ws = ctypes.c_void_p(0x7000_0000_0000), ctypes.c_void_p(0x6000_0000_0000)
+    ins = [ptr(k) for k in range(5)]
+    assert L.cts_apply_uncompressed_ranked(ctypes.byref(p), *ins, None, y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    bad = ctypes.c_void_p(ptr(5).value + 1)
+    assert L.cts_apply_uncompressed_ranked(ctypes.byref(p), *ins, bad, y, ws, 1 << 40, None) == B.CTS_ERR_INVALID_ARG
+    need = cts.workspace_size(p, compressed=False)
+    assert L.cts_apply_uncompressed_ranked(ctypes.byref(p), *ins, ptr(5), y, ws, need - 1,
+                                           None) == B.CTS_ERR_WORKSPACE
+    assert L.cts_apply_uncompressed_ranked(ctypes.byref(_p(T=0)), *[None] * 6, None, None, 0,
+                                           None) == B.CTS_OK

@@ -1,0 +1,104 @@
+"""GPU parity of the mixed-rank entry points (a rank per cluster, Sec. 3.2;
+uncompressed LoRAs of different ranks, App. G) against the oracle's
+apply_ranked / apply_uncompressed_ranked, through the C ABI.  The stored
+entries past each rank are filled with NaN: the result must not see them."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2407_00066_amd as cts
+from paper_2407_00066_amd import workloads as wl
+
+from _gpu_helpers import TOL, dev, host, row_rel_err, say
+from test_gpu_parity import SMALL, _sample_tokens
+
+pytestmark = pytest.mark.gpu
+
+NAN16 = np.uint16(0x7FC0)            # a bf16 quiet NaN
+CASES = ["f32_ragged", "bf16_ragged", "bf16_large_tiles", "bf16_r128_zipf", "bf16_decode_split4",
+         "bf16_ring_ragged", "bf16_mid_tiles", "bf16_wide_split"]
+
+
+def _poisoned_compressed(w, rk):
+    nan = NAN16 if w.dtype == "bf16" else np.float32(np.nan)
+    U, Vt, S = w.U.copy(), w.Vt.copy(), w.Sigma.copy()
+    for k, r_k in enumerate(rk):
+        U[k][:, r_k:] = nan
+        Vt[k][r_k:, :] = nan
+    for i, k in enumerate(w.cluster_of):
+        r_k = rk[k]
+        S[i][r_k:, :] = nan
+        S[i][:, r_k:] = nan
+    return U, Vt, S
+
+
+@pytest.fixture(scope="module")
+def cases():
+    out = {}
+    for name in CASES:
+        kw = dict(SMALL[name])
+        w = wl.synthetic(name, **kw)
+        rk = wl.mixed_ranks(kw["cfg"], w.K, w.r, lo=8)
+        rk[0] = 0 if w.K > 1 else rk[0]          # one cluster without adapter term
+        ra = wl.mixed_ranks(kw["cfg"] + 500, w.n, w.r_l, lo=8)
+        out[name] = (w, rk, ra)
+    return out
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_apply_ranked_small(oracle_mod, cases, name):
+    w, rk, _ = cases[name]
+    U, Vt, S = _poisoned_compressed(w, rk)
+    say("apply_ranked %s ranks %s" % (name, rk.tolist()))
+    y = cts.apply_ranked(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(U), dev(Vt),
+                         dev(S), dev(rk))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    ref = oracle_mod.apply_ranked(w.x, w.adapter_id, w.cluster_of, w.W, U, Vt, S, rk)
+    assert row_rel_err(yh, ref) <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("name", ["f32_ragged", "bf16_ragged", "bf16_large_tiles", "bf16_decode_split4",
+                                  "bf16_ring_ragged"])
+def test_apply_uncompressed_ranked_small(oracle_mod, cases, name):
+    w, _, ra = cases[name]
+    nan = NAN16 if w.dtype == "bf16" else np.float32(np.nan)
+    A, B = w.A.copy(), w.B.copy()
+    for i, r_i in enumerate(ra):
+        A[i][r_i:, :] = nan
+        B[i][:, r_i:] = nan
+    say("apply_uncompressed_ranked %s" % name)
+    y = cts.apply_uncompressed_ranked(dev(w.x), dev(w.adapter_id), dev(w.W), dev(A), dev(B), dev(ra))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    ref = oracle_mod.apply_uncompressed_ranked(w.x, w.adapter_id, w.W, A, B, ra)
+    assert row_rel_err(yh, ref) <= TOL[w.dtype]
+
+
+def test_full_ranks_equal_apply(cases):
+    """Every r_k = r: bit for bit the plain entry point."""
+    w, rk, _ = cases["bf16_large_tiles"]
+    full = np.full_like(rk, w.r)
+    say("apply_ranked at full rank vs apply")
+    args = (dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(w.U), dev(w.Vt), dev(w.Sigma))
+    y_r = cts.apply_ranked(*args, dev(full))
+    y_a = cts.apply(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(y_r, y_a)
+
+
+def test_apply_ranked_prefill_full_size(oracle_mod):
+    w = wl.make("prefill_mix")
+    rk = wl.mixed_ranks(wl.CONFIGS["prefill_mix"]["cfg"], w.K, w.r)
+    U, Vt, S = _poisoned_compressed(w, rk)
+    toks = _sample_tokens(w, oracle_mod, cap=10)
+    say("apply_ranked prefill_mix (full size), %d sampled tokens" % len(toks))
+    y = cts.apply_ranked(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(U), dev(Vt),
+                         dev(S), dev(rk))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    ref = oracle_mod.apply_ranked(w.x, w.adapter_id, w.cluster_of, w.W, U, Vt, S, rk, tokens=toks)
+    assert row_rel_err(yh[toks], ref) <= TOL["bf16"]
