@@ -61,24 +61,35 @@ def to_dev(a, device):
     return torch.from_numpy(a).to(device)
 
 
-def main_kernel_model(w, touched_clusters):
+def main_kernel_model(w, touched_clusters, ranks=None):
     """Algorithmic flops and bytes of one launch of the fused GEMM
-    Y = W X + U_k Z' (bytes: W, X, Y, each touched U_k once, Z')."""
+    Y = W X + U_k Z' (bytes: W, X, Y, each touched U_k once, Z').  With
+    `ranks` (a rank per cluster) the U_k terms count r_k columns."""
     e = 2 if w.dtype == "bf16" else 4
-    flops = 2.0 * w.T * w.d_in * w.d_out + 2.0 * w.T * w.r * w.d_out
-    nbytes = e * (w.d_out * w.d_in + w.T * w.d_in + w.T * w.d_out
-                  + touched_clusters * w.d_out * w.r + w.T * w.r)
+    if ranks is None:
+        flops = 2.0 * w.T * w.d_in * w.d_out + 2.0 * w.T * w.r * w.d_out
+        nbytes = e * (w.d_out * w.d_in + w.T * w.d_in + w.T * w.d_out
+                      + touched_clusters * w.d_out * w.r + w.T * w.r)
+        return flops, nbytes
+    ks = w.cluster_of[w.adapter_id]
+    r_tok = ranks[ks].astype(float)
+    touched_r = float(sum(ranks[k] for k in set(ks.tolist())))
+    flops = 2.0 * w.T * w.d_in * w.d_out + 2.0 * r_tok.sum() * w.d_out
+    nbytes = e * (w.d_out * w.d_in + w.T * w.d_in + w.T * w.d_out + touched_r * w.d_out + r_tok.sum())
     return flops, nbytes
 
 
-def cpu_baseline(w, target_s, sigma=None):
+def cpu_baseline(w, target_s, sigma=None, ranks=None):
     """The oracle on a prefix of the batch (in batch order), grown until about
     target_s seconds of oracle time; tokens/s = tokens / oracle seconds.  With
-    `sigma` ([n][r] diagonals) the diagonal-Sigma oracle is timed."""
+    `sigma` ([n][r] diagonals) the diagonal-Sigma oracle is timed, with
+    `ranks` (a rank per cluster) the mixed-rank one."""
     import numpy as np
     from oracle import oracle
     f64 = [oracle.to_f64(a) for a in (w.x, w.W, w.U, w.Vt, w.Sigma if sigma is None else sigma)]
     fn = oracle.apply if sigma is None else oracle.apply_diag
+    if ranks is not None:
+        fn = lambda *a, **k: oracle.apply_ranked(*a[:7], ranks, **k)
     spent, done, chunk = 0.0, 0, min(64, w.T)
     while done < w.T and spent < target_s:
         toks = np.arange(done, min(w.T, done + chunk))
@@ -224,9 +235,18 @@ def bench_layer(args, torch, np, cts, B, wl, device):
     log("generating %s" % args.workload)
     w = wl.make(args.workload)
     diag = args.sigma == "diag"
+    cfg = wl.CONFIGS[args.workload]["cfg"]
     if diag:   # the diagonal-Sigma variant (Sec. 3.1, JD-Diag): Sigma holds [n][r] diagonals
-        w.Sigma = wl.sigma_diagonals(wl.CONFIGS[args.workload]["cfg"], w.n, w.r, w.dtype)
-    layer = cts.apply_diag if diag else cts.apply
+        w.Sigma = wl.sigma_diagonals(cfg, w.n, w.r, w.dtype)
+    layer = layer1 = cts.apply_diag if diag else cts.apply
+    rk = ra = None
+    if args.ranks == "mixed":   # a rank per cluster (Sec. 3.2), per uncompressed LoRA (App. G)
+        rk = wl.mixed_ranks(cfg, w.K, w.r)
+        ra = wl.mixed_ranks(cfg + 500, w.n, w.r_l, lo=8)
+        rk_d, ra_d = to_dev(rk, device), to_dev(ra, device)
+        layer = lambda *a, **k: cts.apply_ranked(*a, rk_d, **k)
+        # the one-adapter comparison keeps cluster 0 and its rank
+        layer1 = lambda *a, **k: cts.apply_ranked(*a, rk_d[:1], **k)
 
     set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
     n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
@@ -257,7 +277,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     def step1(s):
         x, W, U, Vt, S = s
-        layer(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
+        layer1(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
 
     log("timing cts_apply with one adapter")
     ms1, ms1_g = time_launches(step1, sets, args, torch)
@@ -269,7 +289,10 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     def step_u(s):
         x, W = s[0], s[1]
-        cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
+        if ra is None:
+            cts.apply_uncompressed(x, aid, W, uA, uB, out=y, workspace=wsu)
+        else:
+            cts.apply_uncompressed_ranked(x, aid, W, uA, uB, ra_d, out=y, workspace=wsu)
 
     log("timing cts_apply_uncompressed")
     ms_u, ms_u_g = time_launches(step_u, sets, args, torch)
@@ -277,7 +300,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
     del uA, uB
 
     touched = len(set(w.cluster_of[w.adapter_id].tolist()))
-    flops, nbytes = main_kernel_model(w, touched)
+    flops, nbytes = main_kernel_model(w, touched, rk)
     # the GEMM's duration: its event interval less the marker interval
     gemm_us = g_int - g_mark
     roof = roofline_of(flops, nbytes, gemm_us * 1e-6, w.dtype)
@@ -291,7 +314,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
-        cpu = cpu_baseline(w, args.cpu_seconds, sigma=w.Sigma if diag else None)
+        cpu = cpu_baseline(w, args.cpu_seconds, sigma=w.Sigma if diag else None, ranks=rk)
 
     value = w.T / (ms * 1e-3)
     value1 = w.T / (ms1 * 1e-3)
@@ -301,7 +324,8 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "graph_replay": {"value": round(w.T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5)},
         "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
-        "config": {"workload": args.workload, "sigma": args.sigma, "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
+        "config": {"workload": args.workload, "sigma": args.sigma, "ranks": args.ranks,
+                   "cluster_ranks": None if rk is None else rk.tolist(), "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
                    "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
                    "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
         "roofline": roof,
@@ -482,7 +506,18 @@ def main():
     ap.add_argument("--sigma", default="full", choices=["full", "diag"],
                     help="full r x r Sigma_i (JD-Full, the default) or diagonal Sigma_i "
                          "(JD-Diag, cts_apply_diag); single-layer workloads only")
+    ap.add_argument("--ranks", default="uniform", choices=["uniform", "mixed"],
+                    help="one rank r for every cluster (default) or a rank per cluster drawn in "
+                         "[16, r] and per uncompressed LoRA in [8, r_l] (cts_apply_ranked); "
+                         "single-layer workloads with the full Sigma only")
     args = ap.parse_args()
+
+    if args.sigma == "diag" and args.ranks == "mixed":
+        print("--sigma diag and --ranks mixed are separate variants", file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "stack32" and (args.sigma != "full" or args.ranks != "uniform"):
+        print("--sigma diag and --ranks mixed apply to the single-layer workloads", file=sys.stderr)
+        sys.exit(2)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -501,9 +536,6 @@ def main():
     torch.cuda.set_device(device)
     copy_calibration(torch, device)
     if args.workload == "stack32":
-        if args.sigma != "full":
-            print("--sigma diag applies to the single-layer workloads", file=sys.stderr)
-            sys.exit(2)
         rec = bench_stack(args, torch, np, cts, B, wl, device)
     else:
         rec = bench_layer(args, torch, np, cts, B, wl, device)
