@@ -29,7 +29,7 @@ struct Plan {
   Tile main_tile, shrink_tile;
   int main_split, shrink_split;
   int max_items, max_ctiles;
-  size_t off_perm, off_seg, off_aid, off_offs, off_items, off_nitems, off_ctiles, off_nctiles,
+  size_t off_perm, off_seg, off_aid, off_srank, off_offs, off_items, off_nitems, off_ctiles, off_nctiles,
       off_zpart, off_zp, off_ypart, total;
 };
 
@@ -132,6 +132,7 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   pl->off_perm = off;  off = align_up(off + 4ull * T);
   pl->off_seg = off;   off = align_up(off + 4ull * T);
   pl->off_aid = off;   off = align_up(off + 4ull * T);
+  pl->off_srank = off; off = align_up(off + 4ull * T);
   pl->off_offs = off;  off = align_up(off + 4ull * (pl->nseg + 1));
   pl->off_items = off; off = align_up(off + 4ull * (pl->max_items + 1));
   pl->off_nitems = off; off = align_up(off + 4);
@@ -184,6 +185,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
   int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
   int32_t* said = reinterpret_cast<int32_t*>(ws + pl.off_aid);
+  int32_t* srank = reinterpret_cast<int32_t*>(ws + pl.off_srank);
   int32_t* offs = reinterpret_cast<int32_t*>(ws + pl.off_offs);
   int32_t* items = reinterpret_cast<int32_t*>(ws + pl.off_items);
   int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
@@ -230,7 +232,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
 
   e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
                         pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag,
-                        sseg, seg_rank);
+                        sseg, seg_rank, seg_rank ? srank : nullptr);
   if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
@@ -243,6 +245,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   f.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(p->d_out) * rank * pl.elt);
   f.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * rank * pl.elt);
   f.perm = perm; f.sorted_seg = sseg; f.seg_rank = seg_rank;
+  f.sorted_rank = seg_rank ? srank : nullptr;
   f.ksplit = pl.main_split;
   f.part = pl.main_split > 1 ? ypart : nullptr;
   f.out = y; f.ldo = p->d_out; f.out_perm = 1; f.out_dtype = p->out_dtype;

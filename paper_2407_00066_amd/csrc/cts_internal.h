@@ -81,6 +81,10 @@ struct GemmParams {
   // optional rank of each segment: the segment phase of segment s reads only
   // its first rank_of(s) elements of the reduction (rank_of: see seg_rank_of)
   const int32_t* seg_rank;
+  // with seg_rank: the rank of each sorted position's segment, as seg_rank_of
+  // gives it ([N], written by the core-product stage); the LDS-ring tiles
+  // read their columns' ranks from here
+  const int32_t* sorted_rank;
   int ksplit;
   float* part;
   void* out; int64_t ldo; int out_perm; int out_dtype;
@@ -122,13 +126,14 @@ __device__ __forceinline__ int seg_rank_of(const int32_t* seg_rank, int s, int k
 // zp[j][c] = Sigma_{aid(j)}[c] * (sum_s zpart[s][j][c]).  With seg_rank, the
 // position's segment sorted_seg[j] has rank rk = seg_rank_of(seg_rank, .., r):
 // only c, c' < rk are read (Sigma's leading block, z's first rk entries) and
-// zp[j][c >= rk] = 0.  Rounded to the input type.  One workgroup per item of
-// the sort (max_items workgroups are launched; the extra ones exit).
+// zp[j][c >= rk] = 0, and sorted_rank (if not null) receives rk for every
+// position j.  Rounded to the input type.  One workgroup per item of the
+// sort (max_items workgroups are launched; the extra ones exit).
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag = false, const int32_t* sorted_seg = nullptr,
-                        const int32_t* seg_rank = nullptr);
+                        const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr);
 
 // y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,

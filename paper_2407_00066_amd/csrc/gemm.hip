@@ -494,8 +494,11 @@ struct DmaCfg {
 // (tile_of_block), so the 8 workgroups on one column tile each take every
 // 8th token row; the WSPL workgroups on one row tile (4 with 256 tiles of
 // 256x256) each take every WSPL-th weight row.
+// RANKED: the segments have ranks (p.seg_rank, with each column's rank in
+// p.sorted_rank): a cluster run takes only its adapter k-tiles below its
+// rank, from a schedule listed in LDS.
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT, int PFD = 0, int WSPL = 1,
-          int FSORT = 0>
+          int FSORT = 0, int RANKED = 0>
 __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const GemmParams p) {
   using C = DmaCfg<BM, BN, BK, WM, WN, MB, P, DIRECT>;
   static_assert(PFD == 0 || P <= 3, "prefetch wait counts cover rings of two or three stages");
@@ -510,6 +513,9 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __shared__ int32_t t_seg[BN];
   __shared__ int32_t run_start[BN + 1];
   __shared__ int32_t wave_runs[C::NW];
+  __shared__ uint2 sched[RANKED ? 2 * BN : 1];             // adapter k-tiles (K1 <= 2 BK)
+  __shared__ int32_t t_rank[RANKED ? BN : 1];
+  __shared__ int32_t n_sched_s;
   __shared__ uint32_t pf_sink[PFD > 0 ? 64 : 1];
   constexpr int FS = FSORT ? kFuseSortMaxT : 1;
   __shared__ uint32_t fs_raw[FS], fs_key[FS];                // keys in token order, sorted
@@ -615,7 +621,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   static_assert(BN <= C::NT, "one token column per thread");
 
   // ---- token columns of this tile (loads only; stored to LDS below) -------
-  int v_perm = 0, v_seg = 0;
+  int v_perm = 0, v_seg = 0, v_rank = 0;
   if (tid < jn) {
     if (FSORT) {
       v_perm = fs_perm[j0 + tid];
@@ -623,6 +629,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     } else {
       v_perm = p.perm[j0 + tid];
       v_seg = p.sorted_seg ? p.sorted_seg[j0 + tid] : 0;
+      if (RANKED) v_rank = p.sorted_rank[j0 + tid];
     }
   }
 
@@ -689,6 +696,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   if (tid < BN) {
     t_perm[tid] = v_perm;
     t_seg[tid] = v_seg;
+    if (RANKED) t_rank[tid] = v_rank;
   }
   __syncthreads();
   int n_runs = 0;
@@ -717,7 +725,42 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __syncthreads();
 
   // ---- k-tile schedule: the dense tiles, then each cluster run's tiles ------
-  const int ntiles = nd + n_runs * ns;
+  // With ranks, run q takes only its k-tiles of this split below its rank
+  // (the k-tiles past a cluster's rank are not visited).  Wave 0 lists the
+  // adapter k-tiles in LDS, run by run: .x = first column | columns << 9 |
+  // k-tile << 18, .y = segment | rank << 16.
+  int n_sched = n_runs * ns;
+  if (RANKED && n_runs > 0 && ns > 0) {
+    if (wave == 0) {
+      int tot = 0;
+      for (int base = 0; base < n_runs; base += 64) {
+        const int q = base + lane;
+        int c = 0;
+        uint32_t ex = 0, ey = 0;
+        if (q < n_runs) {
+          const int lo = run_start[q], hi = run_start[q + 1];
+          const int seg = t_seg[lo];
+          const int kl = min(max(t_rank[lo], 0), K1);
+          c = max(0, min(s_hi, (kl + BK - 1) / BK) - s_lo);
+          ex = static_cast<uint32_t>(lo) | (static_cast<uint32_t>(hi - lo) << 9);
+          ey = static_cast<uint32_t>(seg) | (static_cast<uint32_t>(kl) << 16);
+        }
+        int x = c;                                          // inclusive scan over the wave
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+          const int y = __shfl_up(x, d);
+          if (lane >= d) x += y;
+        }
+        for (int i = 0; i < c; ++i)
+          sched[tot + x - c + i] = make_uint2(ex | (static_cast<uint32_t>(s_lo + i) << 18), ey);
+        tot += __shfl(x, 63);
+      }
+      if (lane == 0) n_sched_s = tot;
+    }
+    __syncthreads();
+    n_sched = n_sched_s;
+  }
+  const int ntiles = nd + n_sched;
 
   // ---- token operand rows -------------------------------------------------
 #pragma unroll
@@ -765,7 +808,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     uint32_t kk, kmask, span, dsel;   // kk: uniform k byte offset of the k-tile
     int lo;
   };
-  auto prep_next = [&, jn, n_runs, nd, ntiles, d_lo, s_lo, s_hi]() __attribute__((always_inline)) {
+  auto prep_next = [&, jn, n_runs, n_sched, nd, ntiles, s_lo, s_hi]() __attribute__((always_inline)) {
     TileLoad L;
     const bool valid = lt < ntiles;
     uint32_t k0, klim;
@@ -779,6 +822,22 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       L.dsel = 0xffffffffu;
       k0 = static_cast<uint32_t>(dk(lt) * BK);
       klim = static_cast<uint32_t>(K0);
+    } else if (RANKED) {
+      // adapter phase with ranks: the next entry of the schedule (past its
+      // end, while the ring runs dry, the loads are masked off)
+      const uint2 e = sched[min(lq, max(n_sched - 1, 0))];
+      const uint32_t ex = valid ? __builtin_amdgcn_readfirstlane(e.x) : 0u;
+      const uint32_t ey = valid ? __builtin_amdgcn_readfirstlane(e.y) : 0u;
+      L.lo = static_cast<int>(ex & 511u);
+      L.span = (ex >> 9) & 511u;
+      const int seg = static_cast<int>(ey & 0xffffu);
+      L.rA = make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
+                       p.a1_seg_bytes);
+      L.rB = rB1;
+      L.dsel = 0u;
+      k0 = (ex >> 18) * BK;
+      klim = ey >> 16;
+      ++lq;
     } else {
       // adapter phase (U_k Z'): one cluster run of the tile per k-tile group
       const int q = min(lq, max(n_runs - 1, 0));
@@ -793,7 +852,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       // offset arrays would make the compiler keep them in scratch memory)
       L.dsel = 0u;
       k0 = static_cast<uint32_t>(lkt * BK);
-      klim = static_cast<uint32_t>(p.seg_rank ? seg_rank_of(p.seg_rank, seg, K1) : K1);
+      klim = static_cast<uint32_t>(K1);
       ++lkt;
       if (lkt >= s_hi) { lkt = s_lo; ++lq; }
     }
@@ -1062,13 +1121,26 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0, int PFD = 0,
-          int WSPL = 1, int FSORT = 0>
-hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
+          int WSPL = 1, int FSORT = 0, int RANKED = 0>
+hipError_t launch_dma1(const GemmParams& p, hipStream_t stream) {
   const int gn = (p.tile_start || FSORT) ? p.max_tiles : (p.N + BN - 1) / BN;
   dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT>), grid,
-                     dim3(WM * WN * 64), 0, stream, p);
+  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT, RANKED>),
+                     grid, dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();
+}
+
+// A segment phase with a rank table takes the RANKED kernel; its schedule
+// holds at most two k-tiles per cluster run.
+template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0, int PFD = 0,
+          int WSPL = 1, int FSORT = 0>
+hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
+  const bool ranked = p.seg_rank && p.sorted_seg && p.K1 > 0 && !p.tile_start && !FSORT;
+  if (!ranked) return launch_dma1<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT>(p, stream);
+  if (p.K1 > 2 * BK || !p.sorted_rank) return hipErrorInvalidValue;
+  if constexpr (FSORT == 0)
+    return launch_dma1<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, 0, 1>(p, stream);
+  return hipErrorInvalidValue;
 }
 
 template <typename TI, int BM, int BN, int BK, int WM, int WN, int STAGES, int OCC, int MB = 16>

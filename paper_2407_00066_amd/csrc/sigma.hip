@@ -61,13 +61,15 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
                                                                  const TI* __restrict__ sigma,
                                                                  TI* __restrict__ zp,
                                                                  const int32_t* __restrict__ sorted_seg,
-                                                                 const int32_t* __restrict__ seg_rank) {
+                                                                 const int32_t* __restrict__ seg_rank,
+                                                                 int32_t* __restrict__ sorted_rank) {
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
   const int tid = threadIdx.x;
   const int lo = items[item], hi = items[item + 1];
   const int cnt = (hi - lo) * r;
   const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;   // a multiple of 8
+  if (sorted_rank && tid < hi - lo) sorted_rank[lo + tid] = rk;
   int a = sorted_aid[lo];
   a = a < 0 ? 0 : (a >= n ? n - 1 : a);
   const TI* sa = sigma + static_cast<int64_t>(a) * r;
@@ -104,7 +106,8 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             const TI* __restrict__ Sigma,
                                                             TI* __restrict__ zp,
                                                             const int32_t* __restrict__ sorted_seg,
-                                                            const int32_t* __restrict__ seg_rank) {
+                                                            const int32_t* __restrict__ seg_rank,
+                                                            int32_t* __restrict__ sorted_rank) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
@@ -118,6 +121,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   // rank of the item's segment (a multiple of 8): Sigma's entries past it and
   // z's are neither read nor used; they stage as zeros
   const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;
+  if (sorted_rank && tid < nt) sorted_rank[lo + tid] = rk;
 
   // Sigma_a -> LDS as fp32: every 16-byte load of this thread is issued
   // before the first is widened and stored (one round trip, not a chain)
@@ -237,37 +241,39 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
-                        bool diag, const int32_t* sorted_seg, const int32_t* seg_rank) {
+                        bool diag, const int32_t* sorted_seg, const int32_t* seg_rank,
+                        int32_t* sorted_rank) {
   if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
+  if (sorted_rank && !seg_rank) return hipErrorInvalidValue;
   dim3 grid(max_items);
   if (diag && Sigma) {
     if (in_dtype == 0)
       hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                         static_cast<float*>(zp), sorted_seg, seg_rank);
+                         static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
     else
       hipLaunchKernelGGL(sigma_diag_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
+                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
     return hipGetLastError();
   }
   if (r > 128) return hipErrorInvalidValue;
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
   return hipGetLastError();
 }
 

@@ -102,3 +102,30 @@ def test_apply_ranked_prefill_full_size(oracle_mod):
     assert np.isfinite(yh).all()
     ref = oracle_mod.apply_ranked(w.x, w.adapter_id, w.cluster_of, w.W, U, Vt, S, rk, tokens=toks)
     assert row_rel_err(yh[toks], ref) <= TOL["bf16"]
+
+
+# More than 64 cluster runs in one token tile (the rank schedule is listed 64
+# runs at a time), many clusters at rank 0 or at most one k-tile: the 128x128
+# tiles (T = 512, d_out = 4096) and the 256x256 tiles (T = 2100).
+MANY_RUNS = {
+    "many_runs_mid": dict(cfg=130, T=512, d_in=256, d_out=4096, r=64, n=600, K=400),
+    "many_runs_large": dict(cfg=131, T=2100, d_in=128, d_out=256, r=128, n=900, K=500),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MANY_RUNS))
+def test_apply_ranked_many_runs(oracle_mod, name):
+    kw = MANY_RUNS[name]
+    w = wl.synthetic(name, **kw)
+    rs = np.random.default_rng(kw["cfg"])
+    rk = rs.choice(np.array([0, 8, 24, w.r // 2, w.r], dtype=np.int32), size=w.K).astype(np.int32)
+    U, Vt, S = _poisoned_compressed(w, rk)
+    say("apply_ranked %s (T=%d K=%d)" % (name, w.T, w.K))
+    y = cts.apply_ranked(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(U), dev(Vt),
+                         dev(S), dev(rk))
+    torch.cuda.synchronize()
+    yh = host(y)
+    assert np.isfinite(yh).all()
+    toks = np.arange(0, w.T, 5)                  # every fifth token: all tiles, seconds of oracle time
+    ref = oracle_mod.apply_ranked(w.x, w.adapter_id, w.cluster_of, w.W, U, Vt, S, rk, tokens=toks)
+    assert row_rel_err(yh[toks], ref) <= TOL[w.dtype]
