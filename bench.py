@@ -240,7 +240,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         w.Sigma = wl.sigma_diagonals(cfg, w.n, w.r, w.dtype)
     layer = layer1 = cts.apply_diag if diag else cts.apply
     rk = ra = None
-    if args.ranks == "mixed":   # a rank per cluster (Sec. 3.2), per uncompressed LoRA (App. G)
+    if args.ranks == "mixed":   # a rank per cluster (Sec. 3.2), per uncompressed LoRA (App. H)
         rk = wl.mixed_ranks(cfg, w.K, w.r)
         ra = wl.mixed_ranks(cfg + 500, w.n, w.r_l, lo=8)
         rk_d, ra_d = to_dev(rk, device), to_dev(ra, device)

@@ -150,7 +150,7 @@ int cts_apply_uncompressed(const cts_problem* p, const void* x, const int32_t* a
                            const void* W, const void* A, const void* B, void* y,
                            void* workspace, size_t workspace_bytes, void* stream);
 
-/* Uncompressed LoRAs of different ranks (App. G): as cts_apply_uncompressed,
+/* Uncompressed LoRAs of different ranks (App. H): as cts_apply_uncompressed,
  * with A, B stored at the largest rank p->r_lora and rank_of_adapter (device
  * int32 [n], 4-byte aligned) giving r_i: the layer uses B_i[:, :r_i]
  * A_i[:r_i, :]; entries past r_i are never read into the result.  Each r_i

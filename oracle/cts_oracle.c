@@ -23,7 +23,7 @@
  * and, for the uncompressed comparison path, Delta_i = B_i A_i.
  * Sec. 3.1, the diagonal variant (eq. JD-Diag): Sigma_i is diagonal, given as
  * its r diagonal entries sigma_i, and Delta_i = U_k diag(sigma_i) V_k^T.
- * Mixed ranks (Sec. 3.2: each cluster is given its own rank; App. G: LoRAs of
+ * Mixed ranks (Sec. 3.2: each cluster is given its own rank; App. H: LoRAs of
  * different ranks): arrays are stored at the largest rank, cluster k uses its
  * first r_k columns of U_k, rows of V_k^T and the leading r_k x r_k block of
  * Sigma_i, and uncompressed adapter i its first r_i columns of B_i and rows

@@ -16,7 +16,7 @@ Conventions
 ``apply_diag`` is the diagonal-Sigma variant of Sec. 3.1 (eq. JD-Diag) with
 ``sigma[n][r]`` holding the diagonals.  ``apply_ranked`` and
 ``apply_uncompressed_ranked`` take mixed ranks (a rank per cluster, Sec. 3.2;
-a rank per uncompressed LoRA, App. G) over arrays stored at the largest rank.
+a rank per uncompressed LoRA, App. H) over arrays stored at the largest rank.
 
 Besides the apply/sort oracles this module holds ``exact_compress``: the
 lossless JD-Full construction of Proposition 1 with Sigma_i taken from the
@@ -203,7 +203,7 @@ def apply_ranked(x, adapter_id, cluster_of, W, U, Vt, Sigma, rank_of_cluster, to
 
 
 def apply_uncompressed_ranked(x, adapter_id, W, A, B, rank_of_adapter, tokens=None, timing=None):
-    """Uncompressed LoRAs of different ranks (App. G): y[s] = (W + B_i[:, :r_i]
+    """Uncompressed LoRAs of different ranks (App. H): y[s] = (W + B_i[:, :r_i]
     A_i[:r_i, :]) x_t with r_i = rank_of_adapter[i]; A, B stored at the
     largest rank."""
     x64, W64, A64, B64 = (np.ascontiguousarray(to_f64(a)) for a in (x, W, A, B))

@@ -208,7 +208,7 @@ def sigma_diagonals(cfg: int, n: int, r: int, dtype: str, var: float = 1.0) -> n
 
 
 def mixed_ranks(cfg: int, count: int, r_max: int, lo: int = 16) -> np.ndarray:
-    """A rank per cluster (Sec. 3.2) or per uncompressed LoRA (App. G: ranks
+    """A rank per cluster (Sec. 3.2) or per uncompressed LoRA (App. H: ranks
     drawn uniformly between 16 and 64): multiples of 8, uniform in [lo, r_max]."""
     lo = min(lo, r_max)
     return (8 * _rng(cfg, _S_RANK).integers(lo // 8, r_max // 8 + 1, size=count)).astype(np.int32)

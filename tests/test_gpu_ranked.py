@@ -1,5 +1,5 @@
 """GPU parity of the mixed-rank entry points (a rank per cluster, Sec. 3.2;
-uncompressed LoRAs of different ranks, App. G) against the oracle's
+uncompressed LoRAs of different ranks, App. H) against the oracle's
 apply_ranked / apply_uncompressed_ranked, through the C ABI.  The stored
 entries past each rank are filled with NaN: the result must not see them."""
 import numpy as np

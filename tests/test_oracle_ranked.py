@@ -1,5 +1,5 @@
 """Pins of the oracle's mixed-rank functions (Sec. 3.2: each cluster its own
-rank; App. G: LoRAs of different ranks).  Arrays are stored at the largest
+rank; App. H: LoRAs of different ranks).  Arrays are stored at the largest
 rank; a cluster (or uncompressed adapter) uses only its leading block.  The
 pins: a hand-worked example with poison in the unused entries, the full-rank
 oracles on zero-padded arrays, NaN in every unused entry, the plain-LoRA
