@@ -34,7 +34,10 @@ Readings (where the paper leaves a choice open):
   starts from the centroids Sigma_{i} of the given LoRA indices (ties and
   empty clusters: lowest index wins; an empty cluster keeps its centroid /
   bases); per-cluster JD-Full starts from the given per-cluster bases each
-  round; a LoRA moves to the cluster maximizing ||U_j^T B_i A_i V_j||_F^2,
+  round, and runs only for a cluster whose members supply at least r
+  directions (members x r_l >= r; with fewer the rank-r problem has no unique
+  solution and the cluster keeps its bases); a LoRA moves to the cluster
+  maximizing ||U_j^T B_i A_i V_j||_F^2,
   which for orthonormal U_j, V_j is the cluster minimizing
   min_Sigma ||B_i A_i - U_j Sigma V_j^T||_F^2.
 """
@@ -152,21 +155,29 @@ def jd_full_alternating(A, B, r, U0, V0, iters=10, tau=None):
     return U, V, sigma_star(U, V, A, B), hist
 
 
-def jd_full_eig(A, B, r, U0, V0, iters=10, tau=None):
-    """App. A.2 eigenvalue iteration: from the pair (U, V),
+def eig_step(A, B, U, V):
+    """One step of the App. A.2 eigenvalue iteration from the pair (U, V):
     U0' = sum_i B_i (A_i V)(V^T A_i^T)(B_i^T U),
     V0' = sum_i A_i^T (B_i^T U)(U^T B_i)(A_i V),
-    then U, V = orthogonalize(U0'), orthogonalize(V0').  Returns U, V, Sigma
-    (eq. sigmastar) and the per-round criteria."""
+    returns orthogonalize(U0'), orthogonalize(V0')."""
+    A = np.asarray(A, np.float64)
+    B = np.asarray(B, np.float64)
+    Un0 = sum(B[i] @ (A[i] @ V) @ (V.T @ A[i].T) @ (B[i].T @ U) for i in range(A.shape[0]))
+    Vn0 = sum(A[i].T @ (B[i].T @ U) @ (U.T @ B[i]) @ (A[i] @ V) for i in range(A.shape[0]))
+    return orthogonalize(Un0), orthogonalize(Vn0)
+
+
+def jd_full_eig(A, B, r, U0, V0, iters=10, tau=None):
+    """App. A.2 eigenvalue iteration: `iters` steps of eig_step (or until the
+    criterion drops below tau).  Returns U, V, Sigma (eq. sigmastar) and the
+    per-round criteria."""
     A = np.asarray(A, np.float64)
     B = np.asarray(B, np.float64)
     U = np.asarray(U0, np.float64)
     V = np.asarray(V0, np.float64)
     crits = []
     for _ in range(iters):
-        Un0 = sum(B[i] @ (A[i] @ V) @ (V.T @ A[i].T) @ (B[i].T @ U) for i in range(A.shape[0]))
-        Vn0 = sum(A[i].T @ (B[i].T @ U) @ (U.T @ B[i]) @ (A[i] @ V) for i in range(A.shape[0]))
-        Un, Vn = orthogonalize(Un0), orthogonalize(Vn0)
+        Un, Vn = eig_step(A, B, U, V)
         c = criterion(U, Un, V, Vn)
         U, V = Un, Vn
         crits.append(c)
@@ -253,7 +264,7 @@ def jd_cluster(A, B, k, r, U0, V0, Uc0, Vc0, init_idx, jd_iters=10, max_rounds=2
     for rounds in range(1, max_rounds + 1):
         for j in range(k):
             m = labels == j
-            if np.any(m):
+            if np.count_nonzero(m) * A.shape[1] >= r:
                 Us[j], Vs[j], _, _ = jd(A[m], B[m], r, Uc0[j], Vc0[j], jd_iters)
         new = np.argmax(assign_scores(Us, Vs, A, B), axis=1)
         if np.array_equal(new, labels):

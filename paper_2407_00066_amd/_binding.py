@@ -1,4 +1,4 @@
-"""ctypes binding of libcts.so (include/cts.h).
+"""ctypes binding of libcts.so (include/cts.h, include/cts_compress.h).
 
 Argument marshalling only: shapes, dtypes and devices are checked, raw
 device pointers and the current HIP stream are handed to the C library, and
@@ -24,7 +24,10 @@ CTS_F32, CTS_BF16 = 0, 1
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
-            "cts_set_stage_events")
+            "cts_set_stage_events",
+            # include/cts_compress.h
+            "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
+            "cts_jd_sigma", "cts_jd_cluster")
 N_STAGE_EVENTS = 6
 
 
@@ -32,6 +35,11 @@ class CtsError(RuntimeError):
     def __init__(self, code: int, where: str):
         self.code = code
         super().__init__("%s: %s" % (where, status_string(code)))
+
+
+class JdProblem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("d_out", ctypes.c_int32), ("d_in", ctypes.c_int32),
+                ("r_lora", ctypes.c_int32), ("r", ctypes.c_int32)]
 
 
 class Problem(ctypes.Structure):
@@ -75,6 +83,21 @@ def lib() -> ctypes.CDLL:
                 L.cts_validate_ids.restype = ctypes.c_int
                 L.cts_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
                 L.cts_set_stage_events.restype = ctypes.c_int
+                jp, fl = ctypes.POINTER(JdProblem), ctypes.c_float
+                L.cts_jd_workspace_size.argtypes = [jp]
+                L.cts_jd_workspace_size.restype = sz
+                L.cts_jd_cluster_workspace_size.argtypes = [jp, i32]
+                L.cts_jd_cluster_workspace_size.restype = sz
+                L.cts_lora_norms2.argtypes = [jp, vp, vp, vp, vp, sz, vp]
+                L.cts_lora_norms2.restype = ctypes.c_int
+                L.cts_jd_full.argtypes = [jp, vp, vp, vp, vp, i32, fl, i32, vp, vp, vp, vp,
+                                          ctypes.POINTER(i32), vp, sz, vp]
+                L.cts_jd_full.restype = ctypes.c_int
+                L.cts_jd_sigma.argtypes = [jp, vp, vp, vp, vp, vp, vp, sz, vp]
+                L.cts_jd_sigma.restype = ctypes.c_int
+                L.cts_jd_cluster.argtypes = [jp, i32, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i32), i32, i32,
+                                             i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, sz, vp]
+                L.cts_jd_cluster.restype = ctypes.c_int
                 _lib = L
     return _lib
 

@@ -1,0 +1,1108 @@
+// Offline compressor: joint diagonalization of a LoRA collection by the
+// eigenvalue iteration of App. A.2 and the clustering of App. A.3, fp32.
+//
+// One iteration from the pair (U, V) (bases as [d][r] row-major):
+//   project:  P_i = A_i V, Q_i = B_i^T U          (r_l x r per LoRA, fp32 MFMA)
+//             C_i = (P_i P_i^T) Q_i, D_i = (Q_i Q_i^T) P_i   (in LDS)
+//   expand:   U' = sum_i B_i C_i, V' = sum_i A_i^T D_i   (fp32 MFMA, split over
+//             the collection, partials summed in fixed order)
+//   orthogonalize U', V' by CholeskyQR2 (Gram, Cholesky and triangular
+//   inverse in one workgroup, X R^-1), and the convergence measure.
+// C_i and D_i regroup the paper's chain B_i (A_i V)(V^T A_i^T)(B_i^T U) as
+// B_i ((A_i V)(A_i V)^T)(B_i^T U): the same product, with r_l x r_l inner
+// Gram matrices.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "cts.h"
+#include "cts_compress.h"
+#include "cts_internal.h"
+
+namespace cts {
+namespace {
+
+constexpr int kJT = 256;        // threads per workgroup
+constexpr int kBK = 32;         // k per staged tile
+constexpr int kTM = 64;         // rows per output tile
+constexpr int kRMax = 128;      // largest JD rank
+constexpr int kALD = kBK + 4;   // A tile, m-major: row stride (floats)
+constexpr int kAML = kTM + 16;  // A tile, k-major: row stride
+constexpr int kBLD = kRMax + 16;  // B tile (k-major, r columns): row stride
+constexpr int kAS = (kTM * kALD > kBK * kAML) ? kTM * kALD : kBK * kAML;
+constexpr int kBS = kBK * kBLD;
+constexpr int kStage = kAS + kBS;  // floats per staging buffer
+constexpr int kEpLd = kRMax + 1;   // epilogue rows (odd stride)
+constexpr int kGramRows = 256;     // rows per Gram partial
+constexpr int kMaxKm = 100;        // k-means iterations
+
+__device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- loaders
+// A loader fills slot e (0 <= e < 512: 64 x 32 floats as float4) of the A tile
+// at k0 and gives its LDS offset; a B loader fills slot e (< 8 r) of the
+// 32 x r B tile.  Out-of-range slots read zeros.
+
+// P_i = A_i V: rows m = (LoRA q of the group, row l), k along d_in.
+struct LoadLoraRows {
+  const float* A; const int32_t* lidx; int q0, nq, r_l, d_in;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int m = e >> 3, kq = e & 7;
+    off = m * kALD + 4 * kq;
+    const int q = m / r_l, l = m - q * r_l, k = k0 + 4 * kq;
+    if (q >= nq || k >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
+    const int64_t row = static_cast<int64_t>(lidx[q0 + q]) * r_l + l;
+    return *reinterpret_cast<const float4*>(A + row * d_in + k);
+  }
+};
+
+// Q_i = B_i^T U: k = output row o, m = (LoRA q, column l); a LoRA's 32 x r_l
+// block of rows o is contiguous.
+struct LoadLoraBt {
+  const float* B; const int32_t* lidx; int q0, nq, r_l, d_out;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int per = 8 * r_l;                     // float4 per LoRA block
+    const int q = e / per, rem = e - q * per;
+    const int kk = rem / (r_l >> 2), l = 4 * (rem - kk * (r_l >> 2));
+    off = kk * kAML + q * r_l + l;
+    const int o = k0 + kk;
+    if (q >= nq || o >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
+    const int64_t base = static_cast<int64_t>(lidx[q0 + q]) * d_out * r_l;
+    return *reinterpret_cast<const float4*>(B + base + static_cast<int64_t>(o) * r_l + l);
+  }
+};
+
+// U' = sum B_i C_i: rows m = output row o, k = flat (LoRA, l) index f; a
+// LoRA's 64 x w block (w = min(r_l, 32) columns from l0) is read row by row.
+struct LoadExpandB {
+  const float* B; const int32_t* lidx; int r_l, d_out, o0, f_end;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int w = r_l < kBK ? r_l : kBK;
+    const int w4 = w >> 2;
+    const int j4 = e % w4, m = (e / w4) & (kTM - 1), qq = e / (w4 * kTM);
+    off = m * kALD + qq * w + 4 * j4;
+    const int f = k0 + qq * w + 4 * j4;       // k0: flat index of the tile
+    const int o = o0 + m;
+    if (f >= f_end || o >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
+    const int q = f / r_l, l = f - q * r_l;
+    const int64_t base = static_cast<int64_t>(lidx[q]) * d_out * r_l;
+    return *reinterpret_cast<const float4*>(B + base + static_cast<int64_t>(o) * r_l + l);
+  }
+};
+
+// V' = sum A_i^T D_i: k = flat (LoRA, l), m = input column c.
+struct LoadExpandA {
+  const float* A; const int32_t* lidx; int r_l, d_in, c0, f_end;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int kk = e >> 4, m4 = e & 15;
+    off = kk * kAML + 4 * m4;
+    const int f = k0 + kk, c = c0 + 4 * m4;
+    if (f >= f_end || c >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
+    const int q = f / r_l, l = f - q * r_l;
+    const int64_t row = static_cast<int64_t>(lidx[q]) * r_l + l;
+    return *reinterpret_cast<const float4*>(A + row * d_in + c);
+  }
+};
+
+// B tile: rows k of an [K][r] array (a basis, or C / D rows).
+struct LoadRowsR {
+  const float* X; int r, K;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int r4 = r >> 2;
+    const int kk = e / r4, n = 4 * (e - kk * r4);
+    off = kk * kBLD + n;
+    const int k = k0 + kk;
+    if (k >= K) return float4{0.f, 0.f, 0.f, 0.f};
+    return *reinterpret_cast<const float4*>(X + static_cast<int64_t>(k) * r + n);
+  }
+};
+
+// acc[nb] += A(rows 16 w + ..., k) B(k, 16 nb + ...) over k in [k_begin,
+// k_end), tiles of 32 double-buffered through registers.  Lane l of wave w
+// holds rows 16 w + 4 (l / 16) + v, column 16 nb + l % 16 of block nb.
+template <bool AKM, typename LA, typename LB>
+__device__ void tile_gemm(float* smem, int k_begin, int k_end, int r, const LA& la, const LB& lb,
+                          f32x4 (&acc)[kRMax / 16]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fk = lane >> 4;
+  const int nb_n = r >> 4;
+  const int nbq = 8 * r;                                  // B float4 slots
+  constexpr int NAQ = kTM * kBK / 4 / kJT;                // 2 A slots per thread
+  constexpr int NBQ = kBK * kRMax / 4 / kJT;              // up to 4 B slots per thread
+  float4 ra[NAQ], rb[NBQ];
+  int oa[NAQ], ob[NBQ];
+  const int nt = (k_end - k_begin + kBK - 1) / kBK;
+  auto fetch = [&](int t) {
+    const int k0 = k_begin + t * kBK;
+#pragma unroll
+    for (int u = 0; u < NAQ; ++u) ra[u] = la(tid + u * kJT, k0, oa[u]);
+#pragma unroll
+    for (int u = 0; u < NBQ; ++u) {
+      const int e = tid + u * kJT;
+      if (e < nbq) rb[u] = lb(e, k0, ob[u]);
+    }
+  };
+  auto stash = [&](int buf) {
+    float* As = smem + buf * kStage;
+    float* Bs = As + kAS;
+#pragma unroll
+    for (int u = 0; u < NAQ; ++u) *reinterpret_cast<float4*>(As + oa[u]) = ra[u];
+#pragma unroll
+    for (int u = 0; u < NBQ; ++u)
+      if (tid + u * kJT < nbq) *reinterpret_cast<float4*>(Bs + ob[u]) = rb[u];
+  };
+  if (nt <= 0) return;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    if (t + 1 < nt) fetch(t + 1);
+    const float* As = smem + (t & 1) * kStage;
+    const float* Bs = As + kAS;
+    const int m = 16 * wave + fr;
+#pragma unroll
+    for (int s = 0; s < kBK / 4; ++s) {
+      const int k = 4 * s + fk;
+      const float a = AKM ? As[k * kAML + m] : As[m * kALD + k];
+#pragma unroll
+      for (int nb = 0; nb < kRMax / 16; ++nb)
+        if (nb < nb_n) acc[nb] = mfma4(a, Bs[k * kBLD + 16 * nb + fr], acc[nb]);
+    }
+    if (t + 1 < nt) stash((t + 1) & 1);
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[kRMax / 16]) {
+#pragma unroll
+  for (int nb = 0; nb < kRMax / 16; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// accumulators -> LDS rows [64][kEpLd]
+__device__ __forceinline__ void acc_to_lds(const f32x4 (&acc)[kRMax / 16], float* dst, int r) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fk = lane >> 4;
+#pragma unroll
+  for (int nb = 0; nb < kRMax / 16; ++nb)
+    if (nb < (r >> 4))
+#pragma unroll
+      for (int v = 0; v < 4; ++v) dst[(16 * wave + 4 * fk + v) * kEpLd + 16 * nb + fr] = acc[nb][v];
+}
+
+// ------------------------------------------------------------ project kernel
+struct ProjArgs {
+  const float* A; const float* B; const float* V; const float* U;
+  const int32_t* lidx; int m;
+  int r_l, d_in, d_out, r;
+  int mode;                     // 0: C, D   1: Sigma   2: score
+  const float* w2;              // mode 0: per-LoRA weight of C, D (by id), or null
+  const float* sscale;          // mode 1: per-LoRA scale of Sigma (by id), or null
+  float* C; float* D;           // [m][r_l][r] by list position
+  float* Sigma;                 // [n][r][r] by id
+  float* score; int ld_score, score_col;
+};
+
+constexpr int kProjSmem = (2 * kTM * kEpLd + 2 * kTM * 64 > 2 * kStage) ? 2 * kTM * kEpLd + 2 * kTM * 64
+                                                                      : 2 * kStage;
+
+__global__ __launch_bounds__(kJT) void jd_project_kernel(const ProjArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[kProjSmem];
+  const int lpw = kTM / a.r_l;                       // LoRAs per workgroup
+  const int q0 = blockIdx.x * lpw;
+  const int nq = min(lpw, a.m - q0);
+  if (nq <= 0) return;
+  const int tid = threadIdx.x;
+  const int r = a.r, r_l = a.r_l;
+
+  f32x4 accP[kRMax / 16], accQ[kRMax / 16];
+  zero_acc(accP);
+  zero_acc(accQ);
+  tile_gemm<false>(smem, 0, a.d_in, r, LoadLoraRows{a.A, a.lidx, q0, nq, r_l, a.d_in},
+                   LoadRowsR{a.V, r, a.d_in}, accP);
+  tile_gemm<true>(smem, 0, a.d_out, r, LoadLoraBt{a.B, a.lidx, q0, nq, r_l, a.d_out},
+                  LoadRowsR{a.U, r, a.d_out}, accQ);
+  float* Ps = smem;
+  float* Qs = smem + kTM * kEpLd;
+  acc_to_lds(accP, Ps, r);
+  acc_to_lds(accQ, Qs, r);
+  __syncthreads();
+  const int rows = nq * r_l;
+
+  if (a.mode == 0) {
+    // G_q = P_q P_q^T, H_q = Q_q Q_q^T (r_l x r_l per LoRA)
+    float* Gs = Qs + kTM * kEpLd;
+    float* Hs = Gs + kTM * 64;
+    const int ng = rows * r_l;                        // entries of all G_q
+    for (int e = tid; e < ng; e += kJT) {
+      const int row = e / r_l, l2 = e - row * r_l;
+      const int q = row / r_l;
+      const float* p1 = Ps + row * kEpLd;
+      const float* p2 = Ps + (q * r_l + l2) * kEpLd;
+      const float* s1 = Qs + row * kEpLd;
+      const float* s2 = Qs + (q * r_l + l2) * kEpLd;
+      float g = 0.f, h = 0.f;
+      for (int j = 0; j < r; ++j) {
+        g = fmaf(p1[j], p2[j], g);
+        h = fmaf(s1[j], s2[j], h);
+      }
+      Gs[e] = g;
+      Hs[e] = h;
+    }
+    __syncthreads();
+    // C_q = w G_q Q_q, D_q = w H_q P_q
+    const int nc = rows * r;
+    for (int e = tid; e < nc; e += kJT) {
+      const int row = e / r, j = e - row * r;
+      const int q = row / r_l;
+      const float* g = Gs + row * r_l;
+      const float* h = Hs + row * r_l;
+      float c = 0.f, d = 0.f;
+      for (int l2 = 0; l2 < r_l; ++l2) {
+        c = fmaf(g[l2], Qs[(q * r_l + l2) * kEpLd + j], c);
+        d = fmaf(h[l2], Ps[(q * r_l + l2) * kEpLd + j], d);
+      }
+      const float w = a.w2 ? a.w2[a.lidx[q0 + q]] : 1.f;
+      const int64_t f = static_cast<int64_t>(q0) * r_l + row;
+      a.C[f * r + j] = c * w;
+      a.D[f * r + j] = d * w;
+    }
+    return;
+  }
+  // Sigma_q[x][y] = sum_l Q_q[l][x] P_q[l][y]
+  const int rr = r * r;
+  if (a.mode == 1) {
+    for (int e = tid; e < nq * rr; e += kJT) {
+      const int q = e / rr, xy = e - q * rr, x = xy / r, y = xy - x * r;
+      float s = 0.f;
+      for (int l = 0; l < r_l; ++l) s = fmaf(Qs[(q * r_l + l) * kEpLd + x], Ps[(q * r_l + l) * kEpLd + y], s);
+      const int id = a.lidx[q0 + q];
+      if (a.sscale) s *= a.sscale[id];
+      a.Sigma[static_cast<int64_t>(id) * rr + xy] = s;
+    }
+    return;
+  }
+  // mode 2: score_q = ||Sigma_q||_F^2 (sum per LoRA in a fixed order)
+  float* red = Qs + kTM * kEpLd;                     // [lpw][kJT]
+  for (int q = 0; q < nq; ++q) {
+    float acc = 0.f;
+    for (int xy = tid; xy < rr; xy += kJT) {
+      const int x = xy / r, y = xy - x * r;
+      float s = 0.f;
+      for (int l = 0; l < r_l; ++l) s = fmaf(Qs[(q * r_l + l) * kEpLd + x], Ps[(q * r_l + l) * kEpLd + y], s);
+      acc = fmaf(s, s, acc);
+    }
+    red[q * kJT + tid] = acc;
+  }
+  __syncthreads();
+  if (tid < nq) {
+    float s = 0.f;
+    for (int t = 0; t < kJT; ++t) s += red[tid * kJT + t];
+    a.score[static_cast<int64_t>(a.lidx[q0 + tid]) * a.ld_score + a.score_col] = s;
+  }
+}
+
+// ------------------------------------------------------------- expand kernel
+// blockIdx.z = 0: partU[s] rows of U' = sum B_i C_i; 1: partV[s] rows of
+// V' = sum A_i^T D_i.  blockIdx.y = split s over the flat (LoRA, l) index.
+struct ExpArgs {
+  const float* A; const float* B; const int32_t* lidx; int m;
+  int r_l, d_in, d_out, r;
+  const float* C; const float* D;
+  int split; float* partU; float* partV;
+};
+
+__global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  const bool isv = blockIdx.z == 1;
+  const int d = isv ? a.d_in : a.d_out;
+  const int row0 = blockIdx.x * kTM;
+  if (row0 >= d) return;
+  const int fk_total = a.m * a.r_l;
+  const int ntile = (fk_total + kBK - 1) / kBK;
+  const int s = blockIdx.y;
+  const int f_lo = static_cast<int>(static_cast<int64_t>(ntile) * s / a.split) * kBK;
+  const int f_hi = min(fk_total, static_cast<int>(static_cast<int64_t>(ntile) * (s + 1) / a.split) * kBK);
+  f32x4 acc[kRMax / 16];
+  zero_acc(acc);
+  if (isv)
+    tile_gemm<true>(smem, f_lo, f_hi, a.r, LoadExpandA{a.A, a.lidx, a.r_l, a.d_in, row0, f_hi},
+                    LoadRowsR{a.D, a.r, f_hi}, acc);
+  else
+    tile_gemm<false>(smem, f_lo, f_hi, a.r, LoadExpandB{a.B, a.lidx, a.r_l, a.d_out, row0, f_hi},
+                     LoadRowsR{a.C, a.r, f_hi}, acc);
+  float* part = (isv ? a.partV : a.partU) + static_cast<int64_t>(s) * d * a.r;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fq = lane >> 4;
+#pragma unroll
+  for (int nb = 0; nb < kRMax / 16; ++nb)
+    if (nb < (a.r >> 4))
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = row0 + 16 * wave + 4 * fq + v;
+        if (row < d) part[static_cast<int64_t>(row) * a.r + 16 * nb + fr] = acc[nb][v];
+      }
+}
+
+// X[z][row][j] = sum_s part_z[s][row][j], z = 0 (U, d_out rows), 1 (V, d_in rows)
+__global__ __launch_bounds__(kJT) void jd_reduce_kernel(const float* partU, const float* partV, int S,
+                                                        int d_out, int d_in, int r, float* Uo, float* Vo) {
+  const bool isv = blockIdx.y == 1;
+  const int d = isv ? d_in : d_out;
+  const int64_t n = static_cast<int64_t>(d) * r;
+  const float* part = isv ? partV : partU;
+  float* out = isv ? Vo : Uo;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(kJT) + threadIdx.x; e < n;
+       e += static_cast<int64_t>(gridDim.x) * kJT) {
+    float s = 0.f;
+    for (int k = 0; k < S; ++k) s += part[k * n + e];
+    out[e] = s;
+  }
+}
+
+// ------------------------------------------------------ CholeskyQR pieces
+// Partial Gram matrices: gp[z][b][x][y] = sum over rows of block b of
+// X_z[row][x] Y_z[row][y] (Y = X when Y0/Y1 are null).
+__global__ __launch_bounds__(kJT) void jd_gram_kernel(const float* X0, const float* X1, const float* Y0,
+                                                      const float* Y1, int d0, int d1, int r, int nblk,
+                                                      float* gp) {
+  __shared__ float xs[64 * (kRMax + 1)], ys[64 * (kRMax + 1)];
+  const int z = blockIdx.y, b = blockIdx.x;
+  const int d = z ? d1 : d0;
+  const float* X = z ? X1 : X0;
+  const float* Y = z ? (Y1 ? Y1 : X1) : (Y0 ? Y0 : X0);
+  float* out = gp + (static_cast<int64_t>(z) * nblk + b) * r * r;
+  const int rr = r * r;
+  const int row_lo = b * kGramRows, row_hi = min(d, row_lo + kGramRows);
+  float acc[kRMax * kRMax / kJT];
+#pragma unroll
+  for (int u = 0; u < kRMax * kRMax / kJT; ++u) acc[u] = 0.f;
+  for (int c0 = row_lo; c0 < row_hi; c0 += 64) {
+    const int nr = min(64, row_hi - c0);
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * r; e += kJT) {
+      const int rw = e / r, j = e - rw * r;
+      xs[rw * (kRMax + 1) + j] = rw < nr ? X[static_cast<int64_t>(c0 + rw) * r + j] : 0.f;
+      ys[rw * (kRMax + 1) + j] = rw < nr ? Y[static_cast<int64_t>(c0 + rw) * r + j] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRMax * kRMax / kJT; ++u) {
+      const int e = threadIdx.x + u * kJT;
+      if (e < rr) {
+        const int x = e / r, y = e - x * r;
+        float s = acc[u];
+        for (int rw = 0; rw < 64; ++rw) s = fmaf(xs[rw * (kRMax + 1) + x], ys[rw * (kRMax + 1) + y], s);
+        acc[u] = s;
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kRMax * kRMax / kJT; ++u) {
+    const int e = threadIdx.x + u * kJT;
+    if (e < rr) out[e] = acc[u];
+  }
+}
+
+// One workgroup per z: G = sum_b gp[z][b] (fixed order).  chol = 0: writes G
+// to out[z].  chol = 1: G = R^T R (R upper, positive diagonal), writes R^-1.
+__global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int r, int chol, float* out) {
+  __shared__ float g[kRMax * (kRMax + 1)];
+  __shared__ float t[kRMax];
+  const int z = blockIdx.x, tid = threadIdx.x;
+  const int rr = r * r, ld = kRMax + 1;
+  const float* src = gp + static_cast<int64_t>(z) * nblk * rr;
+  for (int e = tid; e < rr; e += kJT) {
+    float s = 0.f;
+    for (int b = 0; b < nblk; ++b) s += src[static_cast<int64_t>(b) * rr + e];
+    g[(e / r) * ld + e % r] = s;
+  }
+  __syncthreads();
+  float* dst = out + static_cast<int64_t>(z) * rr;
+  if (!chol) {
+    for (int e = tid; e < rr; e += kJT) dst[e] = g[(e / r) * ld + e % r];
+    return;
+  }
+  // left-looking Cholesky, row j of R from rows < j (R overwrites the upper
+  // triangle of g; the strict lower triangle keeps G's entries, unused)
+  for (int j = 0; j < r; ++j) {
+    if (tid >= j && tid < r) {
+      float s = g[j * ld + tid];
+      for (int k = 0; k < j; ++k) s = fmaf(-g[k * ld + j], g[k * ld + tid], s);
+      t[tid] = s;
+    }
+    __syncthreads();
+    if (tid >= j && tid < r) g[j * ld + tid] = t[tid] / sqrtf(t[j]);
+    __syncthreads();
+  }
+  // R^-1 column c by back substitution: thread c owns column c (written to
+  // the lower triangle transposed: inv[c][i] stored at g[c][i] for i <= c is
+  // R's own entry, so use the output array directly)
+  if (tid < r) {
+    const int c = tid;
+    for (int i = r - 1; i >= 0; --i) {
+      float s = (i == c) ? 1.f : 0.f;
+      if (i <= c) {
+        for (int k = i + 1; k <= c; ++k) s = fmaf(-g[i * ld + k], dst[k * r + c], s);
+        s /= g[i * ld + i];
+      }
+      dst[i * r + c] = s;
+    }
+  }
+}
+
+// X_z[row][:] <- X_z[row][:] Rinv_z (rows of 64 per workgroup, in place)
+__global__ __launch_bounds__(kJT) void jd_apply_kernel(float* X0, float* X1, int d0, int d1, int r,
+                                                       const float* rinv) {
+  __shared__ float rs[kRMax * kRMax];
+  __shared__ float xs[64 * (kRMax + 1)];
+  const int z = blockIdx.y;
+  const int d = z ? d1 : d0;
+  float* X = z ? X1 : X0;
+  const int row0 = blockIdx.x * 64;
+  if (row0 >= d) return;
+  const int nr = min(64, d - row0);
+  const float* R = rinv + static_cast<int64_t>(z) * r * r;
+  for (int e = threadIdx.x; e < r * r; e += kJT) rs[e] = R[e];
+  for (int e = threadIdx.x; e < nr * r; e += kJT)
+    xs[(e / r) * (kRMax + 1) + e % r] = X[static_cast<int64_t>(row0) * r + e];
+  __syncthreads();
+  for (int e = threadIdx.x; e < nr * r; e += kJT) {
+    const int rw = e / r, j = e - rw * r;
+    float s = 0.f;
+    for (int k = 0; k <= j; ++k) s = fmaf(xs[rw * (kRMax + 1) + k], rs[k * r + j], s);
+    X[static_cast<int64_t>(row0 + rw) * r + j] = s;
+  }
+}
+
+// Convergence measure, partial sums per 64-row block: E = Xn - Xo M_z,
+// rp[z][b] = (||E||^2, ||Xn||^2) over the block.
+__global__ __launch_bounds__(kJT) void jd_resid_kernel(const float* Uo, const float* Un, const float* Vo,
+                                                       const float* Vn, int d0, int d1, int r,
+                                                       const float* M, int nblk, float* rp) {
+  __shared__ float ms[kRMax * kRMax];
+  __shared__ float xs[64 * (kRMax + 1)];
+  __shared__ float red[2 * kJT];
+  const int z = blockIdx.y, b = blockIdx.x;
+  const int d = z ? d1 : d0;
+  const float* Xo = z ? Vo : Uo;
+  const float* Xn = z ? Vn : Un;
+  const int row0 = b * 64;
+  float e2 = 0.f, x2 = 0.f;
+  if (row0 < d) {
+    const int nr = min(64, d - row0);
+    for (int e = threadIdx.x; e < r * r; e += kJT) ms[e] = M[static_cast<int64_t>(z) * r * r + e];
+    for (int e = threadIdx.x; e < nr * r; e += kJT)
+      xs[(e / r) * (kRMax + 1) + e % r] = Xo[static_cast<int64_t>(row0) * r + e];
+    __syncthreads();
+    for (int e = threadIdx.x; e < nr * r; e += kJT) {
+      const int rw = e / r, j = e - rw * r;
+      float s = 0.f;
+      for (int k = 0; k < r; ++k) s = fmaf(xs[rw * (kRMax + 1) + k], ms[k * r + j], s);
+      const float xn = Xn[static_cast<int64_t>(row0 + rw) * r + j];
+      const float df = xn - s;
+      e2 = fmaf(df, df, e2);
+      x2 = fmaf(xn, xn, x2);
+    }
+  }
+  red[threadIdx.x] = e2;
+  red[kJT + threadIdx.x] = x2;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float se = 0.f, sx = 0.f;
+    for (int t = 0; t < kJT; ++t) { se += red[t]; sx += red[kJT + t]; }
+    rp[(static_cast<int64_t>(z) * nblk + b) * 2] = se;
+    rp[(static_cast<int64_t>(z) * nblk + b) * 2 + 1] = sx;
+  }
+}
+
+__global__ void jd_crit_kernel(const float* rp, int nblk, float* crit) {
+  if (threadIdx.x != 0) return;
+  float c = 0.f;
+  for (int z = 0; z < 2; ++z) {
+    float se = 0.f, sx = 0.f;
+    for (int b = 0; b < nblk; ++b) {
+      se += rp[(z * nblk + b) * 2];
+      sx += rp[(z * nblk + b) * 2 + 1];
+    }
+    c = fmaxf(c, sqrtf(se / sx));
+  }
+  crit[0] = c;
+}
+
+// out[c][x] = in[x][c] for an [R][C] array (transposes a basis)
+__global__ __launch_bounds__(kJT) void jd_transpose_kernel(const float* in, int R, int C, float* out) {
+  __shared__ float tile[32][33];
+  const int bx = blockIdx.x * 32, by = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;      // 32 x 8
+  for (int k = ty; k < 32; k += 8) {
+    const int rr = by + k, cc = bx + tx;
+    tile[k][tx] = (rr < R && cc < C) ? in[static_cast<int64_t>(rr) * C + cc] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int cc = bx + k, rr = by + tx;
+    if (cc < C && rr < R) out[static_cast<int64_t>(cc) * R + rr] = tile[tx][k];
+  }
+}
+
+__global__ void jd_copy_kernel(const float* in, float* out, int64_t n) {
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < n;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    out[e] = in[e];
+}
+
+__global__ void jd_iota_kernel(int32_t* out, int n) {
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) out[e] = e;
+}
+
+// ||B_i A_i||_F^2 = sum_{l,l'} (B_i^T B_i)[l][l'] (A_i A_i^T)[l][l'], one
+// workgroup per LoRA; also w2[i] = 1 / norms2[i] and w[i] = 1 / ||B_i A_i||.
+__global__ __launch_bounds__(kJT) void jd_norms_kernel(const float* A, const float* B, int r_l, int d_in,
+                                                       int d_out, float* norms2, float* w2, float* w) {
+  __shared__ float ga[64 * 64], gb[64 * 64];
+  const int i = blockIdx.x;
+  const float* Ai = A + static_cast<int64_t>(i) * r_l * d_in;
+  const float* Bi = B + static_cast<int64_t>(i) * d_out * r_l;
+  const int nn = r_l * r_l;
+  for (int e = threadIdx.x; e < nn; e += kJT) {
+    const int l = e / r_l, l2 = e - l * r_l;
+    float sa = 0.f, sb = 0.f;
+    for (int c = 0; c < d_in; ++c) sa = fmaf(Ai[static_cast<int64_t>(l) * d_in + c], Ai[static_cast<int64_t>(l2) * d_in + c], sa);
+    for (int o = 0; o < d_out; ++o) sb = fmaf(Bi[static_cast<int64_t>(o) * r_l + l], Bi[static_cast<int64_t>(o) * r_l + l2], sb);
+    ga[e] = sa;
+    gb[e] = sb;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float s = 0.f;
+    for (int e = 0; e < nn; ++e) s = fmaf(ga[e], gb[e], s);
+    norms2[i] = s;
+    if (w2) w2[i] = 1.f / s;
+    if (w) w[i] = 1.f / sqrtf(s);
+  }
+}
+
+// ------------------------------------------------------------ k-means pieces
+// dist[i][j] = ||x_i - c_j||^2 (x = Sigma rows of dim r^2); one workgroup per i
+__global__ __launch_bounds__(kJT) void km_dist_kernel(const float* X, const float* Cn, int dim, int K,
+                                                      float* dist) {
+  __shared__ float red[kJT];
+  const int i = blockIdx.x;
+  const float* x = X + static_cast<int64_t>(i) * dim;
+  for (int j = 0; j < K; ++j) {
+    const float* c = Cn + static_cast<int64_t>(j) * dim;
+    float s = 0.f;
+    for (int e = threadIdx.x; e < dim; e += kJT) {
+      const float df = x[e] - c[e];
+      s = fmaf(df, df, s);
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = kJT / 2; h > 0; h >>= 1) {
+      if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) dist[static_cast<int64_t>(i) * K + j] = red[0];
+    __syncthreads();
+  }
+}
+
+// labels[i] = arg min_j v[i][j] (sign = 1) or arg max (sign = -1), lowest j on
+// ties; changed[0] = number of labels that differ from the previous ones
+// (one workgroup, fixed order)
+__global__ __launch_bounds__(kJT) void km_pick_kernel(const float* v, int n, int K, float sign,
+                                                      int32_t* labels, int32_t* changed) {
+  __shared__ int red[kJT];
+  int cnt = 0;
+  for (int i = threadIdx.x; i < n; i += kJT) {
+    int best = 0;
+    float bv = sign * v[static_cast<int64_t>(i) * K];
+    for (int j = 1; j < K; ++j) {
+      const float x = sign * v[static_cast<int64_t>(i) * K + j];
+      if (x < bv) { bv = x; best = j; }
+    }
+    cnt += (labels[i] != best) ? 1 : 0;
+    labels[i] = best;
+  }
+  red[threadIdx.x] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int t = 0; t < kJT; ++t) s += red[t];
+    changed[0] = s;
+  }
+}
+
+// centroid j = mean of the rows i with labels[i] == j (kept when empty);
+// grid (ceil(dim / 256), K)
+__global__ __launch_bounds__(kJT) void km_centroid_kernel(const float* X, const int32_t* labels, int n,
+                                                          int dim, float* Cn) {
+  const int j = blockIdx.y;
+  const int e = blockIdx.x * kJT + threadIdx.x;
+  if (e >= dim) return;
+  float s = 0.f;
+  int cnt = 0;
+  for (int i = 0; i < n; ++i)
+    if (labels[i] == j) {
+      s += X[static_cast<int64_t>(i) * dim + e];
+      ++cnt;
+    }
+  if (cnt > 0) Cn[static_cast<int64_t>(j) * dim + e] = s / static_cast<float>(cnt);
+}
+
+// centroids from rows init[j]
+__global__ __launch_bounds__(kJT) void km_init_kernel(const float* X, const int32_t* init, int dim,
+                                                      float* Cn) {
+  const int j = blockIdx.y;
+  const int e = blockIdx.x * kJT + threadIdx.x;
+  if (e < dim) Cn[static_cast<int64_t>(j) * dim + e] = X[static_cast<int64_t>(init[j]) * dim + e];
+}
+
+// members of each cluster in increasing id order: memb[offs[j] ...], with
+// offs[j] = number of LoRAs in clusters < j (one workgroup, fixed order)
+__global__ __launch_bounds__(kJT) void km_members_kernel(const int32_t* labels, int n, int K,
+                                                         int32_t* offs, int32_t* memb) {
+  __shared__ int wcnt[kJT / 64];
+  __shared__ int base;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  if (threadIdx.x == 0) base = 0;
+  __syncthreads();
+  for (int j = 0; j < K; ++j) {
+    if (threadIdx.x == 0) offs[j] = base;
+    for (int c0 = 0; c0 < n; c0 += kJT) {
+      const int i = c0 + threadIdx.x;
+      const bool in = i < n && labels[i] == j;
+      const uint64_t bal = __ballot(in);
+      if (lane == 0) wcnt[wave] = __popcll(bal);
+      __syncthreads();
+      int before = 0, total = 0;
+      for (int w = 0; w < kJT / 64; ++w) {
+        before += (w < wave) ? wcnt[w] : 0;
+        total += wcnt[w];
+      }
+      if (in) memb[base + before + __popcll(bal & lt)] = i;
+      __syncthreads();
+      if (threadIdx.x == 0) base += total;
+      __syncthreads();
+    }
+  }
+  if (threadIdx.x == 0) offs[K] = base;
+}
+
+// ------------------------------------------------------------------ host side
+bool bad_ptr(const void* ptr, size_t align) {
+  return ptr == nullptr || (reinterpret_cast<uintptr_t>(ptr) % align) != 0;
+}
+
+int validate(const cts_jd_problem* p) {
+  if (!p) return CTS_ERR_INVALID_ARG;
+  if (p->n <= 0 || p->d_out <= 0 || p->d_in <= 0 || p->r_lora <= 0 || p->r <= 0) return CTS_ERR_INVALID_ARG;
+  const int rl = p->r_lora;
+  if (!(rl == 4 || rl == 8 || rl == 16 || rl == 32 || rl == 64)) return CTS_ERR_UNSUPPORTED;
+  if (p->r % 16 != 0 || p->r > kRMax) return CTS_ERR_UNSUPPORTED;
+  if (p->n > 65536 || static_cast<int64_t>(p->n) * rl < p->r) return CTS_ERR_UNSUPPORTED;
+  if (p->d_in % 4 || p->d_out % 4 || p->d_in < p->r || p->d_out < p->r || p->d_in > 65536 ||
+      p->d_out > 65536)
+    return CTS_ERR_UNSUPPORTED;
+  const int64_t lim = int64_t(1) << 31;
+  if (static_cast<int64_t>(p->n) * rl * p->d_in >= lim || static_cast<int64_t>(p->n) * rl * p->d_out >= lim ||
+      static_cast<int64_t>(p->n) * p->r * p->r >= lim)
+    return CTS_ERR_UNSUPPORTED;
+  return CTS_OK;
+}
+
+// Workspace of one JD run (plus the clustering extras when K > 0).
+struct JdPlan {
+  int split, nblk_out, nblk_in, nblk;
+  size_t off_U, off_V, off_Uo, off_Vo, off_C, off_D, off_pU, off_pV, off_gp, off_mat, off_rp, off_lidx,
+      off_w2, off_w, off_n2, off_crit, total;
+  // clustering
+  size_t off_S, off_cent, off_dist, off_lab, off_chg, off_offs, off_memb, off_score;
+};
+
+size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
+  const int64_t n = p->n, rl = p->r_lora, r = p->r;
+  const int64_t fk = n * rl;
+  const int64_t ntile = (fk + kBK - 1) / kBK;
+  const int64_t rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
+  // about two rounds of 256 workgroups per basis, at least 8 k-tiles each
+  int64_t split = std::max<int64_t>(1, std::min<int64_t>((512 + rowt - 1) / rowt, ntile / 8));
+  pl->split = static_cast<int>(std::max<int64_t>(1, split));
+  pl->nblk_out = (p->d_out + kGramRows - 1) / kGramRows;
+  pl->nblk_in = (p->d_in + kGramRows - 1) / kGramRows;
+  pl->nblk = std::max(pl->nblk_out, pl->nblk_in);
+  const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  pl->off_U = take(4ull * p->d_out * r);
+  pl->off_V = take(4ull * p->d_in * r);
+  pl->off_Uo = take(4ull * p->d_out * r);
+  pl->off_Vo = take(4ull * p->d_in * r);
+  pl->off_C = take(4ull * fk * r);
+  pl->off_D = take(4ull * fk * r);
+  pl->off_pU = take(4ull * pl->split * p->d_out * r);
+  pl->off_pV = take(4ull * pl->split * p->d_in * r);
+  pl->off_gp = take(4ull * 2 * pl->nblk * r * r);
+  pl->off_mat = take(4ull * 2 * r * r);
+  pl->off_rp = take(4ull * 2 * nrb * 2);
+  pl->off_lidx = take(4ull * n);
+  pl->off_w2 = take(4ull * n);
+  pl->off_w = take(4ull * n);
+  pl->off_n2 = take(4ull * n);
+  pl->off_crit = take(4ull * 4);
+  pl->off_S = pl->off_cent = pl->off_dist = pl->off_lab = pl->off_chg = pl->off_offs = pl->off_memb =
+      pl->off_score = 0;
+  if (K > 0) {
+    pl->off_S = take(4ull * n * r * r);
+    pl->off_cent = take(4ull * K * r * r);
+    pl->off_dist = take(4ull * n * K);
+    pl->off_lab = take(4ull * n);
+    pl->off_chg = take(4ull * 4);
+    pl->off_offs = take(4ull * (K + 1));
+    pl->off_memb = take(4ull * n);
+    pl->off_score = take(4ull * n * K);
+  }
+  pl->total = off;
+}
+
+struct Jd {
+  const cts_jd_problem* p;
+  JdPlan pl;
+  char* ws;
+  hipStream_t st;
+  template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+hipError_t launch_project(const Jd& j, const float* A, const float* B, const float* V, const float* U,
+                          const int32_t* lidx, int m, int mode, const float* w2, const float* sscale,
+                          float* Sigma, float* score, int ld_score, int score_col) {
+  const cts_jd_problem* p = j.p;
+  ProjArgs a{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, p->r, mode, w2, sscale,
+             j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D), Sigma, score, ld_score, score_col};
+  const int lpw = kTM / p->r_lora;
+  hipLaunchKernelGGL(jd_project_kernel, dim3((m + lpw - 1) / lpw), dim3(kJT), 0, j.st, a);
+  return hipGetLastError();
+}
+
+// One eigenvalue-iteration step from (U, V) in the workspace to (Uo, Vo)
+// (the new pair), then the measure into crit_out; swaps the buffers.
+hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, const float* w2,
+                   float* crit_out) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  float* U = j.at<float>(j.pl.off_U);
+  float* V = j.at<float>(j.pl.off_V);
+  float* Un = j.at<float>(j.pl.off_Uo);
+  float* Vn = j.at<float>(j.pl.off_Vo);
+  hipError_t e = launch_project(j, A, B, V, U, lidx, m, 0, w2, nullptr, nullptr, nullptr, 0, 0);
+  if (e != hipSuccess) return e;
+  // expand, split so that the collection's share per workgroup is >= 8 k-tiles
+  const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
+  const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
+  ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, r, j.at<float>(j.pl.off_C),
+             j.at<float>(j.pl.off_D), split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV)};
+  const int rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
+  hipLaunchKernelGGL(jd_expand_kernel, dim3(rowt, split, 2), dim3(kJT), 0, j.st, ea);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int64_t nmax = static_cast<int64_t>(std::max(p->d_out, p->d_in)) * r;
+  hipLaunchKernelGGL(jd_reduce_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nmax + kJT - 1) / kJT)), 2),
+                     dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out,
+                     p->d_in, r, Un, Vn);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // CholeskyQR2 on both
+  float* gp = j.at<float>(j.pl.off_gp);
+  float* mat = j.at<float>(j.pl.off_mat);
+  const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
+  for (int pass = 0; pass < 2; ++pass) {
+    hipLaunchKernelGGL(jd_gram_kernel, dim3(j.pl.nblk, 2), dim3(kJT), 0, j.st, Un, Vn, nullptr, nullptr,
+                       p->d_out, p->d_in, r, j.pl.nblk, gp);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(jd_chol_kernel, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, r, 1, mat);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(jd_apply_kernel, dim3(nrb, 2), dim3(kJT), 0, j.st, Un, Vn, p->d_out, p->d_in, r, mat);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // measure: M = X_old^T X_new, E = X_new - X_old M
+  hipLaunchKernelGGL(jd_gram_kernel, dim3(j.pl.nblk, 2), dim3(kJT), 0, j.st, U, V, Un, Vn, p->d_out, p->d_in, r,
+                     j.pl.nblk, gp);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(jd_chol_kernel, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, r, 0, mat);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  float* rp = j.at<float>(j.pl.off_rp);
+  hipLaunchKernelGGL(jd_resid_kernel, dim3(nrb, 2), dim3(kJT), 0, j.st, U, Un, V, Vn, p->d_out, p->d_in, r, mat,
+                     nrb, rp);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(jd_crit_kernel, dim3(1), dim3(64), 0, j.st, rp, nrb, crit_out);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  std::swap(j.pl.off_U, j.pl.off_Uo);
+  std::swap(j.pl.off_V, j.pl.off_Vo);
+  return hipSuccess;
+}
+
+// basis in: U0 [d_out][r] -> U; Vt0 [r][d_in] -> V [d_in][r]
+hipError_t load_bases(Jd& j, const float* U0, const float* Vt0) {
+  const cts_jd_problem* p = j.p;
+  const int64_t nu = static_cast<int64_t>(p->d_out) * p->r;
+  hipLaunchKernelGGL(jd_copy_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nu + 255) / 256))),
+                     dim3(256), 0, j.st, U0, j.at<float>(j.pl.off_U), nu);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(jd_transpose_kernel, dim3((p->d_in + 31) / 32, (p->r + 31) / 32), dim3(kJT), 0, j.st, Vt0,
+                     p->r, p->d_in, j.at<float>(j.pl.off_V));
+  return hipGetLastError();
+}
+
+hipError_t store_bases(Jd& j, float* U, float* Vt) {
+  const cts_jd_problem* p = j.p;
+  const int64_t nu = static_cast<int64_t>(p->d_out) * p->r;
+  hipLaunchKernelGGL(jd_copy_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nu + 255) / 256))),
+                     dim3(256), 0, j.st, j.at<float>(j.pl.off_U), U, nu);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(jd_transpose_kernel, dim3((p->r + 31) / 32, (p->d_in + 31) / 32), dim3(kJT), 0, j.st,
+                     j.at<float>(j.pl.off_V), p->d_in, p->r, Vt);
+  return hipGetLastError();
+}
+
+hipError_t norms(Jd& j, const float* A, const float* B) {
+  const cts_jd_problem* p = j.p;
+  hipLaunchKernelGGL(jd_norms_kernel, dim3(p->n), dim3(kJT), 0, j.st, A, B, p->r_lora, p->d_in, p->d_out,
+                     j.at<float>(j.pl.off_n2), j.at<float>(j.pl.off_w2), j.at<float>(j.pl.off_w));
+  return hipGetLastError();
+}
+
+// `iters` iterations (early stop below tau, waiting per iteration) on the
+// LoRAs lidx[0..m); bases in j's U/V buffers.  crit: device array or null
+// (then the workspace slot).
+int run_jd(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, const float* w2, int iters,
+           float tau, float* crit, int* done) {
+  float* cslot = j.at<float>(j.pl.off_crit);
+  int t = 0;
+  for (; t < iters; ++t) {
+    float* c = crit ? crit + t : cslot;
+    if (jd_step(j, A, B, lidx, m, w2, c) != hipSuccess) return CTS_ERR_HIP;
+    if (tau > 0.f) {
+      float h = 0.f;
+      if (hipMemcpyAsync(&h, c, sizeof(float), hipMemcpyDeviceToHost, j.st) != hipSuccess ||
+          hipStreamSynchronize(j.st) != hipSuccess)
+        return CTS_ERR_HIP;
+      if (h < tau) { ++t; break; }
+    }
+  }
+  if (done) *done = t;
+  return CTS_OK;
+}
+
+}  // namespace
+}  // namespace cts
+
+using cts::Jd;
+
+extern "C" {
+
+size_t cts_jd_workspace_size(const cts_jd_problem* p) {
+  if (cts::validate(p) != CTS_OK) return 0;
+  cts::JdPlan pl;
+  cts::plan_jd(p, 0, &pl);
+  return pl.total;
+}
+
+size_t cts_jd_cluster_workspace_size(const cts_jd_problem* p, int32_t K) {
+  if (cts::validate(p) != CTS_OK || K < 1 || K > p->n) return 0;
+  cts::JdPlan pl;
+  cts::plan_jd(p, K, &pl);
+  return pl.total;
+}
+
+int cts_lora_norms2(const cts_jd_problem* p, const float* A, const float* B, float* norms2, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+  int st = cts::validate(p);
+  if (st != CTS_OK) return st;
+  if (cts::bad_ptr(A, 16) || cts::bad_ptr(B, 16) || cts::bad_ptr(norms2, 4) || cts::bad_ptr(workspace, 16))
+    return CTS_ERR_INVALID_ARG;
+  Jd j{p, {}, static_cast<char*>(workspace), static_cast<hipStream_t>(stream)};
+  cts::plan_jd(p, 0, &j.pl);
+  if (workspace_bytes < j.pl.total) return CTS_ERR_WORKSPACE;
+  hipLaunchKernelGGL(cts::jd_norms_kernel, dim3(p->n), dim3(cts::kJT), 0, j.st, A, B, p->r_lora, p->d_in,
+                     p->d_out, norms2, nullptr, nullptr);
+  return hipGetLastError() == hipSuccess ? CTS_OK : CTS_ERR_HIP;
+}
+
+int cts_jd_full(const cts_jd_problem* p, const float* A, const float* B, const float* U0, const float* Vt0,
+                int32_t iters, float tau, int32_t normalize, float* U, float* Vt, float* Sigma, float* crit,
+                int32_t* iters_done, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = cts::validate(p);
+  if (st != CTS_OK) return st;
+  if (iters < 1 || cts::bad_ptr(A, 16) || cts::bad_ptr(B, 16) || cts::bad_ptr(U0, 16) || cts::bad_ptr(Vt0, 16) ||
+      cts::bad_ptr(U, 16) || cts::bad_ptr(Vt, 16) || cts::bad_ptr(Sigma, 16) || cts::bad_ptr(crit, 4) ||
+      cts::bad_ptr(workspace, 16))
+    return CTS_ERR_INVALID_ARG;
+  Jd j{p, {}, static_cast<char*>(workspace), static_cast<hipStream_t>(stream)};
+  cts::plan_jd(p, 0, &j.pl);
+  if (workspace_bytes < j.pl.total) return CTS_ERR_WORKSPACE;
+  int32_t* lidx = j.at<int32_t>(j.pl.off_lidx);
+  hipLaunchKernelGGL(cts::jd_iota_kernel, dim3((p->n + 255) / 256), dim3(256), 0, j.st, lidx, p->n);
+  if (hipGetLastError() != hipSuccess) return CTS_ERR_HIP;
+  if (normalize && cts::norms(j, A, B) != hipSuccess) return CTS_ERR_HIP;
+  if (cts::load_bases(j, U0, Vt0) != hipSuccess) return CTS_ERR_HIP;
+  int done = 0;
+  st = cts::run_jd(j, A, B, lidx, p->n, normalize ? j.at<float>(j.pl.off_w2) : nullptr, iters, tau, crit, &done);
+  if (st != CTS_OK) return st;
+  if (cts::launch_project(j, A, B, j.at<float>(j.pl.off_V), j.at<float>(j.pl.off_U), lidx, p->n, 1, nullptr,
+                          nullptr, Sigma, nullptr, 0, 0) != hipSuccess)
+    return CTS_ERR_HIP;
+  if (cts::store_bases(j, U, Vt) != hipSuccess) return CTS_ERR_HIP;
+  if (iters_done) *iters_done = done;
+  return CTS_OK;
+}
+
+int cts_jd_sigma(const cts_jd_problem* p, const float* A, const float* B, const float* U, const float* Vt,
+                 float* Sigma, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = cts::validate(p);
+  if (st != CTS_OK) return st;
+  if (cts::bad_ptr(A, 16) || cts::bad_ptr(B, 16) || cts::bad_ptr(U, 16) || cts::bad_ptr(Vt, 16) ||
+      cts::bad_ptr(Sigma, 16) || cts::bad_ptr(workspace, 16))
+    return CTS_ERR_INVALID_ARG;
+  Jd j{p, {}, static_cast<char*>(workspace), static_cast<hipStream_t>(stream)};
+  cts::plan_jd(p, 0, &j.pl);
+  if (workspace_bytes < j.pl.total) return CTS_ERR_WORKSPACE;
+  int32_t* lidx = j.at<int32_t>(j.pl.off_lidx);
+  hipLaunchKernelGGL(cts::jd_iota_kernel, dim3((p->n + 255) / 256), dim3(256), 0, j.st, lidx, p->n);
+  if (hipGetLastError() != hipSuccess) return CTS_ERR_HIP;
+  if (cts::load_bases(j, U, Vt) != hipSuccess) return CTS_ERR_HIP;
+  if (cts::launch_project(j, A, B, j.at<float>(j.pl.off_V), j.at<float>(j.pl.off_U), lidx, p->n, 1, nullptr,
+                          nullptr, Sigma, nullptr, 0, 0) != hipSuccess)
+    return CTS_ERR_HIP;
+  return CTS_OK;
+}
+
+int cts_jd_cluster(const cts_jd_problem* p, int32_t K, const float* A, const float* B, const float* U0,
+                   const float* Vt0, const float* Uc0, const float* Vtc0, const int32_t* init_idx,
+                   int32_t jd_iters, int32_t max_rounds, int32_t normalize, int32_t* cluster_of, float* U,
+                   float* Vt, float* Sigma, int32_t* rounds, void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  int st = cts::validate(p);
+  if (st != CTS_OK) return st;
+  if (K < 1 || K > p->n || jd_iters < 1 || max_rounds < 1 || !init_idx) return CTS_ERR_INVALID_ARG;
+  for (int k = 0; k < K; ++k)
+    if (init_idx[k] < 0 || init_idx[k] >= p->n) return CTS_ERR_INVALID_ARG;
+  if (cts::bad_ptr(A, 16) || cts::bad_ptr(B, 16) || cts::bad_ptr(U0, 16) || cts::bad_ptr(Vt0, 16) ||
+      cts::bad_ptr(Uc0, 16) || cts::bad_ptr(Vtc0, 16) || cts::bad_ptr(cluster_of, 4) || cts::bad_ptr(U, 16) ||
+      cts::bad_ptr(Vt, 16) || cts::bad_ptr(Sigma, 16) || cts::bad_ptr(workspace, 16))
+    return CTS_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(K) * p->d_out * p->r >= (int64_t(1) << 31) ||
+      static_cast<int64_t>(K) * p->r * p->r * p->n >= (int64_t(1) << 40))
+    return CTS_ERR_UNSUPPORTED;
+  Jd j{p, {}, static_cast<char*>(workspace), static_cast<hipStream_t>(stream)};
+  cts::plan_jd(p, K, &j.pl);
+  if (workspace_bytes < j.pl.total) return CTS_ERR_WORKSPACE;
+  const int n = p->n, r = p->r, rr = r * r;
+  const int64_t usz = static_cast<int64_t>(p->d_out) * r, vsz = static_cast<int64_t>(r) * p->d_in;
+  int32_t* lidx = j.at<int32_t>(j.pl.off_lidx);
+  int32_t* lab = j.at<int32_t>(j.pl.off_lab);
+  int32_t* chg = j.at<int32_t>(j.pl.off_chg);
+  int32_t* offs = j.at<int32_t>(j.pl.off_offs);
+  int32_t* memb = j.at<int32_t>(j.pl.off_memb);
+  float* S = j.at<float>(j.pl.off_S);
+  float* cent = j.at<float>(j.pl.off_cent);
+  float* dist = j.at<float>(j.pl.off_dist);
+  float* score = j.at<float>(j.pl.off_score);
+  const float* w2 = normalize ? j.at<float>(j.pl.off_w2) : nullptr;
+  const float* w = normalize ? j.at<float>(j.pl.off_w) : nullptr;
+  hipStream_t s = j.st;
+  auto ok = [](hipError_t e) { return e == hipSuccess; };
+  auto last = []() { return hipGetLastError() == hipSuccess; };
+
+  hipLaunchKernelGGL(cts::jd_iota_kernel, dim3((n + 255) / 256), dim3(256), 0, s, lidx, n);
+  if (!last()) return CTS_ERR_HIP;
+  if (normalize && !ok(cts::norms(j, A, B))) return CTS_ERR_HIP;
+  // single-basis JD and its cores (normalized LoRAs when asked)
+  if (!ok(cts::load_bases(j, U0, Vt0))) return CTS_ERR_HIP;
+  st = cts::run_jd(j, A, B, lidx, n, w2, jd_iters, 0.f, nullptr, nullptr);
+  if (st != CTS_OK) return st;
+  if (!ok(cts::launch_project(j, A, B, j.at<float>(j.pl.off_V), j.at<float>(j.pl.off_U), lidx, n, 1, nullptr, w, S,
+                              nullptr, 0, 0)))
+    return CTS_ERR_HIP;
+  // k-means on vec(Sigma_i)
+  std::vector<int32_t> init(init_idx, init_idx + K);
+  int32_t* init_dev = memb;                         // staging for the K indices
+  if (!ok(hipMemcpyAsync(init_dev, init.data(), sizeof(int32_t) * K, hipMemcpyHostToDevice, s)))
+    return CTS_ERR_HIP;
+  hipLaunchKernelGGL(cts::km_init_kernel, dim3((rr + 255) / 256, K), dim3(cts::kJT), 0, s, S, init_dev, rr, cent);
+  if (!last()) return CTS_ERR_HIP;
+  int32_t h_chg = 0;
+  for (int it = 0; it < cts::kMaxKm; ++it) {
+    hipLaunchKernelGGL(cts::km_dist_kernel, dim3(n), dim3(cts::kJT), 0, s, S, cent, rr, K, dist);
+    if (!last()) return CTS_ERR_HIP;
+    hipLaunchKernelGGL(cts::km_pick_kernel, dim3(1), dim3(cts::kJT), 0, s, dist, n, K, 1.f, lab, chg);
+    if (!last()) return CTS_ERR_HIP;
+    if (!ok(hipMemcpyAsync(&h_chg, chg, sizeof(int32_t), hipMemcpyDeviceToHost, s)) || !ok(hipStreamSynchronize(s)))
+      return CTS_ERR_HIP;
+    if (it > 0 && h_chg == 0) break;   // (the first assignment's count is not used)
+    hipLaunchKernelGGL(cts::km_centroid_kernel, dim3((rr + 255) / 256, K), dim3(cts::kJT), 0, s, S, lab, n, rr,
+                       cent);
+    if (!last()) return CTS_ERR_HIP;
+  }
+  // rounds of per-cluster JD-Full and reassignment
+  std::vector<int32_t> h_offs(K + 1);
+  int rd = 0;
+  for (rd = 1; rd <= max_rounds; ++rd) {
+    hipLaunchKernelGGL(cts::km_members_kernel, dim3(1), dim3(cts::kJT), 0, s, lab, n, K, offs, memb);
+    if (!last()) return CTS_ERR_HIP;
+    if (!ok(hipMemcpyAsync(h_offs.data(), offs, sizeof(int32_t) * (K + 1), hipMemcpyDeviceToHost, s)) ||
+        !ok(hipStreamSynchronize(s)))
+      return CTS_ERR_HIP;
+    for (int k = 0; k < K; ++k) {
+      const int cnt = h_offs[k + 1] - h_offs[k];
+      if (static_cast<int64_t>(cnt) * p->r_lora >= r) {
+        if (!ok(cts::load_bases(j, Uc0 + k * usz, Vtc0 + k * vsz))) return CTS_ERR_HIP;
+        st = cts::run_jd(j, A, B, memb + h_offs[k], cnt, w2, jd_iters, 0.f, nullptr, nullptr);
+        if (st != CTS_OK) return st;
+        if (!ok(cts::store_bases(j, U + k * usz, Vt + k * vsz))) return CTS_ERR_HIP;
+      } else if (rd == 1) {
+        // empty, or fewer than r directions: keeps the given bases
+        if (!ok(cts::load_bases(j, Uc0 + k * usz, Vtc0 + k * vsz)) || !ok(cts::store_bases(j, U + k * usz, Vt + k * vsz)))
+          return CTS_ERR_HIP;
+      }
+    }
+    // scores of every LoRA against every cluster's bases
+    for (int k = 0; k < K; ++k) {
+      if (!ok(cts::load_bases(j, U + k * usz, Vt + k * vsz))) return CTS_ERR_HIP;
+      if (!ok(cts::launch_project(j, A, B, j.at<float>(j.pl.off_V), j.at<float>(j.pl.off_U), lidx, n, 2, nullptr,
+                                  nullptr, nullptr, score, K, k)))
+        return CTS_ERR_HIP;
+    }
+    hipLaunchKernelGGL(cts::km_pick_kernel, dim3(1), dim3(cts::kJT), 0, s, score, n, K, -1.f, lab, chg);
+    if (!last()) return CTS_ERR_HIP;
+    if (!ok(hipMemcpyAsync(&h_chg, chg, sizeof(int32_t), hipMemcpyDeviceToHost, s)) || !ok(hipStreamSynchronize(s)))
+      return CTS_ERR_HIP;
+    if (h_chg == 0) break;
+  }
+  if (rd > max_rounds) rd = max_rounds;
+  // cores in each LoRA's own cluster bases (restored norms)
+  hipLaunchKernelGGL(cts::km_members_kernel, dim3(1), dim3(cts::kJT), 0, s, lab, n, K, offs, memb);
+  if (!last()) return CTS_ERR_HIP;
+  if (!ok(hipMemcpyAsync(h_offs.data(), offs, sizeof(int32_t) * (K + 1), hipMemcpyDeviceToHost, s)) ||
+      !ok(hipStreamSynchronize(s)))
+    return CTS_ERR_HIP;
+  for (int k = 0; k < K; ++k) {
+    const int cnt = h_offs[k + 1] - h_offs[k];
+    if (cnt == 0) continue;
+    if (!ok(cts::load_bases(j, U + k * usz, Vt + k * vsz))) return CTS_ERR_HIP;
+    if (!ok(cts::launch_project(j, A, B, j.at<float>(j.pl.off_V), j.at<float>(j.pl.off_U), memb + h_offs[k], cnt, 1,
+                                nullptr, nullptr, Sigma, nullptr, 0, 0)))
+      return CTS_ERR_HIP;
+  }
+  if (!ok(hipMemcpyAsync(cluster_of, lab, sizeof(int32_t) * n, hipMemcpyDeviceToDevice, s))) return CTS_ERR_HIP;
+  if (rounds) *rounds = rd;
+  return CTS_OK;
+}
+
+}  // extern "C"

@@ -1,4 +1,4 @@
-"""The C-ABI library loads, exports every symbol include/cts.h declares, and
+"""The C-ABI library loads, exports every symbol include/*.h declares, and
 rejects every host-detectable argument error before touching HIP.  CPU only:
 no call here reaches a kernel launch."""
 import ctypes
@@ -11,15 +11,18 @@ import paper_2407_00066_amd as cts
 from paper_2407_00066_amd import _binding as B
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "cts.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 
 FAKE = ctypes.c_void_p(0x10000)   # never dereferenced: validation fails first (16-byte aligned)
 
 
 def _declared():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(cts_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(cts_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_declares_binding_symbols():
@@ -246,3 +249,85 @@ def test_apply_uncompressed_ranked_validation():
                                            None) == B.CTS_ERR_WORKSPACE
     assert L.cts_apply_uncompressed_ranked(ctypes.byref(_p(T=0)), *[None] * 6, None, None, 0,
                                            None) == B.CTS_OK
+
+
+# ------------------------------------------------------------ compressor ABI
+def _jp(**kw):
+    d = dict(n=8, d_out=64, d_in=64, r_lora=4, r=16)
+    d.update(kw)
+    return B.JdProblem(d["n"], d["d_out"], d["d_in"], d["r_lora"], d["r"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=0), B.CTS_ERR_INVALID_ARG), (dict(r=0), B.CTS_ERR_INVALID_ARG),
+    (dict(r=24), B.CTS_ERR_UNSUPPORTED), (dict(r=144), B.CTS_ERR_UNSUPPORTED),
+    (dict(r_lora=12), B.CTS_ERR_UNSUPPORTED), (dict(n=3, r=16), B.CTS_ERR_UNSUPPORTED),
+    (dict(d_in=62), B.CTS_ERR_UNSUPPORTED), (dict(d_out=8), B.CTS_ERR_UNSUPPORTED),
+])
+def test_jd_rejects_bad_problem(kw, code):
+    p = _jp(**kw)
+    L = cts.lib()
+    assert L.cts_jd_workspace_size(ctypes.byref(p)) == 0
+    done = ctypes.c_int32(0)
+    rc = L.cts_jd_full(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 3, 0.0, 0, FAKE, FAKE, FAKE, FAKE,
+                       ctypes.byref(done), FAKE, 1 << 30, None)
+    assert rc == code
+    assert L.cts_jd_sigma(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == code
+    assert L.cts_lora_norms2(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == code
+
+
+def test_jd_full_argument_errors():
+    p = _jp()
+    L = cts.lib()
+    need = L.cts_jd_workspace_size(ctypes.byref(p))
+    assert need > 0
+    done = ctypes.c_int32(0)
+    odd = ctypes.c_void_p(0x10004)
+    args = [FAKE, FAKE, FAKE, FAKE, 3, 0.0, 0, FAKE, FAKE, FAKE, FAKE, ctypes.byref(done), FAKE, need, None]
+    for i in (0, 1, 2, 3, 7, 8, 9, 10, 12):                 # each pointer null, then misaligned
+        a = list(args)
+        a[i] = None
+        assert L.cts_jd_full(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG, i
+        if i != 10:                                          # crit needs 4-byte alignment only
+            a[i] = odd
+            assert L.cts_jd_full(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG, i
+    a = list(args)
+    a[4] = 0                                                 # iters
+    assert L.cts_jd_full(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG
+    a = list(args)
+    a[13] = need - 1
+    assert L.cts_jd_full(ctypes.byref(p), *a) == B.CTS_ERR_WORKSPACE
+    assert L.cts_jd_sigma(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == \
+        B.CTS_ERR_WORKSPACE
+    assert L.cts_lora_norms2(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, need - 1, None) == B.CTS_ERR_WORKSPACE
+    assert L.cts_jd_full(None, *args) == B.CTS_ERR_INVALID_ARG
+
+
+def test_jd_cluster_argument_errors():
+    p = _jp()
+    L = cts.lib()
+    K = 2
+    need = L.cts_jd_cluster_workspace_size(ctypes.byref(p), K)
+    assert need > L.cts_jd_workspace_size(ctypes.byref(p))
+    assert L.cts_jd_cluster_workspace_size(ctypes.byref(p), 0) == 0
+    assert L.cts_jd_cluster_workspace_size(ctypes.byref(p), 9) == 0        # K > n
+    rounds = ctypes.c_int32(0)
+
+    def call(K=2, init=(0, 1), jd_iters=3, max_rounds=5, ws=need, **ptrs):
+        arr = (ctypes.c_int32 * len(init))(*init)
+        P = dict(A=FAKE, B=FAKE, U0=FAKE, Vt0=FAKE, Uc0=FAKE, Vtc0=FAKE, cof=FAKE, U=FAKE, Vt=FAKE, S=FAKE,
+                 W=FAKE)
+        P.update(ptrs)
+        return L.cts_jd_cluster(ctypes.byref(p), K, P["A"], P["B"], P["U0"], P["Vt0"], P["Uc0"], P["Vtc0"], arr,
+                                jd_iters, max_rounds, 0, P["cof"], P["U"], P["Vt"], P["S"],
+                                ctypes.byref(rounds), P["W"], ws, None)
+
+    assert call(K=0, init=(0,)) == B.CTS_ERR_INVALID_ARG
+    assert call(K=9, init=tuple(range(9))) == B.CTS_ERR_INVALID_ARG
+    assert call(init=(0, 8)) == B.CTS_ERR_INVALID_ARG                      # index out of range
+    assert call(init=(-1, 0)) == B.CTS_ERR_INVALID_ARG
+    assert call(jd_iters=0) == B.CTS_ERR_INVALID_ARG
+    assert call(max_rounds=0) == B.CTS_ERR_INVALID_ARG
+    for name in ("A", "B", "U0", "Vt0", "Uc0", "Vtc0", "cof", "U", "Vt", "S", "W"):
+        assert call(**{name: None}) == B.CTS_ERR_INVALID_ARG, name
+    assert call(ws=need - 1) == B.CTS_ERR_WORKSPACE
