@@ -27,6 +27,12 @@ One JSON line is printed.  Besides the throughput it carries:
   single_adapter  the same batch with every token on one LoRA (n = K = 1);
                   ratio = this throughput / that one
   stages_us       mean duration of each stage of the layer (per step)
+
+--workload jd_full measures the offline compressor instead (cts_jd_full, the
+eigenvalue iteration of App. A.2 on 1000 rank-16 LoRAs of a 4096 x 4096
+projection at r = 64): a step is one iteration over the whole collection, a
+timed call runs 10 of them, and the roofline line is the larger of its two
+fp32 matrix-core kernels (projection, expansion).
 """
 from __future__ import annotations
 
@@ -229,6 +235,116 @@ def roofline_of(flops, nbytes, t_s, dtype):
     achieved = nbytes / t_s / 1e9
     return {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+
+
+JD_N, JD_D, JD_RL, JD_R, JD_ITERS = 1000, 4096, 16, 64, 10
+
+
+def jd_kernel_models(n, d_out, d_in, r_l, r, split):
+    """Algorithmic flops and bytes of one iteration's two large stages
+    (fp32).  projection: P_i = A_i V, Q_i = B_i^T U, G_i = P_i P_i^T,
+    H_i = Q_i Q_i^T, C_i = G_i Q_i, D_i = H_i P_i (reads A, B, the bases;
+    writes C, D).  expand: U' = sum_i B_i C_i, V' = sum_i A_i^T D_i (reads A,
+    B, C, D; writes the split partials)."""
+    rows = n * r_l
+    proj_f = 2.0 * rows * r * (d_in + d_out) + 2 * (4.0 * n * r_l * r_l * r)
+    proj_b = 4.0 * (rows * (d_in + d_out) + r * (d_in + d_out) + 2 * rows * r)
+    exp_f = 2.0 * rows * r * (d_in + d_out)
+    exp_b = 4.0 * (rows * (d_in + d_out) + 2 * rows * r + split * r * (d_in + d_out))
+    return (proj_f, proj_b), (exp_f, exp_b)
+
+
+def bench_jd(args, torch, np, cts, B, device):
+    """One step = one iteration of the App. A.2 eigenvalue iteration over the
+    whole collection (1000 rank-16 LoRAs of a 4096 x 4096 projection, r = 64);
+    a timed call runs the paper's 10 iterations (no early stop)."""
+    from paper_2407_00066_amd import compress as GC
+    n, d, r_l, r, iters = JD_N, JD_D, JD_RL, JD_R, JD_ITERS
+    log("generating %d LoRAs of rank %d, %d x %d" % (n, r_l, d, d))
+    rs = np.random.default_rng(2407)
+    A = rs.standard_normal((n, r_l, d), dtype=np.float32) / np.float32(64.0)
+    Bm = rs.standard_normal((n, d, r_l), dtype=np.float32) / np.float32(4.0)
+    U0 = np.linalg.qr(rs.standard_normal((d, r)))[0].astype(np.float32)
+    V0 = np.linalg.qr(rs.standard_normal((d, r)))[0].astype(np.float32)
+    gA, gB = to_dev(A, device), to_dev(Bm, device)
+    gU0, gVt0 = to_dev(U0, device), to_dev(np.ascontiguousarray(V0.T), device)
+    ws = torch.empty(GC.workspace_size(gA, gB, r), dtype=torch.uint8, device=device)
+
+    def call():
+        return GC.jd_full(gA, gB, gU0, gVt0, iters=iters, workspace=ws)
+
+    log("timing cts_jd_full: %d warmup + %d calls of %d iterations" % (args.warmup, args.steps, iters))
+    ms_call = time_steps(lambda _: call(), [None], args.steps, args.warmup, torch)
+    ms_iter = ms_call / iters
+    # the two large kernels of the last iteration of each call, between stage
+    # events, less the interval of two back-to-back events
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        e1, e2, e3, ea, eb = evs[i]
+        B.set_stage_events([None, e1, e2, e3, None, None])
+        call()
+        ea.record()
+        eb.record()
+    B.set_stage_events(None)
+    torch.cuda.synchronize()
+    mk = 1e3 * sum(e[3].elapsed_time(e[4]) for e in evs) / args.steps
+    proj_us = 1e3 * sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps - mk
+    exp_us = 1e3 * sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps - mk
+    rowt = (d + 63) // 64
+    ntile = (n * r_l + 31) // 32
+    split = max(1, min((512 + rowt - 1) // rowt, ntile // 8))
+    (pf, pb), (ef, eb_) = jd_kernel_models(n, d, d, r_l, r, split)
+    if exp_us >= proj_us:
+        name, fl, nb, us = "jd_expand_kernel (U' = sum B_i C_i, V' = sum A_i^T D_i)", ef, eb_, exp_us
+    else:
+        name, fl, nb, us = ("projection: jd_pq_kernel + jd_combine_kernel (A_i V, B_i^T U, per-LoRA "
+                            "products)", pf, pb, proj_us)
+    roof = roofline_of(fl, nb, us * 1e-6, "f32")
+    roof.update({"kernel": name, "mean_us": round(us, 2), "marker_us": round(mk, 2),
+                 "algorithmic_flops": fl, "algorithmic_bytes": nb,
+                 "project_us": round(proj_us, 2), "expand_us": round(exp_us, 2)})
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = jd_cpu_baseline(A, Bm, U0, V0, args.cpu_seconds)
+    return {
+        "metric": "LoRA-iterations/s of the JD-Full eigenvalue iteration (1000 rank-16 LoRAs, "
+                  "4096 x 4096, r = 64), one MI355X",
+        "value": round(n * iters / (ms_call * 1e-3), 1), "unit": "LoRA-iterations/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_iter, 5), "ms_per_compression": round(ms_call, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded Gaussian LoRAs, random orthonormal initial bases)",
+        "config": {"workload": "jd_full", "n_loras": n, "d_out": d, "d_in": d, "r_lora": r_l, "r": r,
+                   "iterations": iters, "parallelism": "single GPU"},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+
+
+def jd_cpu_baseline(A, Bm, U0, V0, target_s):
+    """The oracle's eigenvalue-iteration step (fp64) on the first LoRAs of the
+    collection, grown until about target_s seconds; LoRA-iterations/s."""
+    import numpy as np
+    from oracle import compress as OC
+    from oracle import oracle
+    U, V = U0.astype(np.float64), V0.astype(np.float64)
+    spent, m = 0.0, 16
+    while True:
+        a, b = A[:m].astype(np.float64), Bm[:m].astype(np.float64)
+        t0 = time.perf_counter()
+        OC.eig_step(a, b, U, V)
+        dt = time.perf_counter() - t0
+        if dt >= target_s / 4 or m >= A.shape[0]:
+            spent = dt
+            break
+        m = min(A.shape[0], int(m * max(2.0, target_s / 4 / max(dt, 1e-3))))
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info() if t.get("user_api") == "blas"] or [1])
+    except ImportError:
+        cores = oracle.num_threads()
+    return {"value": m / spent, "unit": "LoRA-iterations/s", "cores": cores, "kind": "oracle",
+            "sample": "one fp64 eigenvalue-iteration step over the first %d of %d LoRAs, %.1f s"
+                      % (m, A.shape[0], spent)}
 
 
 def bench_layer(args, torch, np, cts, B, wl, device):
@@ -500,7 +616,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill_mix",
-                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32"])
+                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32", "jd_full"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sigma", default="full", choices=["full", "diag"],
@@ -515,7 +631,7 @@ def main():
     if args.sigma == "diag" and args.ranks == "mixed":
         print("--sigma diag and --ranks mixed are separate variants", file=sys.stderr)
         sys.exit(2)
-    if args.workload == "stack32" and (args.sigma != "full" or args.ranks != "uniform"):
+    if args.workload in ("stack32", "jd_full") and (args.sigma != "full" or args.ranks != "uniform"):
         print("--sigma diag and --ranks mixed apply to the single-layer workloads", file=sys.stderr)
         sys.exit(2)
 
@@ -535,7 +651,9 @@ def main():
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     copy_calibration(torch, device)
-    if args.workload == "stack32":
+    if args.workload == "jd_full":
+        rec = bench_jd(args, torch, np, cts, B, device)
+    elif args.workload == "stack32":
         rec = bench_stack(args, torch, np, cts, B, wl, device)
     else:
         rec = bench_layer(args, torch, np, cts, B, wl, device)

@@ -24,6 +24,12 @@
  * Inputs with fewer than r independent directions (n * r_lora < r, or
  * degenerate LoRAs) make the orthogonalization divide by zero: results are
  * then NaN.
+ *
+ * Profiling: while the stage events of cts_set_stage_events (cts.h) are on,
+ * every iteration of the JD records [1] before and [2] after its projection
+ * kernels (P_i = A_i V, Q_i = B_i^T U, then the per-LoRA products) and [3]
+ * after its expansion kernel (the sums over the collection); the last
+ * iteration's records are the ones left.
  */
 #ifndef CTS_COMPRESS_H
 #define CTS_COMPRESS_H
@@ -36,7 +42,7 @@ extern "C" {
 #endif
 
 /* Limits (else CTS_ERR_UNSUPPORTED): 1 <= n <= 65536; r_lora in {4, 8, 16,
- * 32, 64}; r a multiple of 16 in [16, 128] with r <= n * r_lora; d_in and
+ * 32, 64}; r in {16, 32, 48, 64, 96, 128} with r <= n * r_lora; d_in and
  * d_out multiples of 4 in [r, 65536]; every array below 2^31 elements. */
 typedef struct {
     int32_t n;        /* LoRAs in the collection */

@@ -262,6 +262,11 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
 
 }  // namespace
 
+namespace cts {
+hipError_t stage_mark(int i, hipStream_t s) { return mark(i, s); }
+}  // namespace cts
+
+
 extern "C" {
 
 const char* cts_status_string(int status) {

@@ -135,6 +135,10 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         bool diag = false, const int32_t* sorted_seg = nullptr,
                         const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr);
 
+// Records stage event i of the profiling aid (cts_set_stage_events) on s when
+// it is on; a no-op otherwise.
+hipError_t stage_mark(int i, hipStream_t s);
+
 // y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,
                                 void* out, int64_t ldo, int out_dtype, hipStream_t stream);

@@ -15,6 +15,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <vector>
 
 #include "cts.h"
@@ -122,82 +123,144 @@ struct LoadRowsR {
 };
 
 // acc[nb] += A(rows 16 w + ..., k) B(k, 16 nb + ...) over k in [k_begin,
-// k_end), tiles of 32 double-buffered through registers.  Lane l of wave w
-// holds rows 16 w + 4 (l / 16) + v, column 16 nb + l % 16 of block nb.
-template <bool AKM, typename LA, typename LB>
-__device__ void tile_gemm(float* smem, int k_begin, int k_end, int r, const LA& la, const LB& lb,
-                          f32x4 (&acc)[kRMax / 16]) {
+// k_end), tiles of 32 double-buffered through registers; NB = r / 16 column
+// blocks.  Lane l of wave w holds rows 16 w + 4 (l / 16) + v, column
+// 16 nb + l % 16 of block nb.
+template <int NB, bool AKM, typename LA, typename LB>
+__device__ void tile_gemm(float* smem, int k_begin, int k_end, const LA& la, const LB& lb, f32x4 (&acc)[NB]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fk = lane >> 4;
-  const int nb_n = r >> 4;
-  const int nbq = 8 * r;                                  // B float4 slots
+  constexpr int R = 16 * NB;
+  constexpr int NBS = 8 * R;                              // B float4 slots
   constexpr int NAQ = kTM * kBK / 4 / kJT;                // 2 A slots per thread
-  constexpr int NBQ = kBK * kRMax / 4 / kJT;              // up to 4 B slots per thread
-  float4 ra[NAQ], rb[NBQ];
-  int oa[NAQ], ob[NBQ];
+  constexpr int NBQ = (NBS + kJT - 1) / kJT;              // 1..4 B slots per thread
+  // two register sets: while k-tile t is multiplied from LDS, the loads of
+  // k-tiles t+1 (issued one step earlier) and t+2 are in flight
+  float4 ra[2][NAQ], rb[2][NBQ];
+  int oa[2][NAQ], ob[2][NBQ];
   const int nt = (k_end - k_begin + kBK - 1) / kBK;
-  auto fetch = [&](int t) {
+  auto fetch = [&](int t, float4 (&ra_)[NAQ], float4 (&rb_)[NBQ], int (&oa_)[NAQ], int (&ob_)[NBQ]) {
     const int k0 = k_begin + t * kBK;
 #pragma unroll
-    for (int u = 0; u < NAQ; ++u) ra[u] = la(tid + u * kJT, k0, oa[u]);
+    for (int u = 0; u < NAQ; ++u) ra_[u] = la(tid + u * kJT, k0, oa_[u]);
 #pragma unroll
-    for (int u = 0; u < NBQ; ++u) {
-      const int e = tid + u * kJT;
-      if (e < nbq) rb[u] = lb(e, k0, ob[u]);
-    }
+    for (int u = 0; u < NBQ; ++u)
+      if (NBS % kJT == 0 || tid + u * kJT < NBS) rb_[u] = lb(tid + u * kJT, k0, ob_[u]);
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf, const float4 (&ra_)[NAQ], const float4 (&rb_)[NBQ], const int (&oa_)[NAQ],
+                   const int (&ob_)[NBQ]) {
     float* As = smem + buf * kStage;
     float* Bs = As + kAS;
 #pragma unroll
-    for (int u = 0; u < NAQ; ++u) *reinterpret_cast<float4*>(As + oa[u]) = ra[u];
+    for (int u = 0; u < NAQ; ++u) *reinterpret_cast<float4*>(As + oa_[u]) = ra_[u];
 #pragma unroll
     for (int u = 0; u < NBQ; ++u)
-      if (tid + u * kJT < nbq) *reinterpret_cast<float4*>(Bs + ob[u]) = rb[u];
+      if (NBS % kJT == 0 || tid + u * kJT < NBS) *reinterpret_cast<float4*>(Bs + ob_[u]) = rb_[u];
   };
   if (nt <= 0) return;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    if (t + 1 < nt) fetch(t + 1);
-    const float* As = smem + (t & 1) * kStage;
+  const int m = 16 * wave + fr;
+  auto multiply = [&](int buf) {
+    const float* As = smem + buf * kStage;
     const float* Bs = As + kAS;
-    const int m = 16 * wave + fr;
 #pragma unroll
     for (int s = 0; s < kBK / 4; ++s) {
       const int k = 4 * s + fk;
       const float a = AKM ? As[k * kAML + m] : As[m * kALD + k];
 #pragma unroll
-      for (int nb = 0; nb < kRMax / 16; ++nb)
-        if (nb < nb_n) acc[nb] = mfma4(a, Bs[k * kBLD + 16 * nb + fr], acc[nb]);
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a, Bs[k * kBLD + 16 * nb + fr], acc[nb]);
     }
-    if (t + 1 < nt) stash((t + 1) & 1);
+  };
+  fetch(0, ra[0], rb[0], oa[0], ob[0]);
+  if (nt > 1) fetch(1, ra[1], rb[1], oa[1], ob[1]);
+  stash(0, ra[0], rb[0], oa[0], ob[0]);
+  __syncthreads();
+  // step t (parity P = t & 1): loads of t+2 into set P (stashed at step t-1),
+  // multiply k-tile t from LDS buffer P, stash set 1-P (k-tile t+1) into
+  // buffer 1-P.  Unrolled by two so that the register sets are static.
+  auto step = [&](int t, float4 (&raP)[NAQ], float4 (&rbP)[NBQ], int (&oaP)[NAQ], int (&obP)[NBQ],
+                  float4 (&raQ)[NAQ], float4 (&rbQ)[NBQ], int (&oaQ)[NAQ], int (&obQ)[NBQ], int bufP) {
+    if (t + 2 < nt) fetch(t + 2, raP, rbP, oaP, obP);
+    multiply(bufP);
+    if (t + 1 < nt) stash(bufP ^ 1, raQ, rbQ, oaQ, obQ);
     __syncthreads();
+  };
+  for (int t = 0; t < nt; t += 2) {
+    step(t, ra[0], rb[0], oa[0], ob[0], ra[1], rb[1], oa[1], ob[1], 0);
+    if (t + 1 < nt) step(t + 1, ra[1], rb[1], oa[1], ob[1], ra[0], rb[0], oa[0], ob[0], 1);
   }
 }
 
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[kRMax / 16]) {
+template <int NB>
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[NB]) {
 #pragma unroll
-  for (int nb = 0; nb < kRMax / 16; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
 // accumulators -> LDS rows [64][kEpLd]
-__device__ __forceinline__ void acc_to_lds(const f32x4 (&acc)[kRMax / 16], float* dst, int r) {
+template <int NB>
+__device__ __forceinline__ void acc_to_lds(const f32x4 (&acc)[NB], float* dst) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fk = lane >> 4;
 #pragma unroll
-  for (int nb = 0; nb < kRMax / 16; ++nb)
-    if (nb < (r >> 4))
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) dst[(16 * wave + 4 * fk + v) * kEpLd + 16 * nb + fr] = acc[nb][v];
+    for (int v = 0; v < 4; ++v) dst[(16 * wave + 4 * fk + v) * kEpLd + 16 * nb + fr] = acc[nb][v];
 }
 
-// ------------------------------------------------------------ project kernel
-struct ProjArgs {
+// ------------------------------------------------------------ project kernels
+// jd_pq_kernel: partial P or Q rows of a group of 64 / r_l LoRAs over one
+// half of the reduction; jd_combine_kernel: sums the halves and forms the
+// per-LoRA products of the requested mode.
+constexpr int kPqSplit = 2;   // halves of d_in (P) and d_out (Q)
+
+struct PqArgs {
   const float* A; const float* B; const float* V; const float* U;
   const int32_t* lidx; int m;
-  int r_l, d_in, d_out, r;
+  int r_l, d_in, d_out;
+  float* part;                  // [kPqSplit][2][m * r_l][r]
+};
+
+template <int NB>
+__global__ __launch_bounds__(kJT) void jd_pq_kernel(const PqArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  constexpr int r = 16 * NB;
+  const int lpw = kTM / a.r_l;
+  const int q0 = blockIdx.x * lpw;
+  const int nq = min(lpw, a.m - q0);
+  if (nq <= 0) return;
+  const bool isq = blockIdx.y == 1;
+  const int ks = blockIdx.z;
+  const int d = isq ? a.d_out : a.d_in;
+  const int ntile = (d + kBK - 1) / kBK;
+  const int k_lo = (ntile * ks / kPqSplit) * kBK;
+  const int k_hi = min(d, (ntile * (ks + 1) / kPqSplit) * kBK);
+  f32x4 acc[NB];
+  zero_acc(acc);
+  if (isq)
+    tile_gemm<NB, true>(smem, k_lo, k_hi, LoadLoraBt{a.B, a.lidx, q0, nq, a.r_l, a.d_out},
+                        LoadRowsR{a.U, r, k_hi}, acc);
+  else
+    tile_gemm<NB, false>(smem, k_lo, k_hi, LoadLoraRows{a.A, a.lidx, q0, nq, a.r_l, a.d_in},
+                         LoadRowsR{a.V, r, k_hi}, acc);
+  const int64_t rows_all = static_cast<int64_t>(a.m) * a.r_l;
+  float* out = a.part + ((static_cast<int64_t>(ks) * 2 + (isq ? 1 : 0)) * rows_all +
+                         static_cast<int64_t>(q0) * a.r_l) * r;
+  const int rows = nq * a.r_l;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fq = lane >> 4;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = 16 * wave + 4 * fq + v;
+      if (row < rows) out[static_cast<int64_t>(row) * r + 16 * nb + fr] = acc[nb][v];
+    }
+}
+
+struct ProjArgs {
+  const int32_t* lidx; int m;
+  int r_l;
+  const float* part;            // from jd_pq_kernel
   int mode;                     // 0: C, D   1: Sigma   2: score
   const float* w2;              // mode 0: per-LoRA weight of C, D (by id), or null
   const float* sscale;          // mode 1: per-LoRA scale of Sigma (by id), or null
@@ -206,31 +269,36 @@ struct ProjArgs {
   float* score; int ld_score, score_col;
 };
 
-constexpr int kProjSmem = (2 * kTM * kEpLd + 2 * kTM * 64 > 2 * kStage) ? 2 * kTM * kEpLd + 2 * kTM * 64
-                                                                      : 2 * kStage;
+constexpr int kProjSmem = 2 * kTM * kEpLd + 2 * kTM * 64;
 
-__global__ __launch_bounds__(kJT) void jd_project_kernel(const ProjArgs a) {
+template <int NB>
+__global__ __launch_bounds__(kJT) void jd_combine_kernel(const ProjArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[kProjSmem];
   const int lpw = kTM / a.r_l;                       // LoRAs per workgroup
   const int q0 = blockIdx.x * lpw;
   const int nq = min(lpw, a.m - q0);
   if (nq <= 0) return;
   const int tid = threadIdx.x;
-  const int r = a.r, r_l = a.r_l;
-
-  f32x4 accP[kRMax / 16], accQ[kRMax / 16];
-  zero_acc(accP);
-  zero_acc(accQ);
-  tile_gemm<false>(smem, 0, a.d_in, r, LoadLoraRows{a.A, a.lidx, q0, nq, r_l, a.d_in},
-                   LoadRowsR{a.V, r, a.d_in}, accP);
-  tile_gemm<true>(smem, 0, a.d_out, r, LoadLoraBt{a.B, a.lidx, q0, nq, r_l, a.d_out},
-                  LoadRowsR{a.U, r, a.d_out}, accQ);
+  constexpr int r = 16 * NB;
+  const int r_l = a.r_l;
+  const int rows = nq * r_l;
   float* Ps = smem;
   float* Qs = smem + kTM * kEpLd;
-  acc_to_lds(accP, Ps, r);
-  acc_to_lds(accQ, Qs, r);
+  {
+    const int64_t rows_all = static_cast<int64_t>(a.m) * r_l;
+    const float* base = a.part + static_cast<int64_t>(q0) * r_l * r;
+    for (int e = tid; e < rows * r; e += kJT) {
+      float p = 0.f, q = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < kPqSplit; ++ks) {
+        p += base[(static_cast<int64_t>(ks) * 2) * rows_all * r + e];
+        q += base[(static_cast<int64_t>(ks) * 2 + 1) * rows_all * r + e];
+      }
+      Ps[(e / r) * kEpLd + e % r] = p;
+      Qs[(e / r) * kEpLd + e % r] = q;
+    }
+  }
   __syncthreads();
-  const int rows = nq * r_l;
 
   if (a.mode == 0) {
     // G_q = P_q P_q^T, H_q = Q_q Q_q^T (r_l x r_l per LoRA)
@@ -245,6 +313,7 @@ __global__ __launch_bounds__(kJT) void jd_project_kernel(const ProjArgs a) {
       const float* s1 = Qs + row * kEpLd;
       const float* s2 = Qs + (q * r_l + l2) * kEpLd;
       float g = 0.f, h = 0.f;
+#pragma unroll 8
       for (int j = 0; j < r; ++j) {
         g = fmaf(p1[j], p2[j], g);
         h = fmaf(s1[j], s2[j], h);
@@ -273,7 +342,7 @@ __global__ __launch_bounds__(kJT) void jd_project_kernel(const ProjArgs a) {
     return;
   }
   // Sigma_q[x][y] = sum_l Q_q[l][x] P_q[l][y]
-  const int rr = r * r;
+  constexpr int rr = r * r;
   if (a.mode == 1) {
     for (int e = tid; e < nq * rr; e += kJT) {
       const int q = e / rr, xy = e - q * rr, x = xy / r, y = xy - x * r;
@@ -310,13 +379,15 @@ __global__ __launch_bounds__(kJT) void jd_project_kernel(const ProjArgs a) {
 // V' = sum A_i^T D_i.  blockIdx.y = split s over the flat (LoRA, l) index.
 struct ExpArgs {
   const float* A; const float* B; const int32_t* lidx; int m;
-  int r_l, d_in, d_out, r;
+  int r_l, d_in, d_out;
   const float* C; const float* D;
   int split; float* partU; float* partV;
 };
 
+template <int NB>
 __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  constexpr int r = 16 * NB;
   const bool isv = blockIdx.z == 1;
   const int d = isv ? a.d_in : a.d_out;
   const int row0 = blockIdx.x * kTM;
@@ -326,25 +397,24 @@ __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
   const int s = blockIdx.y;
   const int f_lo = static_cast<int>(static_cast<int64_t>(ntile) * s / a.split) * kBK;
   const int f_hi = min(fk_total, static_cast<int>(static_cast<int64_t>(ntile) * (s + 1) / a.split) * kBK);
-  f32x4 acc[kRMax / 16];
+  f32x4 acc[NB];
   zero_acc(acc);
   if (isv)
-    tile_gemm<true>(smem, f_lo, f_hi, a.r, LoadExpandA{a.A, a.lidx, a.r_l, a.d_in, row0, f_hi},
-                    LoadRowsR{a.D, a.r, f_hi}, acc);
+    tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA{a.A, a.lidx, a.r_l, a.d_in, row0, f_hi},
+                        LoadRowsR{a.D, r, f_hi}, acc);
   else
-    tile_gemm<false>(smem, f_lo, f_hi, a.r, LoadExpandB{a.B, a.lidx, a.r_l, a.d_out, row0, f_hi},
-                     LoadRowsR{a.C, a.r, f_hi}, acc);
-  float* part = (isv ? a.partV : a.partU) + static_cast<int64_t>(s) * d * a.r;
+    tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB{a.B, a.lidx, a.r_l, a.d_out, row0, f_hi},
+                         LoadRowsR{a.C, r, f_hi}, acc);
+  float* part = (isv ? a.partV : a.partU) + static_cast<int64_t>(s) * d * r;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fq = lane >> 4;
 #pragma unroll
-  for (int nb = 0; nb < kRMax / 16; ++nb)
-    if (nb < (a.r >> 4))
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = row0 + 16 * wave + 4 * fq + v;
-        if (row < d) part[static_cast<int64_t>(row) * a.r + 16 * nb + fr] = acc[nb][v];
-      }
+    for (int v = 0; v < 4; ++v) {
+      const int row = row0 + 16 * wave + 4 * fq + v;
+      if (row < d) part[static_cast<int64_t>(row) * r + 16 * nb + fr] = acc[nb][v];
+    }
 }
 
 // X[z][row][j] = sum_s part_z[s][row][j], z = 0 (U, d_out rows), 1 (V, d_in rows)
@@ -364,61 +434,108 @@ __global__ __launch_bounds__(kJT) void jd_reduce_kernel(const float* partU, cons
 }
 
 // ------------------------------------------------------ CholeskyQR pieces
+// Rows of a basis X [d][r] as the A operand (m = row, k = column).
+struct LoadBasisRows {
+  const float* X; int r, row0, d;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int m = e >> 3, kq = e & 7;
+    off = m * kALD + 4 * kq;
+    const int row = row0 + m, k = k0 + 4 * kq;
+    if (row >= d || k >= r) return float4{0.f, 0.f, 0.f, 0.f};
+    return *reinterpret_cast<const float4*>(X + static_cast<int64_t>(row) * r + k);
+  }
+};
+
+// X^T as the A operand (m = column a of X, k = row of X): k-major.
+struct LoadBasisT {
+  const float* X; int r, a0, k_end;
+  __device__ float4 operator()(int e, int k0, int& off) const {
+    const int kk = e >> 4, m4 = e & 15;
+    off = kk * kAML + 4 * m4;
+    const int row = k0 + kk, col = a0 + 4 * m4;
+    if (row >= k_end || col >= r) return float4{0.f, 0.f, 0.f, 0.f};
+    return *reinterpret_cast<const float4*>(X + static_cast<int64_t>(row) * r + col);
+  }
+};
+
 // Partial Gram matrices: gp[z][b][x][y] = sum over rows of block b of
-// X_z[row][x] Y_z[row][y] (Y = X when Y0/Y1 are null).
+// X_z[row][x] Y_z[row][y] (Y = X when Y0/Y1 are null); grid (blocks, 2, r/64
+// rounded up).
+template <int NB>
 __global__ __launch_bounds__(kJT) void jd_gram_kernel(const float* X0, const float* X1, const float* Y0,
-                                                      const float* Y1, int d0, int d1, int r, int nblk,
-                                                      float* gp) {
-  __shared__ float xs[64 * (kRMax + 1)], ys[64 * (kRMax + 1)];
-  const int z = blockIdx.y, b = blockIdx.x;
+                                                      const float* Y1, int d0, int d1, int nblk, float* gp) {
+  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  constexpr int r = 16 * NB;
+  const int z = blockIdx.y, b = blockIdx.x, a0 = blockIdx.z * kTM;
   const int d = z ? d1 : d0;
   const float* X = z ? X1 : X0;
   const float* Y = z ? (Y1 ? Y1 : X1) : (Y0 ? Y0 : X0);
-  float* out = gp + (static_cast<int64_t>(z) * nblk + b) * r * r;
-  const int rr = r * r;
   const int row_lo = b * kGramRows, row_hi = min(d, row_lo + kGramRows);
-  float acc[kRMax * kRMax / kJT];
+  f32x4 acc[NB];
+  zero_acc(acc);
+  if (row_lo < row_hi)
+    tile_gemm<NB, true>(smem, row_lo, row_hi, LoadBasisT{X, r, a0, row_hi}, LoadRowsR{Y, r, row_hi}, acc);
+  float* out = gp + (static_cast<int64_t>(z) * nblk + b) * r * r;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fq = lane >> 4;
 #pragma unroll
-  for (int u = 0; u < kRMax * kRMax / kJT; ++u) acc[u] = 0.f;
-  for (int c0 = row_lo; c0 < row_hi; c0 += 64) {
-    const int nr = min(64, row_hi - c0);
-    __syncthreads();
-    for (int e = threadIdx.x; e < 64 * r; e += kJT) {
-      const int rw = e / r, j = e - rw * r;
-      xs[rw * (kRMax + 1) + j] = rw < nr ? X[static_cast<int64_t>(c0 + rw) * r + j] : 0.f;
-      ys[rw * (kRMax + 1) + j] = rw < nr ? Y[static_cast<int64_t>(c0 + rw) * r + j] : 0.f;
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int x = a0 + 16 * wave + 4 * fq + v;
+      if (x < r) out[x * r + 16 * nb + fr] = acc[nb][v];
     }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kRMax * kRMax / kJT; ++u) {
-      const int e = threadIdx.x + u * kJT;
-      if (e < rr) {
-        const int x = e / r, y = e - x * r;
-        float s = acc[u];
-        for (int rw = 0; rw < 64; ++rw) s = fmaf(xs[rw * (kRMax + 1) + x], ys[rw * (kRMax + 1) + y], s);
-        acc[u] = s;
-      }
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kRMax * kRMax / kJT; ++u) {
-    const int e = threadIdx.x + u * kJT;
-    if (e < rr) out[e] = acc[u];
-  }
 }
 
 // One workgroup per z: G = sum_b gp[z][b] (fixed order).  chol = 0: writes G
 // to out[z].  chol = 1: G = R^T R (R upper, positive diagonal), writes R^-1.
-__global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int r, int chol, float* out) {
-  __shared__ float g[kRMax * (kRMax + 1)];
-  __shared__ float t[kRMax];
+// The columns are equilibrated first (G' = D^-1 G D^-1, D = diag(G)^(1/2),
+// R = R' D): the columns of X = M U scale with M's eigenvalues, and without
+// it the fp32 Cholesky of a nearly converged basis breaks down.  A pivot
+// below 1e-12 (relative to the unit diagonal of G') is taken as 1e-12.
+// Blocked in 16 x 16 tiles so that the workgroup meets few barriers: per
+// block column, one wave factors the diagonal tile in registers, the threads
+// solve the block row, then update the trailing triangle; R'^-1 from the
+// inverses of the diagonal tiles, outward one block diagonal at a time.
+template <int NB>
+__global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int chol, float* out) {
+  constexpr int r = 16 * NB;
+  constexpr int ld = r + 1;
+  constexpr int rr = r * r;
+  __shared__ float g[r * ld];
+  __shared__ float inv[r * ld];
+  __shared__ float dsc[r];
   const int z = blockIdx.x, tid = threadIdx.x;
-  const int rr = r * r, ld = kRMax + 1;
+  const int lane = tid & 63, wave = tid >> 6;
   const float* src = gp + static_cast<int64_t>(z) * nblk * rr;
-  for (int e = tid; e < rr; e += kJT) {
-    float s = 0.f;
-    for (int b = 0; b < nblk; ++b) s += src[static_cast<int64_t>(b) * rr + e];
-    g[(e / r) * ld + e % r] = s;
+  {
+    // partials summed in block order, four blocks' loads in flight
+    constexpr int NU = (rr + kJT - 1) / kJT;
+    float acc[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) acc[u] = 0.f;
+    int b = 0;
+    for (; b + 4 <= nblk; b += 4) {
+      float v[4][NU];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < NU; ++u)
+          v[q][u] = (tid + u * kJT < rr) ? src[static_cast<int64_t>(b + q) * rr + tid + u * kJT] : 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < NU; ++u) acc[u] += v[q][u];
+    }
+    for (; b < nblk; ++b)
+#pragma unroll
+      for (int u = 0; u < NU; ++u)
+        if (tid + u * kJT < rr) acc[u] += src[static_cast<int64_t>(b) * rr + tid + u * kJT];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int e = tid + u * kJT;
+      if (e < rr) g[(e / r) * ld + e % r] = acc[u];
+    }
   }
   __syncthreads();
   float* dst = out + static_cast<int64_t>(z) * rr;
@@ -426,87 +543,181 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
     for (int e = tid; e < rr; e += kJT) dst[e] = g[(e / r) * ld + e % r];
     return;
   }
-  // left-looking Cholesky, row j of R from rows < j (R overwrites the upper
-  // triangle of g; the strict lower triangle keeps G's entries, unused)
-  for (int j = 0; j < r; ++j) {
-    if (tid >= j && tid < r) {
-      float s = g[j * ld + tid];
-      for (int k = 0; k < j; ++k) s = fmaf(-g[k * ld + j], g[k * ld + tid], s);
-      t[tid] = s;
-    }
-    __syncthreads();
-    if (tid >= j && tid < r) g[j * ld + tid] = t[tid] / sqrtf(t[j]);
-    __syncthreads();
-  }
-  // R^-1 column c by back substitution: thread c owns column c (written to
-  // the lower triangle transposed: inv[c][i] stored at g[c][i] for i <= c is
-  // R's own entry, so use the output array directly)
   if (tid < r) {
-    const int c = tid;
-    for (int i = r - 1; i >= 0; --i) {
-      float s = (i == c) ? 1.f : 0.f;
-      if (i <= c) {
-        for (int k = i + 1; k <= c; ++k) s = fmaf(-g[i * ld + k], dst[k * r + c], s);
-        s /= g[i * ld + i];
-      }
-      dst[i * r + c] = s;
-    }
+    const float dj = g[tid * ld + tid];
+    dsc[tid] = dj > 0.f ? sqrtf(dj) : 1.f;
   }
+  __syncthreads();
+  for (int e = tid; e < rr; e += kJT) {
+    const int i = e / r, c = e - i * r;
+    g[i * ld + c] /= dsc[i] * dsc[c];
+  }
+  __syncthreads();
+
+  // ---- blocked right-looking Cholesky of G' (R' in the upper triangle of g)
+  for (int J = 0; J < NB; ++J) {
+    const int o = 16 * J;
+    if (wave == 0) {
+      // lane c < 16 holds column c of the diagonal tile (rows 0..15)
+      const int c = lane & 15;
+      float col[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) col[i] = (i <= c) ? g[(o + i) * ld + o + c] : 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const float piv = sqrtf(fmaxf(__shfl(col[k], k), 1e-12f));
+        col[k] = (c == k) ? piv : (c > k ? col[k] / piv : col[k]);
+#pragma unroll
+        for (int i = k + 1; i < 16; ++i) {
+          const float rki = __shfl(col[k], i);            // R'[k][i], row k from lane i
+          if (c >= i) col[i] = fmaf(-rki, col[k], col[i]);
+        }
+      }
+      if (lane < 16)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (i <= c) g[(o + i) * ld + o + c] = col[i];
+    }
+    __syncthreads();
+    // block row: R'[o..o+16)[c] = R_JJ^-T G'[o..o+16)[c] for c >= o + 16
+    for (int c = o + 16 + tid; c < r; c += kJT) {
+      float y[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float s = g[(o + i) * ld + c];
+#pragma unroll
+        for (int k = 0; k < i; ++k) s = fmaf(-g[(o + k) * ld + o + i], y[k], s);
+        y[i] = s / g[(o + i) * ld + o + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) g[(o + i) * ld + c] = y[i];
+    }
+    __syncthreads();
+    // trailing triangle: G'[i][c] -= sum_k R'[o+k][i] R'[o+k][c], o+16 <= i <= c
+    const int w = r - o - 16;
+    for (int e = tid; e < w * w; e += kJT) {
+      const int i = o + 16 + e / w, c = o + 16 + e % w;
+      if (c >= i) {
+        float s = g[i * ld + c];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) s = fmaf(-g[(o + k) * ld + i], g[(o + k) * ld + c], s);
+        g[i * ld + c] = s;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- R'^-1: diagonal tiles first (wave w: tiles w, w + 4, ...), lane c
+  // holding column c of the tile's inverse
+  for (int e = tid; e < r * ld; e += kJT) inv[e] = 0.f;
+  __syncthreads();
+  for (int I = wave; I < NB; I += kJT / 64) {
+    const int o = 16 * I;
+    const int c = lane & 15;
+    float x[16];
+#pragma unroll
+    for (int i = 15; i >= 0; --i) {
+      float s = (i == c) ? 1.f : 0.f;
+#pragma unroll
+      for (int k = i + 1; k < 16; ++k) s = fmaf(-g[(o + i) * ld + o + k], x[k], s);
+      x[i] = (i <= c) ? s / g[(o + i) * ld + o + i] : 0.f;
+    }
+    if (lane < 16)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) inv[(o + i) * ld + o + c] = x[i];
+  }
+  __syncthreads();
+  // off-diagonal tiles by distance d: X_IJ = -X_II sum_{K=I+1..J} R'_IK X_KJ.
+  // T_IJ is kept transposed in tile JI of g's strict lower triangle, which
+  // nothing reads after the factorization.
+  for (int d = 1; d < NB; ++d) {
+    for (int e = tid; e < (NB - d) * 256; e += kJT) {
+      const int I = e / 256, a = (e % 256) / 16, bcol = e % 16;
+      const int J = I + d;
+      float s = 0.f;
+      for (int K = I + 1; K <= J; ++K)
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          s = fmaf(g[(16 * I + a) * ld + 16 * K + k], inv[(16 * K + k) * ld + 16 * J + bcol], s);
+      g[(16 * J + bcol) * ld + 16 * I + a] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < (NB - d) * 256; e += kJT) {
+      const int I = e / 256, a = (e % 256) / 16, bcol = e % 16;
+      const int J = I + d;
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        s = fmaf(inv[(16 * I + a) * ld + 16 * I + k], g[(16 * J + bcol) * ld + 16 * I + k], s);
+      inv[(16 * I + a) * ld + 16 * J + bcol] = -s;
+    }
+    __syncthreads();
+  }
+  // R^-1 = D^-1 R'^-1
+  for (int e = tid; e < rr; e += kJT) dst[e] = inv[(e / r) * ld + e % r] / dsc[e / r];
 }
 
-// X_z[row][:] <- X_z[row][:] Rinv_z (rows of 64 per workgroup, in place)
-__global__ __launch_bounds__(kJT) void jd_apply_kernel(float* X0, float* X1, int d0, int d1, int r,
+// X_z[row][:] <- X_z[row][:] Rinv_z (64 rows per workgroup, in place: a
+// workgroup reads only its own rows, and all of them before it writes)
+template <int NB>
+__global__ __launch_bounds__(kJT) void jd_apply_kernel(float* X0, float* X1, int d0, int d1,
                                                        const float* rinv) {
-  __shared__ float rs[kRMax * kRMax];
-  __shared__ float xs[64 * (kRMax + 1)];
+  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  constexpr int r = 16 * NB;
   const int z = blockIdx.y;
   const int d = z ? d1 : d0;
   float* X = z ? X1 : X0;
-  const int row0 = blockIdx.x * 64;
+  const int row0 = blockIdx.x * kTM;
   if (row0 >= d) return;
-  const int nr = min(64, d - row0);
-  const float* R = rinv + static_cast<int64_t>(z) * r * r;
-  for (int e = threadIdx.x; e < r * r; e += kJT) rs[e] = R[e];
-  for (int e = threadIdx.x; e < nr * r; e += kJT)
-    xs[(e / r) * (kRMax + 1) + e % r] = X[static_cast<int64_t>(row0) * r + e];
-  __syncthreads();
-  for (int e = threadIdx.x; e < nr * r; e += kJT) {
-    const int rw = e / r, j = e - rw * r;
-    float s = 0.f;
-    for (int k = 0; k <= j; ++k) s = fmaf(xs[rw * (kRMax + 1) + k], rs[k * r + j], s);
-    X[static_cast<int64_t>(row0 + rw) * r + j] = s;
-  }
+  f32x4 acc[NB];
+  zero_acc(acc);
+  tile_gemm<NB, false>(smem, 0, r, LoadBasisRows{X, r, row0, d},
+                       LoadRowsR{rinv + static_cast<int64_t>(z) * r * r, r, r}, acc);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fq = lane >> 4;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = row0 + 16 * wave + 4 * fq + v;
+      if (row < d) X[static_cast<int64_t>(row) * r + 16 * nb + fr] = acc[nb][v];
+    }
 }
 
 // Convergence measure, partial sums per 64-row block: E = Xn - Xo M_z,
 // rp[z][b] = (||E||^2, ||Xn||^2) over the block.
+template <int NB>
 __global__ __launch_bounds__(kJT) void jd_resid_kernel(const float* Uo, const float* Un, const float* Vo,
-                                                       const float* Vn, int d0, int d1, int r,
-                                                       const float* M, int nblk, float* rp) {
-  __shared__ float ms[kRMax * kRMax];
-  __shared__ float xs[64 * (kRMax + 1)];
+                                                       const float* Vn, int d0, int d1, const float* M,
+                                                       int nblk, float* rp) {
+  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
   __shared__ float red[2 * kJT];
+  constexpr int r = 16 * NB;
   const int z = blockIdx.y, b = blockIdx.x;
   const int d = z ? d1 : d0;
   const float* Xo = z ? Vo : Uo;
   const float* Xn = z ? Vn : Un;
-  const int row0 = b * 64;
+  const int row0 = b * kTM;
   float e2 = 0.f, x2 = 0.f;
   if (row0 < d) {
-    const int nr = min(64, d - row0);
-    for (int e = threadIdx.x; e < r * r; e += kJT) ms[e] = M[static_cast<int64_t>(z) * r * r + e];
-    for (int e = threadIdx.x; e < nr * r; e += kJT)
-      xs[(e / r) * (kRMax + 1) + e % r] = Xo[static_cast<int64_t>(row0) * r + e];
-    __syncthreads();
-    for (int e = threadIdx.x; e < nr * r; e += kJT) {
-      const int rw = e / r, j = e - rw * r;
-      float s = 0.f;
-      for (int k = 0; k < r; ++k) s = fmaf(xs[rw * (kRMax + 1) + k], ms[k * r + j], s);
-      const float xn = Xn[static_cast<int64_t>(row0 + rw) * r + j];
-      const float df = xn - s;
-      e2 = fmaf(df, df, e2);
-      x2 = fmaf(xn, xn, x2);
-    }
+    f32x4 acc[NB];
+    zero_acc(acc);
+    tile_gemm<NB, false>(smem, 0, r, LoadBasisRows{Xo, r, row0, d},
+                         LoadRowsR{M + static_cast<int64_t>(z) * r * r, r, r}, acc);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int fr = lane & 15, fq = lane >> 4;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = row0 + 16 * wave + 4 * fq + v;
+        if (row < d) {
+          const float xn = Xn[static_cast<int64_t>(row) * r + 16 * nb + fr];
+          const float df = xn - acc[nb][v];
+          e2 = fmaf(df, df, e2);
+          x2 = fmaf(xn, xn, x2);
+        }
+      }
   }
   red[threadIdx.x] = e2;
   red[kJT + threadIdx.x] = x2;
@@ -519,14 +730,27 @@ __global__ __launch_bounds__(kJT) void jd_resid_kernel(const float* Uo, const fl
   }
 }
 
+// one wave: lane l sums blocks l, l + 64, ...; then lane 0 sums the lanes in order
 __global__ void jd_crit_kernel(const float* rp, int nblk, float* crit) {
-  if (threadIdx.x != 0) return;
+  __shared__ float part[4][64];
+  const int l = threadIdx.x;
+  for (int z = 0; z < 2; ++z) {
+    float se = 0.f, sx = 0.f;
+    for (int b = l; b < nblk; b += 64) {
+      se += rp[(z * nblk + b) * 2];
+      sx += rp[(z * nblk + b) * 2 + 1];
+    }
+    part[2 * z][l] = se;
+    part[2 * z + 1][l] = sx;
+  }
+  __syncthreads();
+  if (l != 0) return;
   float c = 0.f;
   for (int z = 0; z < 2; ++z) {
     float se = 0.f, sx = 0.f;
-    for (int b = 0; b < nblk; ++b) {
-      se += rp[(z * nblk + b) * 2];
-      sx += rp[(z * nblk + b) * 2 + 1];
+    for (int k = 0; k < 64; ++k) {
+      se += part[2 * z][k];
+      sx += part[2 * z + 1][k];
     }
     c = fmaxf(c, sqrtf(se / sx));
   }
@@ -695,6 +919,21 @@ __global__ __launch_bounds__(kJT) void km_members_kernel(const int32_t* labels, 
 }
 
 // ------------------------------------------------------------------ host side
+// Calls f(std::integral_constant<int, NB>) for the compiled column-block
+// counts NB = r / 16.
+template <typename F>
+hipError_t with_nb(int r, F f) {
+  switch (r / 16) {
+    case 1: return f(std::integral_constant<int, 1>{});
+    case 2: return f(std::integral_constant<int, 2>{});
+    case 3: return f(std::integral_constant<int, 3>{});
+    case 4: return f(std::integral_constant<int, 4>{});
+    case 6: return f(std::integral_constant<int, 6>{});
+    case 8: return f(std::integral_constant<int, 8>{});
+    default: return hipErrorInvalidValue;
+  }
+}
+
 bool bad_ptr(const void* ptr, size_t align) {
   return ptr == nullptr || (reinterpret_cast<uintptr_t>(ptr) % align) != 0;
 }
@@ -704,7 +943,8 @@ int validate(const cts_jd_problem* p) {
   if (p->n <= 0 || p->d_out <= 0 || p->d_in <= 0 || p->r_lora <= 0 || p->r <= 0) return CTS_ERR_INVALID_ARG;
   const int rl = p->r_lora;
   if (!(rl == 4 || rl == 8 || rl == 16 || rl == 32 || rl == 64)) return CTS_ERR_UNSUPPORTED;
-  if (p->r % 16 != 0 || p->r > kRMax) return CTS_ERR_UNSUPPORTED;
+  if (!(p->r == 16 || p->r == 32 || p->r == 48 || p->r == 64 || p->r == 96 || p->r == 128))
+    return CTS_ERR_UNSUPPORTED;
   if (p->n > 65536 || static_cast<int64_t>(p->n) * rl < p->r) return CTS_ERR_UNSUPPORTED;
   if (p->d_in % 4 || p->d_out % 4 || p->d_in < p->r || p->d_out < p->r || p->d_in > 65536 ||
       p->d_out > 65536)
@@ -719,7 +959,7 @@ int validate(const cts_jd_problem* p) {
 // Workspace of one JD run (plus the clustering extras when K > 0).
 struct JdPlan {
   int split, nblk_out, nblk_in, nblk;
-  size_t off_U, off_V, off_Uo, off_Vo, off_C, off_D, off_pU, off_pV, off_gp, off_mat, off_rp, off_lidx,
+  size_t off_U, off_V, off_Uo, off_Vo, off_C, off_D, off_pq, off_pU, off_pV, off_gp, off_mat, off_rp, off_lidx,
       off_w2, off_w, off_n2, off_crit, total;
   // clustering
   size_t off_S, off_cent, off_dist, off_lab, off_chg, off_offs, off_memb, off_score;
@@ -747,6 +987,7 @@ void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   pl->off_Vo = take(4ull * p->d_in * r);
   pl->off_C = take(4ull * fk * r);
   pl->off_D = take(4ull * fk * r);
+  pl->off_pq = take(4ull * kPqSplit * 2 * fk * r);
   pl->off_pU = take(4ull * pl->split * p->d_out * r);
   pl->off_pV = take(4ull * pl->split * p->d_in * r);
   pl->off_gp = take(4ull * 2 * pl->nblk * r * r);
@@ -784,11 +1025,19 @@ hipError_t launch_project(const Jd& j, const float* A, const float* B, const flo
                           const int32_t* lidx, int m, int mode, const float* w2, const float* sscale,
                           float* Sigma, float* score, int ld_score, int score_col) {
   const cts_jd_problem* p = j.p;
-  ProjArgs a{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, p->r, mode, w2, sscale,
-             j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D), Sigma, score, ld_score, score_col};
+  float* part = j.at<float>(j.pl.off_pq);
+  PqArgs pa{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, part};
+  ProjArgs a{lidx, m, p->r_lora, part, mode, w2, sscale, j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D),
+             Sigma, score, ld_score, score_col};
   const int lpw = kTM / p->r_lora;
-  hipLaunchKernelGGL(jd_project_kernel, dim3((m + lpw - 1) / lpw), dim3(kJT), 0, j.st, a);
-  return hipGetLastError();
+  const unsigned groups = static_cast<unsigned>((m + lpw - 1) / lpw);
+  return with_nb(p->r, [&](auto c) {
+    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, 2, kPqSplit), dim3(kJT), 0, j.st, pa);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(jd_combine_kernel<decltype(c)::value>, dim3(groups), dim3(kJT), 0, j.st, a);
+    return hipGetLastError();
+  });
 }
 
 // One eigenvalue-iteration step from (U, V) in the workspace to (Uo, Vo)
@@ -801,16 +1050,21 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   float* V = j.at<float>(j.pl.off_V);
   float* Un = j.at<float>(j.pl.off_Uo);
   float* Vn = j.at<float>(j.pl.off_Vo);
-  hipError_t e = launch_project(j, A, B, V, U, lidx, m, 0, w2, nullptr, nullptr, nullptr, 0, 0);
+  hipError_t e = stage_mark(1, j.st);
   if (e != hipSuccess) return e;
+  e = launch_project(j, A, B, V, U, lidx, m, 0, w2, nullptr, nullptr, nullptr, 0, 0);
+  if (e != hipSuccess || (e = stage_mark(2, j.st)) != hipSuccess) return e;
   // expand, split so that the collection's share per workgroup is >= 8 k-tiles
   const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
   const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
-  ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, r, j.at<float>(j.pl.off_C),
+  ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, j.at<float>(j.pl.off_C),
              j.at<float>(j.pl.off_D), split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV)};
   const int rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
-  hipLaunchKernelGGL(jd_expand_kernel, dim3(rowt, split, 2), dim3(kJT), 0, j.st, ea);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  e = with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_expand_kernel<decltype(c)::value>, dim3(rowt, split, 2), dim3(kJT), 0, j.st, ea);
+    return hipGetLastError();
+  });
+  if (e != hipSuccess || (e = stage_mark(3, j.st)) != hipSuccess) return e;
   const int64_t nmax = static_cast<int64_t>(std::max(p->d_out, p->d_in)) * r;
   hipLaunchKernelGGL(jd_reduce_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nmax + kJT - 1) / kJT)), 2),
                      dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out,
@@ -820,25 +1074,42 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   float* gp = j.at<float>(j.pl.off_gp);
   float* mat = j.at<float>(j.pl.off_mat);
   const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
+  const dim3 ggrid(j.pl.nblk, 2, (r + kTM - 1) / kTM);
+  auto gram = [&](const float* X0, const float* X1, const float* Y0, const float* Y1) {
+    return with_nb(r, [&](auto c) {
+      hipLaunchKernelGGL(jd_gram_kernel<decltype(c)::value>, ggrid, dim3(kJT), 0, j.st, X0, X1, Y0, Y1, p->d_out,
+                         p->d_in, j.pl.nblk, gp);
+      return hipGetLastError();
+    });
+  };
   for (int pass = 0; pass < 2; ++pass) {
-    hipLaunchKernelGGL(jd_gram_kernel, dim3(j.pl.nblk, 2), dim3(kJT), 0, j.st, Un, Vn, nullptr, nullptr,
-                       p->d_out, p->d_in, r, j.pl.nblk, gp);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(jd_chol_kernel, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, r, 1, mat);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(jd_apply_kernel, dim3(nrb, 2), dim3(kJT), 0, j.st, Un, Vn, p->d_out, p->d_in, r, mat);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = gram(Un, Vn, nullptr, nullptr)) != hipSuccess) return e;
+    e = with_nb(r, [&](auto c) {
+      hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 1, mat);
+      return hipGetLastError();
+    });
+    if (e != hipSuccess) return e;
+    e = with_nb(r, [&](auto c) {
+      hipLaunchKernelGGL(jd_apply_kernel<decltype(c)::value>, dim3(nrb, 2), dim3(kJT), 0, j.st, Un, Vn, p->d_out,
+                         p->d_in, mat);
+      return hipGetLastError();
+    });
+    if (e != hipSuccess) return e;
   }
   // measure: M = X_old^T X_new, E = X_new - X_old M
-  hipLaunchKernelGGL(jd_gram_kernel, dim3(j.pl.nblk, 2), dim3(kJT), 0, j.st, U, V, Un, Vn, p->d_out, p->d_in, r,
-                     j.pl.nblk, gp);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(jd_chol_kernel, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, r, 0, mat);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = gram(U, V, Un, Vn)) != hipSuccess) return e;
+  e = with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 0, mat);
+    return hipGetLastError();
+  });
+  if (e != hipSuccess) return e;
   float* rp = j.at<float>(j.pl.off_rp);
-  hipLaunchKernelGGL(jd_resid_kernel, dim3(nrb, 2), dim3(kJT), 0, j.st, U, Un, V, Vn, p->d_out, p->d_in, r, mat,
-                     nrb, rp);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  e = with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_resid_kernel<decltype(c)::value>, dim3(nrb, 2), dim3(kJT), 0, j.st, U, Un, V, Vn,
+                       p->d_out, p->d_in, mat, nrb, rp);
+    return hipGetLastError();
+  });
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(jd_crit_kernel, dim3(1), dim3(64), 0, j.st, rp, nrb, crit_out);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   std::swap(j.pl.off_U, j.pl.off_Uo);

@@ -63,7 +63,7 @@ CASES = {
     # name: seed, n, d_out, d_in, r_l, r, iters
     "small_r16": (31, 12, 96, 80, 4, 16, 6),
     "ragged_tiles": (32, 13, 132, 100, 8, 32, 5),       # d not multiples of 64, n r_l not of 32
-    "rank16_loras": (33, 20, 200, 136, 16, 48, 4),
+    "rank16_loras": (33, 20, 200, 136, 16, 48, 4),       # r = 48: three column blocks
     "rank32_loras": (34, 9, 160, 192, 32, 64, 4),
     "rank64_loras": (35, 5, 128, 140, 64, 128, 3),
 }
