@@ -83,6 +83,21 @@ int cts_jd_full(const cts_jd_problem* p, const float* A, const float* B, const f
                 float* Sigma, float* crit, int32_t* iters_done, void* workspace,
                 size_t workspace_bytes, void* stream);
 
+/* JD-Diag by the alternating least squares of App. A.1 case 2: unconstrained
+ * U, V (r columns) and diagonal cores.  From (U0, Vt0) the diagonals are solved
+ * first, sigma_i = (U^T U o V^T V)^-1 (U^T B_i o V^T A_i^T) 1; then each of
+ * `sweeps` sweeps solves U = (sum_i B_i A_i V S_i)(sum_i S_i V^T V S_i)^-1,
+ * then V likewise with the new U, then the diagonals again (S_i =
+ * diag(sigma_i)).  normalize != 0 then rescales the diagonals to
+ * sum_i ||sigma_i||^2 = 1 and multiplies U and V by the square root of the
+ * removed factor (every U diag(sigma_i) V^T unchanged).  The r x r systems
+ * are solved by Cholesky (columns equilibrated).  Outputs U [d_out][r], Vt
+ * [r][d_in], sigma [n][r] (the cores cts_apply_diag serves).  Same workspace
+ * as cts_jd_full.  Does not wait.  sweeps >= 0. */
+int cts_jd_diag(const cts_jd_problem* p, const float* A, const float* B, const float* U0,
+                const float* Vt0, int32_t sweeps, int32_t normalize, float* U, float* Vt,
+                float* sigma, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Cores for given orthonormal bases (eq. sigmastar): Sigma_i = U^T B_i A_i V
  * for every LoRA.  Same workspace as cts_jd_full.  Does not wait. */
 int cts_jd_sigma(const cts_jd_problem* p, const float* A, const float* B, const float* U,

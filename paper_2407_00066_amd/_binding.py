@@ -27,7 +27,7 @@ EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncom
             "cts_set_stage_events",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
-            "cts_jd_sigma", "cts_jd_cluster")
+            "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
 N_STAGE_EVENTS = 6
 
 
@@ -93,6 +93,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_jd_full.argtypes = [jp, vp, vp, vp, vp, i32, fl, i32, vp, vp, vp, vp,
                                           ctypes.POINTER(i32), vp, sz, vp]
                 L.cts_jd_full.restype = ctypes.c_int
+                L.cts_jd_diag.argtypes = [jp, vp, vp, vp, vp, i32, i32, vp, vp, vp, vp, sz, vp]
+                L.cts_jd_diag.restype = ctypes.c_int
                 L.cts_jd_sigma.argtypes = [jp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_jd_sigma.restype = ctypes.c_int
                 L.cts_jd_cluster.argtypes = [jp, i32, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i32), i32, i32,

@@ -1,5 +1,6 @@
 """Offline compressor (include/cts_compress.h): JD-Full by the eigenvalue
-iteration of App. A.2 and the clustering of App. A.3 on the GPU.
+iteration of App. A.2, JD-Diag by the alternating least squares of App. A.1
+case 2 and the clustering of App. A.3, on the GPU.
 
 Argument marshalling only, like the layer's binding: every step runs in
 libcts.so's kernels.  Arrays are fp32 torch tensors on one device, in the
@@ -62,6 +63,24 @@ def jd_full(A, B, U0, Vt0, iters=10, tau=0.0, normalize=False, workspace=None):
                              _dev(crit, "crit", dev, F32), ctypes.byref(done), ctypes.c_void_p(ws.data_ptr()),
                              ws.numel(), _stream(dev)), "cts_jd_full")
     return U, Vt, S, crit, int(done.value)
+
+
+def jd_diag(A, B, U0, Vt0, sweeps=10, normalize=False, workspace=None):
+    """JD-Diag by alternating least squares (cts_jd_diag).  Returns
+    (U [d_out][r], Vt [r][d_in], sigma [n][r])."""
+    dev = A.device
+    r = U0.shape[1]
+    p, n, r_l, d_in, d_out = _problem(A, B, r)
+    U = torch.empty((d_out, r), dtype=F32, device=dev)
+    Vt = torch.empty((r, d_in), dtype=F32, device=dev)
+    sig = torch.empty((n, r), dtype=F32, device=dev)
+    ws = _workspace(dev, workspace_size(A, B, r), workspace)
+    _check(lib().cts_jd_diag(ctypes.byref(p), _dev(A, "A", dev, F32, (n, r_l, d_in)),
+                             _dev(B, "B", dev, F32, (n, d_out, r_l)), _dev(U0, "U0", dev, F32, (d_out, r)),
+                             _dev(Vt0, "Vt0", dev, F32, (r, d_in)), int(sweeps), int(bool(normalize)),
+                             _dev(U, "U", dev, F32), _dev(Vt, "Vt", dev, F32), _dev(sig, "sigma", dev, F32),
+                             ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)), "cts_jd_diag")
+    return U, Vt, sig
 
 
 def jd_sigma(A, B, U, Vt, workspace=None):

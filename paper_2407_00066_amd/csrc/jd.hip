@@ -218,6 +218,7 @@ struct PqArgs {
   const int32_t* lidx; int m;
   int r_l, d_in, d_out;
   float* part;                  // [kPqSplit][2][m * r_l][r]
+  int zbase;                    // blockIdx.y + zbase: 0 = P, 1 = Q
 };
 
 template <int NB>
@@ -228,7 +229,7 @@ __global__ __launch_bounds__(kJT) void jd_pq_kernel(const PqArgs a) {
   const int q0 = blockIdx.x * lpw;
   const int nq = min(lpw, a.m - q0);
   if (nq <= 0) return;
-  const bool isq = blockIdx.y == 1;
+  const bool isq = blockIdx.y + a.zbase == 1;
   const int ks = blockIdx.z;
   const int d = isq ? a.d_out : a.d_in;
   const int ntile = (d + kBK - 1) / kBK;
@@ -261,7 +262,10 @@ struct ProjArgs {
   const int32_t* lidx; int m;
   int r_l;
   const float* part;            // from jd_pq_kernel
-  int mode;                     // 0: C, D   1: Sigma   2: score
+  int mode;                     // 0: C, D   1: Sigma   2: score   3: C = P diag(s)
+                                // 4: D = Q diag(s)   5: w = colsum(Q o P)
+  const float* sdiag;           // modes 3, 4: [n][r] diagonals (by id)
+  float* wout;                  // mode 5: [n][r] (by id)
   const float* w2;              // mode 0: per-LoRA weight of C, D (by id), or null
   const float* sscale;          // mode 1: per-LoRA scale of Sigma (by id), or null
   float* C; float* D;           // [m][r_l][r] by list position
@@ -300,6 +304,27 @@ __global__ __launch_bounds__(kJT) void jd_combine_kernel(const ProjArgs a) {
   }
   __syncthreads();
 
+  if (a.mode == 3 || a.mode == 4) {
+    // JD-Diag: C_q = P_q diag(s_q) (mode 3) or D_q = Q_q diag(s_q) (mode 4)
+    const float* X = a.mode == 3 ? Ps : Qs;
+    float* out = a.mode == 3 ? a.C : a.D;
+    for (int e = tid; e < rows * r; e += kJT) {
+      const int row = e / r, j = e - row * r;
+      const int id = a.lidx[q0 + row / r_l];
+      out[(static_cast<int64_t>(q0) * r_l + row) * r + j] = X[row * kEpLd + j] * a.sdiag[static_cast<int64_t>(id) * r + j];
+    }
+    return;
+  }
+  if (a.mode == 5) {
+    // w_q[j] = sum_l Q_q[l][j] P_q[l][j] = (U^T B_q o V^T A_q^T) 1
+    for (int e = tid; e < nq * r; e += kJT) {
+      const int q = e / r, j = e - q * r;
+      float w = 0.f;
+      for (int l = 0; l < r_l; ++l) w = fmaf(Qs[(q * r_l + l) * kEpLd + j], Ps[(q * r_l + l) * kEpLd + j], w);
+      a.wout[static_cast<int64_t>(a.lidx[q0 + q]) * r + j] = w;
+    }
+    return;
+  }
   if (a.mode == 0) {
     // G_q = P_q P_q^T, H_q = Q_q Q_q^T (r_l x r_l per LoRA)
     float* Gs = Qs + kTM * kEpLd;
@@ -382,13 +407,14 @@ struct ExpArgs {
   int r_l, d_in, d_out;
   const float* C; const float* D;
   int split; float* partU; float* partV;
+  int zbase;                    // blockIdx.z + zbase: 0 = U', 1 = V'
 };
 
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
   constexpr int r = 16 * NB;
-  const bool isv = blockIdx.z == 1;
+  const bool isv = blockIdx.z + a.zbase == 1;
   const int d = isv ? a.d_in : a.d_out;
   const int row0 = blockIdx.x * kTM;
   if (row0 >= d) return;
@@ -419,8 +445,9 @@ __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
 
 // X[z][row][j] = sum_s part_z[s][row][j], z = 0 (U, d_out rows), 1 (V, d_in rows)
 __global__ __launch_bounds__(kJT) void jd_reduce_kernel(const float* partU, const float* partV, int S,
-                                                        int d_out, int d_in, int r, float* Uo, float* Vo) {
-  const bool isv = blockIdx.y == 1;
+                                                        int d_out, int d_in, int r, float* Uo, float* Vo,
+                                                        int zbase) {
+  const bool isv = blockIdx.y + zbase == 1;
   const int d = isv ? d_in : d_out;
   const int64_t n = static_cast<int64_t>(d) * r;
   const float* part = isv ? partV : partU;
@@ -489,6 +516,7 @@ __global__ __launch_bounds__(kJT) void jd_gram_kernel(const float* X0, const flo
 
 // One workgroup per z: G = sum_b gp[z][b] (fixed order).  chol = 0: writes G
 // to out[z].  chol = 1: G = R^T R (R upper, positive diagonal), writes R^-1.
+// chol = 2 (G symmetric positive definite): writes G^-1 = R^-1 R^-T.
 // The columns are equilibrated first (G' = D^-1 G D^-1, D = diag(G)^(1/2),
 // R = R' D): the columns of X = M U scale with M's eigenvalues, and without
 // it the fp32 Cholesky of a nearly converged basis breaks down.  A pivot
@@ -654,17 +682,29 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
     __syncthreads();
   }
   // R^-1 = D^-1 R'^-1
-  for (int e = tid; e < rr; e += kJT) dst[e] = inv[(e / r) * ld + e % r] / dsc[e / r];
+  if (chol == 1) {
+    for (int e = tid; e < rr; e += kJT) dst[e] = inv[(e / r) * ld + e % r] / dsc[e / r];
+    return;
+  }
+  for (int e = tid; e < rr; e += kJT) inv[(e / r) * ld + e % r] /= dsc[e / r];
+  __syncthreads();
+  // G^-1[i][c] = sum_{k >= max(i, c)} R^-1[i][k] R^-1[c][k]
+  for (int e = tid; e < rr; e += kJT) {
+    const int i = e / r, c = e - i * r;
+    float sacc = 0.f;
+    for (int k = i > c ? i : c; k < r; ++k) sacc = fmaf(inv[i * ld + k], inv[c * ld + k], sacc);
+    dst[e] = sacc;
+  }
 }
 
 // X_z[row][:] <- X_z[row][:] Rinv_z (64 rows per workgroup, in place: a
 // workgroup reads only its own rows, and all of them before it writes)
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_apply_kernel(float* X0, float* X1, int d0, int d1,
-                                                       const float* rinv) {
+                                                       const float* rinv, int zbase = 0) {
   __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
   constexpr int r = 16 * NB;
-  const int z = blockIdx.y;
+  const int z = blockIdx.y + zbase;
   const int d = z ? d1 : d0;
   float* X = z ? X1 : X0;
   const int row0 = blockIdx.x * kTM;
@@ -918,6 +958,48 @@ __global__ __launch_bounds__(kJT) void km_members_kernel(const int32_t* labels, 
   if (threadIdx.x == 0) offs[K] = base;
 }
 
+// ---------------------------------------------------------- JD-Diag pieces
+// out = X o Y (elementwise), n entries
+__global__ void jd_hadamard_kernel(const float* X, const float* Y, float* out, int n) {
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) out[e] = X[e] * Y[e];
+}
+
+// s_i = Ginv w_i for every LoRA (Ginv symmetric r x r): s[i][j] = sum_k Ginv[j][k] w[i][k]
+__global__ __launch_bounds__(kJT) void jd_diag_solve_kernel(const float* ginv, const float* w, int n, int r,
+                                                            float* s) {
+  const int64_t tot = static_cast<int64_t>(n) * r;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(kJT) + threadIdx.x; e < tot;
+       e += static_cast<int64_t>(gridDim.x) * kJT) {
+    const int64_t i = e / r;
+    const int jj = static_cast<int>(e - i * r);
+    float acc = 0.f;
+    for (int k = 0; k < r; ++k) acc = fmaf(ginv[jj * r + k], w[i * r + k], acc);
+    s[e] = acc;
+  }
+}
+
+// nu[0] = sqrt(sum s^2) (one workgroup, fixed order)
+__global__ __launch_bounds__(kJT) void jd_norm_kernel(const float* s, int64_t n, float* nu) {
+  __shared__ float red[kJT];
+  float acc = 0.f;
+  for (int64_t e = threadIdx.x; e < n; e += kJT) acc = fmaf(s[e], s[e], acc);
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+    for (int k = 0; k < kJT; ++k) t += red[k];
+    nu[0] = sqrtf(t);
+  }
+}
+
+// x[e] *= nu[0]^p (p = -1 or 1/2)
+__global__ void jd_scale_kernel(float* x, int64_t n, const float* nu, int inverse) {
+  const float f = inverse ? 1.f / nu[0] : sqrtf(nu[0]);
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < n;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    x[e] *= f;
+}
+
 // ------------------------------------------------------------------ host side
 // Calls f(std::integral_constant<int, NB>) for the compiled column-block
 // counts NB = r / 16.
@@ -958,11 +1040,13 @@ int validate(const cts_jd_problem* p) {
 
 // Workspace of one JD run (plus the clustering extras when K > 0).
 struct JdPlan {
-  int split, nblk_out, nblk_in, nblk;
+  int split, nblk_out, nblk_in, nblk, nblk_n;
   size_t off_U, off_V, off_Uo, off_Vo, off_C, off_D, off_pq, off_pU, off_pV, off_gp, off_mat, off_rp, off_lidx,
       off_w2, off_w, off_n2, off_crit, total;
   // clustering
   size_t off_S, off_cent, off_dist, off_lab, off_chg, off_offs, off_memb, off_score;
+  // JD-Diag
+  size_t off_sd, off_wv, off_m, off_nu;
 };
 
 size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -978,6 +1062,7 @@ void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   pl->nblk_out = (p->d_out + kGramRows - 1) / kGramRows;
   pl->nblk_in = (p->d_in + kGramRows - 1) / kGramRows;
   pl->nblk = std::max(pl->nblk_out, pl->nblk_in);
+  pl->nblk_n = (p->n + kGramRows - 1) / kGramRows;
   const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
@@ -990,7 +1075,7 @@ void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   pl->off_pq = take(4ull * kPqSplit * 2 * fk * r);
   pl->off_pU = take(4ull * pl->split * p->d_out * r);
   pl->off_pV = take(4ull * pl->split * p->d_in * r);
-  pl->off_gp = take(4ull * 2 * pl->nblk * r * r);
+  pl->off_gp = take(4ull * 2 * std::max(pl->nblk, pl->nblk_n) * r * r);
   pl->off_mat = take(4ull * 2 * r * r);
   pl->off_rp = take(4ull * 2 * nrb * 2);
   pl->off_lidx = take(4ull * n);
@@ -998,6 +1083,10 @@ void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   pl->off_w = take(4ull * n);
   pl->off_n2 = take(4ull * n);
   pl->off_crit = take(4ull * 4);
+  pl->off_sd = take(4ull * n * r);
+  pl->off_wv = take(4ull * n * r);
+  pl->off_m = take(4ull * 8 * r * r);
+  pl->off_nu = take(4ull * 4);
   pl->off_S = pl->off_cent = pl->off_dist = pl->off_lab = pl->off_chg = pl->off_offs = pl->off_memb =
       pl->off_score = 0;
   if (K > 0) {
@@ -1021,18 +1110,21 @@ struct Jd {
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 };
 
+// P = A_i V and/or Q = B_i^T U (zbase, zcount: halves 0 = P, 1 = Q), then
+// the per-LoRA products of `mode` (see jd_combine_kernel).
 hipError_t launch_project(const Jd& j, const float* A, const float* B, const float* V, const float* U,
                           const int32_t* lidx, int m, int mode, const float* w2, const float* sscale,
-                          float* Sigma, float* score, int ld_score, int score_col) {
+                          float* Sigma, float* score, int ld_score, int score_col, int zbase = 0,
+                          int zcount = 2, const float* sdiag = nullptr, float* wout = nullptr) {
   const cts_jd_problem* p = j.p;
   float* part = j.at<float>(j.pl.off_pq);
-  PqArgs pa{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, part};
-  ProjArgs a{lidx, m, p->r_lora, part, mode, w2, sscale, j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D),
-             Sigma, score, ld_score, score_col};
+  PqArgs pa{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, part, zbase};
+  ProjArgs a{lidx, m, p->r_lora, part, mode, sdiag, wout, w2, sscale, j.at<float>(j.pl.off_C),
+             j.at<float>(j.pl.off_D), Sigma, score, ld_score, score_col};
   const int lpw = kTM / p->r_lora;
   const unsigned groups = static_cast<unsigned>((m + lpw - 1) / lpw);
   return with_nb(p->r, [&](auto c) {
-    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, 2, kPqSplit), dim3(kJT), 0, j.st, pa);
+    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, zcount, kPqSplit), dim3(kJT), 0, j.st, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(jd_combine_kernel<decltype(c)::value>, dim3(groups), dim3(kJT), 0, j.st, a);
@@ -1058,7 +1150,7 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
   const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
   ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, j.at<float>(j.pl.off_C),
-             j.at<float>(j.pl.off_D), split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV)};
+             j.at<float>(j.pl.off_D), split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), 0};
   const int rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
   e = with_nb(r, [&](auto c) {
     hipLaunchKernelGGL(jd_expand_kernel<decltype(c)::value>, dim3(rowt, split, 2), dim3(kJT), 0, j.st, ea);
@@ -1068,7 +1160,7 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   const int64_t nmax = static_cast<int64_t>(std::max(p->d_out, p->d_in)) * r;
   hipLaunchKernelGGL(jd_reduce_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nmax + kJT - 1) / kJT)), 2),
                      dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out,
-                     p->d_in, r, Un, Vn);
+                     p->d_in, r, Un, Vn, 0);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // CholeskyQR2 on both
   float* gp = j.at<float>(j.pl.off_gp);
@@ -1171,6 +1263,143 @@ int run_jd(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, co
   return CTS_OK;
 }
 
+// ---- JD-Diag by alternating least squares (App. A.1 case 2)
+// out2[0] = X0^T X0 (d0 rows), out2[1] = X1^T X1 (d1 rows)
+hipError_t two_grams(Jd& j, const float* X0, int d0, const float* X1, int d1, float* out2) {
+  const int r = j.p->r;
+  const int nb = (std::max(d0, d1) + kGramRows - 1) / kGramRows;
+  float* gp = j.at<float>(j.pl.off_gp);
+  return with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_gram_kernel<decltype(c)::value>, dim3(nb, 2, (r + kTM - 1) / kTM), dim3(kJT), 0, j.st,
+                       X0, X1, nullptr, nullptr, d0, d1, nb, gp);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, nb, 0, out2);
+    return hipGetLastError();
+  });
+}
+
+// out = (X o Y)^-1 for symmetric positive definite X o Y (r x r)
+hipError_t hadamard_inverse(Jd& j, const float* X, const float* Y, float* tmp, float* out) {
+  const int r = j.p->r;
+  hipLaunchKernelGGL(jd_hadamard_kernel, dim3((r * r + 255) / 256), dim3(256), 0, j.st, X, Y, tmp, r * r);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(1), dim3(kJT), 0, j.st, tmp, 1, 2, out);
+    return hipGetLastError();
+  });
+}
+
+// X (d rows, z-th basis slot of the apply kernel) <- X M
+hipError_t apply_one(Jd& j, float* X, int d, int z, const float* M2) {
+  const int r = j.p->r;
+  return with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_apply_kernel<decltype(c)::value>, dim3((d + kTM - 1) / kTM, 1), dim3(kJT), 0, j.st,
+                       z == 0 ? X : nullptr, z == 1 ? X : nullptr, d, d, M2, z);
+    return hipGetLastError();
+  });
+}
+
+// one half of the expansion (z = 0: U' = sum B_i C_i into Uo; 1: V' = sum A_i^T D_i into Vo)
+hipError_t expand_one(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, int z, float* out) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
+  const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
+  ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D),
+             split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), z};
+  const int d = z ? p->d_in : p->d_out;
+  hipError_t e = with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_expand_kernel<decltype(c)::value>, dim3((d + kTM - 1) / kTM, split, 1), dim3(kJT), 0, j.st,
+                       ea);
+    return hipGetLastError();
+  });
+  if (e != hipSuccess) return e;
+  const int64_t nel = static_cast<int64_t>(d) * r;
+  hipLaunchKernelGGL(jd_reduce_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nel + kJT - 1) / kJT)), 1),
+                     dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out, p->d_in,
+                     r, z ? nullptr : out, z ? out : nullptr, z);
+  return hipGetLastError();
+}
+
+// diagonals from the current pair: s_i = (U^T U o V^T V)^-1 (U^T B_i o V^T A_i^T) 1;
+// P and Q must be current in the partial buffers unless `fresh` (then both
+// are recomputed)
+hipError_t als_sigma(Jd& j, const float* A, const float* B, const int32_t* lidx, bool fresh) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  float* U = j.at<float>(j.pl.off_U);
+  float* V = j.at<float>(j.pl.off_V);
+  float* sd = j.at<float>(j.pl.off_sd);
+  float* w = j.at<float>(j.pl.off_wv);
+  float* m = j.at<float>(j.pl.off_m);            // [0..1]: grams, [2]: tmp, [3]: inverse
+  hipError_t e = launch_project(j, A, B, V, U, lidx, p->n, 5, nullptr, nullptr, nullptr, nullptr, 0, 0,
+                                fresh ? 0 : 0, fresh ? 2 : 1, nullptr, w);
+  if (e != hipSuccess) return e;
+  if ((e = two_grams(j, U, p->d_out, V, p->d_in, m)) != hipSuccess) return e;
+  const int64_t rr = static_cast<int64_t>(r) * r;
+  if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 3 * rr)) != hipSuccess) return e;
+  const int64_t tot = static_cast<int64_t>(p->n) * r;
+  hipLaunchKernelGGL(jd_diag_solve_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (tot + kJT - 1) / kJT))),
+                     dim3(kJT), 0, j.st, m + 3 * rr, w, p->n, r, sd);
+  return hipGetLastError();
+}
+
+// one sweep: U, then V (with the new U), then the diagonals, then the
+// optional normalization
+hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx, bool normalize) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  const int64_t rr = static_cast<int64_t>(r) * r;
+  float* sd = j.at<float>(j.pl.off_sd);
+  float* m = j.at<float>(j.pl.off_m);
+  hipError_t e;
+  // U = (sum_i B_i A_i V S_i)(V^T V o S2)^-1, S2 = sum_i s_i s_i^T
+  {
+    float* U = j.at<float>(j.pl.off_U);
+    float* V = j.at<float>(j.pl.off_V);
+    float* Un = j.at<float>(j.pl.off_Uo);
+    if ((e = launch_project(j, A, B, V, U, lidx, p->n, 3, nullptr, nullptr, nullptr, nullptr, 0, 0, 0, 1, sd,
+                            nullptr)) != hipSuccess)
+      return e;
+    if ((e = expand_one(j, A, B, lidx, p->n, 0, Un)) != hipSuccess) return e;
+    if ((e = two_grams(j, V, p->d_in, sd, p->n, m)) != hipSuccess) return e;
+    if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 4 * rr)) != hipSuccess) return e;
+    if ((e = apply_one(j, Un, p->d_out, 0, m + 4 * rr)) != hipSuccess) return e;
+    std::swap(j.pl.off_U, j.pl.off_Uo);
+  }
+  // V = (sum_i A_i^T B_i^T U S_i)(U^T U o S2)^-1
+  {
+    float* U = j.at<float>(j.pl.off_U);
+    float* V = j.at<float>(j.pl.off_V);
+    float* Vn = j.at<float>(j.pl.off_Vo);
+    if ((e = launch_project(j, A, B, V, U, lidx, p->n, 4, nullptr, nullptr, nullptr, nullptr, 0, 0, 1, 1, sd,
+                            nullptr)) != hipSuccess)
+      return e;
+    if ((e = expand_one(j, A, B, lidx, p->n, 1, Vn)) != hipSuccess) return e;
+    if ((e = two_grams(j, U, p->d_out, sd, p->n, m)) != hipSuccess) return e;
+    if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 5 * rr)) != hipSuccess) return e;
+    if ((e = apply_one(j, Vn, p->d_in, 1, m + 4 * rr)) != hipSuccess) return e;   // slot 1 = m + 5 rr
+    std::swap(j.pl.off_V, j.pl.off_Vo);
+  }
+  // diagonals: Q = B^T U is current from the V step; P = A V is recomputed
+  if ((e = als_sigma(j, A, B, lidx, false)) != hipSuccess) return e;
+  if (normalize) {
+    float* nu = j.at<float>(j.pl.off_nu);
+    const int64_t ns = static_cast<int64_t>(p->n) * r;
+    hipLaunchKernelGGL(jd_norm_kernel, dim3(1), dim3(kJT), 0, j.st, sd, ns, nu);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(jd_scale_kernel, dim3(256), dim3(256), 0, j.st, sd, ns, nu, 1);
+    hipLaunchKernelGGL(jd_scale_kernel, dim3(256), dim3(256), 0, j.st, j.at<float>(j.pl.off_U),
+                       static_cast<int64_t>(p->d_out) * r, nu, 0);
+    hipLaunchKernelGGL(jd_scale_kernel, dim3(256), dim3(256), 0, j.st, j.at<float>(j.pl.off_V),
+                       static_cast<int64_t>(p->d_in) * r, nu, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace
 }  // namespace cts
 
@@ -1231,6 +1460,31 @@ int cts_jd_full(const cts_jd_problem* p, const float* A, const float* B, const f
     return CTS_ERR_HIP;
   if (cts::store_bases(j, U, Vt) != hipSuccess) return CTS_ERR_HIP;
   if (iters_done) *iters_done = done;
+  return CTS_OK;
+}
+
+int cts_jd_diag(const cts_jd_problem* p, const float* A, const float* B, const float* U0, const float* Vt0,
+                int32_t sweeps, int32_t normalize, float* U, float* Vt, float* sigma, void* workspace,
+                size_t workspace_bytes, void* stream) {
+  int st = cts::validate(p);
+  if (st != CTS_OK) return st;
+  if (sweeps < 0 || cts::bad_ptr(A, 16) || cts::bad_ptr(B, 16) || cts::bad_ptr(U0, 16) || cts::bad_ptr(Vt0, 16) ||
+      cts::bad_ptr(U, 16) || cts::bad_ptr(Vt, 16) || cts::bad_ptr(sigma, 16) || cts::bad_ptr(workspace, 16))
+    return CTS_ERR_INVALID_ARG;
+  Jd j{p, {}, static_cast<char*>(workspace), static_cast<hipStream_t>(stream)};
+  cts::plan_jd(p, 0, &j.pl);
+  if (workspace_bytes < j.pl.total) return CTS_ERR_WORKSPACE;
+  int32_t* lidx = j.at<int32_t>(j.pl.off_lidx);
+  hipLaunchKernelGGL(cts::jd_iota_kernel, dim3((p->n + 255) / 256), dim3(256), 0, j.st, lidx, p->n);
+  if (hipGetLastError() != hipSuccess) return CTS_ERR_HIP;
+  if (cts::load_bases(j, U0, Vt0) != hipSuccess) return CTS_ERR_HIP;
+  if (cts::als_sigma(j, A, B, lidx, true) != hipSuccess) return CTS_ERR_HIP;
+  for (int t = 0; t < sweeps; ++t)
+    if (cts::als_sweep(j, A, B, lidx, normalize != 0) != hipSuccess) return CTS_ERR_HIP;
+  if (cts::store_bases(j, U, Vt) != hipSuccess) return CTS_ERR_HIP;
+  if (hipMemcpyAsync(sigma, j.at<float>(j.pl.off_sd), sizeof(float) * p->n * p->r, hipMemcpyDeviceToDevice,
+                     j.st) != hipSuccess)
+    return CTS_ERR_HIP;
   return CTS_OK;
 }
 

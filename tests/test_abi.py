@@ -273,6 +273,8 @@ def test_jd_rejects_bad_problem(kw, code):
                        ctypes.byref(done), FAKE, 1 << 30, None)
     assert rc == code
     assert L.cts_jd_sigma(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == code
+    assert L.cts_jd_diag(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 3, 0, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                         None) == code
     assert L.cts_lora_norms2(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == code
 
 
@@ -331,3 +333,22 @@ def test_jd_cluster_argument_errors():
     for name in ("A", "B", "U0", "Vt0", "Uc0", "Vtc0", "cof", "U", "Vt", "S", "W"):
         assert call(**{name: None}) == B.CTS_ERR_INVALID_ARG, name
     assert call(ws=need - 1) == B.CTS_ERR_WORKSPACE
+
+
+def test_jd_diag_argument_errors():
+    p = _jp()
+    L = cts.lib()
+    need = L.cts_jd_workspace_size(ctypes.byref(p))
+    args = [FAKE, FAKE, FAKE, FAKE, 3, 0, FAKE, FAKE, FAKE, FAKE, need, None]
+    for i in (0, 1, 2, 3, 6, 7, 8, 9):
+        a = list(args)
+        a[i] = None
+        assert L.cts_jd_diag(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG, i
+        a[i] = ctypes.c_void_p(0x10004)
+        assert L.cts_jd_diag(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG, i
+    a = list(args)
+    a[4] = -1
+    assert L.cts_jd_diag(ctypes.byref(p), *a) == B.CTS_ERR_INVALID_ARG
+    a = list(args)
+    a[10] = need - 1
+    assert L.cts_jd_diag(ctypes.byref(p), *a) == B.CTS_ERR_WORKSPACE

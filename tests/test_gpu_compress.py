@@ -255,3 +255,60 @@ def test_jd_cluster_rounds_and_small_clusters():
     recon = np.stack([Ug[lab[i]] @ Sg[i] @ Vg[lab[i]].T for i in range(len(A))])
     want = np.stack([Us[lab[i]] @ So[i] @ Vs[lab[i]].T for i in range(len(A))])
     assert _rel(recon, want) < 1e-3
+
+
+# ---------------------------------------------------------------- JD-Diag ALS
+DIAG_CASES = {
+    # name: seed, n, d_out, d_in, r_l, r, sweeps, normalize
+    "diag_r16": (51, 12, 96, 80, 4, 16, 4, False),
+    "diag_r32_norm": (52, 20, 132, 100, 8, 32, 3, True),
+    "diag_r64_rank16": (53, 10, 160, 144, 16, 64, 2, False),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DIAG_CASES))
+def test_jd_diag_matches_oracle(name):
+    seed, n, d_out, d_in, r_l, r, sweeps, normalize = DIAG_CASES[name]
+    A, B, rs = _loras(seed, n, d_out, d_in, r_l)
+    U0 = _f32(rs.standard_normal((d_out, r)) / np.sqrt(d_out))
+    V0 = _f32(rs.standard_normal((d_in, r)) / np.sqrt(d_in))
+    say("jd_diag %s" % name)
+    U, Vt, sig = GC.jd_diag(dev(A), dev(B), dev(U0), dev(V0.T), sweeps=sweeps, normalize=normalize)
+    torch.cuda.synchronize()
+    Uo, Vo, so, _ = OC.jd_diag_als(A, B, r, U0, V0, sweeps=sweeps, normalize=normalize)
+    Ug, Vg, sg = host(U), host(Vt).T, host(sig)
+    assert _rel(Ug, Uo) < 1e-3 and _rel(Vg, Vo) < 1e-3 and _rel(sg, so) < 1e-3
+    rec = np.stack([Ug @ np.diag(sg[i]) @ Vg.T for i in range(n)])
+    reco = np.stack([Uo @ np.diag(so[i]) @ Vo.T for i in range(n)])
+    assert _rel(rec, reco) < 1e-3
+    if normalize:
+        assert abs((sg ** 2).sum() - 1.0) < 1e-4
+
+
+def test_jd_diag_zero_sweeps_is_closed_form():
+    n, d_out, d_in, r_l, r = 9, 84, 76, 4, 16
+    A, B, rs = _loras(54, n, d_out, d_in, r_l)
+    U0 = _f32(rs.standard_normal((d_out, r)) / np.sqrt(d_out))
+    V0 = _f32(rs.standard_normal((d_in, r)) / np.sqrt(d_in))
+    U, Vt, sig = GC.jd_diag(dev(A), dev(B), dev(U0), dev(V0.T), sweeps=0)
+    assert _rel(host(sig), OC.diag_sigma(U0, V0, A, B)) < 1e-4
+    assert np.array_equal(host(U), U0) and np.array_equal(host(Vt).T, V0)
+
+
+def test_jd_diag_recovers_diagonalizable_collection():
+    # B_i A_i = U* diag(sigma_i) V*^T with shared U*, V* (r = 16): ALS from a
+    # perturbed start reaches the collection (relative error << 1)
+    n, d_out, d_in, r = 24, 96, 80, 16
+    rs = np.random.default_rng(55)
+    Us, Vs = rs.standard_normal((d_out, r)) / np.sqrt(d_out), rs.standard_normal((d_in, r)) / np.sqrt(d_in)
+    S = rs.standard_normal((n, r))
+    A = _f32(np.stack([np.diag(S[i]) @ Vs.T for i in range(n)]))          # r_l = r = 16
+    B = _f32(np.stack([Us for _ in range(n)]))
+    U0 = _f32(Us + 0.3 * rs.standard_normal(Us.shape) / np.sqrt(d_out))
+    V0 = _f32(Vs + 0.3 * rs.standard_normal(Vs.shape) / np.sqrt(d_in))
+    U, Vt, sig = GC.jd_diag(dev(A), dev(B), dev(U0), dev(V0.T), sweeps=30)
+    Ug, Vg, sg = host(U), host(Vt).T, host(sig)
+    err = OC.objective(Ug, Vg, sg, A, B) / sum(np.linalg.norm(P) ** 2 for P in OC.products(A, B))
+    Uo, Vo, so, _ = OC.jd_diag_als(A, B, r, U0, V0, sweeps=30)
+    err_o = OC.recon_error(Uo, Vo, so, A, B)
+    assert err_o < 1e-4 and err < 1e-4
