@@ -254,10 +254,23 @@ def jd_kernel_models(n, d_out, d_in, r_l, r, split):
     return (proj_f, proj_b), (exp_f, exp_b)
 
 
+def jd_diag_kernel_models(n, d_out, d_in, r_l, r, split):
+    """Flops and bytes of the JD-Diag sweep's U-step stages: projection of
+    one half (P_i = A_i V, C_i = P_i S_i: reads A and V, writes C) and the
+    expansion of one half (U' = sum_i B_i C_i: reads B and C, writes the
+    split partials)."""
+    rows = n * r_l
+    proj = (2.0 * rows * r * d_in + rows * r, 4.0 * (rows * d_in + r * d_in + rows * r))
+    expd = (2.0 * rows * r * d_out, 4.0 * (rows * d_out + rows * r + split * r * d_out))
+    return proj, expd
+
+
 def bench_jd(args, torch, np, cts, B, device):
     """One step = one iteration of the App. A.2 eigenvalue iteration over the
     whole collection (1000 rank-16 LoRAs of a 4096 x 4096 projection, r = 64);
-    a timed call runs the paper's 10 iterations (no early stop)."""
+    a timed call runs the paper's 10 iterations (no early stop).  With
+    --workload jd_diag a step is one sweep of the JD-Diag alternating least
+    squares (App. A.1 case 2) from random bases, 10 sweeps per call."""
     from paper_2407_00066_amd import compress as GC
     n, d, r_l, r, iters = JD_N, JD_D, JD_RL, JD_R, JD_ITERS
     log("generating %d LoRAs of rank %d, %d x %d" % (n, r_l, d, d))
@@ -270,10 +283,18 @@ def bench_jd(args, torch, np, cts, B, device):
     gU0, gVt0 = to_dev(U0, device), to_dev(np.ascontiguousarray(V0.T), device)
     ws = torch.empty(GC.workspace_size(gA, gB, r), dtype=torch.uint8, device=device)
 
+    diag = args.workload == "jd_diag"
+    if diag:
+        gU0 = to_dev((rs.standard_normal((d, r)) / np.sqrt(d)).astype(np.float32), device)
+        gVt0 = to_dev((rs.standard_normal((r, d)) / np.sqrt(d)).astype(np.float32), device)
+
     def call():
+        if diag:
+            return GC.jd_diag(gA, gB, gU0, gVt0, sweeps=iters, workspace=ws)
         return GC.jd_full(gA, gB, gU0, gVt0, iters=iters, workspace=ws)
 
-    log("timing cts_jd_full: %d warmup + %d calls of %d iterations" % (args.warmup, args.steps, iters))
+    log("timing %s: %d warmup + %d calls of %d steps" % ("cts_jd_diag" if diag else "cts_jd_full", args.warmup,
+                                                         args.steps, iters))
     ms_call = time_steps(lambda _: call(), [None], args.steps, args.warmup, torch)
     ms_iter = ms_call / iters
     # the two large kernels of the last iteration of each call, between stage
@@ -293,31 +314,72 @@ def bench_jd(args, torch, np, cts, B, device):
     rowt = (d + 63) // 64
     ntile = (n * r_l + 31) // 32
     split = max(1, min((512 + rowt - 1) // rowt, ntile // 8))
-    (pf, pb), (ef, eb_) = jd_kernel_models(n, d, d, r_l, r, split)
-    if exp_us >= proj_us:
-        name, fl, nb, us = "jd_expand_kernel (U' = sum B_i C_i, V' = sum A_i^T D_i)", ef, eb_, exp_us
+    if diag:
+        (pf, pb), (ef, eb_) = jd_diag_kernel_models(n, d, d, r_l, r, split)
+        if exp_us >= proj_us:
+            name, fl, nb, us = "jd_expand_kernel, U step (U' = sum B_i C_i)", ef, eb_, exp_us
+        else:
+            name, fl, nb, us = ("projection, U step: jd_pq_kernel + jd_combine_kernel (A_i V, C_i = P_i S_i)",
+                                pf, pb, proj_us)
     else:
-        name, fl, nb, us = ("projection: jd_pq_kernel + jd_combine_kernel (A_i V, B_i^T U, per-LoRA "
-                            "products)", pf, pb, proj_us)
+        (pf, pb), (ef, eb_) = jd_kernel_models(n, d, d, r_l, r, split)
+        if exp_us >= proj_us:
+            name, fl, nb, us = "jd_expand_kernel (U' = sum B_i C_i, V' = sum A_i^T D_i)", ef, eb_, exp_us
+        else:
+            name, fl, nb, us = ("projection: jd_pq_kernel + jd_combine_kernel (A_i V, B_i^T U, per-LoRA "
+                                "products)", pf, pb, proj_us)
     roof = roofline_of(fl, nb, us * 1e-6, "f32")
     roof.update({"kernel": name, "mean_us": round(us, 2), "marker_us": round(mk, 2),
                  "algorithmic_flops": fl, "algorithmic_bytes": nb,
                  "project_us": round(proj_us, 2), "expand_us": round(exp_us, 2)})
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not diag:
         cpu = jd_cpu_baseline(A, Bm, U0, V0, args.cpu_seconds)
+    if diag:
+        cpu = None if args.no_cpu_baseline else jd_diag_cpu_baseline(A, Bm, host_of(gU0), host_of(gVt0).T,
+                                                                       args.cpu_seconds)
     return {
-        "metric": "LoRA-iterations/s of the JD-Full eigenvalue iteration (1000 rank-16 LoRAs, "
-                  "4096 x 4096, r = 64), one MI355X",
-        "value": round(n * iters / (ms_call * 1e-3), 1), "unit": "LoRA-iterations/s",
+        "metric": ("LoRA-sweeps/s of the JD-Diag alternating least squares" if diag else
+                   "LoRA-iterations/s of the JD-Full eigenvalue iteration") +
+                  " (1000 rank-16 LoRAs, 4096 x 4096, r = 64), one MI355X",
+        "value": round(n * iters / (ms_call * 1e-3), 1), "unit": "LoRA-sweeps/s" if diag else "LoRA-iterations/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_iter, 5), "ms_per_compression": round(ms_call, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic (seeded Gaussian LoRAs, random orthonormal initial bases)",
-        "config": {"workload": "jd_full", "n_loras": n, "d_out": d, "d_in": d, "r_lora": r_l, "r": r,
-                   "iterations": iters, "parallelism": "single GPU"},
+        "data": "synthetic (seeded Gaussian LoRAs; random %s initial bases)" % ("Gaussian" if diag else "orthonormal"),
+        "config": {"workload": args.workload, "n_loras": n, "d_out": d, "d_in": d, "r_lora": r_l, "r": r,
+                   ("sweeps" if diag else "iterations"): iters, "parallelism": "single GPU"},
         "roofline": roof, "cpu_baseline": cpu,
     }
+
+
+def host_of(t):
+    return t.detach().cpu().numpy().astype("float64")
+
+
+def jd_diag_cpu_baseline(A, Bm, U0, V0, target_s):
+    """The oracle's JD-Diag sweep (fp64) on the first LoRAs of the collection,
+    grown until about target_s / 4 seconds or 32 LoRAs (it forms every
+    d_out x d_in update B_i A_i, 134 MB each here); LoRA-sweeps/s."""
+    import numpy as np
+    from oracle import compress as OC
+    m = 4
+    while True:
+        a, b = A[:m].astype(np.float64), Bm[:m].astype(np.float64)
+        t0 = time.perf_counter()
+        OC.jd_diag_als(a, b, U0.shape[1], U0, V0, sweeps=1)
+        dt = time.perf_counter() - t0
+        if dt >= target_s / 4 or m >= min(32, A.shape[0]):
+            break
+        m = min(32, A.shape[0], int(m * max(2.0, target_s / 4 / max(dt, 1e-3))))
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info() if t.get("user_api") == "blas"] or [1])
+    except ImportError:
+        cores = os.cpu_count()
+    return {"value": m / dt, "unit": "LoRA-sweeps/s", "cores": cores, "kind": "oracle",
+            "sample": "one fp64 JD-Diag sweep (plus its initial diagonals) over the first %d of %d LoRAs, %.1f s"
+                      % (m, A.shape[0], dt)}
 
 
 def jd_cpu_baseline(A, Bm, U0, V0, target_s):
@@ -616,7 +678,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="prefill_mix",
-                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32", "jd_full"])
+                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32", "jd_full", "jd_diag"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sigma", default="full", choices=["full", "diag"],
@@ -631,7 +693,7 @@ def main():
     if args.sigma == "diag" and args.ranks == "mixed":
         print("--sigma diag and --ranks mixed are separate variants", file=sys.stderr)
         sys.exit(2)
-    if args.workload in ("stack32", "jd_full") and (args.sigma != "full" or args.ranks != "uniform"):
+    if args.workload in ("stack32", "jd_full", "jd_diag") and (args.sigma != "full" or args.ranks != "uniform"):
         print("--sigma diag and --ranks mixed apply to the single-layer workloads", file=sys.stderr)
         sys.exit(2)
 
@@ -651,7 +713,7 @@ def main():
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     copy_calibration(torch, device)
-    if args.workload == "jd_full":
+    if args.workload in ("jd_full", "jd_diag"):
         rec = bench_jd(args, torch, np, cts, B, device)
     elif args.workload == "stack32":
         rec = bench_stack(args, torch, np, cts, B, wl, device)

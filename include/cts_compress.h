@@ -29,7 +29,9 @@
  * every iteration of the JD records [1] before and [2] after its projection
  * kernels (P_i = A_i V, Q_i = B_i^T U, then the per-LoRA products) and [3]
  * after its expansion kernel (the sums over the collection); the last
- * iteration's records are the ones left.
+ * iteration's records are the ones left.  cts_jd_diag records the same
+ * three events around its U step's projection (P_i = A_i V, C_i = P_i S_i)
+ * and expansion (sum_i B_i C_i).
  */
 #ifndef CTS_COMPRESS_H
 #define CTS_COMPRESS_H

@@ -1360,10 +1360,13 @@ hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx,
     float* U = j.at<float>(j.pl.off_U);
     float* V = j.at<float>(j.pl.off_V);
     float* Un = j.at<float>(j.pl.off_Uo);
+    if ((e = stage_mark(1, j.st)) != hipSuccess) return e;
     if ((e = launch_project(j, A, B, V, U, lidx, p->n, 3, nullptr, nullptr, nullptr, nullptr, 0, 0, 0, 1, sd,
                             nullptr)) != hipSuccess)
       return e;
+    if ((e = stage_mark(2, j.st)) != hipSuccess) return e;
     if ((e = expand_one(j, A, B, lidx, p->n, 0, Un)) != hipSuccess) return e;
+    if ((e = stage_mark(3, j.st)) != hipSuccess) return e;
     if ((e = two_grams(j, V, p->d_in, sd, p->n, m)) != hipSuccess) return e;
     if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 4 * rr)) != hipSuccess) return e;
     if ((e = apply_one(j, Un, p->d_out, 0, m + 4 * rr)) != hipSuccess) return e;
