@@ -161,6 +161,28 @@ int cts_apply_uncompressed_ranked(const cts_problem* p, const void* x, const int
                                   const int32_t* rank_of_adapter, void* y,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
+/* Multi-module batching: M projections of one layer that read the same x
+ * (q, k and v, or gate and up) with the same LoRA per token and the same
+ * cluster map.  Module m has its own W_m [d_out[m]][d_in], U_m
+ * [K][d_out[m]][r] and Sigma_m [n][r][r]; the V_k^T of the modules come
+ * stacked along r in one array Vt [K][M r][d_in] (rows m r .. m r + r - 1 of
+ * cluster k are module m's V_k^T).  Then for every module
+ *     y_m[t] = W_m x_t + U_k^(m) Sigma_i^(m) V_k^(m)T x_t
+ * exactly as cts_apply with that module's arrays (Sec. 3.1, 3.2).  The
+ * bucketing and the shrink run once for all modules (one GEMM over the M r
+ * stacked rows, x read once), the core product and the fused GEMM once per
+ * module.  d_out is a host array of M sizes; W, U, Sigma and y are host
+ * arrays of M device pointers.  p->d_out is ignored; every other field of p
+ * applies to all modules, and the limits of cts_apply hold per module, with
+ * 1 <= M <= CTS_MAX_MODULES.  Outputs must not overlap each other, an input
+ * or the workspace (cts_workspace_size_multi bytes). */
+#define CTS_MAX_MODULES 8
+size_t cts_workspace_size_multi(const cts_problem* p, int32_t M, const int32_t* d_out);
+int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
+                    const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
+                    const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
 /* Synchronous id check for tests and debugging: copies the ids to the host
  * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is
  * outside [0, n) or any cluster_of outside [0, K) (cluster_of may be NULL). */

@@ -175,6 +175,17 @@ def apply_diag(x, adapter_id, cluster_of, W, U, Vt, sigma, tokens=None, timing=N
     return y[:len(tok)]
 
 
+def apply_multi(x, adapter_id, cluster_of, Ws, Us, Vt, Sigmas, tokens=None):
+    """Several modules of one layer on the same x, ids and cluster map (Sec.
+    3.1, 3.2 applied to each projection): module m is the layer with W_m, U_m,
+    Sigma_m and the rows m r .. m r + r - 1 of the stacked Vt [K][M r][d_in].
+    Returns the list of y_m."""
+    r = np.asarray(Us[0]).shape[2]
+    Vt = np.asarray(Vt)
+    return [apply(x, adapter_id, cluster_of, Ws[m], Us[m], np.ascontiguousarray(Vt[:, m * r:(m + 1) * r, :]),
+                  Sigmas[m], tokens=tokens) for m in range(len(Ws))]
+
+
 def apply_ranked(x, adapter_id, cluster_of, W, U, Vt, Sigma, rank_of_cluster, tokens=None, timing=None):
     """Mixed ranks (Sec. 3.2: each cluster its own rank): y[s] = (W + U_k[:, :r_k]
     Sigma_i[:r_k, :r_k] V_k^T[:r_k, :]) x_t with r_k = rank_of_cluster[k]; U,

@@ -24,7 +24,7 @@ CTS_F32, CTS_BF16 = 0, 1
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
-            "cts_set_stage_events",
+            "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
             "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
@@ -83,6 +83,12 @@ def lib() -> ctypes.CDLL:
                 L.cts_validate_ids.restype = ctypes.c_int
                 L.cts_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
                 L.cts_set_stage_events.restype = ctypes.c_int
+                i32p = ctypes.POINTER(i32)
+                vpp = ctypes.POINTER(ctypes.c_void_p)
+                L.cts_workspace_size_multi.argtypes = [pp, i32, i32p]
+                L.cts_workspace_size_multi.restype = sz
+                L.cts_apply_multi.argtypes = [pp, i32, i32p, vp, vp, vp, vpp, vpp, vp, vpp, vpp, vp, sz, vp]
+                L.cts_apply_multi.restype = ctypes.c_int
                 jp, fl = ctypes.POINTER(JdProblem), ctypes.c_float
                 L.cts_jd_workspace_size.argtypes = [jp]
                 L.cts_jd_workspace_size.restype = sz
@@ -325,6 +331,46 @@ def apply_uncompressed(x, adapter_id, W, A, B, out=None, out_dtype=None, workspa
     _check(lib().cts_apply_uncompressed(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()),
                                         ws.numel(), _stream(dev)), "cts_apply_uncompressed")
     return out
+
+
+def workspace_size_multi(p: Problem, d_out) -> int:
+    arr = (ctypes.c_int32 * len(d_out))(*[int(v) for v in d_out])
+    return int(lib().cts_workspace_size_multi(ctypes.byref(p), len(d_out), arr))
+
+
+def apply_multi(x, adapter_id, cluster_of, Ws, Us, Vt, Sigmas, outs=None, out_dtype=None, workspace=None):
+    """Several modules sharing x, the adapter ids and the cluster map
+    (cts_apply_multi): Ws, Us, Sigmas are sequences of the modules' W_m,
+    U_m, Sigma_m; Vt [K][M r][d_in] stacks their V_k^T along r.  Returns the
+    list of outputs y_m [T][d_out_m]."""
+    dev = x.device
+    T, d_in = x.shape
+    M = len(Ws)
+    if not (len(Us) == len(Sigmas) == M):
+        raise ValueError("Ws, Us and Sigmas must have one entry per module")
+    K, _, r = Us[0].shape
+    n = Sigmas[0].shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    d_out = [int(w.shape[0]) for w in Ws]
+    if outs is None:
+        outs = [torch.empty((T, dm), dtype=odt, device=dev) for dm in d_out]
+    p = make_problem(T, d_in, 8, r=r, n_adapters=n, n_clusters=K, dtype=dt, out_dtype=_dt(outs[0], "out"))
+    vp = ctypes.c_void_p
+    Wp = (vp * M)(*[_dev(w, "W[%d]" % m, dev, tdt, (d_out[m], d_in)) for m, w in enumerate(Ws)])
+    Up = (vp * M)(*[_dev(u, "U[%d]" % m, dev, tdt, (K, d_out[m], r)) for m, u in enumerate(Us)])
+    Sp = (vp * M)(*[_dev(sg, "Sigma[%d]" % m, dev, tdt, (n, r, r)) for m, sg in enumerate(Sigmas)])
+    Yp = (vp * M)(*[_dev(y, "out[%d]" % m, dev, None, (T, d_out[m])) for m, y in enumerate(outs)])
+    dims = (ctypes.c_int32 * M)(*d_out)
+    nbytes = workspace_size_multi(p, d_out)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_multi(ctypes.byref(p), M, dims, _dev(x, "x", dev, tdt, (T, d_in)),
+                                 _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+                                 _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)), Wp, Up,
+                                 _dev(Vt, "Vt", dev, tdt, (K, M * r, d_in)), Sp, Yp,
+                                 ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)), "cts_apply_multi")
+    return outs
 
 
 def validate_ids(adapter_id, cluster_of, n: int, K: int = 1) -> bool:

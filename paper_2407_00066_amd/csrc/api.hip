@@ -12,6 +12,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <vector>
 
 #include "cts.h"
 #include "cts_internal.h"
@@ -364,6 +365,187 @@ int cts_apply_ranked(const cts_problem* p, const void* x, const int32_t* adapter
                      size_t workspace_bytes, void* stream) {
   return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
                           workspace_bytes, stream, false, rank_of_cluster, true);
+}
+
+namespace {
+
+// ---- several modules sharing x, the adapter ids and the cluster map
+struct MultiPlan {
+  Plan mod[CTS_MAX_MODULES];   // per-module plans (fused GEMM tile and split)
+  int M, rtot, shrink_split;
+  size_t off_zpart, off_zp, off_ypart, total;
+};
+
+int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan* mp) {
+  if (!p || M < 1 || !d_out) return CTS_ERR_INVALID_ARG;
+  if (M > CTS_MAX_MODULES) return CTS_ERR_UNSUPPORTED;
+  mp->M = M;
+  for (int m = 0; m < M; ++m) {
+    cts_problem q = *p;
+    q.d_out = d_out[m];
+    const int rc = make_plan(&q, true, &mp->mod[m]);
+    if (rc != CTS_OK) return rc;
+  }
+  const Plan& p0 = mp->mod[0];
+  const int T = p->T;
+  mp->rtot = M * p->r;
+  if (static_cast<uint64_t>(mp->rtot) * p->d_in * p0.elt > kMaxOperandBytes) return CTS_ERR_UNSUPPORTED;
+  // shrink over the stacked rank: as for one module, with M r rank rows
+  int BM, BN, BK;
+  cts::tile_dims(p0.shrink_tile, &BM, &BN, &BK);
+  {
+    const int expect = ceil_div(std::max(T, 1), BN) + std::min(p0.nseg, std::max(T, 1)) / 2;
+    const int tiles = ceil_div(mp->rtot, BM) * std::max(expect, 1);
+    const int nk = ceil_div(p->d_in, BK);
+    const int target = (p->dtype == CTS_F32) ? 512 : 256;
+    mp->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 64));
+  }
+  size_t off = p0.off_zpart;                        // the shared sort arrays of module 0's layout
+  mp->off_zpart = off; off = align_up(off + 4ull * mp->shrink_split * T * mp->rtot);
+  mp->off_zp = off;    off = align_up(off + static_cast<size_t>(p0.elt) * T * mp->rtot);
+  mp->off_ypart = off;
+  size_t yp = 0;
+  for (int m = 0; m < M; ++m)
+    if (mp->mod[m].main_split > 1) yp = std::max<size_t>(yp, 4ull * mp->mod[m].main_split * T * d_out[m]);
+  off = align_up(off + yp);
+  mp->total = off;
+  return CTS_OK;
+}
+
+int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, const void* x,
+              const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
+              const void* const* U, const void* Vt, const void* const* Sigma, void* const* y, void* workspace,
+              hipStream_t stream) {
+  const Plan& pl = mp.mod[0];
+  char* ws = static_cast<char*>(workspace);
+  int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
+  int32_t* sseg = reinterpret_cast<int32_t*>(ws + pl.off_seg);
+  int32_t* said = reinterpret_cast<int32_t*>(ws + pl.off_aid);
+  int32_t* offs = reinterpret_cast<int32_t*>(ws + pl.off_offs);
+  int32_t* items = reinterpret_cast<int32_t*>(ws + pl.off_items);
+  int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
+  int32_t* ctiles = reinterpret_cast<int32_t*>(ws + pl.off_ctiles);
+  int32_t* n_ctiles = reinterpret_cast<int32_t*>(ws + pl.off_nctiles);
+  float* zpart = reinterpret_cast<float*>(ws + mp.off_zpart);
+  char* zp = ws + mp.off_zp;
+  float* ypart = reinterpret_cast<float*>(ws + mp.off_ypart);
+  const int T = p->T, r = p->r, rt = mp.rtot;
+
+  hipError_t e = mark(0, stream);
+  if (e != hipSuccess) return CTS_ERR_HIP;
+  const bool fuse_sort = T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
+  if (!fuse_sort) {
+    e = cts::launch_sort(adapter_id, cluster_of, T, p->n_adapters, pl.nseg, perm, offs, sseg, said, items, n_items,
+                         ctiles, n_ctiles, stream);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+  }
+  if (mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
+
+  // one shrink over the stacked V_k^T of all modules: Z [T][M r]
+  cts::GemmParams g{};
+  g.M = rt; g.N = T;
+  g.A0 = nullptr; g.K0 = 0;
+  g.A1 = Vt; g.seg_stride_a1 = static_cast<int64_t>(rt) * p->d_in; g.lda1 = p->d_in;
+  g.B1 = x; g.ldb1 = p->d_in; g.K1 = p->d_in; g.b1_gather = 1;
+  g.a0_bytes = 0; g.b0_bytes = 0;
+  g.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(rt) * p->d_in * pl.elt);
+  g.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
+  g.perm = perm; g.sorted_seg = sseg;
+  g.ksplit = mp.shrink_split; g.part = zpart;
+  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  if (fuse_sort) {
+    g.tile_start = nullptr; g.n_tiles = nullptr;
+    g.fs_adapter = adapter_id; g.fs_cluster = cluster_of;
+    g.fs_n = p->n_adapters; g.fs_K = pl.nseg;
+    int bits_n = 0;
+    while ((1 << bits_n) < p->n_adapters) ++bits_n;
+    g.fs_bits_n = bits_n;
+    g.fs_perm = perm; g.fs_seg = sseg; g.fs_aid = said; g.fs_items = items; g.fs_nitems = n_items;
+  }
+  e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
+  if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
+
+  // core product per module on its slice of Z (rows M r apart)
+  for (int m = 0; m < mp.M; ++m) {
+    e = cts::launch_sigma(zpart + static_cast<int64_t>(m) * r, mp.shrink_split, T, r, said, p->n_adapters, items,
+                          n_items, pl.max_items, Sigma[m], zp + static_cast<size_t>(m) * r * pl.elt, p->dtype,
+                          stream, false, sseg, nullptr, nullptr, rt);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+  }
+  if (mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
+
+  // fused W_m X + U_k^(m) Z'^(m) per module
+  for (int m = 0; m < mp.M; ++m) {
+    const Plan& pm = mp.mod[m];
+    const int dm = d_out[m];
+    cts::GemmParams f{};
+    f.M = dm; f.N = T;
+    f.A0 = W[m]; f.lda0 = p->d_in; f.B0 = x; f.ldb0 = p->d_in; f.K0 = p->d_in;
+    f.A1 = U[m]; f.seg_stride_a1 = static_cast<int64_t>(dm) * r; f.lda1 = r;
+    f.B1 = zp + static_cast<size_t>(m) * r * pl.elt; f.ldb1 = rt; f.K1 = r; f.b1_gather = 0;
+    f.a0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(dm) * p->d_in * pl.elt);
+    f.b0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
+    f.a1_seg_bytes = static_cast<uint32_t>(static_cast<uint64_t>(dm) * r * pl.elt);
+    f.b1_bytes = static_cast<uint32_t>((static_cast<uint64_t>(T) * rt - static_cast<uint64_t>(m) * r) * pl.elt);
+    f.perm = perm; f.sorted_seg = sseg;
+    f.ksplit = pm.main_split;
+    f.part = pm.main_split > 1 ? ypart : nullptr;
+    f.out = y[m]; f.ldo = dm; f.out_perm = 1; f.out_dtype = p->out_dtype;
+    e = cts::launch_seg_gemm(f, p->dtype, pm.main_tile, stream);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+    if (pm.main_split > 1) {
+      e = cts::launch_splitk_reduce(ypart, pm.main_split, T, dm, perm, y[m], dm, p->out_dtype, stream);
+      if (e != hipSuccess) return CTS_ERR_HIP;
+    }
+  }
+  if (mark(4, stream) != hipSuccess) return CTS_ERR_HIP;
+  return mark(5, stream) == hipSuccess ? CTS_OK : CTS_ERR_HIP;
+}
+
+}  // namespace
+
+size_t cts_workspace_size_multi(const cts_problem* p, int32_t M, const int32_t* d_out) {
+  MultiPlan mp;
+  return make_multi_plan(p, M, d_out, &mp) == CTS_OK ? mp.total : 0;
+}
+
+int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
+                    const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
+                    const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  MultiPlan mp;
+  const int rc = make_multi_plan(p, M, d_out, &mp);
+  if (rc != CTS_OK) return rc;
+  if (p->T == 0) return CTS_OK;
+  if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || !workspace) return CTS_ERR_INVALID_ARG;
+  for (int m = 0; m < M; ++m)
+    if (!W[m] || !U[m] || !Sigma[m] || !y[m] || misaligned(W[m], 16) || misaligned(U[m], 16) ||
+        misaligned(Sigma[m], 16) || misaligned(y[m], 16))
+      return CTS_ERR_INVALID_ARG;
+  for (const void* q : {x, Vt, static_cast<const void*>(workspace)})
+    if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
+  if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4)) return CTS_ERR_INVALID_ARG;
+  if (workspace_bytes < mp.total) return CTS_ERR_WORKSPACE;
+  const size_t e = mp.mod[0].elt;
+  const size_t T = p->T, di = p->d_in, r = p->r, n = p->n_adapters, K = p->n_clusters;
+  // every output against the workspace, every input and the other outputs
+  std::vector<Range> in = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
+                           {Vt, K * static_cast<size_t>(mp.rtot) * di * e}};
+  for (int m = 0; m < M; ++m) {
+    const size_t dm = d_out[m];
+    in.push_back({W[m], dm * di * e});
+    in.push_back({U[m], K * dm * r * e});
+    in.push_back({Sigma[m], n * r * r * e});
+  }
+  for (int m = 0; m < M; ++m) {
+    const Range ym{y[m], T * static_cast<size_t>(d_out[m]) * mp.mod[m].out_elt};
+    if (any_overlap(ym, {workspace, workspace_bytes}, in.data(), static_cast<int>(in.size())))
+      return CTS_ERR_INVALID_ARG;
+    for (int k = 0; k < m; ++k)
+      if (overlap(ym, {y[k], T * static_cast<size_t>(d_out[k]) * mp.mod[k].out_elt})) return CTS_ERR_INVALID_ARG;
+  }
+  return run_multi(p, mp, d_out, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
+                   static_cast<hipStream_t>(stream));
 }
 
 namespace {

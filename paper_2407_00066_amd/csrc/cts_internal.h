@@ -128,12 +128,15 @@ __device__ __forceinline__ int seg_rank_of(const int32_t* seg_rank, int s, int k
 // only c, c' < rk are read (Sigma's leading block, z's first rk entries) and
 // zp[j][c >= rk] = 0, and sorted_rank (if not null) receives rk for every
 // position j.  Rounded to the input type.  One workgroup per item of the
-// sort (max_items workgroups are launched; the extra ones exit).
+// sort (max_items workgroups are launched; the extra ones exit).  ldz (0 =
+// r): row stride of zpart's rows and of zp (full Sigma only), for the slice
+// of one module in Z stacked over several modules.
 hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* sorted_aid, int n,
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag = false, const int32_t* sorted_seg = nullptr,
-                        const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr);
+                        const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr,
+                        int ldz = 0);
 
 // Records stage event i of the profiling aid (cts_set_stage_events) on s when
 // it is on; a no-op otherwise.

@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             TI* __restrict__ zp,
                                                             const int32_t* __restrict__ sorted_seg,
                                                             const int32_t* __restrict__ seg_rank,
-                                                            int32_t* __restrict__ sorted_rank) {
+                                                            int32_t* __restrict__ sorted_rank, int ldz) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
@@ -153,16 +153,18 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     }
   }
   // z = sum over the shrink's k-splits in fixed order; 4 consecutive values
-  // per thread, 16 splits' loads in flight at a time
-  const int64_t split_stride = static_cast<int64_t>(T) * r;
-  const float* zbase = zpart + static_cast<int64_t>(lo) * r;
+  // per thread, 16 splits' loads in flight at a time.  Rows of zpart and zp
+  // are ldz apart (ldz = r, or the stacked rank of several modules).
+  const int64_t split_stride = static_cast<int64_t>(T) * ldz;
+  const float* zbase = zpart + static_cast<int64_t>(lo) * ldz;
   for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int64_t zo = static_cast<int64_t>(e4 / r) * ldz + e4 % r;
     for (int q = 0; e4 % r < rk && q < S; q += 16) {
       f32x4 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u)
-        if (q + u < S) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + e4);
+        if (q + u < S) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + zo);
 #pragma unroll
       for (int u = 0; u < 16; ++u)
         if (q + u < S) acc += v[u];
@@ -172,9 +174,10 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   }
   __syncthreads();
 
-  TI* out = zp + static_cast<int64_t>(lo) * r;
+  TI* out = zp + static_cast<int64_t>(lo) * ldz;
   if (Sigma == nullptr) {
-    for (int e = tid; e < cnt; e += kSigThreads) st<TI>(out, e, z[(e / r) * kSigLd + e % r]);
+    for (int e = tid; e < cnt; e += kSigThreads)
+      st<TI>(out, static_cast<int64_t>(e / r) * ldz + e % r, z[(e / r) * kSigLd + e % r]);
     return;
   }
   // z'[i][c] = sum_q Sigma[c][q] z[i][q] on the fp32 matrix cores: one
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int i = 4 * fk + v;
-      if (i < nt && c < r) st<TI>(out, static_cast<int64_t>(i) * r + c, acc[v]);
+      if (i < nt && c < r) st<TI>(out, static_cast<int64_t>(i) * ldz + c, acc[v]);
     }
   }
 }
@@ -242,9 +245,11 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag, const int32_t* sorted_seg, const int32_t* seg_rank,
-                        int32_t* sorted_rank) {
+                        int32_t* sorted_rank, int ldz) {
   if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
   if (sorted_rank && !seg_rank) return hipErrorInvalidValue;
+  if (ldz <= 0) ldz = r;
+  if (ldz != r && (diag || ldz < r || ldz % 4)) return hipErrorInvalidValue;
   dim3 grid(max_items);
   if (diag && Sigma) {
     if (in_dtype == 0)
@@ -261,19 +266,19 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
   return hipGetLastError();
 }
 

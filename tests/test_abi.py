@@ -352,3 +352,39 @@ def test_jd_diag_argument_errors():
     a = list(args)
     a[10] = need - 1
     assert L.cts_jd_diag(ctypes.byref(p), *a) == B.CTS_ERR_WORKSPACE
+
+
+# ------------------------------------------------------------ multi-module ABI
+def _mcall(p, M=2, d_out=(64, 32), W=None, U=None, S=None, Y=None, Vt=FAKE, ws_bytes=1 << 30, ws=FAKE):
+    vp = ctypes.c_void_p
+    dims = (ctypes.c_int32 * len(d_out))(*d_out)
+    def arr(v):
+        return (vp * max(M, 1))(*([FAKE] * max(M, 1) if v is None else v))
+    return cts.lib().cts_apply_multi(ctypes.byref(p), M, dims, FAKE, FAKE, FAKE, arr(W), arr(U), Vt, arr(S),
+                                     arr(Y), ws, ws_bytes, None)
+
+
+def test_multi_validation():
+    p = B.make_problem(32, 64, 8, r=16, n_adapters=4, n_clusters=2)
+    L = cts.lib()
+    d2 = (ctypes.c_int32 * 2)(64, 32)
+    need = L.cts_workspace_size_multi(ctypes.byref(p), 2, d2)
+    assert need > 0
+    assert L.cts_workspace_size_multi(ctypes.byref(p), 0, d2) == 0
+    assert _mcall(p, M=0, d_out=(64,)) == B.CTS_ERR_INVALID_ARG
+    nine = tuple([64] * 9)
+    assert _mcall(p, M=9, d_out=nine) == B.CTS_ERR_UNSUPPORTED
+    assert _mcall(p, d_out=(64, 30)) == B.CTS_ERR_UNSUPPORTED               # d_out % 8
+    for name in ("W", "U", "S", "Y"):
+        kw = {name: [FAKE, None]}
+        assert _mcall(p, ws_bytes=need, **kw) == B.CTS_ERR_INVALID_ARG, name
+        kw = {name: [FAKE, ctypes.c_void_p(0x10008)]}
+        assert _mcall(p, ws_bytes=need, **kw) == B.CTS_ERR_INVALID_ARG, name
+    assert _mcall(p, Vt=None, ws_bytes=need) == B.CTS_ERR_INVALID_ARG
+    assert _mcall(p, ws_bytes=need - 1) == B.CTS_ERR_WORKSPACE
+    # the two outputs on the same memory
+    assert _mcall(p, ws_bytes=need, Y=[ctypes.c_void_p(0x40000000), ctypes.c_void_p(0x40000000)],
+                  ws=ctypes.c_void_p(0x80000000)) == B.CTS_ERR_INVALID_ARG
+    p0 = B.make_problem(0, 64, 8, r=16, n_adapters=4, n_clusters=2)
+    assert cts.lib().cts_apply_multi(ctypes.byref(p0), 2, d2, None, None, None, None, None, None, None, None, None,
+                                     0, None) == B.CTS_OK

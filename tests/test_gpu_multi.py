@@ -1,0 +1,63 @@
+"""GPU parity of multi-module batching (cts_apply_multi): M projections of one
+layer on the same x, adapter ids and cluster map, the V_k^T stacked along r,
+against the oracle's per-module layer and against cts_apply per module."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2407_00066_amd as cts
+from paper_2407_00066_amd import workloads as wl
+
+from _gpu_helpers import TOL, dev, host, row_rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # q, k, v of a decode batch: bucketing inside the shrink (T <= 128), 64x64 tiles split along d_in
+    "qkv_decode": dict(cfg=140, T=64, d_in=512, d_outs=(512, 128, 128), r=32, n=40, K=4),
+    # mid-size batch, Zipf ids
+    "qkv_mid": dict(cfg=141, T=300, d_in=256, d_outs=(256, 64, 64), r=16, n=50, K=5, ids="zipf"),
+    # gate and up of a prefill batch: 256x256 tiles
+    "gate_up_prefill": dict(cfg=142, T=2100, d_in=128, d_outs=(512, 512), r=64, n=60, K=6, ids="prefill",
+                            n_seq=12, seq_len=(60, 300)),
+    # fp32, ragged
+    "f32_pair": dict(cfg=143, T=77, d_in=128, d_outs=(96, 64), r=16, n=10, K=3, dtype="f32"),
+}
+
+
+def _modules(kw):
+    kw = dict(kw)
+    d_outs = kw.pop("d_outs")
+    cfg = kw.pop("cfg")
+    mods = [wl.synthetic("m%d" % m, cfg=cfg + 37 * m, d_out=d, with_lora=False, **kw) for m, d in enumerate(d_outs)]
+    w0 = mods[0]
+    Vt = np.concatenate([m.Vt for m in mods], axis=1)          # [K][M r][d_in]
+    return w0, mods, Vt
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_apply_multi_matches_oracle(oracle_mod, name):
+    w0, mods, Vt = _modules(CASES[name])
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    say("apply_multi %s (M=%d)" % (name, len(mods)))
+    ys = cts.apply_multi(x, aid, cof, [dev(m.W) for m in mods], [dev(m.U) for m in mods], dev(Vt),
+                         [dev(m.Sigma) for m in mods])
+    torch.cuda.synchronize()
+    refs = oracle_mod.apply_multi(w0.x, w0.adapter_id, w0.cluster_of, [m.W for m in mods], [m.U for m in mods],
+                                  Vt, [m.Sigma for m in mods])
+    for m, (y, ref) in enumerate(zip(ys, refs)):
+        assert row_rel_err(host(y), ref) <= TOL[w0.dtype], m
+    # and against the single-module call with that module's arrays
+    for m, mod in enumerate(mods):
+        y1 = cts.apply(x, aid, cof, dev(mod.W), dev(mod.U), dev(mod.Vt), dev(mod.Sigma))
+        torch.cuda.synchronize()
+        assert row_rel_err(host(ys[m]), host(y1)) <= TOL[w0.dtype], m
+
+
+def test_apply_multi_one_module_is_apply():
+    w0, mods, Vt = _modules(dict(cfg=144, T=500, d_in=256, d_outs=(320,), r=32, n=30, K=4, ids="zipf"))
+    args = [dev(a) for a in (w0.x, w0.adapter_id, w0.cluster_of)]
+    ys = cts.apply_multi(*args, [dev(w0.W)], [dev(w0.U)], dev(Vt), [dev(w0.Sigma)])
+    y1 = cts.apply(*args, dev(w0.W), dev(w0.U), dev(w0.Vt), dev(w0.Sigma))
+    torch.cuda.synchronize()
+    assert torch.equal(ys[0], y1)
