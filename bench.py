@@ -7,7 +7,9 @@ A step is one call of the whole layer (bucketing, shrink, core product, fused
 base + up-projection GEMM) over one batch of seeded synthetic inputs that are
 already resident in HBM; for the workload stack32 it is one pass over all 224
 linear projections of a 32-layer 7B-shaped decoder (q, k, v, o, gate, up,
-down), each its own cts_apply call with its own weights.  The timed region is
+down) with their own weights: q/k/v and gate/up through one cts_apply_multi
+call each (they read the same x), o and down through cts_apply; the same
+pass with every projection its own cts_apply call is reported beside it.  The timed region is
 K consecutive steps between two HIP events on the stream the library launches
 on; the steps are launched call by call.  The same steps replayed from HIP
 graphs captured from their cts_apply calls (as a serving loop replays a decode
@@ -574,9 +576,27 @@ def bench_stack(args, torch, np, cts, B, wl, device):
             p1 = cts.make_problem(T, d_in, d_out, r=r, n_adapters=1, n_clusters=1, dtype=B.CTS_BF16)
             wsz, wsz1 = max(wsz, cts.workspace_size(pb)), max(wsz1, cts.workspace_size(p1))
         projs.append(layer)
+    # multi-module batching: q/k/v and gate/up each read one x; their V_k^T
+    # stacked along r (separate outputs, since the modules run in one call)
+    groups = (("q", "k", "v"), ("gate", "up"))
+    extra_y = {("k",): torch.empty((T, 1024), dtype=torch.bfloat16, device=device),
+               ("v",): torch.empty((T, 1024), dtype=torch.bfloat16, device=device),
+               ("up",): torch.empty((T, 14336), dtype=torch.bfloat16, device=device)}
+    stacked = []
+    for L in projs:
+        stacked.append({grp: torch.cat([L[nm][3] for nm in grp], dim=1).contiguous() for grp in groups})
+    outs_of = {("q", "k", "v"): [ys[4096], extra_y[("k",)], extra_y[("v",)]],
+               ("gate", "up"): [ys[14336], extra_y[("up",)]]}
+    wszm = 1
+    for grp in groups:
+        d_in = dict((nm, di) for nm, di, _ in wl.STACK_PROJ)[grp[0]]
+        dims = [dict((nm, do) for nm, _, do in wl.STACK_PROJ)[g_] for g_ in grp]
+        pm = cts.make_problem(T, d_in, 8, r=r, n_adapters=n, n_clusters=K, dtype=B.CTS_BF16)
+        wszm = max(wszm, cts.workspace_size_multi(pm, dims))
     torch.cuda.synchronize()
     ws = torch.empty(wsz, dtype=torch.uint8, device=device)
     ws1 = torch.empty(wsz1, dtype=torch.uint8, device=device)
+    wsm = torch.empty(wszm, dtype=torch.uint8, device=device)
     aid1 = torch.zeros_like(aid)
     cof1 = torch.zeros(1, dtype=torch.int32, device=device)
     resident = sum(t.numel() * t.element_size() for L in projs for v in L.values() for t in v[1:5])
@@ -587,6 +607,16 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                 x, W, U, Vt, S, y = L[name]
                 cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
 
+    def step_multi(_):
+        for L, SV in zip(projs, stacked):
+            for grp in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+                if len(grp) == 1:
+                    x, W, U, Vt, S, y = L[grp[0]]
+                    cts.apply(x, aid, cof, W, U, Vt, S, out=y, workspace=ws)
+                else:
+                    cts.apply_multi(L[grp[0]][0], aid, cof, [L[nm][1] for nm in grp], [L[nm][2] for nm in grp],
+                                    SV[grp], [L[nm][4] for nm in grp], outs=outs_of[grp], workspace=wsm)
+
     def step1(_):
         for L in projs:
             for name, _, _ in wl.STACK_PROJ:
@@ -594,7 +624,9 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                 cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
 
     log("timing the stack: %.1f GB of weights, %d warmup + %d steps" % (resident / 1e9, args.warmup, args.steps))
-    ms, ms_g = time_launches(step, [None], args, torch)
+    ms_sep, ms_sep_g = time_launches(step, [None], args, torch)
+    log("timing the stack with q/k/v and gate/up batched (cts_apply_multi)")
+    ms, ms_g = time_launches(step_multi, [None], args, torch)
     log("timing the stack with one adapter")
     ms1, ms1_g = time_launches(step1, [None], args, torch)
 
@@ -654,6 +686,9 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         cpu = stack_cpu_baseline(projs, aid_h, cof_h, args.cpu_seconds, torch, np)
     value, value1 = T / (ms * 1e-3), T / (ms1 * 1e-3)
     return {
+        "separate_calls": {"value": round(T / (ms_sep * 1e-3), 1), "ms_per_step": round(ms_sep, 5),
+                           "graph_replay_ms_per_step": round(ms_sep_g, 5),
+                           "note": "every projection its own cts_apply call"},
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -661,6 +696,7 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         "dtype": "bf16",
         "data": "synthetic (seeded, generated on the device; %.1f GB of weights resident in HBM)" % (resident / 1e9),
         "config": {"workload": "stack32", "T": T, "layers": wl.STACK_LAYERS,
+                   "batching": "q/k/v and gate/up per cts_apply_multi call, o and down per cts_apply call",
                    "projections": [list(pr) for pr in wl.STACK_PROJ], "r": r, "n_adapters": n,
                    "n_clusters": K, "touched_clusters": touched,
                    "distinct_adapters": len(set(aid_h.tolist())), "parallelism": "single GPU"},
