@@ -517,14 +517,25 @@ __global__ __launch_bounds__(kJT) void jd_gram_kernel(const float* X0, const flo
 // One workgroup per z: G = sum_b gp[z][b] (fixed order).  chol = 0: writes G
 // to out[z].  chol = 1: G = R^T R (R upper, positive diagonal), writes R^-1.
 // chol = 2 (G symmetric positive definite): writes G^-1 = R^-1 R^-T.
-// The columns are equilibrated first (G' = D^-1 G D^-1, D = diag(G)^(1/2),
-// R = R' D): the columns of X = M U scale with M's eigenvalues, and without
-// it the fp32 Cholesky of a nearly converged basis breaks down.  A pivot
-// below 1e-12 (relative to the unit diagonal of G') is taken as 1e-12.
-// Blocked in 16 x 16 tiles so that the workgroup meets few barriers: per
-// block column, one wave factors the diagonal tile in registers, the threads
-// solve the block row, then update the trailing triangle; R'^-1 from the
-// inverses of the diagonal tiles, outward one block diagonal at a time.
+// chol = 3 (one workgroup): G = (sum_b gp[0][b]) o (sum_b gp[1][b]), the
+// elementwise product of two Gram matrices (positive definite when both
+// are), and writes G^-1 to out.
+// The columns are equilibrated first (G' = E G E, E = diag(G)^(-1/2), R =
+// R' E^-1): the columns of X = M U scale with M's eigenvalues, and without it
+// the fp32 Cholesky of a nearly converged basis breaks down.  A pivot below
+// 1e-12 (relative to the unit diagonal of G') is taken as 1e-12.
+// Blocked in 16 x 16 tiles so that the workgroup meets few barriers.  Per
+// block column J: wave 0 alone factors the diagonal tile in registers (lane c
+// holds column c; the entries other lanes need are read with readlane, at
+// constant lane indices) and inverts it the same way; then the waves form the
+// block row R'_J,c = R'_JJ^-T G'_J,c as products with that inverse, and every
+// thread updates the trailing triangle.  R'^-1 is built from the diagonal
+// tiles' inverses outward, one block diagonal at a time, and G'^-1 = R'^-1
+// R'^-T with an NB x NB register block of outputs per thread.
+__device__ __forceinline__ float lane_val(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int chol, float* out) {
   constexpr int r = 16 * NB;
@@ -532,14 +543,12 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
   constexpr int rr = r * r;
   __shared__ float g[r * ld];
   __shared__ float inv[r * ld];
-  __shared__ float dsc[r];
+  __shared__ float esc[r];
   const int z = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const float* src = gp + static_cast<int64_t>(z) * nblk * rr;
-  {
-    // partials summed in block order, four blocks' loads in flight
-    constexpr int NU = (rr + kJT - 1) / kJT;
-    float acc[NU];
+  constexpr int NU = (rr + kJT - 1) / kJT;
+  // partials summed in block order, four blocks' loads in flight
+  auto sum_partials = [&](const float* src, float (&acc)[NU]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < NU; ++u) acc[u] = 0.f;
     int b = 0;
@@ -559,105 +568,122 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
 #pragma unroll
       for (int u = 0; u < NU; ++u)
         if (tid + u * kJT < rr) acc[u] += src[static_cast<int64_t>(b) * rr + tid + u * kJT];
+  };
+  float acc[NU];
+  sum_partials(gp + static_cast<int64_t>(z) * nblk * rr, acc);
+  if (chol == 3) {
+    float acc1[NU];
+    sum_partials(gp + static_cast<int64_t>(nblk) * rr, acc1);
 #pragma unroll
-    for (int u = 0; u < NU; ++u) {
-      const int e = tid + u * kJT;
-      if (e < rr) g[(e / r) * ld + e % r] = acc[u];
-    }
+    for (int u = 0; u < NU; ++u) acc[u] *= acc1[u];
   }
-  __syncthreads();
   float* dst = out + static_cast<int64_t>(z) * rr;
   if (!chol) {
-    for (int e = tid; e < rr; e += kJT) dst[e] = g[(e / r) * ld + e % r];
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+      if (tid + u * kJT < rr) dst[tid + u * kJT] = acc[u];
     return;
   }
-  if (tid < r) {
-    const float dj = g[tid * ld + tid];
-    dsc[tid] = dj > 0.f ? sqrtf(dj) : 1.f;
+  // diagonal first (lane e % (r + 1) == 0 of the sums), then G' = E G E in place
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    const int e = tid + u * kJT;
+    if (e < rr && e % (r + 1) == 0) esc[e / (r + 1)] = acc[u] > 0.f ? 1.f / sqrtf(acc[u]) : 1.f;
   }
+  for (int e = tid; e < r * ld; e += kJT) inv[e] = 0.f;
   __syncthreads();
-  for (int e = tid; e < rr; e += kJT) {
-    const int i = e / r, c = e - i * r;
-    g[i * ld + c] /= dsc[i] * dsc[c];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    const int e = tid + u * kJT;
+    if (e < rr) g[(e / r) * ld + e % r] = acc[u] * esc[e / r] * esc[e % r];
   }
   __syncthreads();
 
-  // ---- blocked right-looking Cholesky of G' (R' in the upper triangle of g)
+  // ---- blocked right-looking Cholesky of G' (R' in the upper triangle of g,
+  // the diagonal tiles of R'^-1 in inv)
+#pragma unroll
   for (int J = 0; J < NB; ++J) {
     const int o = 16 * J;
     if (wave == 0) {
-      // lane c < 16 holds column c of the diagonal tile (rows 0..15)
+      // Lanes 16..63 repeat lanes 0..15.  Entries below the diagonal (i > c)
+      // are updated too, with values nothing reads: that saves the selects.
       const int c = lane & 15;
-      float col[16];
+      float col[16], rdg[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) col[i] = (i <= c) ? g[(o + i) * ld + o + c] : 0.f;
+      for (int i = 0; i < 16; ++i) col[i] = g[(o + i) * ld + o + c];
 #pragma unroll
       for (int k = 0; k < 16; ++k) {
-        const float piv = sqrtf(fmaxf(__shfl(col[k], k), 1e-12f));
-        col[k] = (c == k) ? piv : (c > k ? col[k] / piv : col[k]);
+        const float dk = fmaxf(lane_val(col[k], k), 1e-12f);
+        const float rp = __builtin_amdgcn_rsqf(dk);      // 1 / R'[k][k]
+        rdg[k] = rp;
+        col[k] = (c == k) ? dk * rp : col[k] * rp;
 #pragma unroll
-        for (int i = k + 1; i < 16; ++i) {
-          const float rki = __shfl(col[k], i);            // R'[k][i], row k from lane i
-          if (c >= i) col[i] = fmaf(-rki, col[k], col[i]);
-        }
+        for (int i = k + 1; i < 16; ++i) col[i] = fmaf(-lane_val(col[k], i), col[k], col[i]);
+      }
+      // column c of R'_JJ^-1 by back substitution; R'[i][k] from lane k
+      float x[16];
+#pragma unroll
+      for (int i = 15; i >= 0; --i) {
+        float s = (i == c) ? 1.f : 0.f;
+#pragma unroll
+        for (int k = i + 1; k < 16; ++k) s = fmaf(-lane_val(col[i], k), x[k], s);
+        x[i] = (i <= c) ? s * rdg[i] : 0.f;
       }
       if (lane < 16)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
+        for (int i = 0; i < 16; ++i) {
           if (i <= c) g[(o + i) * ld + o + c] = col[i];
+          inv[(o + i) * ld + o + c] = x[i];
+        }
     }
+    if (J + 1 == NB) break;
     __syncthreads();
-    // block row: R'[o..o+16)[c] = R_JJ^-T G'[o..o+16)[c] for c >= o + 16
-    for (int c = o + 16 + tid; c < r; c += kJT) {
-      float y[16];
+    // block row: R'[o+i][cc] = sum_{k <= i} (R'_JJ^-1)[k][i] G'[o+k][cc] for
+    // cc >= o + 16.  Wave q takes columns o + 16 + 16 q + (lane % 16), lane / 16
+    // picks four rows.  Each column belongs to one wave, and no lane of it
+    // writes before every lane has read the whole column: each written value
+    // depends on all sixteen reads, and a wave executes in lockstep.
+    {
+      const int w = r - o - 16;
+      for (int cb = 16 * wave; cb < w; cb += 16 * (kJT / 64)) {
+        const int cc = o + 16 + cb + (lane & 15);
+        const int i0 = 4 * (lane >> 4);
+        float gk[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float s = g[(o + i) * ld + c];
+        for (int k = 0; k < 16; ++k) gk[k] = g[(o + k) * ld + cc];
+        float y[4];
 #pragma unroll
-        for (int k = 0; k < i; ++k) s = fmaf(-g[(o + k) * ld + o + i], y[k], s);
-        y[i] = s / g[(o + i) * ld + o + i];
+        for (int q = 0; q < 4; ++q) {
+          y[q] = 0.f;
+#pragma unroll
+          for (int k = 0; k < 16; ++k) y[q] = fmaf(inv[(o + k) * ld + o + i0 + q], gk[k], y[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) g[(o + i0 + q) * ld + cc] = y[q];
       }
-#pragma unroll
-      for (int i = 0; i < 16; ++i) g[(o + i) * ld + c] = y[i];
     }
     __syncthreads();
     // trailing triangle: G'[i][c] -= sum_k R'[o+k][i] R'[o+k][c], o+16 <= i <= c
-    const int w = r - o - 16;
-    for (int e = tid; e < w * w; e += kJT) {
-      const int i = o + 16 + e / w, c = o + 16 + e % w;
-      if (c >= i) {
-        float s = g[i * ld + c];
+    {
+      const int w = r - o - 16;
+      for (int e = tid; e < w * w; e += kJT) {
+        const int i = o + 16 + e / w, c = o + 16 + e % w;
+        if (c >= i) {
+          float s = g[i * ld + c];
 #pragma unroll
-        for (int k = 0; k < 16; ++k) s = fmaf(-g[(o + k) * ld + i], g[(o + k) * ld + c], s);
-        g[i * ld + c] = s;
+          for (int k = 0; k < 16; ++k) s = fmaf(-g[(o + k) * ld + i], g[(o + k) * ld + c], s);
+          g[i * ld + c] = s;
+        }
       }
     }
     __syncthreads();
   }
+  __syncthreads();
 
-  // ---- R'^-1: diagonal tiles first (wave w: tiles w, w + 4, ...), lane c
-  // holding column c of the tile's inverse
-  for (int e = tid; e < r * ld; e += kJT) inv[e] = 0.f;
-  __syncthreads();
-  for (int I = wave; I < NB; I += kJT / 64) {
-    const int o = 16 * I;
-    const int c = lane & 15;
-    float x[16];
-#pragma unroll
-    for (int i = 15; i >= 0; --i) {
-      float s = (i == c) ? 1.f : 0.f;
-#pragma unroll
-      for (int k = i + 1; k < 16; ++k) s = fmaf(-g[(o + i) * ld + o + k], x[k], s);
-      x[i] = (i <= c) ? s / g[(o + i) * ld + o + i] : 0.f;
-    }
-    if (lane < 16)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) inv[(o + i) * ld + o + c] = x[i];
-  }
-  __syncthreads();
-  // off-diagonal tiles by distance d: X_IJ = -X_II sum_{K=I+1..J} R'_IK X_KJ.
+  // off-diagonal tiles of R'^-1 by distance d: X_IJ = -X_II sum_{K=I+1..J} R'_IK X_KJ.
   // T_IJ is kept transposed in tile JI of g's strict lower triangle, which
   // nothing reads after the factorization.
+#pragma unroll
   for (int d = 1; d < NB; ++d) {
     for (int e = tid; e < (NB - d) * 256; e += kJT) {
       const int I = e / 256, a = (e % 256) / 16, bcol = e % 16;
@@ -681,19 +707,39 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
     }
     __syncthreads();
   }
-  // R^-1 = D^-1 R'^-1
   if (chol == 1) {
-    for (int e = tid; e < rr; e += kJT) dst[e] = inv[(e / r) * ld + e % r] / dsc[e / r];
+    // R^-1 = E R'^-1
+    for (int e = tid; e < rr; e += kJT) dst[e] = inv[(e / r) * ld + e % r] * esc[e / r];
     return;
   }
-  for (int e = tid; e < rr; e += kJT) inv[(e / r) * ld + e % r] /= dsc[e / r];
-  __syncthreads();
-  // G^-1[i][c] = sum_{k >= max(i, c)} R^-1[i][k] R^-1[c][k]
-  for (int e = tid; e < rr; e += kJT) {
-    const int i = e / r, c = e - i * r;
-    float sacc = 0.f;
-    for (int k = i > c ? i : c; k < r; ++k) sacc = fmaf(inv[i * ld + k], inv[c * ld + k], sacc);
-    dst[e] = sacc;
+  // G^-1 = E R'^-1 R'^-T E; R'^-1 is upper triangular with explicit zeros
+  // below the diagonal, so every product runs over all r terms.  Thread
+  // (ti, tc) owns rows ti + 16 a and columns tc + 16 b (a, b < NB).
+  {
+    const int ti = tid >> 4, tc = tid & 15;
+    float accm[NB][NB];
+#pragma unroll
+    for (int a = 0; a < NB; ++a)
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) accm[a][bb] = 0.f;
+    for (int k = 0; k < r; ++k) {
+      float ra[NB], rb[NB];
+#pragma unroll
+      for (int a = 0; a < NB; ++a) ra[a] = inv[(ti + 16 * a) * ld + k];
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) rb[bb] = inv[(tc + 16 * bb) * ld + k];
+#pragma unroll
+      for (int a = 0; a < NB; ++a)
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) accm[a][bb] = fmaf(ra[a], rb[bb], accm[a][bb]);
+    }
+#pragma unroll
+    for (int a = 0; a < NB; ++a)
+#pragma unroll
+      for (int bb = 0; bb < NB; ++bb) {
+        const int i = ti + 16 * a, c = tc + 16 * bb;
+        dst[i * r + c] = accm[a][bb] * esc[i] * esc[c];
+      }
   }
 }
 
@@ -959,11 +1005,6 @@ __global__ __launch_bounds__(kJT) void km_members_kernel(const int32_t* labels, 
 }
 
 // ---------------------------------------------------------- JD-Diag pieces
-// out = X o Y (elementwise), n entries
-__global__ void jd_hadamard_kernel(const float* X, const float* Y, float* out, int n) {
-  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) out[e] = X[e] * Y[e];
-}
-
 // s_i = Ginv w_i for every LoRA (Ginv symmetric r x r): s[i][j] = sum_k Ginv[j][k] w[i][k]
 __global__ __launch_bounds__(kJT) void jd_diag_solve_kernel(const float* ginv, const float* w, int n, int r,
                                                             float* s) {
@@ -1264,8 +1305,10 @@ int run_jd(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, co
 }
 
 // ---- JD-Diag by alternating least squares (App. A.1 case 2)
-// out2[0] = X0^T X0 (d0 rows), out2[1] = X1^T X1 (d1 rows)
-hipError_t two_grams(Jd& j, const float* X0, int d0, const float* X1, int d1, float* out2) {
+// out = (X0^T X0 o X1^T X1)^-1 (X0: d0 rows, X1: d1 rows, r columns each);
+// the elementwise product of the two Gram matrices is positive definite
+// when both are
+hipError_t gram_hadamard_inverse(Jd& j, const float* X0, int d0, const float* X1, int d1, float* out) {
   const int r = j.p->r;
   const int nb = (std::max(d0, d1) + kGramRows - 1) / kGramRows;
   float* gp = j.at<float>(j.pl.off_gp);
@@ -1274,19 +1317,7 @@ hipError_t two_grams(Jd& j, const float* X0, int d0, const float* X1, int d1, fl
                        X0, X1, nullptr, nullptr, d0, d1, nb, gp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, nb, 0, out2);
-    return hipGetLastError();
-  });
-}
-
-// out = (X o Y)^-1 for symmetric positive definite X o Y (r x r)
-hipError_t hadamard_inverse(Jd& j, const float* X, const float* Y, float* tmp, float* out) {
-  const int r = j.p->r;
-  hipLaunchKernelGGL(jd_hadamard_kernel, dim3((r * r + 255) / 256), dim3(256), 0, j.st, X, Y, tmp, r * r);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return with_nb(r, [&](auto c) {
-    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(1), dim3(kJT), 0, j.st, tmp, 1, 2, out);
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(1), dim3(kJT), 0, j.st, gp, nb, 3, out);
     return hipGetLastError();
   });
 }
@@ -1333,13 +1364,12 @@ hipError_t als_sigma(Jd& j, const float* A, const float* B, const int32_t* lidx,
   float* V = j.at<float>(j.pl.off_V);
   float* sd = j.at<float>(j.pl.off_sd);
   float* w = j.at<float>(j.pl.off_wv);
-  float* m = j.at<float>(j.pl.off_m);            // [0..1]: grams, [2]: tmp, [3]: inverse
+  float* m = j.at<float>(j.pl.off_m);            // [3]: (U^T U o V^T V)^-1
   hipError_t e = launch_project(j, A, B, V, U, lidx, p->n, 5, nullptr, nullptr, nullptr, nullptr, 0, 0,
                                 fresh ? 0 : 0, fresh ? 2 : 1, nullptr, w);
   if (e != hipSuccess) return e;
-  if ((e = two_grams(j, U, p->d_out, V, p->d_in, m)) != hipSuccess) return e;
   const int64_t rr = static_cast<int64_t>(r) * r;
-  if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 3 * rr)) != hipSuccess) return e;
+  if ((e = gram_hadamard_inverse(j, U, p->d_out, V, p->d_in, m + 3 * rr)) != hipSuccess) return e;
   const int64_t tot = static_cast<int64_t>(p->n) * r;
   hipLaunchKernelGGL(jd_diag_solve_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (tot + kJT - 1) / kJT))),
                      dim3(kJT), 0, j.st, m + 3 * rr, w, p->n, r, sd);
@@ -1367,8 +1397,7 @@ hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx,
     if ((e = stage_mark(2, j.st)) != hipSuccess) return e;
     if ((e = expand_one(j, A, B, lidx, p->n, 0, Un)) != hipSuccess) return e;
     if ((e = stage_mark(3, j.st)) != hipSuccess) return e;
-    if ((e = two_grams(j, V, p->d_in, sd, p->n, m)) != hipSuccess) return e;
-    if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 4 * rr)) != hipSuccess) return e;
+    if ((e = gram_hadamard_inverse(j, V, p->d_in, sd, p->n, m + 4 * rr)) != hipSuccess) return e;
     if ((e = apply_one(j, Un, p->d_out, 0, m + 4 * rr)) != hipSuccess) return e;
     std::swap(j.pl.off_U, j.pl.off_Uo);
   }
@@ -1381,8 +1410,7 @@ hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx,
                             nullptr)) != hipSuccess)
       return e;
     if ((e = expand_one(j, A, B, lidx, p->n, 1, Vn)) != hipSuccess) return e;
-    if ((e = two_grams(j, U, p->d_out, sd, p->n, m)) != hipSuccess) return e;
-    if ((e = hadamard_inverse(j, m, m + rr, m + 2 * rr, m + 5 * rr)) != hipSuccess) return e;
+    if ((e = gram_hadamard_inverse(j, U, p->d_out, sd, p->n, m + 5 * rr)) != hipSuccess) return e;
     if ((e = apply_one(j, Vn, p->d_in, 1, m + 4 * rr)) != hipSuccess) return e;   // slot 1 = m + 5 rr
     std::swap(j.pl.off_V, j.pl.off_Vo);
   }

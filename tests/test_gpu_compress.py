@@ -66,6 +66,7 @@ CASES = {
     "rank16_loras": (33, 20, 200, 136, 16, 48, 4),       # r = 48: three column blocks
     "rank32_loras": (34, 9, 160, 192, 32, 64, 4),
     "rank64_loras": (35, 5, 128, 140, 64, 128, 3),
+    "rank32_r96": (36, 6, 160, 120, 32, 96, 3),          # r = 96: six column blocks
 }
 
 
@@ -263,6 +264,8 @@ DIAG_CASES = {
     "diag_r16": (51, 12, 96, 80, 4, 16, 4, False),
     "diag_r32_norm": (52, 20, 132, 100, 8, 32, 3, True),
     "diag_r64_rank16": (53, 10, 160, 144, 16, 64, 2, False),
+    "diag_r96_norm": (54, 24, 128, 112, 16, 96, 2, True),
+    "diag_r128": (55, 16, 136, 128, 16, 128, 2, False),
 }
 
 

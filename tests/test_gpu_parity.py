@@ -103,6 +103,11 @@ SMALL = {
     # 128x128 ring tiles (at least 128 of them, too few 256x128 tiles): ragged
     # token tail and d_in
     "bf16_mid_tiles": dict(cfg=113, T=200, d_in=200, d_out=8192, r=24, n=30, K=4, ids="zipf"),
+    # the largest batch, rank and LoRA rank the ABI takes (T = 8192, r = r_lora = 128), ragged
+    "bf16_max_T": dict(cfg=114, T=8192, d_in=264, d_out=200, r=128, n=2000, K=40, r_l=128, ids="prefill",
+                       n_seq=48, seq_len=(60, 300)),
+    # the largest id spaces (n = K = 65536), every token its own adapter and cluster
+    "bf16_max_ids": dict(cfg=115, T=600, d_in=64, d_out=64, r=8, n=65536, K=65536, r_l=8),
 }
 
 
@@ -128,7 +133,8 @@ def test_apply_small(oracle_mod, small_cases, name):
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "f32_ragged", "bf16_ragged", "bf16_large_tiles",
-                                  "bf16_T1", "bf16_one_adapter", "bf16_ring_ragged"])
+                                  "bf16_T1", "bf16_one_adapter", "bf16_ring_ragged", "bf16_max_T",
+                                  "bf16_max_ids"])
 def test_uncompressed_small(oracle_mod, small_cases, name):
     w = small_cases[name]
     say("apply_uncompressed %s T=%d r_l=%d n=%d" % (name, w.T, w.r_l, w.n))
