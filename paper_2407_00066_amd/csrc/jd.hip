@@ -38,6 +38,7 @@ constexpr int kStage = kAS + kBS;  // floats per staging buffer
 constexpr int kEpLd = kRMax + 1;   // epilogue rows (odd stride)
 constexpr int kGramRows = 256;     // rows per Gram partial
 constexpr int kMaxKm = 100;        // k-means iterations
+constexpr int kExpIds = 2048;      // LoRA ids an expansion workgroup stages in LDS
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -48,40 +49,67 @@ __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
 // at k0 and gives its LDS offset; a B loader fills slot e (< 8 r) of the
 // 32 x r B tile.  Out-of-range slots read zeros.
 
-// P_i = A_i V: rows m = (LoRA q of the group, row l), k along d_in.
-struct LoadLoraRows {
-  const float* A; const int32_t* lidx; int q0, nq, r_l, d_in;
-  __device__ float4 operator()(int e, int k0, int& off) const {
-    const int m = e >> 3, kq = e & 7;
-    off = m * kALD + 4 * kq;
-    const int q = m / r_l, l = m - q * r_l, k = k0 + 4 * kq;
-    if (q >= nq || k >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
-    const int64_t row = static_cast<int64_t>(lidx[q0 + q]) * r_l + l;
-    return *reinterpret_cast<const float4*>(A + row * d_in + k);
+// A loader is called as la(u, e, k0, off) with e = threadIdx.x + u * kJT.
+static_assert(kTM * kBK / 4 / kJT == 2, "two A slots per thread");
+
+// P_i = A_i V, with the row address of each of the thread's two A slots
+// computed once (the LoRA id lookup is off the k loop): rows m = (LoRA q of
+// the group, row l), k along d_in.
+struct LoadLoraRowsP {
+  const float* p[2];
+  int off[2], kq4[2], d_in;
+  __device__ LoadLoraRowsP(const float* A, const int32_t* lidx, int q0, int nq, int r_l, int d_in_)
+      : d_in(d_in_) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = threadIdx.x + u * kJT;
+      const int m = e >> 3, kq = e & 7;
+      off[u] = m * kALD + 4 * kq;
+      kq4[u] = 4 * kq;
+      const int q = m / r_l, l = m - q * r_l;
+      p[u] = (q < nq) ? A + (static_cast<int64_t>(lidx[q0 + q]) * r_l + l) * d_in + 4 * kq : nullptr;
+    }
+  }
+  __device__ float4 operator()(int u, int, int k0, int& o) const {
+    o = off[u];
+    if (!p[u] || k0 + kq4[u] >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
+    return *reinterpret_cast<const float4*>(p[u] + k0);
   }
 };
 
-// Q_i = B_i^T U: k = output row o, m = (LoRA q, column l); a LoRA's 32 x r_l
-// block of rows o is contiguous.
-struct LoadLoraBt {
-  const float* B; const int32_t* lidx; int q0, nq, r_l, d_out;
-  __device__ float4 operator()(int e, int k0, int& off) const {
-    const int per = 8 * r_l;                     // float4 per LoRA block
-    const int q = e / per, rem = e - q * per;
-    const int kk = rem / (r_l >> 2), l = 4 * (rem - kk * (r_l >> 2));
-    off = kk * kAML + q * r_l + l;
-    const int o = k0 + kk;
-    if (q >= nq || o >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
-    const int64_t base = static_cast<int64_t>(lidx[q0 + q]) * d_out * r_l;
-    return *reinterpret_cast<const float4*>(B + base + static_cast<int64_t>(o) * r_l + l);
+// Q_i = B_i^T U likewise: k = output row o, m = (LoRA q, column l); a LoRA's
+// 32 x r_l block of rows o is contiguous.
+struct LoadLoraBtP {
+  const float* p[2];
+  int off[2], kk[2], r_l, d_out;
+  __device__ LoadLoraBtP(const float* B, const int32_t* lidx, int q0, int nq, int r_l_, int d_out_)
+      : r_l(r_l_), d_out(d_out_) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = threadIdx.x + u * kJT;
+      const int per = 8 * r_l;
+      const int q = e / per, rem = e - q * per;
+      const int k = rem / (r_l >> 2), l = 4 * (rem - k * (r_l >> 2));
+      off[u] = k * kAML + q * r_l + l;
+      kk[u] = k;
+      p[u] = (q < nq) ? B + static_cast<int64_t>(lidx[q0 + q]) * d_out * r_l + static_cast<int64_t>(k) * r_l + l
+                      : nullptr;
+    }
+  }
+  __device__ float4 operator()(int u, int, int k0, int& o) const {
+    o = off[u];
+    if (!p[u] || k0 + kk[u] >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
+    return *reinterpret_cast<const float4*>(p[u] + static_cast<int64_t>(k0) * r_l);
   }
 };
 
 // U' = sum B_i C_i: rows m = output row o, k = flat (LoRA, l) index f; a
 // LoRA's 64 x w block (w = min(r_l, 32) columns from l0) is read row by row.
+// LoRA q of the list is ids[q - id0] (ids: the workgroup's slice of the list
+// staged in LDS, or the list itself); r_l = 1 << lg.
 struct LoadExpandB {
-  const float* B; const int32_t* lidx; int r_l, d_out, o0, f_end;
-  __device__ float4 operator()(int e, int k0, int& off) const {
+  const float* B; const int32_t* ids; int id0, lg, r_l, d_out, o0, f_end;
+  __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int w = r_l < kBK ? r_l : kBK;
     const int w4 = w >> 2;
     const int j4 = e % w4, m = (e / w4) & (kTM - 1), qq = e / (w4 * kTM);
@@ -89,22 +117,22 @@ struct LoadExpandB {
     const int f = k0 + qq * w + 4 * j4;       // k0: flat index of the tile
     const int o = o0 + m;
     if (f >= f_end || o >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
-    const int q = f / r_l, l = f - q * r_l;
-    const int64_t base = static_cast<int64_t>(lidx[q]) * d_out * r_l;
+    const int q = f >> lg, l = f & (r_l - 1);
+    const int64_t base = static_cast<int64_t>(ids[q - id0]) * d_out * r_l;
     return *reinterpret_cast<const float4*>(B + base + static_cast<int64_t>(o) * r_l + l);
   }
 };
 
 // V' = sum A_i^T D_i: k = flat (LoRA, l), m = input column c.
 struct LoadExpandA {
-  const float* A; const int32_t* lidx; int r_l, d_in, c0, f_end;
-  __device__ float4 operator()(int e, int k0, int& off) const {
+  const float* A; const int32_t* ids; int id0, lg, r_l, d_in, c0, f_end;
+  __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int kk = e >> 4, m4 = e & 15;
     off = kk * kAML + 4 * m4;
     const int f = k0 + kk, c = c0 + 4 * m4;
     if (f >= f_end || c >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
-    const int q = f / r_l, l = f - q * r_l;
-    const int64_t row = static_cast<int64_t>(lidx[q]) * r_l + l;
+    const int q = f >> lg, l = f & (r_l - 1);
+    const int64_t row = static_cast<int64_t>(ids[q - id0]) * r_l + l;
     return *reinterpret_cast<const float4*>(A + row * d_in + c);
   }
 };
@@ -112,7 +140,7 @@ struct LoadExpandA {
 // B tile: rows k of an [K][r] array (a basis, or C / D rows).
 struct LoadRowsR {
   const float* X; int r, K;
-  __device__ float4 operator()(int e, int k0, int& off) const {
+  __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int r4 = r >> 2;
     const int kk = e / r4, n = 4 * (e - kk * r4);
     off = kk * kBLD + n;
@@ -142,10 +170,10 @@ __device__ void tile_gemm(float* smem, int k_begin, int k_end, const LA& la, con
   auto fetch = [&](int t, float4 (&ra_)[NAQ], float4 (&rb_)[NBQ], int (&oa_)[NAQ], int (&ob_)[NBQ]) {
     const int k0 = k_begin + t * kBK;
 #pragma unroll
-    for (int u = 0; u < NAQ; ++u) ra_[u] = la(tid + u * kJT, k0, oa_[u]);
+    for (int u = 0; u < NAQ; ++u) ra_[u] = la(u, tid + u * kJT, k0, oa_[u]);
 #pragma unroll
     for (int u = 0; u < NBQ; ++u)
-      if (NBS % kJT == 0 || tid + u * kJT < NBS) rb_[u] = lb(tid + u * kJT, k0, ob_[u]);
+      if (NBS % kJT == 0 || tid + u * kJT < NBS) rb_[u] = lb(u, tid + u * kJT, k0, ob_[u]);
   };
   auto stash = [&](int buf, const float4 (&ra_)[NAQ], const float4 (&rb_)[NBQ], const int (&oa_)[NAQ],
                    const int (&ob_)[NBQ]) {
@@ -238,10 +266,10 @@ __global__ __launch_bounds__(kJT) void jd_pq_kernel(const PqArgs a) {
   f32x4 acc[NB];
   zero_acc(acc);
   if (isq)
-    tile_gemm<NB, true>(smem, k_lo, k_hi, LoadLoraBt{a.B, a.lidx, q0, nq, a.r_l, a.d_out},
+    tile_gemm<NB, true>(smem, k_lo, k_hi, LoadLoraBtP(a.B, a.lidx, q0, nq, a.r_l, a.d_out),
                         LoadRowsR{a.U, r, k_hi}, acc);
   else
-    tile_gemm<NB, false>(smem, k_lo, k_hi, LoadLoraRows{a.A, a.lidx, q0, nq, a.r_l, a.d_in},
+    tile_gemm<NB, false>(smem, k_lo, k_hi, LoadLoraRowsP(a.A, a.lidx, q0, nq, a.r_l, a.d_in),
                          LoadRowsR{a.V, r, k_hi}, acc);
   const int64_t rows_all = static_cast<int64_t>(a.m) * a.r_l;
   float* out = a.part + ((static_cast<int64_t>(ks) * 2 + (isq ? 1 : 0)) * rows_all +
@@ -423,13 +451,26 @@ __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
   const int s = blockIdx.y;
   const int f_lo = static_cast<int>(static_cast<int64_t>(ntile) * s / a.split) * kBK;
   const int f_hi = min(fk_total, static_cast<int>(static_cast<int64_t>(ntile) * (s + 1) / a.split) * kBK);
+  // the workgroup's slice of the LoRA list, staged in LDS when it fits (the
+  // loads' addresses then wait on an LDS read, not on a global one)
+  __shared__ int32_t s_ids[kExpIds];
+  const int lg = __builtin_ctz(a.r_l);
+  const int q_lo = f_lo >> lg, nids = ((f_hi + a.r_l - 1) >> lg) - q_lo;
+  const int32_t* ids = a.lidx;
+  int id0 = 0;
+  if (nids <= kExpIds) {
+    for (int i = threadIdx.x; i < nids; i += kJT) s_ids[i] = a.lidx[q_lo + i];
+    __syncthreads();
+    ids = s_ids;
+    id0 = q_lo;
+  }
   f32x4 acc[NB];
   zero_acc(acc);
   if (isv)
-    tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA{a.A, a.lidx, a.r_l, a.d_in, row0, f_hi},
+    tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA{a.A, ids, id0, lg, a.r_l, a.d_in, row0, f_hi},
                         LoadRowsR{a.D, r, f_hi}, acc);
   else
-    tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB{a.B, a.lidx, a.r_l, a.d_out, row0, f_hi},
+    tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB{a.B, ids, id0, lg, a.r_l, a.d_out, row0, f_hi},
                          LoadRowsR{a.C, r, f_hi}, acc);
   float* part = (isv ? a.partV : a.partU) + static_cast<int64_t>(s) * d * r;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -464,7 +505,7 @@ __global__ __launch_bounds__(kJT) void jd_reduce_kernel(const float* partU, cons
 // Rows of a basis X [d][r] as the A operand (m = row, k = column).
 struct LoadBasisRows {
   const float* X; int r, row0, d;
-  __device__ float4 operator()(int e, int k0, int& off) const {
+  __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int m = e >> 3, kq = e & 7;
     off = m * kALD + 4 * kq;
     const int row = row0 + m, k = k0 + 4 * kq;
@@ -476,7 +517,7 @@ struct LoadBasisRows {
 // X^T as the A operand (m = column a of X, k = row of X): k-major.
 struct LoadBasisT {
   const float* X; int r, a0, k_end;
-  __device__ float4 operator()(int e, int k0, int& off) const {
+  __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int kk = e >> 4, m4 = e & 15;
     off = kk * kAML + 4 * m4;
     const int row = k0 + kk, col = a0 + 4 * m4;
