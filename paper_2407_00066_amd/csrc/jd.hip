@@ -31,14 +31,18 @@ constexpr int kTM = 64;         // rows per output tile
 constexpr int kRMax = 128;      // largest JD rank
 constexpr int kALD = kBK + 4;   // A tile, m-major: row stride (floats)
 constexpr int kAML = kTM + 16;  // A tile, k-major: row stride
-constexpr int kBLD = kRMax + 16;  // B tile (k-major, r columns): row stride
 constexpr int kAS = (kTM * kALD > kBK * kAML) ? kTM * kALD : kBK * kAML;
-constexpr int kBS = kBK * kBLD;
-constexpr int kStage = kAS + kBS;  // floats per staging buffer
+// B tile (k-major, r columns): row stride.  It is 16 or 48 mod 64 floats, so
+// the four k rows one MFMA reads fall on different LDS banks.
+__host__ __device__ constexpr int b_ld(int r) { return r + (((r / 16) & 1) ? 32 : 16); }
+// floats per staging buffer (A tile, then B tile) for rank 16 NB
+template <int NB>
+__host__ __device__ constexpr int stage_floats() { return kAS + kBK * b_ld(16 * NB); }
 constexpr int kEpLd = kRMax + 1;   // epilogue rows (odd stride)
 constexpr int kGramRows = 256;     // rows per Gram partial
 constexpr int kMaxKm = 100;        // k-means iterations
 constexpr int kExpIds = 2048;      // LoRA ids an expansion workgroup stages in LDS
+constexpr int kMaxExpSplit = 16;   // most pieces of the collection in the expansion
 
 __device__ __forceinline__ f32x4 mfma4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -143,7 +147,7 @@ struct LoadRowsR {
   __device__ float4 operator()(int, int e, int k0, int& off) const {
     const int r4 = r >> 2;
     const int kk = e / r4, n = 4 * (e - kk * r4);
-    off = kk * kBLD + n;
+    off = kk * b_ld(r) + n;
     const int k = k0 + kk;
     if (k >= K) return float4{0.f, 0.f, 0.f, 0.f};
     return *reinterpret_cast<const float4*>(X + static_cast<int64_t>(k) * r + n);
@@ -177,7 +181,7 @@ __device__ void tile_gemm(float* smem, int k_begin, int k_end, const LA& la, con
   };
   auto stash = [&](int buf, const float4 (&ra_)[NAQ], const float4 (&rb_)[NBQ], const int (&oa_)[NAQ],
                    const int (&ob_)[NBQ]) {
-    float* As = smem + buf * kStage;
+    float* As = smem + buf * stage_floats<NB>();
     float* Bs = As + kAS;
 #pragma unroll
     for (int u = 0; u < NAQ; ++u) *reinterpret_cast<float4*>(As + oa_[u]) = ra_[u];
@@ -188,14 +192,14 @@ __device__ void tile_gemm(float* smem, int k_begin, int k_end, const LA& la, con
   if (nt <= 0) return;
   const int m = 16 * wave + fr;
   auto multiply = [&](int buf) {
-    const float* As = smem + buf * kStage;
+    const float* As = smem + buf * stage_floats<NB>();
     const float* Bs = As + kAS;
 #pragma unroll
     for (int s = 0; s < kBK / 4; ++s) {
       const int k = 4 * s + fk;
       const float a = AKM ? As[k * kAML + m] : As[m * kALD + k];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a, Bs[k * kBLD + 16 * nb + fr], acc[nb]);
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma4(a, Bs[k * b_ld(R) + 16 * nb + fr], acc[nb]);
     }
   };
   fetch(0, ra[0], rb[0], oa[0], ob[0]);
@@ -239,19 +243,19 @@ __device__ __forceinline__ void acc_to_lds(const f32x4 (&acc)[NB], float* dst) {
 // jd_pq_kernel: partial P or Q rows of a group of 64 / r_l LoRAs over one
 // half of the reduction; jd_combine_kernel: sums the halves and forms the
 // per-LoRA products of the requested mode.
-constexpr int kPqSplit = 2;   // halves of d_in (P) and d_out (Q)
 
 struct PqArgs {
   const float* A; const float* B; const float* V; const float* U;
   const int32_t* lidx; int m;
   int r_l, d_in, d_out;
-  float* part;                  // [kPqSplit][2][m * r_l][r]
+  float* part;                  // [split][2][m * r_l][r]
+  int split;                    // pieces of the reduction (blockIdx.z)
   int zbase;                    // blockIdx.y + zbase: 0 = P, 1 = Q
 };
 
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_pq_kernel(const PqArgs a) {
-  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) float smem[2 * stage_floats<NB>()];
   constexpr int r = 16 * NB;
   const int lpw = kTM / a.r_l;
   const int q0 = blockIdx.x * lpw;
@@ -261,8 +265,8 @@ __global__ __launch_bounds__(kJT) void jd_pq_kernel(const PqArgs a) {
   const int ks = blockIdx.z;
   const int d = isq ? a.d_out : a.d_in;
   const int ntile = (d + kBK - 1) / kBK;
-  const int k_lo = (ntile * ks / kPqSplit) * kBK;
-  const int k_hi = min(d, (ntile * (ks + 1) / kPqSplit) * kBK);
+  const int k_lo = (ntile * ks / a.split) * kBK;
+  const int k_hi = min(d, (ntile * (ks + 1) / a.split) * kBK);
   f32x4 acc[NB];
   zero_acc(acc);
   if (isq)
@@ -290,6 +294,7 @@ struct ProjArgs {
   const int32_t* lidx; int m;
   int r_l;
   const float* part;            // from jd_pq_kernel
+  int split;                    // its pieces of the reduction
   int mode;                     // 0: C, D   1: Sigma   2: score   3: C = P diag(s)
                                 // 4: D = Q diag(s)   5: w = colsum(Q o P)
   const float* sdiag;           // modes 3, 4: [n][r] diagonals (by id)
@@ -321,8 +326,7 @@ __global__ __launch_bounds__(kJT) void jd_combine_kernel(const ProjArgs a) {
     const float* base = a.part + static_cast<int64_t>(q0) * r_l * r;
     for (int e = tid; e < rows * r; e += kJT) {
       float p = 0.f, q = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < kPqSplit; ++ks) {
+      for (int ks = 0; ks < a.split; ++ks) {
         p += base[(static_cast<int64_t>(ks) * 2) * rows_all * r + e];
         q += base[(static_cast<int64_t>(ks) * 2 + 1) * rows_all * r + e];
       }
@@ -440,7 +444,7 @@ struct ExpArgs {
 
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
-  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) float smem[2 * stage_floats<NB>()];
   constexpr int r = 16 * NB;
   const bool isv = blockIdx.z + a.zbase == 1;
   const int d = isv ? a.d_in : a.d_out;
@@ -532,7 +536,7 @@ struct LoadBasisT {
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_gram_kernel(const float* X0, const float* X1, const float* Y0,
                                                       const float* Y1, int d0, int d1, int nblk, float* gp) {
-  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) float smem[2 * stage_floats<NB>()];
   constexpr int r = 16 * NB;
   const int z = blockIdx.y, b = blockIdx.x, a0 = blockIdx.z * kTM;
   const int d = z ? d1 : d0;
@@ -789,7 +793,7 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
 template <int NB>
 __global__ __launch_bounds__(kJT) void jd_apply_kernel(float* X0, float* X1, int d0, int d1,
                                                        const float* rinv, int zbase = 0) {
-  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) float smem[2 * stage_floats<NB>()];
   constexpr int r = 16 * NB;
   const int z = blockIdx.y + zbase;
   const int d = z ? d1 : d0;
@@ -817,7 +821,7 @@ template <int NB>
 __global__ __launch_bounds__(kJT) void jd_resid_kernel(const float* Uo, const float* Un, const float* Vo,
                                                        const float* Vn, int d0, int d1, const float* M,
                                                        int nblk, float* rp) {
-  __shared__ __attribute__((aligned(16))) float smem[2 * kStage];
+  __shared__ __attribute__((aligned(16))) float smem[2 * stage_floats<NB>()];
   __shared__ float red[2 * kJT];
   constexpr int r = 16 * NB;
   const int z = blockIdx.y, b = blockIdx.x;
@@ -1122,7 +1126,7 @@ int validate(const cts_jd_problem* p) {
 
 // Workspace of one JD run (plus the clustering extras when K > 0).
 struct JdPlan {
-  int split, nblk_out, nblk_in, nblk, nblk_n;
+  int split, pq_split, nblk_out, nblk_in, nblk, nblk_n;
   size_t off_U, off_V, off_Uo, off_Vo, off_C, off_D, off_pq, off_pU, off_pV, off_gp, off_mat, off_rp, off_lidx,
       off_w2, off_w, off_n2, off_crit, total;
   // clustering
@@ -1133,14 +1137,37 @@ struct JdPlan {
 
 size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
+// Workgroups of the projection and expansion kernels one compute unit holds
+// at rank r (their LDS and registers, as compiled for gfx950), and the
+// smallest split of a launch of `base` workgroups per piece that fills the
+// resident slots of 256 compute units within 5% of the best such split.
+int resident_wgs(int r) { return r <= 32 ? 4 : (r <= 64 ? 3 : 2); }
+
+int pick_split(int64_t base, int occ, int smax) {
+  const int64_t slots = 256LL * occ;
+  int best = 1;
+  double best_eff = 0.0;
+  for (int s = 1; s <= smax; ++s) {
+    const int64_t w = base * s, rounds = (w + slots - 1) / slots;
+    const double eff = static_cast<double>(w) / static_cast<double>(rounds * slots);
+    if (eff > best_eff + 0.05) {
+      best = s;
+      best_eff = eff;
+    }
+  }
+  return best;
+}
+
 void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   const int64_t n = p->n, rl = p->r_lora, r = p->r;
   const int64_t fk = n * rl;
   const int64_t ntile = (fk + kBK - 1) / kBK;
-  const int64_t rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
-  // about two rounds of 256 workgroups per basis, at least 8 k-tiles each
-  int64_t split = std::max<int64_t>(1, std::min<int64_t>((512 + rowt - 1) / rowt, ntile / 8));
-  pl->split = static_cast<int>(std::max<int64_t>(1, split));
+  // the expansion's pieces of the collection: at most kMaxExpSplit (chosen
+  // per launch), at least 8 k-tiles each; the projection's pieces of d_in
+  // and d_out: two (measured: more pieces were slower at 1000 LoRAs, 4096 x
+  // 4096), one when a piece would have fewer than 8 k-tiles
+  pl->split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxExpSplit, ntile / 8)));
+  pl->pq_split = (std::min(p->d_in, p->d_out) + kBK - 1) / kBK >= 16 ? 2 : 1;
   pl->nblk_out = (p->d_out + kGramRows - 1) / kGramRows;
   pl->nblk_in = (p->d_in + kGramRows - 1) / kGramRows;
   pl->nblk = std::max(pl->nblk_out, pl->nblk_in);
@@ -1154,7 +1181,7 @@ void plan_jd(const cts_jd_problem* p, int K, JdPlan* pl) {
   pl->off_Vo = take(4ull * p->d_in * r);
   pl->off_C = take(4ull * fk * r);
   pl->off_D = take(4ull * fk * r);
-  pl->off_pq = take(4ull * kPqSplit * 2 * fk * r);
+  pl->off_pq = take(4ull * pl->pq_split * 2 * fk * r);
   pl->off_pU = take(4ull * pl->split * p->d_out * r);
   pl->off_pV = take(4ull * pl->split * p->d_in * r);
   pl->off_gp = take(4ull * 2 * std::max(pl->nblk, pl->nblk_n) * r * r);
@@ -1200,13 +1227,13 @@ hipError_t launch_project(const Jd& j, const float* A, const float* B, const flo
                           int zcount = 2, const float* sdiag = nullptr, float* wout = nullptr) {
   const cts_jd_problem* p = j.p;
   float* part = j.at<float>(j.pl.off_pq);
-  PqArgs pa{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, part, zbase};
-  ProjArgs a{lidx, m, p->r_lora, part, mode, sdiag, wout, w2, sscale, j.at<float>(j.pl.off_C),
+  PqArgs pa{A, B, V, U, lidx, m, p->r_lora, p->d_in, p->d_out, part, j.pl.pq_split, zbase};
+  ProjArgs a{lidx, m, p->r_lora, part, j.pl.pq_split, mode, sdiag, wout, w2, sscale, j.at<float>(j.pl.off_C),
              j.at<float>(j.pl.off_D), Sigma, score, ld_score, score_col};
   const int lpw = kTM / p->r_lora;
   const unsigned groups = static_cast<unsigned>((m + lpw - 1) / lpw);
   return with_nb(p->r, [&](auto c) {
-    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, zcount, kPqSplit), dim3(kJT), 0, j.st, pa);
+    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, zcount, j.pl.pq_split), dim3(kJT), 0, j.st, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(jd_combine_kernel<decltype(c)::value>, dim3(groups), dim3(kJT), 0, j.st, a);
@@ -1230,10 +1257,11 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   if (e != hipSuccess || (e = stage_mark(2, j.st)) != hipSuccess) return e;
   // expand, split so that the collection's share per workgroup is >= 8 k-tiles
   const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
-  const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
+  const int rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
+  const int split = pick_split(2LL * rowt, resident_wgs(r),
+                               static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8))));
   ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, j.at<float>(j.pl.off_C),
              j.at<float>(j.pl.off_D), split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), 0};
-  const int rowt = (std::max(p->d_out, p->d_in) + kTM - 1) / kTM;
   e = with_nb(r, [&](auto c) {
     hipLaunchKernelGGL(jd_expand_kernel<decltype(c)::value>, dim3(rowt, split, 2), dim3(kJT), 0, j.st, ea);
     return hipGetLastError();
@@ -1378,10 +1406,11 @@ hipError_t expand_one(Jd& j, const float* A, const float* B, const int32_t* lidx
   const cts_jd_problem* p = j.p;
   const int r = p->r;
   const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
-  const int split = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8)));
+  const int d = z ? p->d_in : p->d_out;
+  const int split = pick_split((d + kTM - 1) / kTM, resident_wgs(r),
+                               static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(j.pl.split, ntile / 8))));
   ExpArgs ea{A, B, lidx, m, p->r_lora, p->d_in, p->d_out, j.at<float>(j.pl.off_C), j.at<float>(j.pl.off_D),
              split, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), z};
-  const int d = z ? p->d_in : p->d_out;
   hipError_t e = with_nb(r, [&](auto c) {
     hipLaunchKernelGGL(jd_expand_kernel<decltype(c)::value>, dim3((d + kTM - 1) / kTM, split, 1), dim3(kJT), 0, j.st,
                        ea);
