@@ -322,16 +322,37 @@ __global__ __launch_bounds__(kJT) void jd_combine_kernel(const ProjArgs a) {
   float* Ps = smem;
   float* Qs = smem + kTM * kEpLd;
   {
+    // the pieces summed in order; every load of a piece is issued before any
+    // is used, and a half the mode does not read is not loaded
+    const bool need_p = a.mode != 4, need_q = a.mode != 3;
+    constexpr int EPT = kTM * r / kJT;                // elements per thread
     const int64_t rows_all = static_cast<int64_t>(a.m) * r_l;
     const float* base = a.part + static_cast<int64_t>(q0) * r_l * r;
-    for (int e = tid; e < rows * r; e += kJT) {
-      float p = 0.f, q = 0.f;
-      for (int ks = 0; ks < a.split; ++ks) {
-        p += base[(static_cast<int64_t>(ks) * 2) * rows_all * r + e];
-        q += base[(static_cast<int64_t>(ks) * 2 + 1) * rows_all * r + e];
+    float pv[EPT], qv[EPT];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) pv[u] = qv[u] = 0.f;
+    for (int ks = 0; ks < a.split; ++ks) {
+      const float* bp = base + (static_cast<int64_t>(ks) * 2) * rows_all * r;
+      const float* bq = bp + rows_all * r;
+      float lp[EPT], lq[EPT];
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + u * kJT;
+        const bool in = e < rows * r;
+        lp[u] = (in && need_p) ? bp[e] : 0.f;
+        lq[u] = (in && need_q) ? bq[e] : 0.f;
       }
-      Ps[(e / r) * kEpLd + e % r] = p;
-      Qs[(e / r) * kEpLd + e % r] = q;
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) {
+        pv[u] += lp[u];
+        qv[u] += lq[u];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const int e = tid + u * kJT;
+      Ps[(e / r) * kEpLd + e % r] = pv[u];
+      Qs[(e / r) * kEpLd + e % r] = qv[u];
     }
   }
   __syncthreads();
