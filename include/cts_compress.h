@@ -31,7 +31,7 @@
  * after its expansion kernel (the sums over the collection); the last
  * iteration's records are the ones left.  cts_jd_diag records the same
  * three events around its U step's projection (P_i = A_i V, C_i = P_i S_i)
- * and expansion (sum_i B_i C_i).
+ * and expansion kernel (sum_i B_i C_i, before the sum of its pieces).
  */
 #ifndef CTS_COMPRESS_H
 #define CTS_COMPRESS_H

@@ -1422,8 +1422,11 @@ hipError_t apply_one(Jd& j, float* X, int d, int z, const float* M2) {
   });
 }
 
-// one half of the expansion (z = 0: U' = sum B_i C_i into Uo; 1: V' = sum A_i^T D_i into Vo)
-hipError_t expand_one(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, int z, float* out) {
+// one half of the expansion (z = 0: U' = sum B_i C_i into Uo; 1: V' = sum A_i^T D_i into Vo);
+// mark > 0 records that profiling event between the expansion kernel and the
+// sum of its pieces
+hipError_t expand_one(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, int z, float* out,
+                      int mark = 0) {
   const cts_jd_problem* p = j.p;
   const int r = p->r;
   const int64_t ntile = (static_cast<int64_t>(m) * p->r_lora + kBK - 1) / kBK;
@@ -1437,7 +1440,7 @@ hipError_t expand_one(Jd& j, const float* A, const float* B, const int32_t* lidx
                        ea);
     return hipGetLastError();
   });
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || (mark > 0 && (e = stage_mark(mark, j.st)) != hipSuccess)) return e;
   const int64_t nel = static_cast<int64_t>(d) * r;
   hipLaunchKernelGGL(jd_reduce_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (nel + kJT - 1) / kJT)), 1),
                      dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out, p->d_in,
@@ -1486,8 +1489,7 @@ hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx,
                             nullptr)) != hipSuccess)
       return e;
     if ((e = stage_mark(2, j.st)) != hipSuccess) return e;
-    if ((e = expand_one(j, A, B, lidx, p->n, 0, Un)) != hipSuccess) return e;
-    if ((e = stage_mark(3, j.st)) != hipSuccess) return e;
+    if ((e = expand_one(j, A, B, lidx, p->n, 0, Un, 3)) != hipSuccess) return e;
     if ((e = gram_hadamard_inverse(j, V, p->d_in, sd, p->n, m + 4 * rr)) != hipSuccess) return e;
     if ((e = apply_one(j, Un, p->d_out, 0, m + 4 * rr)) != hipSuccess) return e;
     std::swap(j.pl.off_U, j.pl.off_Uo);
