@@ -665,10 +665,15 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // ---- dense k range of this split ----------------------------------------
   const int nk0 = (K0 > 0) ? (K0 + BK - 1) / BK : 0;
   const int nk1 = (K1 > 0) ? (K1 + BK - 1) / BK : 0;
-  int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0;
+  // With a dense phase, split ks takes its share of the dense k-tiles and the
+  // cluster runs ks, ks + S, ks + 2S, ... (all of each run's k-tiles), so the
+  // adapter phase is spread over the splits; without one, the splits share
+  // the segment's k-tiles.
+  int d_lo = 0, d_hi = 0, s_lo = 0, s_hi = 0, q_first = 0, q_step = 1;
   if (nk0 > 0) {
     d_lo = split_lo(nk0, ks, S); d_hi = split_lo(nk0, ks + 1, S);
-    if (ks == 0) { s_lo = 0; s_hi = nk1; }
+    s_lo = 0; s_hi = nk1;
+    q_first = ks; q_step = S;
   } else {
     s_lo = split_lo(nk1, ks, S); s_hi = split_lo(nk1, ks + 1, S);
   }
@@ -723,21 +728,23 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   if (!(p.sorted_seg && K1 > 0)) n_runs = 0;
   if (tid == 0) run_start[n_runs] = jn;
   __syncthreads();
+  // this split's runs: q_first + i q_step, i < my_runs
+  const int my_runs = (n_runs > q_first) ? (n_runs - q_first + q_step - 1) / q_step : 0;
 
   // ---- k-tile schedule: the dense tiles, then each cluster run's tiles ------
   // With ranks, run q takes only its k-tiles of this split below its rank
   // (the k-tiles past a cluster's rank are not visited).  Wave 0 lists the
   // adapter k-tiles in LDS, run by run: .x = first column | columns << 9 |
   // k-tile << 18, .y = segment | rank << 16.
-  int n_sched = n_runs * ns;
-  if (RANKED && n_runs > 0 && ns > 0) {
+  int n_sched = my_runs * ns;
+  if (RANKED && my_runs > 0 && ns > 0) {
     if (wave == 0) {
       int tot = 0;
-      for (int base = 0; base < n_runs; base += 64) {
-        const int q = base + lane;
+      for (int base = 0; base < my_runs; base += 64) {
+        const int q = q_first + (base + lane) * q_step;
         int c = 0;
         uint32_t ex = 0, ey = 0;
-        if (q < n_runs) {
+        if (base + lane < my_runs) {
           const int lo = run_start[q], hi = run_start[q + 1];
           const int seg = t_seg[lo];
           const int kl = min(max(t_rank[lo], 0), K1);
@@ -808,7 +815,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     uint32_t kk, kmask, span, dsel;   // kk: uniform k byte offset of the k-tile
     int lo;
   };
-  auto prep_next = [&, jn, n_runs, n_sched, nd, ntiles, s_lo, s_hi]() __attribute__((always_inline)) {
+  auto prep_next = [&, jn, n_runs, n_sched, nd, ntiles, s_lo, s_hi, q_first, q_step]() __attribute__((always_inline)) {
     TileLoad L;
     const bool valid = lt < ntiles;
     uint32_t k0, klim;
@@ -840,7 +847,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       ++lq;
     } else {
       // adapter phase (U_k Z'): one cluster run of the tile per k-tile group
-      const int q = min(lq, max(n_runs - 1, 0));
+      const int q = min(q_first + lq * q_step, max(n_runs - 1, 0));
       L.lo = run_start[q];
       const int hi = run_start[q + 1];
       const int seg = __builtin_amdgcn_readfirstlane(t_seg[L.lo]);
