@@ -31,12 +31,36 @@ struct Plan {
   int main_split, shrink_split;
   int max_items, max_ctiles;
   size_t off_perm, off_seg, off_aid, off_srank, off_offs, off_items, off_nitems, off_ctiles, off_nctiles,
-      off_zpart, off_zp, off_ypart, total;
+      off_ssplit, off_zpart, off_zp, off_ypart, total;
 };
 
 constexpr uint64_t kMaxOperandBytes = 0x7fffffffull;   // buffer-load offsets are 31-bit
 
 int ceil_div(int64_t a, int64_t b) { return static_cast<int>((a + b - 1) / b); }
+
+// The shrink's split along d_in for `rank` rank rows.  When the tiles come
+// from the separate sort (bf16, T > kFuseSortMaxT) the split follows the
+// tile count on the device: 512 workgroups, at least 8 k-tiles each, and
+// this returns the most it could use (the split for the fewest tiles,
+// ceil(T / 64)).  Otherwise (fp32, or the bucketing inside the shrink) it is
+// fixed: 256 (bf16) or 512 (fp32) workgroups over an estimate of the tiles
+// (token tiles plus half of the possible segment starts), at least 2
+// k-tiles each.
+constexpr int kShrinkAdaptiveTarget = 512;
+
+bool shrink_adaptive(int T, Tile t) { return t == Tile::Shrink && T > cts::kFuseSortMaxT; }
+
+int shrink_split_of(int T, int rank, int nseg, int d_in, Tile t) {
+  int BM, BN, BK;
+  cts::tile_dims(t, &BM, &BN, &BK);
+  const bool adaptive = shrink_adaptive(T, t);
+  const int expect = ceil_div(std::max(T, 1), BN) + (adaptive ? 0 : std::min(nseg, std::max(T, 1)) / 2);
+  const int tiles = ceil_div(rank, BM) * std::max(expect, 1);
+  const int nk = ceil_div(d_in, BK);
+  const int target = adaptive ? kShrinkAdaptiveTarget : (t == Tile::F32 ? 512 : 256);
+  const int kmin = adaptive ? 8 : 2;
+  return std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / kmin)), 64));
+}
 
 // Validates the sizes of `p` for the compressed (compressed=true) or the
 // uncompressed path and fills the launch plan.  Pure host arithmetic.
@@ -107,17 +131,14 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   }
   // shrink: one workgroup per (cluster segment tile of <= kSegTile tokens,
   // 64 rank rows), split along d_in so that about 256 (bf16) or 512 (fp32)
-  // workgroups run; the Sigma stage sums the split partials
+  // workgroups run; the Sigma stage sums the split partials.  The bf16
+  // shrink takes its split from the tile count on the device (at most
+  // shrink_split, the split for the fewest tiles T can make); the fp32 one
+  // from an estimate of the tile count.
   pl->shrink_tile = (p->dtype == CTS_F32) ? Tile::F32 : Tile::Shrink;
   cts::tile_dims(pl->shrink_tile, &BM, &BN, &BK);
   pl->max_ctiles = cts::max_seg_tiles(T, pl->nseg);
-  {
-    const int expect = ceil_div(std::max(T, 1), BN) + std::min(pl->nseg, std::max(T, 1)) / 2;
-    const int tiles = ceil_div(pl->rank, BM) * std::max(expect, 1);
-    const int nk = ceil_div(p->d_in, BK);
-    const int target = (p->dtype == CTS_F32) ? 512 : 256;
-    pl->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 64));
-  }
+  pl->shrink_split = shrink_split_of(T, pl->rank, pl->nseg, p->d_in, pl->shrink_tile);
   pl->max_items = cts::max_sigma_items(T, p->n_adapters);
 
   // every operand a kernel reads through a buffer resource must stay below 2^31 bytes
@@ -139,6 +160,7 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   pl->off_nitems = off; off = align_up(off + 4);
   pl->off_ctiles = off; off = align_up(off + 4ull * (pl->max_ctiles + 1));
   pl->off_nctiles = off; off = align_up(off + 4);
+  pl->off_ssplit = off; off = align_up(off + 4);
   pl->off_zpart = off; off = align_up(off + 4ull * pl->shrink_split * T * pl->rank);
   pl->off_zp = off;    off = align_up(off + static_cast<size_t>(pl->elt) * T * pl->rank);
   pl->off_ypart = off;
@@ -219,6 +241,11 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = pl.shrink_split; g.part = zpart;
   g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  int32_t* ssplit = nullptr;
+  if (shrink_adaptive(T, pl.shrink_tile)) {
+    ssplit = reinterpret_cast<int32_t*>(ws + pl.off_ssplit);
+    g.split_target = kShrinkAdaptiveTarget; g.split_out = ssplit;
+  }
   if (fuse_sort) {
     g.tile_start = nullptr; g.n_tiles = nullptr;
     g.fs_adapter = adapter_id; g.fs_cluster = compressed ? cluster_of : nullptr;
@@ -233,7 +260,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
 
   e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
                         pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag,
-                        sseg, seg_rank, seg_rank ? srank : nullptr);
+                        sseg, seg_rank, seg_rank ? srank : nullptr, 0, ssplit);
   if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
@@ -391,15 +418,7 @@ int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan
   mp->rtot = M * p->r;
   if (static_cast<uint64_t>(mp->rtot) * p->d_in * p0.elt > kMaxOperandBytes) return CTS_ERR_UNSUPPORTED;
   // shrink over the stacked rank: as for one module, with M r rank rows
-  int BM, BN, BK;
-  cts::tile_dims(p0.shrink_tile, &BM, &BN, &BK);
-  {
-    const int expect = ceil_div(std::max(T, 1), BN) + std::min(p0.nseg, std::max(T, 1)) / 2;
-    const int tiles = ceil_div(mp->rtot, BM) * std::max(expect, 1);
-    const int nk = ceil_div(p->d_in, BK);
-    const int target = (p->dtype == CTS_F32) ? 512 : 256;
-    mp->shrink_split = std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / 2)), 64));
-  }
+  mp->shrink_split = shrink_split_of(T, mp->rtot, p0.nseg, p->d_in, p0.shrink_tile);
   size_t off = p0.off_zpart;                        // the shared sort arrays of module 0's layout
   mp->off_zpart = off; off = align_up(off + 4ull * mp->shrink_split * T * mp->rtot);
   mp->off_zp = off;    off = align_up(off + static_cast<size_t>(p0.elt) * T * mp->rtot);
@@ -453,6 +472,11 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = mp.shrink_split; g.part = zpart;
   g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  int32_t* ssplit = nullptr;
+  if (shrink_adaptive(T, pl.shrink_tile)) {
+    ssplit = reinterpret_cast<int32_t*>(ws + pl.off_ssplit);
+    g.split_target = kShrinkAdaptiveTarget; g.split_out = ssplit;
+  }
   if (fuse_sort) {
     g.tile_start = nullptr; g.n_tiles = nullptr;
     g.fs_adapter = adapter_id; g.fs_cluster = cluster_of;
@@ -469,7 +493,7 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   for (int m = 0; m < mp.M; ++m) {
     e = cts::launch_sigma(zpart + static_cast<int64_t>(m) * r, mp.shrink_split, T, r, said, p->n_adapters, items,
                           n_items, pl.max_items, Sigma[m], zp + static_cast<size_t>(m) * r * pl.elt, p->dtype,
-                          stream, false, sseg, nullptr, nullptr, rt);
+                          stream, false, sseg, nullptr, nullptr, rt, ssplit);
     if (e != hipSuccess) return CTS_ERR_HIP;
   }
   if (mark(3, stream) != hipSuccess) return CTS_ERR_HIP;

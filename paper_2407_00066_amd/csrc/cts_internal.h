@@ -101,6 +101,12 @@ struct GemmParams {
   const int32_t* fs_adapter; const int32_t* fs_cluster;   // fs_cluster null: key = adapter
   int fs_n, fs_K, fs_bits_n;
   int32_t* fs_perm; int32_t* fs_seg; int32_t* fs_aid; int32_t* fs_items; int32_t* fs_nitems;
+  // token-tile mode of the LDS-ring tiles: split_target > 0 makes the split
+  // along k follow the tile count n known on the device: S = min(ksplit,
+  // ceil(split_target / (ceil(M / BM) n))) pieces.  The grid is then sized
+  // ceil(M / BM) max_tiles + split_target (enough for every n) and workgroup
+  // 0 writes S to split_out[0] for the core-product stage.
+  int split_target; int32_t* split_out;
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide
@@ -136,7 +142,7 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag = false, const int32_t* sorted_seg = nullptr,
                         const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr,
-                        int ldz = 0);
+                        int ldz = 0, const int32_t* split_dev = nullptr);
 
 // Records stage event i of the profiling aid (cts_set_stage_events) on s when
 // it is on; a no-op otherwise.

@@ -110,10 +110,11 @@ __device__ __forceinline__ int split_lo(int n, int ks, int S) { return (int)((in
 // grid size.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
-__device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, int* ks) {
+__device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, int* ks, int nb_used = 0) {
   const int b = blockIdx.x;
   const int nb_mn = gm * gn;
-  const int nb = static_cast<int>(gridDim.x);       // nb_mn * ksplit
+  // nb_mn * ksplit workgroups (the grid, or its first nb_used)
+  const int nb = nb_used > 0 ? nb_used : static_cast<int>(gridDim.x);
   const int q = nb / kXcds, rem = nb % kXcds;
   const int x = b % kXcds, i = b / kXcds;
   const int L = x * q + min(x, rem) + i;
@@ -592,7 +593,25 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   // so the whole k loop takes the dense load path and there is no second phase.
   const bool tlist = FSORT || p.tile_start != nullptr;
   int mt, nt, ks;
-  tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  int s_pieces = p.ksplit;
+  // the split along k follows the tile count only in the shrink's tile shape
+  // (64 x 64 x 64); the other shapes keep the straight mapping
+  constexpr bool kAdaptive = BM == 64 && BN == 64 && BK == 64;
+  if (kAdaptive && tlist && p.split_target > 0) {
+    // workgroups [0, gm n S) take the (row tile, tile, piece) triples, the
+    // rest exit (whole workgroup, after every barrier above)
+    const int gm = (p.M + BM - 1) / BM;
+    const int ntl = FSORT ? fs_cnt[0] : p.n_tiles[0];
+    const int per = max(gm * ntl, 1);
+    s_pieces = min(max((p.split_target + per - 1) / per, 1), p.ksplit);
+    if (blockIdx.x == 0 && tid == 0 && p.split_out) p.split_out[0] = s_pieces;
+    const int used = gm * ntl * s_pieces;
+    if (static_cast<int>(blockIdx.x) >= used) return;
+    tile_of_block(gm, ntl, &mt, &nt, &ks, used);
+  } else {
+    tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks);
+  }
+  const int S = s_pieces;
   int j0, jn;
   if (tlist) {
     // whole workgroup, after every barrier above
@@ -617,7 +636,6 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     K1 = 0;
   }
   const int m0 = mt * BM;
-  const int S = p.ksplit;
   static_assert(BN <= C::NT, "one token column per thread");
 
   // ---- token columns of this tile (loads only; stored to LDS below) -------
@@ -1132,6 +1150,13 @@ template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0,
 hipError_t launch_dma1(const GemmParams& p, hipStream_t stream) {
   const int gn = (p.tile_start || FSORT) ? p.max_tiles : (p.N + BN - 1) / BN;
   dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
+  if ((p.tile_start || FSORT) && p.split_target > 0) {
+    if (!(BM == 64 && BN == 64 && BK == 64)) return hipErrorInvalidValue;   // no adaptive split here
+    // gm n S workgroups are used: fewer than gm max_tiles + split_target, and
+    // at most gm max_tiles ksplit
+    const int64_t gmt = (p.M + BM - 1) / BM;
+    grid = dim3(static_cast<unsigned>(std::min<int64_t>(gmt * gn + p.split_target, gmt * gn * p.ksplit)));
+  }
   hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT, RANKED>),
                      grid, dim3(WM * WN * 64), 0, stream, p);
   return hipGetLastError();

@@ -62,9 +62,11 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
                                                                  TI* __restrict__ zp,
                                                                  const int32_t* __restrict__ sorted_seg,
                                                                  const int32_t* __restrict__ seg_rank,
-                                                                 int32_t* __restrict__ sorted_rank) {
+                                                                 int32_t* __restrict__ sorted_rank,
+                                                                 const int32_t* __restrict__ split_dev) {
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
+  if (split_dev) S = min(split_dev[0], S);
   const int tid = threadIdx.x;
   const int lo = items[item], hi = items[item + 1];
   const int cnt = (hi - lo) * r;
@@ -107,13 +109,16 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             TI* __restrict__ zp,
                                                             const int32_t* __restrict__ sorted_seg,
                                                             const int32_t* __restrict__ seg_rank,
-                                                            int32_t* __restrict__ sorted_rank, int ldz) {
+                                                            int32_t* __restrict__ sorted_rank, int ldz,
+                                                            const int32_t* __restrict__ split_dev) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
 
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
+  // pieces the shrink actually split the reduction into (at most S)
+  if (split_dev) S = min(split_dev[0], S);
   const int tid = threadIdx.x;
   const int lo = items[item], hi = items[item + 1];
   const int nt = hi - lo;                 // tokens of this item (<= kSigmaChunk), one adapter
@@ -245,7 +250,7 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag, const int32_t* sorted_seg, const int32_t* seg_rank,
-                        int32_t* sorted_rank, int ldz) {
+                        int32_t* sorted_rank, int ldz, const int32_t* split_dev) {
   if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
   if (sorted_rank && !seg_rank) return hipErrorInvalidValue;
   if (ldz <= 0) ldz = r;
@@ -255,30 +260,30 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
     if (in_dtype == 0)
       hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                         static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank);
+                         static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev);
     else
       hipLaunchKernelGGL(sigma_diag_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank);
+                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev);
     return hipGetLastError();
   }
   if (r > 128) return hipErrorInvalidValue;
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
   return hipGetLastError();
 }
 
