@@ -243,6 +243,31 @@ def test_out_of_range_ids_do_not_fault(small_cases):
     assert torch.isfinite(y.float()).all()
 
 
+def test_shrink_split_follows_tile_count(oracle_mod):
+    """The shrink splits d_in by the tile count found on the device, and the
+    core-product stage sums exactly that many pieces: a call with many tiles
+    (one split piece) after a call with few (eight pieces) on the same
+    workspace must not pick up the earlier call's stale partials."""
+    T, d_in, d_out, n, r_l = 600, 4096, 64, 600, 16
+    w = wl.synthetic("split_reuse", cfg=116, T=T, d_in=d_in, d_out=d_out, r=16, n=n, K=1, r_l=r_l)
+    x, W, A, B = dev(w.x), dev(w.W), dev(w.A), dev(w.B)
+    p = cts.make_problem(T, d_in, d_out, 16, n, 1, r_l, cts.CTS_BF16, cts.CTS_BF16)
+    ws = torch.zeros(cts.workspace_size(p, compressed=False), dtype=torch.uint8, device="cuda")
+    few = np.zeros(T, np.int32)                       # one adapter: 10 tiles
+    many = np.arange(T, dtype=np.int32)               # 600 adapters: 600 tiles
+    say("shrink split reuse T=%d d_in=%d n=%d" % (T, d_in, n))
+    y_few = cts.apply_uncompressed(x, dev(few), W, A, B, workspace=ws)
+    y_many = cts.apply_uncompressed(x, dev(many), W, A, B, workspace=ws)
+    torch.cuda.synchronize()
+    for ids, y in ((few, y_few), (many, y_many)):
+        ref = oracle_mod.apply_uncompressed(w.x, ids, w.W, w.A, w.B)
+        assert row_rel_err(host(y), ref) <= TOL["bf16"]
+    ws.zero_()
+    y_fresh = cts.apply_uncompressed(x, dev(many), W, A, B, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y_fresh, y_many)
+
+
 # --------------------------------------------------------------------------
 # full-size workloads: sampled tokens
 
