@@ -313,9 +313,19 @@ def bench_jd(args, torch, np, cts, B, device):
     mk = 1e3 * sum(e[3].elapsed_time(e[4]) for e in evs) / args.steps
     proj_us = 1e3 * sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps - mk
     exp_us = 1e3 * sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps - mk
+    # the expansion's pieces of the collection, as the library picks them:
+    # the fewest that fill the resident slots (256 CUs x 3 workgroups at
+    # r = 64) within 5%, at most 16 and at least 8 k-tiles each
     rowt = (d + 63) // 64
     ntile = (n * r_l + 31) // 32
-    split = max(1, min((512 + rowt - 1) // rowt, ntile // 8))
+    occ = 4 if r <= 32 else (3 if r <= 64 else 2)
+    base = rowt * (1 if diag else 2)
+    split, best = 1, 0.0
+    for s_ in range(1, max(1, min(16, ntile // 8)) + 1):
+        w_ = base * s_
+        eff = w_ / (-(-w_ // (256 * occ)) * 256 * occ)
+        if eff > best + 0.05:
+            split, best = s_, eff
     if diag:
         (pf, pb), (ef, eb_) = jd_diag_kernel_models(n, d, d, r_l, r, split)
         if exp_us >= proj_us:

@@ -30,8 +30,10 @@
  * kernels (P_i = A_i V, Q_i = B_i^T U, then the per-LoRA products) and [3]
  * after its expansion kernel (the sums over the collection); the last
  * iteration's records are the ones left.  cts_jd_diag records the same
- * three events around its U step's projection (P_i = A_i V, C_i = P_i S_i)
- * and expansion kernel (sum_i B_i C_i, before the sum of its pieces).
+ * three events around its U step's projection (C_i = P_i S_i; P_i = A_i V
+ * comes from the preceding diagonal step unless the normalization rescaled
+ * V since) and expansion kernel (sum_i B_i C_i, before the sum of its
+ * pieces).
  */
 #ifndef CTS_COMPRESS_H
 #define CTS_COMPRESS_H

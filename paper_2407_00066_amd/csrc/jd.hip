@@ -1240,8 +1240,9 @@ struct Jd {
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
 };
 
-// P = A_i V and/or Q = B_i^T U (zbase, zcount: halves 0 = P, 1 = Q), then
-// the per-LoRA products of `mode` (see jd_combine_kernel).
+// P = A_i V and/or Q = B_i^T U (zbase, zcount: halves 0 = P, 1 = Q; zcount
+// 0: neither, the partials already hold them), then the per-LoRA products of
+// `mode` (see jd_combine_kernel).
 hipError_t launch_project(const Jd& j, const float* A, const float* B, const float* V, const float* U,
                           const int32_t* lidx, int m, int mode, const float* w2, const float* sscale,
                           float* Sigma, float* score, int ld_score, int score_col, int zbase = 0,
@@ -1254,9 +1255,12 @@ hipError_t launch_project(const Jd& j, const float* A, const float* B, const flo
   const int lpw = kTM / p->r_lora;
   const unsigned groups = static_cast<unsigned>((m + lpw - 1) / lpw);
   return with_nb(p->r, [&](auto c) {
-    hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, zcount, j.pl.pq_split), dim3(kJT), 0, j.st, pa);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (zcount > 0) {
+      hipLaunchKernelGGL(jd_pq_kernel<decltype(c)::value>, dim3(groups, zcount, j.pl.pq_split), dim3(kJT), 0, j.st,
+                         pa);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     hipLaunchKernelGGL(jd_combine_kernel<decltype(c)::value>, dim3(groups), dim3(kJT), 0, j.st, a);
     return hipGetLastError();
   });
@@ -1471,8 +1475,11 @@ hipError_t als_sigma(Jd& j, const float* A, const float* B, const int32_t* lidx,
 }
 
 // one sweep: U, then V (with the new U), then the diagonals, then the
-// optional normalization
-hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx, bool normalize) {
+// optional normalization.  p_current: the projection partials of P = A_i V
+// are those of the current V (the diagonal step before this sweep computed
+// them, and no normalization has rescaled V since); the U step then only
+// forms C_i = P_i S_i from them.
+hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx, bool normalize, bool p_current) {
   const cts_jd_problem* p = j.p;
   const int r = p->r;
   const int64_t rr = static_cast<int64_t>(r) * r;
@@ -1485,8 +1492,8 @@ hipError_t als_sweep(Jd& j, const float* A, const float* B, const int32_t* lidx,
     float* V = j.at<float>(j.pl.off_V);
     float* Un = j.at<float>(j.pl.off_Uo);
     if ((e = stage_mark(1, j.st)) != hipSuccess) return e;
-    if ((e = launch_project(j, A, B, V, U, lidx, p->n, 3, nullptr, nullptr, nullptr, nullptr, 0, 0, 0, 1, sd,
-                            nullptr)) != hipSuccess)
+    if ((e = launch_project(j, A, B, V, U, lidx, p->n, 3, nullptr, nullptr, nullptr, nullptr, 0, 0, 0,
+                            p_current ? 0 : 1, sd, nullptr)) != hipSuccess)
       return e;
     if ((e = stage_mark(2, j.st)) != hipSuccess) return e;
     if ((e = expand_one(j, A, B, lidx, p->n, 0, Un, 3)) != hipSuccess) return e;
@@ -1603,8 +1610,11 @@ int cts_jd_diag(const cts_jd_problem* p, const float* A, const float* B, const f
   if (hipGetLastError() != hipSuccess) return CTS_ERR_HIP;
   if (cts::load_bases(j, U0, Vt0) != hipSuccess) return CTS_ERR_HIP;
   if (cts::als_sigma(j, A, B, lidx, true) != hipSuccess) return CTS_ERR_HIP;
+  // P = A_i V from the initial diagonals' step is current for the first U
+  // step, and so is each sweep's diagonal step's P for the next one (V is
+  // unchanged between them unless the normalization rescaled it)
   for (int t = 0; t < sweeps; ++t)
-    if (cts::als_sweep(j, A, B, lidx, normalize != 0) != hipSuccess) return CTS_ERR_HIP;
+    if (cts::als_sweep(j, A, B, lidx, normalize != 0, t == 0 || normalize == 0) != hipSuccess) return CTS_ERR_HIP;
   if (cts::store_bases(j, U, Vt) != hipSuccess) return CTS_ERR_HIP;
   if (hipMemcpyAsync(sigma, j.at<float>(j.pl.off_sd), sizeof(float) * p->n * p->r, hipMemcpyDeviceToDevice,
                      j.st) != hipSuccess)
