@@ -110,7 +110,15 @@ struct LoadLoraBtP {
 // U' = sum B_i C_i: rows m = output row o, k = flat (LoRA, l) index f; a
 // LoRA's 64 x w block (w = min(r_l, 32) columns from l0) is read row by row.
 // LoRA q of the list is ids[q - id0] (ids: the workgroup's slice of the list
-// staged in LDS, or the list itself); r_l = 1 << lg.
+// staged in LDS when kLds, read with LDS loads, else the list itself);
+// r_l = 1 << lg.
+template <bool kLds>
+__device__ __forceinline__ int list_id(const int32_t* ids, int i) {
+  if constexpr (kLds) return ((const __attribute__((address_space(3))) int32_t*)ids)[i];
+  return ids[i];
+}
+
+template <bool kLds>
 struct LoadExpandB {
   const float* B; const int32_t* ids; int id0, lg, r_l, d_out, o0, f_end;
   __device__ float4 operator()(int, int e, int k0, int& off) const {
@@ -122,12 +130,13 @@ struct LoadExpandB {
     const int o = o0 + m;
     if (f >= f_end || o >= d_out) return float4{0.f, 0.f, 0.f, 0.f};
     const int q = f >> lg, l = f & (r_l - 1);
-    const int64_t base = static_cast<int64_t>(ids[q - id0]) * d_out * r_l;
+    const int64_t base = static_cast<int64_t>(list_id<kLds>(ids, q - id0)) * d_out * r_l;
     return *reinterpret_cast<const float4*>(B + base + static_cast<int64_t>(o) * r_l + l);
   }
 };
 
 // V' = sum A_i^T D_i: k = flat (LoRA, l), m = input column c.
+template <bool kLds>
 struct LoadExpandA {
   const float* A; const int32_t* ids; int id0, lg, r_l, d_in, c0, f_end;
   __device__ float4 operator()(int, int e, int k0, int& off) const {
@@ -136,7 +145,7 @@ struct LoadExpandA {
     const int f = k0 + kk, c = c0 + 4 * m4;
     if (f >= f_end || c >= d_in) return float4{0.f, 0.f, 0.f, 0.f};
     const int q = f >> lg, l = f & (r_l - 1);
-    const int64_t row = static_cast<int64_t>(ids[q - id0]) * r_l + l;
+    const int64_t row = static_cast<int64_t>(list_id<kLds>(ids, q - id0)) * r_l + l;
     return *reinterpret_cast<const float4*>(A + row * d_in + c);
   }
 };
@@ -481,22 +490,24 @@ __global__ __launch_bounds__(kJT) void jd_expand_kernel(const ExpArgs a) {
   __shared__ int32_t s_ids[kExpIds];
   const int lg = __builtin_ctz(a.r_l);
   const int q_lo = f_lo >> lg, nids = ((f_hi + a.r_l - 1) >> lg) - q_lo;
-  const int32_t* ids = a.lidx;
-  int id0 = 0;
+  f32x4 acc[NB];
+  zero_acc(acc);
   if (nids <= kExpIds) {
     for (int i = threadIdx.x; i < nids; i += kJT) s_ids[i] = a.lidx[q_lo + i];
     __syncthreads();
-    ids = s_ids;
-    id0 = q_lo;
-  }
-  f32x4 acc[NB];
-  zero_acc(acc);
-  if (isv)
-    tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA{a.A, ids, id0, lg, a.r_l, a.d_in, row0, f_hi},
+    if (isv)
+      tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA<true>{a.A, s_ids, q_lo, lg, a.r_l, a.d_in, row0, f_hi},
+                          LoadRowsR{a.D, r, f_hi}, acc);
+    else
+      tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB<true>{a.B, s_ids, q_lo, lg, a.r_l, a.d_out, row0, f_hi},
+                           LoadRowsR{a.C, r, f_hi}, acc);
+  } else if (isv) {
+    tile_gemm<NB, true>(smem, f_lo, f_hi, LoadExpandA<false>{a.A, a.lidx, 0, lg, a.r_l, a.d_in, row0, f_hi},
                         LoadRowsR{a.D, r, f_hi}, acc);
-  else
-    tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB{a.B, ids, id0, lg, a.r_l, a.d_out, row0, f_hi},
+  } else {
+    tile_gemm<NB, false>(smem, f_lo, f_hi, LoadExpandB<false>{a.B, a.lidx, 0, lg, a.r_l, a.d_out, row0, f_hi},
                          LoadRowsR{a.C, r, f_hi}, acc);
+  }
   float* part = (isv ? a.partV : a.partU) + static_cast<int64_t>(s) * d * r;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fq = lane >> 4;
