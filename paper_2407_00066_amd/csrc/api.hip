@@ -489,13 +489,10 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   e = cts::launch_seg_gemm(g, p->dtype, pl.shrink_tile, stream);
   if (e != hipSuccess || mark(2, stream) != hipSuccess) return CTS_ERR_HIP;
 
-  // core product per module on its slice of Z (rows M r apart)
-  for (int m = 0; m < mp.M; ++m) {
-    e = cts::launch_sigma(zpart + static_cast<int64_t>(m) * r, mp.shrink_split, T, r, said, p->n_adapters, items,
-                          n_items, pl.max_items, Sigma[m], zp + static_cast<size_t>(m) * r * pl.elt, p->dtype,
-                          stream, false, sseg, nullptr, nullptr, rt, ssplit);
-    if (e != hipSuccess) return CTS_ERR_HIP;
-  }
+  // core product of every module on its slice of Z (rows M r apart), one launch
+  e = cts::launch_sigma(zpart, mp.shrink_split, T, r, said, p->n_adapters, items, n_items, pl.max_items, Sigma[0],
+                        zp, p->dtype, stream, false, sseg, nullptr, nullptr, rt, ssplit, Sigma, mp.M);
+  if (e != hipSuccess) return CTS_ERR_HIP;
   if (mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   // fused W_m X + U_k^(m) Z'^(m) per module

@@ -142,7 +142,8 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag = false, const int32_t* sorted_seg = nullptr,
                         const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr,
-                        int ldz = 0, const int32_t* split_dev = nullptr);
+                        int ldz = 0, const int32_t* split_dev = nullptr,
+                        const void* const* sigmas = nullptr, int nmod = 0);
 
 // Records stage event i of the profiling aid (cts_set_stage_events) on s when
 // it is on; a no-op otherwise.

@@ -11,6 +11,7 @@
 // z_t is first summed over the shrink's k-splits in fixed order.  No atomics:
 // the result is bitwise reproducible.  With Sigma == null (uncompressed path)
 // the stage only sums and converts.
+#include "cts.h"
 #include "cts_internal.h"
 
 namespace cts {
@@ -99,6 +100,13 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
   }
 }
 
+// Several modules in one launch (blockIdx.y = module m): module m's Sigma
+// is sigma[m], and its z and z' are the columns [m r, m r + r) of rows ldz
+// apart.
+struct SigmaMods {
+  const void* sigma[CTS_MAX_MODULES];
+};
+
 template <typename TI, int MAXR>
 __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restrict__ zpart, int S,
                                                             int T, int r,
@@ -110,13 +118,20 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             const int32_t* __restrict__ sorted_seg,
                                                             const int32_t* __restrict__ seg_rank,
                                                             int32_t* __restrict__ sorted_rank, int ldz,
-                                                            const int32_t* __restrict__ split_dev) {
+                                                            const int32_t* __restrict__ split_dev,
+                                                            const SigmaMods mods, int nmod) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
 
   const int item = blockIdx.x;
   if (item >= n_items[0]) return;
+  if (nmod > 0) {
+    const int m = blockIdx.y;
+    Sigma = static_cast<const TI*>(mods.sigma[m]);
+    zpart += static_cast<int64_t>(m) * r;
+    zp += static_cast<int64_t>(m) * r;
+  }
   // pieces the shrink actually split the reduction into (at most S)
   if (split_dev) S = min(split_dev[0], S);
   const int tid = threadIdx.x;
@@ -250,12 +265,17 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const int32_t* items, const int32_t* n_items, int max_items,
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag, const int32_t* sorted_seg, const int32_t* seg_rank,
-                        int32_t* sorted_rank, int ldz, const int32_t* split_dev) {
+                        int32_t* sorted_rank, int ldz, const int32_t* split_dev,
+                        const void* const* sigmas, int nmod) {
   if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
   if (sorted_rank && !seg_rank) return hipErrorInvalidValue;
   if (ldz <= 0) ldz = r;
   if (ldz != r && (diag || ldz < r || ldz % 4)) return hipErrorInvalidValue;
-  dim3 grid(max_items);
+  if (nmod < 0 || nmod > CTS_MAX_MODULES || (nmod > 0 && (!sigmas || diag || ldz < nmod * r)))
+    return hipErrorInvalidValue;
+  SigmaMods mods{};
+  for (int m = 0; m < nmod; ++m) mods.sigma[m] = sigmas[m];
+  dim3 grid(max_items, nmod > 0 ? nmod : 1);
   if (diag && Sigma) {
     if (in_dtype == 0)
       hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
@@ -271,19 +291,19 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
   return hipGetLastError();
 }
 
