@@ -82,3 +82,48 @@ def test_graph_replay_sort_outputs():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(perm, perm0) and torch.equal(offs, offs0), rep
+
+
+def test_graph_replay_multi_and_uncompressed():
+    # cts_apply_multi (one shrink, one core-product launch for all modules)
+    # and cts_apply_uncompressed, both with T > 128 (shrink split chosen on
+    # the device), captured together; every replay bit for bit the eager result
+    kw = dict(T=300, d_in=256, r=16, n=50, K=5, ids="zipf")
+    mods = [wl.synthetic("gm%d" % m, cfg=150 + m, d_out=d, with_lora=False, **kw)
+            for m, d in enumerate((256, 64, 64))]
+    w0 = mods[0]
+    Vt = dev(np.concatenate([m.Vt for m in mods], axis=1))
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    Ws, Us, Ss = [dev(m.W) for m in mods], [dev(m.U) for m in mods], [dev(m.Sigma) for m in mods]
+    ys = [torch.empty((w0.T, m.d_out), dtype=torch.bfloat16, device="cuda") for m in mods]
+    p = cts.make_problem(w0.T, w0.d_in, 256, r=16, n_adapters=50, n_clusters=5)
+    wsm = torch.empty(cts.workspace_size_multi(p, [m.d_out for m in mods]), dtype=torch.uint8, device="cuda")
+    u = wl.synthetic("gu", cfg=155, T=600, d_in=512, d_out=128, r=16, n=300, K=1, r_l=16)
+    ux, uaid, uW, uA, uB = dev(u.x), dev(u.adapter_id), dev(u.W), dev(u.A), dev(u.B)
+    yu = torch.empty((u.T, u.d_out), dtype=torch.bfloat16, device="cuda")
+    pu = cts.make_problem(u.T, u.d_in, u.d_out, n_adapters=u.n, r_lora=16)
+    wsu = torch.empty(cts.workspace_size(pu, compressed=False), dtype=torch.uint8, device="cuda")
+
+    def calls():
+        cts.apply_multi(x, aid, cof, Ws, Us, Vt, Ss, outs=ys, workspace=wsm)
+        cts.apply_uncompressed(ux, uaid, uW, uA, uB, out=yu, workspace=wsu)
+
+    say("graph multi/uncompressed: eager reference")
+    calls()
+    torch.cuda.synchronize()
+    ref = [y.clone() for y in ys] + [yu.clone()]
+    say("graph multi/uncompressed: capture")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        calls()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for y in ys + [yu]:
+            y.fill_(float("nan"))
+        z = cts.apply_uncompressed(ux, uaid, uW, uA, uB)
+        say("graph multi/uncompressed: replay %d" % rep)
+        g.replay()
+        torch.cuda.synchronize()
+        for y, e in zip(ys + [yu], ref):
+            assert torch.equal(y, e), rep
+        assert torch.equal(z, ref[-1]), rep
