@@ -1215,6 +1215,8 @@ hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStre
   if (p.tile_start &&
       !(tile == Tile::Decode || tile == Tile::Shrink || tile == Tile::Small || tile == Tile::F32))
     return hipErrorInvalidValue;
+  // the split chosen on the device exists in the bf16 shrink tile only
+  if (p.split_target > 0 && (in_dtype == 0 || tile != Tile::Shrink)) return hipErrorInvalidValue;
   // in-kernel bucketing exists in the bf16 shrink tile only
   if (p.fs_adapter && (in_dtype == 0 || tile != Tile::Shrink || p.N > kFuseSortMaxT || p.tile_start))
     return hipErrorInvalidValue;
