@@ -391,6 +391,55 @@ __global__ __launch_bounds__(kJT) void jd_combine_kernel(const ProjArgs a) {
     // G_q = P_q P_q^T, H_q = Q_q Q_q^T (r_l x r_l per LoRA)
     float* Gs = Qs + kTM * kEpLd;
     float* Hs = Gs + kTM * 64;
+    if (r_l <= 16) {
+      // r_l divides 16, so every LoRA's rows sit inside one 16-row block:
+      // G_q and H_q are the LoRA blocks on the diagonal of the 16 x 16
+      // diagonal tiles of P P^T and Q Q^T (fp32 MFMA; wave w takes rows
+      // 16 w .. 16 w + 15).  The tiles, zero off the LoRA blocks, then
+      // multiply Q and P as block-diagonal matrices: C = w G Q, D = w H P.
+      // Each tile is written and read by its own wave only.
+      const int lane = tid & 63, wave = tid >> 6;
+      const int fr = lane & 15, fk = lane >> 4;
+      const int rb = 16 * wave;
+      f32x4 g = {0.f, 0.f, 0.f, 0.f}, h = {0.f, 0.f, 0.f, 0.f};
+      for (int k0 = 0; k0 < r; k0 += 4) {
+        const float pv = Ps[(rb + fr) * kEpLd + k0 + fk];
+        const float qv = Qs[(rb + fr) * kEpLd + k0 + fk];
+        g = mfma4(pv, pv, g);
+        h = mfma4(qv, qv, h);
+      }
+      float* Gt = Gs + wave * 16 * 17;
+      float* Ht = Hs + wave * 16 * 17;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = 4 * fk + v;
+        const bool same = i / r_l == fr / r_l;
+        Gt[i * 17 + fr] = same ? g[v] : 0.f;
+        Ht[i * 17 + fr] = same ? h[v] : 0.f;
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f32x4 c = {0.f, 0.f, 0.f, 0.f}, d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const int k = 4 * ks + fk;
+          c = mfma4(Gt[fr * 17 + k], Qs[(rb + k) * kEpLd + 16 * nb + fr], c);
+          d = mfma4(Ht[fr * 17 + k], Ps[(rb + k) * kEpLd + 16 * nb + fr], d);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = rb + 4 * fk + v;
+          if (row < rows) {
+            const int q = row / r_l;
+            const float w = a.w2 ? a.w2[a.lidx[q0 + q]] : 1.f;
+            const int64_t f = static_cast<int64_t>(q0) * r_l + row;
+            a.C[f * r + 16 * nb + fr] = c[v] * w;
+            a.D[f * r + 16 * nb + fr] = d[v] * w;
+          }
+        }
+      }
+      return;
+    }
     const int ng = rows * r_l;                        // entries of all G_q
     for (int e = tid; e < ng; e += kJT) {
       const int row = e / r_l, l2 = e - row * r_l;
