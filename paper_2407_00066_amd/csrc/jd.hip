@@ -663,7 +663,8 @@ __device__ __forceinline__ float lane_val(float v, int l) {
 }
 
 template <int NB>
-__global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int chol, float* out) {
+__global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk, int chol, float* out,
+                                                      int nblk1) {
   constexpr int r = 16 * NB;
   constexpr int ld = r + 1;
   constexpr int rr = r * r;
@@ -674,11 +675,11 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
   const int lane = tid & 63, wave = tid >> 6;
   constexpr int NU = (rr + kJT - 1) / kJT;
   // partials summed in block order, four blocks' loads in flight
-  auto sum_partials = [&](const float* src, float (&acc)[NU]) __attribute__((always_inline)) {
+  auto sum_partials = [&](const float* src, int cnt, float (&acc)[NU]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < NU; ++u) acc[u] = 0.f;
     int b = 0;
-    for (; b + 4 <= nblk; b += 4) {
+    for (; b + 4 <= cnt; b += 4) {
       float v[4][NU];
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -690,16 +691,18 @@ __global__ __launch_bounds__(kJT) void jd_chol_kernel(const float* gp, int nblk,
 #pragma unroll
         for (int u = 0; u < NU; ++u) acc[u] += v[q][u];
     }
-    for (; b < nblk; ++b)
+    for (; b < cnt; ++b)
 #pragma unroll
       for (int u = 0; u < NU; ++u)
         if (tid + u * kJT < rr) acc[u] += src[static_cast<int64_t>(b) * rr + tid + u * kJT];
   };
   float acc[NU];
-  sum_partials(gp + static_cast<int64_t>(z) * nblk * rr, acc);
+  sum_partials(gp + static_cast<int64_t>(z) * nblk * rr, nblk, acc);
   if (chol == 3) {
+    // the second set's partials are nblk apart too, but only its first
+    // nblk1 blocks hold rows
     float acc1[NU];
-    sum_partials(gp + static_cast<int64_t>(nblk) * rr, acc1);
+    sum_partials(gp + static_cast<int64_t>(nblk) * rr, nblk1, acc1);
 #pragma unroll
     for (int u = 0; u < NU; ++u) acc[u] *= acc1[u];
   }
@@ -1372,7 +1375,8 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   for (int pass = 0; pass < 2; ++pass) {
     if ((e = gram(Un, Vn, nullptr, nullptr)) != hipSuccess) return e;
     e = with_nb(r, [&](auto c) {
-      hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 1, mat);
+      hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 1, mat,
+                         j.pl.nblk);
       return hipGetLastError();
     });
     if (e != hipSuccess) return e;
@@ -1386,7 +1390,8 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
   // measure: M = X_old^T X_new, E = X_new - X_old M
   if ((e = gram(U, V, Un, Vn)) != hipSuccess) return e;
   e = with_nb(r, [&](auto c) {
-    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 0, mat);
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 0, mat,
+                       j.pl.nblk);
     return hipGetLastError();
   });
   if (e != hipSuccess) return e;
@@ -1471,7 +1476,8 @@ hipError_t gram_hadamard_inverse(Jd& j, const float* X0, int d0, const float* X1
                        X0, X1, nullptr, nullptr, d0, d1, nb, gp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(1), dim3(kJT), 0, j.st, gp, nb, 3, out);
+    hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(1), dim3(kJT), 0, j.st, gp, nb, 3, out,
+                       (d1 + kGramRows - 1) / kGramRows);
     return hipGetLastError();
   });
 }
