@@ -1135,15 +1135,21 @@ __global__ __launch_bounds__(kJT) void km_members_kernel(const int32_t* labels, 
 
 // ---------------------------------------------------------- JD-Diag pieces
 // s_i = Ginv w_i for every LoRA (Ginv symmetric r x r): s[i][j] = sum_k Ginv[j][k] w[i][k]
-__global__ __launch_bounds__(kJT) void jd_diag_solve_kernel(const float* ginv, const float* w, int n, int r,
-                                                            float* s) {
+template <int NB>
+__global__ __launch_bounds__(kJT) void jd_diag_solve_kernel(const float* ginv, const float* w, int n, float* s) {
+  constexpr int r = 16 * NB;
+  __shared__ float sg[r * (r + 1)];                  // Ginv rows, padded against bank conflicts
+  for (int e = threadIdx.x; e < r * r; e += kJT) sg[(e / r) * (r + 1) + e % r] = ginv[e];
+  __syncthreads();
   const int64_t tot = static_cast<int64_t>(n) * r;
   for (int64_t e = blockIdx.x * static_cast<int64_t>(kJT) + threadIdx.x; e < tot;
        e += static_cast<int64_t>(gridDim.x) * kJT) {
     const int64_t i = e / r;
     const int jj = static_cast<int>(e - i * r);
+    const float* wr = w + i * r;                     // one row per r consecutive threads
     float acc = 0.f;
-    for (int k = 0; k < r; ++k) acc = fmaf(ginv[jj * r + k], w[i * r + k], acc);
+#pragma unroll 16
+    for (int k = 0; k < r; ++k) acc = fmaf(sg[jj * (r + 1) + k], wr[k], acc);
     s[e] = acc;
   }
 }
@@ -1535,9 +1541,12 @@ hipError_t als_sigma(Jd& j, const float* A, const float* B, const int32_t* lidx,
   const int64_t rr = static_cast<int64_t>(r) * r;
   if ((e = gram_hadamard_inverse(j, U, p->d_out, V, p->d_in, m + 3 * rr)) != hipSuccess) return e;
   const int64_t tot = static_cast<int64_t>(p->n) * r;
-  hipLaunchKernelGGL(jd_diag_solve_kernel, dim3(static_cast<unsigned>(std::min<int64_t>(1024, (tot + kJT - 1) / kJT))),
-                     dim3(kJT), 0, j.st, m + 3 * rr, w, p->n, r, sd);
-  return hipGetLastError();
+  return with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_diag_solve_kernel<decltype(c)::value>,
+                       dim3(static_cast<unsigned>(std::min<int64_t>(1024, (tot + kJT - 1) / kJT))), dim3(kJT), 0,
+                       j.st, m + 3 * rr, w, p->n, sd);
+    return hipGetLastError();
+  });
 }
 
 // one sweep: U, then V (with the new U), then the diagonals, then the
