@@ -745,9 +745,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one MI355X: the layer has no cross-GPU communication, and its "
-              "throughput on N GPUs is N data-parallel copies of this measurement; run it with "
-              "--gpus 1", file=sys.stderr)
+        print("bench.py measures one MI355X (the layer's tokens would shard across GPUs with no "
+              "communication inside the layer; that path is not run here); run it with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
