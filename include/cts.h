@@ -183,6 +183,26 @@ int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const
                     const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* cts_apply without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops and
+ * harnesses that forbid allocation.  Same arguments (minus the workspace),
+ * layouts, limits, results and errors as cts_apply; the call computes
+ * exactly what cts_apply computes, with the same kernels.
+ * Its scratch memory is one static device array of
+ * CTS_NOALLOC_SCRATCH_BYTES bytes inside the library: every GPU the library
+ * runs on holds its own copy of it until the process ends.  A problem whose
+ * cts_workspace_size(p) exceeds that size is refused with
+ * CTS_ERR_UNSUPPORTED before anything is launched.  The call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine); its first
+ * call on a device looks up that device's copy of the array (with the
+ * stream's device current, as for every call).  All calls on one GPU share
+ * that GPU's array: calls that overlap in time on one GPU (different
+ * streams, or different host threads) race and give undefined results. */
+#define CTS_NOALLOC_SCRATCH_BYTES (48u << 20)
+int cts_apply_noalloc(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                      const int32_t* cluster_of, const void* W, const void* U,
+                      const void* Vt, const void* Sigma, void* y, void* stream);
+
 /* Synchronous id check for tests and debugging: copies the ids to the host
  * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is
  * outside [0, n) or any cluster_of outside [0, K) (cluster_of may be NULL). */

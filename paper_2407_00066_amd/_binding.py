@@ -24,7 +24,7 @@ CTS_F32, CTS_BF16 = 0, 1
 EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncompressed",
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
-            "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi",
+            "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi", "cts_apply_noalloc",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
             "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_sort_by_cluster.restype = ctypes.c_int
                 L.cts_apply.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply.restype = ctypes.c_int
+                L.cts_apply_noalloc.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+                L.cts_apply_noalloc.restype = ctypes.c_int
                 L.cts_apply_diag.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply_diag.restype = ctypes.c_int
                 L.cts_apply_ranked.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -215,6 +217,38 @@ def apply(x, adapter_id, cluster_of, W, U, Vt, Sigma, out=None, out_dtype=None, 
     ws = _workspace(dev, nbytes, workspace)
     _check(lib().cts_apply(ctypes.byref(p), *args, ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                            _stream(dev)), "cts_apply")
+    return out
+
+
+# scratch bytes of cts_apply_noalloc (CTS_NOALLOC_SCRATCH_BYTES in include/cts.h)
+NOALLOC_SCRATCH_BYTES = 48 << 20
+
+
+def apply_noalloc(x, adapter_id, cluster_of, W, U, Vt, Sigma, out=None, out_dtype=None):
+    """As apply, through cts_apply_noalloc: no workspace, the library's static
+    per-device scratch array instead (see include/cts.h).  `out` is the
+    caller's; when it is None a new output tensor is made here."""
+    dev = x.device
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    K, _, r = U.shape
+    n = Sigma.shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty((T, d_out), dtype=odt, device=dev)
+    p = make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=dt,
+                     out_dtype=_dt(out, "out"))
+    args = [_dev(x, "x", dev, tdt, (T, d_in)),
+            _dev(adapter_id, "adapter_id", dev, torch.int32, (T,)),
+            _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)),
+            _dev(W, "W", dev, tdt, (d_out, d_in)),
+            _dev(U, "U", dev, tdt, (K, d_out, r)),
+            _dev(Vt, "Vt", dev, tdt, (K, r, d_in)),
+            _dev(Sigma, "Sigma", dev, tdt, (n, r, r)),
+            _dev(out, "out", dev, None, (T, d_out))]
+    _check(lib().cts_apply_noalloc(ctypes.byref(p), *args, _stream(dev)), "cts_apply_noalloc")
     return out
 
 

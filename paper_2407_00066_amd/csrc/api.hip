@@ -12,10 +12,17 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "cts.h"
 #include "cts_internal.h"
+
+// Scratch memory of cts_apply_noalloc: one static array per device (each
+// GPU the library runs on holds its own copy until the process ends); it
+// stands in for the workspace argument of cts_apply.
+__device__ __align__(256) unsigned char scratch[CTS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -342,29 +349,64 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
 
 namespace {
 
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (hipGetSymbolAddress with that device current) and kept.  The
+// array's name is a host-side stand-in in host code: only this address may
+// be handed to kernels.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return CTS_ERR_HIP;
+  if (dev >= kMaxDevices) return CTS_ERR_UNSUPPORTED;
+  void* ptr = g_scratch[dev].load(std::memory_order_acquire);
+  if (!ptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ptr = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!ptr) {
+      if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return CTS_ERR_HIP;
+      g_scratch[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return CTS_OK;
+}
+
+// workspace == nullptr with noalloc: the call runs in this device's static
+// scratch array (the problem's workspace must fit in it).
 int apply_compressed(const cts_problem* p, const void* x, const int32_t* adapter_id,
                      const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
                      const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream,
-                     bool sigma_diag, const int32_t* rank_of_cluster = nullptr, bool ranked = false) {
+                     bool sigma_diag, const int32_t* rank_of_cluster = nullptr, bool ranked = false,
+                     bool noalloc = false) {
   Plan pl;
   const int rc = make_plan(p, true, &pl);
   if (rc != CTS_OK) return rc;
   if (p->T == 0) return CTS_OK;
-  if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || !workspace)
+  if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || (!workspace && !noalloc))
     return CTS_ERR_INVALID_ARG;
   for (const void* q : {x, W, U, Vt, Sigma, static_cast<const void*>(y), static_cast<const void*>(workspace)})
     if (misaligned(q, 16)) return CTS_ERR_INVALID_ARG;
   if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4)) return CTS_ERR_INVALID_ARG;
   if (ranked && (!rank_of_cluster || misaligned(rank_of_cluster, 4))) return CTS_ERR_INVALID_ARG;
-  if (workspace_bytes < pl.total) return CTS_ERR_WORKSPACE;
+  if (noalloc ? pl.total > CTS_NOALLOC_SCRATCH_BYTES : workspace_bytes < pl.total)
+    return noalloc ? CTS_ERR_UNSUPPORTED : CTS_ERR_WORKSPACE;
   const size_t e = pl.elt;
   const size_t T = p->T, di = p->d_in, dout = p->d_out, r = p->r, n = p->n_adapters, K = p->n_clusters;
   const Range in[8] = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
                        {W, dout * di * e}, {U, K * dout * r * e}, {Vt, K * r * di * e},
                        {Sigma, n * (sigma_diag ? 1 : r) * r * e},
                        {rank_of_cluster, ranked ? 4 * K : 0}};
-  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 8))
+  // (the static scratch array is an allocation of its own: no caller array
+  // can overlap it)
+  if (any_overlap({y, T * dout * pl.out_elt}, {workspace, noalloc ? 0 : workspace_bytes}, in, 8))
     return CTS_ERR_INVALID_ARG;
+  if (noalloc) {
+    const int sc = scratch_of_current_device(&workspace);
+    if (sc != CTS_OK) return sc;
+  }
   return run_layer(p, pl, true, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
                    static_cast<hipStream_t>(stream), sigma_diag, ranked ? rank_of_cluster : nullptr);
 }
@@ -376,6 +418,13 @@ int cts_apply(const cts_problem* p, const void* x, const int32_t* adapter_id,
               const void* Sigma, void* y, void* workspace, size_t workspace_bytes, void* stream) {
   return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
                           workspace_bytes, stream, false);
+}
+
+int cts_apply_noalloc(const cts_problem* p, const void* x, const int32_t* adapter_id,
+                      const int32_t* cluster_of, const void* W, const void* U, const void* Vt,
+                      const void* Sigma, void* y, void* stream) {
+  return apply_compressed(p, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, nullptr, 0, stream, false,
+                          nullptr, false, true);
 }
 
 int cts_apply_diag(const cts_problem* p, const void* x, const int32_t* adapter_id,

@@ -388,3 +388,33 @@ def test_multi_validation():
     p0 = B.make_problem(0, 64, 8, r=16, n_adapters=4, n_clusters=2)
     assert cts.lib().cts_apply_multi(ctypes.byref(p0), 2, d2, None, None, None, None, None, None, None, None, None,
                                      0, None) == B.CTS_OK
+
+
+def _apply_na(p, ptrs=None, y=None):
+    ptrs = ptrs or [FAKE] * 7
+    y = y if y is not None else ctypes.c_void_p(0x7000_0000_0000)
+    return cts.lib().cts_apply_noalloc(ctypes.byref(p), *ptrs[:7], y, None)
+
+
+def test_noalloc_validation_before_any_launch():
+    """cts_apply_noalloc: the argument checks of cts_apply, and a problem
+    whose workspace exceeds the static scratch array is refused."""
+    assert cts.lib().cts_apply_noalloc(ctypes.byref(_p(T=0)), *[None] * 8, None) == B.CTS_OK
+    assert cts.lib().cts_apply_noalloc(None, *[FAKE] * 8, None) == B.CTS_ERR_INVALID_ARG
+    for i in range(7):
+        ptrs = [FAKE] * 7
+        ptrs[i] = None
+        assert _apply_na(_p(), ptrs) == B.CTS_ERR_INVALID_ARG, i
+    assert _apply_na(_p(), y=ctypes.c_void_p(0x7000_0000_0000 + 8)) == B.CTS_ERR_INVALID_ARG
+    assert _apply_na(_p(r=12)) == B.CTS_ERR_UNSUPPORTED
+    base = 0x5000_0000_0000
+    ptrs = [ctypes.c_void_p(base + i * (1 << 30)) for i in range(7)]
+    assert _apply_na(_p(T=64, d_in=64, d_out=64, r=8, n_adapters=4), ptrs,
+                     y=ctypes.c_void_p(base + 3 * (1 << 30) + 64)) == B.CTS_ERR_INVALID_ARG
+    assert cts.workspace_size(_p()) <= B.NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_scratch_size_matches_header():
+    src = open(os.path.join(ROOT, "include", "cts.h")).read()
+    m = re.search(r"#define CTS_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == B.NOALLOC_SCRATCH_BYTES
