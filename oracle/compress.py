@@ -34,9 +34,13 @@ Readings (where the paper leaves a choice open):
   starts from the centroids Sigma_{i} of the given LoRA indices (ties and
   empty clusters: lowest index wins; an empty cluster keeps its centroid /
   bases); per-cluster JD-Full starts from the given per-cluster bases each
-  round, and runs only for a cluster whose members supply at least r
-  directions (members x r_l >= r; with fewer the rank-r problem has no unique
-  solution and the cluster keeps its bases); a LoRA moves to the cluster
+  round when its members supply at least r directions (members x r_l >= r).
+  A non-empty cluster with fewer (members x r_l < r) takes ``span_bases``: by
+  Prop. 1 any U_j holding every member's B_i columns and V_j holding every
+  A_i^T column reconstructs the members exactly, so such a pair minimizes the
+  cluster's objective of App. A.3 Step 1 (at zero); of these minimizers the
+  one taken completes the members' columns with the leading columns of the
+  given bases, orthogonalized in that order.  A LoRA moves to the cluster
   maximizing ||U_j^T B_i A_i V_j||_F^2,
   which for orthonormal U_j, V_j is the cluster minimizing
   min_Sigma ||B_i A_i - U_j Sigma V_j^T||_F^2.
@@ -247,6 +251,25 @@ def kmeans(X, init_idx, max_iter=100):
     return labels
 
 
+def span_bases(A, B, r, Uc, Vc):
+    """App. A.3 Step 1 for a cluster whose m members supply fewer than r
+    directions (m r_l < r).  Every pair U, V with U containing the columns of
+    all members' B_i and V those of all A_i^T gives U U^T B_i A_i V V^T =
+    B_i A_i (Prop. 1), i.e. zero objective, the minimum.  Returned: the
+    positive-diagonal QR factors of [B_1 ... B_m | Uc[:, :r - m r_l]] and
+    [A_1^T ... A_m^T | Vc[:, :r - m r_l]] (members in increasing index
+    order, the given bases' leading columns completing the rank)."""
+    A = np.asarray(A, np.float64)
+    B = np.asarray(B, np.float64)
+    m, r_l = A.shape[0], A.shape[1]
+    q = r - m * r_l
+    if q <= 0:
+        raise ValueError("span_bases needs fewer than r member directions")
+    XU = np.concatenate([B[i] for i in range(m)] + [np.asarray(Uc, np.float64)[:, :q]], axis=1)
+    XV = np.concatenate([A[i].T for i in range(m)] + [np.asarray(Vc, np.float64)[:, :q]], axis=1)
+    return orthogonalize(XU), orthogonalize(XV)
+
+
 def jd_cluster(A, B, k, r, U0, V0, Uc0, Vc0, init_idx, jd_iters=10, max_rounds=20, solver="eig"):
     """App. A.3: a single-basis JD-Full from (U0, V0), k-means on vec(Sigma_i)
     from the centroids of LoRAs init_idx, then rounds of per-cluster JD-Full
@@ -264,8 +287,11 @@ def jd_cluster(A, B, k, r, U0, V0, Uc0, Vc0, init_idx, jd_iters=10, max_rounds=2
     for rounds in range(1, max_rounds + 1):
         for j in range(k):
             m = labels == j
-            if np.count_nonzero(m) * A.shape[1] >= r:
+            cnt = np.count_nonzero(m)
+            if cnt * A.shape[1] >= r:
                 Us[j], Vs[j], _, _ = jd(A[m], B[m], r, Uc0[j], Vc0[j], jd_iters)
+            elif cnt > 0:
+                Us[j], Vs[j] = span_bases(A[m], B[m], r, Uc0[j], Vc0[j])
         new = np.argmax(assign_scores(Us, Vs, A, B), axis=1)
         if np.array_equal(new, labels):
             break

@@ -351,3 +351,37 @@ def test_workload_recipe():
     b = wl.f32_to_bf16_bits(np.array([1.0, 1.00390625, 1.01171875, -3.0], np.float32))
     # 1+2^-8 and 1+3*2^-8 are ties: they round to the even neighbours 0x3F80 and 0x3F82
     assert b.tolist() == [0x3F80, 0x3F80, 0x3F82, 0xC040]
+
+
+def test_apply_multi_stacking_against_bruteforce(oracle_mod):
+    """Multi-module batching (modules of one layer on the same x, ids and
+    cluster map, Sec. 3.1, 3.2 per projection): apply_multi with module m's
+    V_k^T in rows m r .. m r + r - 1 of the stacked array equals, per module,
+    the dense brute force (W_m + U_k^(m) S_i^(m) V_k^(m)T) x_t built from
+    that module's own arrays.  Planted mistake: the same modules stacked
+    interleaved (row q of module m at q M + m) must not match."""
+    rs = np.random.default_rng(91)
+    T, d_in, r, n, K, d_outs = 7, 12, 4, 5, 3, (9, 6, 6)
+    x = rs.standard_normal((T, d_in))
+    aid = rs.integers(0, n, T).astype(np.int32)
+    cof = rs.integers(0, K, n).astype(np.int32)
+    Ws = [rs.standard_normal((d, d_in)) for d in d_outs]
+    Us = [rs.standard_normal((K, d, r)) for d in d_outs]
+    Vts = [rs.standard_normal((K, r, d_in)) for _ in d_outs]
+    Ss = [rs.standard_normal((n, r, r)) for _ in d_outs]
+    M = len(d_outs)
+    stacked = np.zeros((K, M * r, d_in))
+    for m in range(M):
+        for q in range(r):
+            stacked[:, m * r + q, :] = Vts[m][:, q, :]
+    ys = oracle_mod.apply_multi(x, aid, cof, Ws, Us, stacked, Ss)
+    for m in range(M):
+        dense = np.stack([Us[m][cof[a]] @ Ss[m][a] @ Vts[m][cof[a]] for a in range(n)])
+        want = np.einsum("toc,tc->to", Ws[m][None] + dense[aid], x)
+        assert _rel(ys[m], want) < 1e-13, m
+    inter = np.zeros_like(stacked)
+    for m in range(M):
+        for q in range(r):
+            inter[:, q * M + m, :] = Vts[m][:, q, :]
+    bad = oracle_mod.apply_multi(x, aid, cof, Ws, Us, inter, Ss)
+    assert max(_rel(bad[m], ys[m]) for m in range(M)) > 1e-2

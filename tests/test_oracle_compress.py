@@ -360,3 +360,66 @@ def test_planted_mistakes_fail_the_pins():
         return U, V, C.sigma_star(U, V, A, B), [1.0]
     ru, rv, _ = _eig_stationarity(bad_eig)
     assert max(ru, rv) > 1e-4
+
+
+# ----------------------------------- App. A.3 Step 1 for a cluster below rank
+def test_span_bases_reconstruct_small_cluster_exactly():
+    """A cluster whose m members supply fewer than r directions (m r_l < r):
+    span_bases returns orthonormal bases containing every member's B_i
+    columns and A_i^T columns, so the members' optimal cores (eq. sigmastar)
+    reconstruct them with zero residual (Prop. 1) -- the minimum of the
+    cluster's Step 1 objective.  The given bases alone (what the cluster had
+    before Step 1) do not."""
+    rs = np.random.default_rng(70)
+    d_out, d_in, r_l, r = 30, 26, 3, 16
+    for m in (1, 2, 5):
+        A, B = _random_loras(rs, m, d_out, d_in, r_l)
+        Uc, Vc = C.random_orthonormal(rs, d_out, r), C.random_orthonormal(rs, d_in, r)
+        U, V = C.span_bases(A, B, r, Uc, Vc)
+        assert U.shape == (d_out, r) and V.shape == (d_in, r)
+        assert np.abs(U.T @ U - np.eye(r)).max() < 1e-12
+        assert np.abs(V.T @ V - np.eye(r)).max() < 1e-12
+        S = C.sigma_star(U, V, A, B)
+        total = sum(np.linalg.norm(P) ** 2 for P in C.products(A, B))
+        assert C.objective(U, V, S, A, B) < 1e-24 * total
+        # the leading m r_l columns span the members' B_i columns (A_i^T rows)
+        Bs = np.concatenate(list(B), axis=1)
+        As = np.concatenate([a.T for a in A], axis=1)
+        Ul, Vl = U[:, :m * r_l], V[:, :m * r_l]
+        assert np.abs(Bs - Ul @ (Ul.T @ Bs)).max() < 1e-10 * np.abs(Bs).max()
+        assert np.abs(As - Vl @ (Vl.T @ As)).max() < 1e-10 * np.abs(As).max()
+        # the rest of the rank comes from the given bases' leading columns
+        q = r - m * r_l
+        Xu = np.concatenate([Bs, Uc[:, :q]], axis=1)
+        assert np.abs(Xu - U @ (U.T @ Xu)).max() < 1e-10 * np.abs(Xu).max()
+        # planted mistake: keeping the given bases leaves a residual
+        S0 = C.sigma_star(Uc, Vc, A, B)
+        assert C.objective(Uc, Vc, S0, A, B) > 0.1 * total
+    with pytest.raises(ValueError):
+        C.span_bases(*_random_loras(rs, 6, d_out, d_in, r_l), r, Uc, Vc)   # 6 x 3 >= 16
+
+
+def test_cluster_small_clusters_reconstruct_their_members():
+    """Clustering with K = 3 on a collection where the k-means labels leave
+    clusters below rank: after the rounds, every member of a cluster with
+    members x r_l < r is reconstructed exactly by its cluster's bases, and
+    every cluster with at least r directions by its JD bases to the JD's
+    accuracy -- Step 1 minimized for every non-empty cluster."""
+    rs = np.random.default_rng(71)
+    d_out, d_in, r_l, r, K = 40, 36, 4, 16, 3
+    # a large group of 10 LoRAs sharing 16-dim spaces and two LoRAs of their own
+    A1, B1 = _shared_space_loras(rs, n=10, d_out=d_out, d_in=d_in, r_l=r_l, rt=16)
+    A2, B2 = _random_loras(rs, 2, d_out, d_in, r_l)
+    A, B = np.concatenate([A1, A2 * 8.0]), np.concatenate([B1, B2 * 8.0])
+    U0, V0 = C.random_orthonormal(rs, d_out, r), C.random_orthonormal(rs, d_in, r)
+    Uc = [C.random_orthonormal(rs, d_out, r) for _ in range(K)]
+    Vc = [C.random_orthonormal(rs, d_in, r) for _ in range(K)]
+    labels, Us, Vs, S, rounds = C.jd_cluster(A, B, K, r, U0, V0, Uc, Vc, [0, 10, 11], jd_iters=30)
+    P = C.products(A, B)
+    sizes = np.bincount(labels, minlength=K)
+    small = [j for j in range(K) if 0 < sizes[j] * r_l < r]
+    assert small, sizes                                  # the case under test occurs
+    for i in range(len(A)):
+        j = labels[i]
+        err = np.linalg.norm(P[i] - Us[j] @ S[i] @ Vs[j].T) ** 2 / np.linalg.norm(P[i]) ** 2
+        assert err < (1e-20 if j in small else 1e-6), (i, j, err)
