@@ -115,8 +115,12 @@ int cts_jd_sigma(const cts_jd_problem* p, const float* A, const float* B, const 
  * reassignment of every LoRA to the cluster maximizing ||U_k^T B_i A_i V_k||_F
  * (= minimizing min_S ||B_i A_i - U_k S V_k^T||_F), until no LoRA moves or
  * after max_rounds rounds.  Ties go to the lowest index; an empty cluster
- * keeps its centroid and bases, and a cluster whose members supply fewer than
- * r directions (members * r_lora < r) keeps its bases (no per-cluster JD).
+ * keeps its centroid and bases.  A cluster whose m members supply fewer than
+ * r directions (m * r_lora < r) gets, in place of the per-cluster JD, the
+ * positive-diagonal QR factors of [B_{i_1} ... B_{i_m} | Uc0[k][:, :q]] and
+ * [A_{i_1}^T ... A_{i_m}^T | Vc0[k][:, :q]] (members in increasing id order,
+ * q = r - m r_lora): bases that contain every member's columns and so
+ * reconstruct the members exactly (Prop. 1), a minimizer of Step 1.
  * Outputs: cluster_of [n] (device int32), U [K][d_out][r], Vt [K][r][d_in],
  * Sigma [n][r][r] (each LoRA's core in its own cluster's bases), *rounds
  * (host, may be NULL).  normalize as in cts_jd_full.  Waits for the stream

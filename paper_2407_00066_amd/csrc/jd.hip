@@ -994,6 +994,30 @@ __global__ void jd_copy_kernel(const float* in, float* out, int64_t n) {
     out[e] = in[e];
 }
 
+// Bases of a cluster whose m members supply fewer than r directions (App. A.3
+// Step 1 with m r_l < r; every pair holding the members' B_i and A_i^T
+// columns reconstructs them exactly, Prop. 1), before orthonormalization:
+//   Un [d_out][r] = [B_{memb[0]} ... B_{memb[m-1]} | Uc[:, :r - m r_l]]
+//   Vn [d_in][r]  = [A_{memb[0]}^T ... A_{memb[m-1]}^T | Vtc[:r - m r_l]^T]
+// grid (ceil(max(d_out, d_in) r / 256), 2): y = 0 fills Un, y = 1 Vn.
+__global__ void jd_span_kernel(const float* A, const float* B, const int32_t* memb, int m, int r_l, int d_in,
+                               int d_out, int r, const float* Uc, const float* Vtc, float* Un, float* Vn) {
+  const bool u = blockIdx.y == 0;
+  const int64_t rows = u ? d_out : d_in;
+  const int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+  if (e >= rows * r) return;
+  const int row = static_cast<int>(e / r), c = static_cast<int>(e % r);
+  const int mc = m * r_l;
+  float v;
+  if (c < mc) {
+    const int64_t i = memb[c / r_l], l = c % r_l;
+    v = u ? B[(i * d_out + row) * r_l + l] : A[(i * r_l + l) * d_in + row];
+  } else {
+    v = u ? Uc[static_cast<int64_t>(row) * r + (c - mc)] : Vtc[static_cast<int64_t>(c - mc) * d_in + row];
+  }
+  (u ? Un : Vn)[e] = v;
+}
+
 __global__ void jd_iota_kernel(int32_t* out, int n) {
   for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x) out[e] = e;
 }
@@ -1337,6 +1361,61 @@ hipError_t launch_project(const Jd& j, const float* A, const float* B, const flo
 
 // One eigenvalue-iteration step from (U, V) in the workspace to (Uo, Vo)
 // (the new pair), then the measure into crit_out; swaps the buffers.
+// Gram partials X0^T Y0 (d_out rows) and X1^T Y1 (d_in rows); Y null: X^T X.
+hipError_t gram_pair(Jd& j, const float* X0, const float* X1, const float* Y0, const float* Y1) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  const dim3 ggrid(j.pl.nblk, 2, (r + kTM - 1) / kTM);
+  float* gp = j.at<float>(j.pl.off_gp);
+  return with_nb(r, [&](auto c) {
+    hipLaunchKernelGGL(jd_gram_kernel<decltype(c)::value>, ggrid, dim3(kJT), 0, j.st, X0, X1, Y0, Y1, p->d_out,
+                       p->d_in, j.pl.nblk, gp);
+    return hipGetLastError();
+  });
+}
+
+// CholeskyQR2 on Un [d_out][r] and Vn [d_in][r] together, in place: the Q of
+// the QR factorization with a positive diagonal of R.
+hipError_t orthonormalize(Jd& j, float* Un, float* Vn) {
+  const cts_jd_problem* p = j.p;
+  const int r = p->r;
+  float* gp = j.at<float>(j.pl.off_gp);
+  float* mat = j.at<float>(j.pl.off_mat);
+  const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
+  hipError_t e;
+  for (int pass = 0; pass < 2; ++pass) {
+    if ((e = gram_pair(j, Un, Vn, nullptr, nullptr)) != hipSuccess) return e;
+    e = with_nb(r, [&](auto c) {
+      hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 1, mat,
+                         j.pl.nblk);
+      return hipGetLastError();
+    });
+    if (e != hipSuccess) return e;
+    e = with_nb(r, [&](auto c) {
+      hipLaunchKernelGGL(jd_apply_kernel<decltype(c)::value>, dim3(nrb, 2), dim3(kJT), 0, j.st, Un, Vn, p->d_out,
+                         p->d_in, mat);
+      return hipGetLastError();
+    });
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// App. A.3 Step 1 for a cluster of m members with m r_l < r (the members'
+// ids at memb, device): the bases of jd_span_kernel, orthonormalized, in j's
+// U / V buffers.
+hipError_t span_bases(Jd& j, const float* A, const float* B, const int32_t* memb, int m, const float* Uc,
+                      const float* Vtc) {
+  const cts_jd_problem* p = j.p;
+  const int64_t cells = static_cast<int64_t>(std::max(p->d_out, p->d_in)) * p->r;
+  hipLaunchKernelGGL(jd_span_kernel, dim3(static_cast<unsigned>((cells + 255) / 256), 2), dim3(256), 0, j.st, A, B,
+                     memb, m, p->r_lora, p->d_in, p->d_out, p->r, Uc, Vtc, j.at<float>(j.pl.off_U),
+                     j.at<float>(j.pl.off_V));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return orthonormalize(j, j.at<float>(j.pl.off_U), j.at<float>(j.pl.off_V));
+}
+
 hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, int m, const float* w2,
                    float* crit_out) {
   const cts_jd_problem* p = j.p;
@@ -1366,35 +1445,12 @@ hipError_t jd_step(Jd& j, const float* A, const float* B, const int32_t* lidx, i
                      dim3(kJT), 0, j.st, j.at<float>(j.pl.off_pU), j.at<float>(j.pl.off_pV), split, p->d_out,
                      p->d_in, r, Un, Vn, 0);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  // CholeskyQR2 on both
+  if ((e = orthonormalize(j, Un, Vn)) != hipSuccess) return e;
+  // measure: M = X_old^T X_new, E = X_new - X_old M
   float* gp = j.at<float>(j.pl.off_gp);
   float* mat = j.at<float>(j.pl.off_mat);
   const int nrb = (std::max(p->d_out, p->d_in) + 63) / 64;
-  const dim3 ggrid(j.pl.nblk, 2, (r + kTM - 1) / kTM);
-  auto gram = [&](const float* X0, const float* X1, const float* Y0, const float* Y1) {
-    return with_nb(r, [&](auto c) {
-      hipLaunchKernelGGL(jd_gram_kernel<decltype(c)::value>, ggrid, dim3(kJT), 0, j.st, X0, X1, Y0, Y1, p->d_out,
-                         p->d_in, j.pl.nblk, gp);
-      return hipGetLastError();
-    });
-  };
-  for (int pass = 0; pass < 2; ++pass) {
-    if ((e = gram(Un, Vn, nullptr, nullptr)) != hipSuccess) return e;
-    e = with_nb(r, [&](auto c) {
-      hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 1, mat,
-                         j.pl.nblk);
-      return hipGetLastError();
-    });
-    if (e != hipSuccess) return e;
-    e = with_nb(r, [&](auto c) {
-      hipLaunchKernelGGL(jd_apply_kernel<decltype(c)::value>, dim3(nrb, 2), dim3(kJT), 0, j.st, Un, Vn, p->d_out,
-                         p->d_in, mat);
-      return hipGetLastError();
-    });
-    if (e != hipSuccess) return e;
-  }
-  // measure: M = X_old^T X_new, E = X_new - X_old M
-  if ((e = gram(U, V, Un, Vn)) != hipSuccess) return e;
+  if ((e = gram_pair(j, U, V, Un, Vn)) != hipSuccess) return e;
   e = with_nb(r, [&](auto c) {
     hipLaunchKernelGGL(jd_chol_kernel<decltype(c)::value>, dim3(2), dim3(kJT), 0, j.st, gp, j.pl.nblk, 0, mat,
                        j.pl.nblk);
@@ -1800,8 +1856,14 @@ int cts_jd_cluster(const cts_jd_problem* p, int32_t K, const float* A, const flo
         st = cts::run_jd(j, A, B, memb + h_offs[k], cnt, w2, jd_iters, 0.f, nullptr, nullptr);
         if (st != CTS_OK) return st;
         if (!ok(cts::store_bases(j, U + k * usz, Vt + k * vsz))) return CTS_ERR_HIP;
+      } else if (cnt > 0) {
+        // fewer than r directions: the members' columns completed by the
+        // given bases (a Step 1 minimizer, exact for every member)
+        if (!ok(cts::span_bases(j, A, B, memb + h_offs[k], cnt, Uc0 + k * usz, Vtc0 + k * vsz)) ||
+            !ok(cts::store_bases(j, U + k * usz, Vt + k * vsz)))
+          return CTS_ERR_HIP;
       } else if (rd == 1) {
-        // empty, or fewer than r directions: keeps the given bases
+        // empty: keeps the given bases
         if (!ok(cts::load_bases(j, Uc0 + k * usz, Vtc0 + k * vsz)) || !ok(cts::store_bases(j, U + k * usz, Vt + k * vsz)))
           return CTS_ERR_HIP;
       }

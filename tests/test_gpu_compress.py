@@ -227,12 +227,15 @@ def test_jd_full_size_one_step_against_oracle():
     assert np.abs(Ug.T @ Ug - np.eye(r)).max() < 1e-5
 
 
-def test_jd_cluster_rounds_and_small_clusters():
-    """Three noisy groups, K = 3 from LoRAs 0, 1, 2: k-means leaves clusters of
-    fewer than r / r_lora members (no per-cluster JD) and the reassignment
-    moves LoRAs in a second round; score margins on this input exceed 0.6, so
-    fp32 and fp64 take the same decisions."""
-    rs = np.random.default_rng(60)
+@pytest.mark.parametrize("seed,min_rounds", [(60, 1), (80, 3)])
+def test_jd_cluster_rounds_and_small_clusters(seed, min_rounds):
+    """Three noisy groups, K = 3 from LoRAs 0, 1, 2.  k-means leaves a cluster
+    of fewer than r / r_lora members; App. A.3 Step 1 gives it bases holding
+    its members' B_i and A_i^T columns (exact for them, Prop. 1).  Seed 60
+    stops after one round; seed 80 moves LoRAs in rounds 2 and 3 (relative
+    score margins >= 1% in every round, far above fp32 error), so the GPU
+    must take the oracle's decisions in every round."""
+    rs = np.random.default_rng(seed)
     d_out, d_in, r_l, r, K = 96, 80, 4, 16, 3
     parts = [_group(rs, 8, d_out, d_in, r_l, 24, 1.0) for _ in range(3)]
     A = np.concatenate([p[0] for p in parts])
@@ -243,8 +246,11 @@ def test_jd_cluster_rounds_and_small_clusters():
     Uc = np.stack([_f32(OC.random_orthonormal(rs, d_out, r)) for _ in range(K)])
     Vc = np.stack([_f32(OC.random_orthonormal(rs, d_in, r)) for _ in range(K)])
     lab, Us, Vs, So, ro = OC.jd_cluster(A, B, K, r, U0, V0, list(Uc), list(Vc), [0, 1, 2], jd_iters=8)
-    assert ro == 2
-    say("jd_cluster three groups")
+    assert ro >= min_rounds
+    sizes = np.bincount(lab, minlength=K)
+    small = [k for k in range(K) if 0 < sizes[k] * r_l < r]
+    assert small, sizes
+    say("jd_cluster three groups seed=%d" % seed)
     cof, U, Vt, S, rounds = GC.jd_cluster(dev(A), dev(B), K, dev(U0), dev(V0.T), dev(Uc),
                                           dev(np.transpose(Vc, (0, 2, 1))), [0, 1, 2], jd_iters=8)
     torch.cuda.synchronize()
@@ -256,6 +262,10 @@ def test_jd_cluster_rounds_and_small_clusters():
     recon = np.stack([Ug[lab[i]] @ Sg[i] @ Vg[lab[i]].T for i in range(len(A))])
     want = np.stack([Us[lab[i]] @ So[i] @ Vs[lab[i]].T for i in range(len(A))])
     assert _rel(recon, want) < 1e-3
+    # the small clusters' members are reconstructed (to fp32 accuracy)
+    P = OC.products(A, B)
+    for i in np.where(np.isin(lab, small))[0]:
+        assert _rel(recon[i], P[i]) < 1e-4, i
 
 
 # ---------------------------------------------------------------- JD-Diag ALS
