@@ -563,25 +563,19 @@ def stack_cpu_baseline(projs, aid_h, cof_h, target_s, torch, np):
 
 def bench_stack(args, torch, np, cts, B, wl, device):
     T, r, n, K = wl.STACK["T"], wl.STACK["r"], wl.STACK["n"], wl.STACK["K"]
-    g = torch.Generator(device=device)
-    g.manual_seed(wl.SEED_BASE + 500)
-    rs = np.random.default_rng(wl.SEED_BASE + 501)
-    aid_h = rs.integers(0, n, T).astype(np.int32)
-    cof_h = wl.balanced_clusters(rs, n, K)
+    aid_h, cof_h = wl.stack_ids()
     aid, cof = to_dev(aid_h, device), to_dev(cof_h, device)
 
-    def gauss(shape, var):
-        return (torch.randn(shape, generator=g, device=device) * math.sqrt(var)).to(torch.bfloat16)
-
     log("generating the 32-layer stack on the device")
-    xs = {4096: gauss((T, 4096), 1.0), 14336: gauss((T, 14336), 1.0)}
+    xs = {4096: wl.stack_x(torch, device, 4096), 14336: wl.stack_x(torch, device, 14336)}
+    x_o = wl.stack_x_o(torch, device)
     ys = {d: torch.empty((T, d), dtype=torch.bfloat16, device=device) for d in (1024, 4096, 14336)}
     projs, wsz, wsz1 = [], 1, 1
-    for _ in range(wl.STACK_LAYERS):
+    for li in range(wl.STACK_LAYERS):
         layer = {}
         for name, d_in, d_out in wl.STACK_PROJ:
-            layer[name] = (xs[d_in], gauss((d_out, d_in), 1.0 / d_in), gauss((K, d_out, r), 1.0 / d_out),
-                           gauss((K, r, d_in), 1.0 / d_in), gauss((n, r, r), 1.0 / r), ys[d_out])
+            layer[name] = ((x_o if name == "o" else xs[d_in]),) + wl.stack_module(torch, device, li, name) + \
+                (ys[d_out],)
             pb = cts.make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=B.CTS_BF16)
             p1 = cts.make_problem(T, d_in, d_out, r=r, n_adapters=1, n_clusters=1, dtype=B.CTS_BF16)
             wsz, wsz1 = max(wsz, cts.workspace_size(pb)), max(wsz1, cts.workspace_size(p1))

@@ -100,6 +100,23 @@ size_t cts_workspace_size(const cts_problem* p);
 /* Bytes of device workspace cts_apply_uncompressed needs for `p`. */
 size_t cts_workspace_size_uncompressed(const cts_problem* p);
 
+/* Debugging aid: where the bucketing of a call lies in its workspace.  Once
+ * a cts_apply, cts_apply_diag, cts_apply_ranked or cts_apply_multi call
+ * (compressed != 0; for cts_apply_multi, p with module 0's d_out) or a
+ * cts_apply_uncompressed(_ranked) call (compressed == 0) for problem `p` has
+ * completed, its workspace holds, at these byte offsets, the bucketing that
+ * call used (the same as cts_sort_by_cluster's order):
+ *   offsets[0]  int32 perm[T]     token of the j-th sorted position
+ *   offsets[1]  int32 seg[T]      its cluster (uncompressed path: its adapter)
+ *   offsets[2]  int32 aid[T]      its adapter
+ *   offsets[3]  int32 items[c+1]  core-product items: the sorted positions
+ *                                 where a run of one adapter starts or crosses
+ *                                 a multiple of 16, ascending, then items[c] = T
+ *   offsets[4]  int32 c           the number of items
+ * `offsets` is a host array of 5 entries.  Returns CTS_ERR_INVALID_ARG or
+ * CTS_ERR_UNSUPPORTED for a problem the call would refuse. */
+int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* offsets);
+
 /* Token bucketing (the grouping of tokens by cluster that makes the shared-
  * basis products contiguous GEMMs; Sec. 3.2 gives every LoRA of a cluster the
  * same U_k, V_k).  Sorts the tokens by the key (cluster_of[adapter_id[t]],

@@ -7,5 +7,6 @@ binds it with ctypes.  torch is used only for device memory and streams.
 from ._binding import (CtsError, Problem, apply, apply_diag, apply_multi, apply_noalloc, apply_ranked,  # noqa: F401
                        apply_uncompressed,
                        apply_uncompressed_ranked, lib, make_problem,
-                       set_stage_events, sort_by_cluster, status_string, validate_ids, workspace_size, workspace_size_multi,
+                       set_stage_events, sort_by_cluster, status_string, validate_ids, workspace_bucketing, workspace_size,
+                       workspace_size_multi,
                        CTS_F32, CTS_BF16, NOALLOC_SCRATCH_BYTES)

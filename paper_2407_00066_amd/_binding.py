@@ -25,6 +25,7 @@ EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncom
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
             "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi", "cts_apply_noalloc",
+            "cts_workspace_bucketing",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
             "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
@@ -67,6 +68,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_workspace_size.restype = sz
                 L.cts_workspace_size_uncompressed.argtypes = [pp]
                 L.cts_workspace_size_uncompressed.restype = sz
+                L.cts_workspace_bucketing.argtypes = [pp, i32, ctypes.POINTER(sz)]
+                L.cts_workspace_bucketing.restype = ctypes.c_int
                 L.cts_sort_by_cluster.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp]
                 L.cts_sort_by_cluster.restype = ctypes.c_int
                 L.cts_apply.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -172,6 +175,14 @@ def make_problem(T, d_in, d_out, r=0, n_adapters=1, n_clusters=1, r_lora=0,
 def workspace_size(p: Problem, compressed: bool = True) -> int:
     f = lib().cts_workspace_size if compressed else lib().cts_workspace_size_uncompressed
     return int(f(ctypes.byref(p)))
+
+
+def workspace_bucketing(p: Problem, compressed: bool = True) -> dict:
+    """Byte offsets of the bucketing a completed call leaves in its workspace
+    (cts_workspace_bucketing): keys perm, seg, aid, items, n_items."""
+    offs = (ctypes.c_size_t * 5)()
+    _check(lib().cts_workspace_bucketing(ctypes.byref(p), 1 if compressed else 0, offs), "cts_workspace_bucketing")
+    return dict(zip(("perm", "seg", "aid", "items", "n_items"), (int(v) for v in offs)))
 
 
 def sort_by_cluster(adapter_id: torch.Tensor, cluster_of: torch.Tensor | None, n: int, K: int,

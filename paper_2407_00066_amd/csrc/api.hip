@@ -326,6 +326,19 @@ size_t cts_workspace_size_uncompressed(const cts_problem* p) {
   return make_plan(p, false, &pl) == CTS_OK ? pl.total : 0;
 }
 
+int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* offsets) {
+  if (!offsets) return CTS_ERR_INVALID_ARG;
+  Plan pl;
+  const int rc = make_plan(p, compressed != 0, &pl);
+  if (rc != CTS_OK) return rc;
+  offsets[0] = pl.off_perm;
+  offsets[1] = pl.off_seg;
+  offsets[2] = pl.off_aid;
+  offsets[3] = pl.off_items;
+  offsets[4] = pl.off_nitems;
+  return CTS_OK;
+}
+
 int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, int32_t T, int32_t n,
                         int32_t K, int32_t* perm, int32_t* cluster_offsets, void* stream) {
   if (T < 0 || n < 1 || K < 1 || !cluster_offsets) return CTS_ERR_INVALID_ARG;

@@ -218,3 +218,55 @@ def make(name: str, **overrides) -> Workload:
     spec = dict(CONFIGS[name])
     spec.update(overrides)
     return synthetic(name, **spec)
+
+
+# ---- the 32-layer stack's tensors, generated on the device ----------------
+# The stack holds ~32 GB of weights, so its tensors are drawn on the GPU with
+# torch's generator, each from a seed of its own (layer, projection, tensor),
+# so that any projection can be regenerated alone: the benchmark and the
+# parity test of its inputs draw the same values.  Variances: W ~N(0,1/d_in),
+# U ~N(0,1/d_out), V_k^T ~N(0,1/d_in) (Gaussian bases, not orthonormalized:
+# the layer's cost does not depend on it), Sigma ~N(0,1/r), x ~N(0,1).
+_STACK_SEED = SEED_BASE + 500_000
+STACK_TENSORS = ("W", "U", "Vt", "Sigma")
+
+
+def stack_ids():
+    """(adapter_id[T], cluster_of[n]) of the stack batch: uniform ids, one
+    balanced cluster map shared by all projections."""
+    rs = np.random.default_rng(SEED_BASE + 501)
+    aid = rs.integers(0, STACK["n"], STACK["T"]).astype(np.int32)
+    cof = balanced_clusters(rs, STACK["n"], STACK["K"])
+    return aid, cof
+
+
+def _stack_draw(torch, device, seed, shape, var):
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return (torch.randn(shape, generator=g, device=device) * float(np.sqrt(var))).to(torch.bfloat16)
+
+
+def stack_x(torch, device, d_in: int):
+    """The stack's input rows for projections reading d_in features: q/k/v
+    and gate/up share x[T][4096]; o gets its own x[T][4096] (index 1); down
+    x[T][14336]."""
+    return _stack_draw(torch, device, _STACK_SEED + d_in, (STACK["T"], d_in), 1.0)
+
+
+def stack_x_o(torch, device):
+    return _stack_draw(torch, device, _STACK_SEED + 1, (STACK["T"], 4096), 1.0)
+
+
+def stack_module(torch, device, layer: int, proj: str):
+    """(W, U, Vt, Sigma) of one projection of the stack (bf16, on device)."""
+    names = [p[0] for p in STACK_PROJ]
+    pi = names.index(proj)
+    _, d_in, d_out = STACK_PROJ[pi]
+    T, r, n, K = STACK["T"], STACK["r"], STACK["n"], STACK["K"]
+    shapes = {"W": ((d_out, d_in), 1.0 / d_in), "U": ((K, d_out, r), 1.0 / d_out),
+              "Vt": ((K, r, d_in), 1.0 / d_in), "Sigma": ((n, r, r), 1.0 / r)}
+    out = []
+    for ti, t in enumerate(STACK_TENSORS):
+        shape, var = shapes[t]
+        out.append(_stack_draw(torch, device, _STACK_SEED + 100_000 + 1000 * layer + 10 * pi + ti, shape, var))
+    return tuple(out)

@@ -74,7 +74,7 @@ def test_diag_matches_full_path_with_diagonal_sigma(cases):
 def test_apply_diag_full_size_sampled(oracle_mod, name):
     w = wl.make(name)
     sig = wl.sigma_diagonals(wl.CONFIGS[name]["cfg"], w.n, w.r, w.dtype)
-    toks = _sample_tokens(w, oracle_mod, cap=12)
+    toks = _sample_tokens(w, oracle_mod)
     say("apply_diag %s (full size), %d sampled tokens" % (name, len(toks)))
     y = cts.apply_diag(*_args(w, sig))
     torch.cuda.synchronize()

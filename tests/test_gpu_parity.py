@@ -76,6 +76,62 @@ def test_sort_bit_exact(oracle_mod, T, n, K, kind):
 
 
 # --------------------------------------------------------------------------
+# the bucketing each layer call actually runs (for T <= 128 bf16 batches it
+# happens inside the shrink kernel, for larger ones in the sort kernel),
+# read back from the call's workspace and compared bit for bit with the
+# oracle's sort and the runs derived from it
+
+BUCKET_CASES = [c for c in SORT_CASES if 0 < c[0] <= 128] + [
+    (128, 1000, 50, "zipf"), (100, 65536, 65536, "uniform"), (128, 20, 4, "runs7"),
+    (96, 300, 7, "runs30"), (17, 4, 4, "same"), (127, 6, 3, "reverse"), (2, 2, 2, "uniform"),
+    (129, 1000, 50, "uniform"), (4096, 1000, 25, "zipf"), (600, 40, 30, "empty"),
+]
+
+
+def _expected_bucketing(aid, cof, perm):
+    """seg, aid and core-product items of the sorted order perm: items are
+    the sorted positions where a run of one (cluster, adapter) starts or
+    crosses a multiple of 16."""
+    a = aid[perm]
+    seg = cof[a] if cof is not None else a
+    T = len(perm)
+    items = [j for j in range(T) if j % 16 == 0 or seg[j] != seg[j - 1] or a[j] != a[j - 1]]
+    return seg.astype(np.int32), a.astype(np.int32), np.array(items + [T], np.int32)
+
+
+def _read_i32(ws, off, count):
+    return ws[off:off + 4 * count].cpu().numpy().view(np.int32).copy()
+
+
+@pytest.mark.parametrize("T,n,K,kind", BUCKET_CASES)
+def test_layer_bucketing_bit_exact(oracle_mod, T, n, K, kind):
+    aid, cof = _sort_case(T, n, K, kind, seed=7 * T + 13 * n + K)
+    compressed = kind != "identity"
+    d, r = 64, 8
+    say("layer bucketing T=%d n=%d K=%d %s (%s)" % (T, n, K, kind, "compressed" if compressed else "uncompressed"))
+    z = lambda *shape: torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    if compressed:
+        p = cts.make_problem(T, d, d, r=r, n_adapters=n, n_clusters=K)
+        ws = torch.full((cts.workspace_size(p),), 0xAB, dtype=torch.uint8, device="cuda")
+        cts.apply(z(T, d), dev(aid), dev(cof), z(d, d), z(K, d, r), z(K, r, d), z(n, r, r), workspace=ws)
+    else:
+        K = n
+        p = cts.make_problem(T, d, d, n_adapters=n, r_lora=r)
+        ws = torch.full((cts.workspace_size(p, compressed=False),), 0xAB, dtype=torch.uint8, device="cuda")
+        cts.apply_uncompressed(z(T, d), dev(aid), z(d, d), z(n, r, d), z(n, d, r), workspace=ws)
+    torch.cuda.synchronize()
+    off = cts.workspace_bucketing(p, compressed)
+    rp, _ = oracle_mod.sort_by_cluster(aid, cof if compressed else None, n, K)
+    seg, a, items = _expected_bucketing(aid, cof if compressed else None, rp)
+    np.testing.assert_array_equal(_read_i32(ws, off["perm"], T), rp)
+    np.testing.assert_array_equal(_read_i32(ws, off["seg"], T), seg)
+    np.testing.assert_array_equal(_read_i32(ws, off["aid"], T), a)
+    c = int(_read_i32(ws, off["n_items"], 1)[0])
+    assert c == len(items) - 1
+    np.testing.assert_array_equal(_read_i32(ws, off["items"], c + 1), items)
+
+
+# --------------------------------------------------------------------------
 # small and medium cases: every output compared
 
 SMALL = {
@@ -143,6 +199,72 @@ def test_uncompressed_small(oracle_mod, small_cases, name):
     ref = oracle_mod.apply_uncompressed(w.x, w.adapter_id, w.W, w.A, w.B)
     err = row_rel_err(host(y), ref)
     assert err <= TOL[w.dtype], err
+
+
+# --------------------------------------------------------------------------
+# the adapter term alone: W = 0, so y = U_k Sigma_i V_k^T x (resp. B_i A_i x)
+# and the error is measured against that term's own row maximum (with W the
+# adapter term is about 1/8 of the output, so an error in it would be hidden
+# by the base term's scale).  Every bf16 tile shape: Narrow, Mid, Wide with a
+# split along d_in, Large, Decode (split in four), the bucketing inside the
+# shrink (T <= 128) and the separate sort.
+
+ADAPTER_TERM_CASES = ["bf16_ragged", "bf16_large_tiles", "bf16_r128_zipf", "bf16_ring_ragged",
+                      "bf16_wide_split", "bf16_decode_ragged", "bf16_decode_split4", "bf16_mid_tiles",
+                      "bf16_k_eq_n", "bf16_T1"]
+
+
+def _zero_base(w):
+    return np.zeros_like(w.W)
+
+
+@pytest.mark.parametrize("name", ADAPTER_TERM_CASES)
+def test_adapter_term_alone(oracle_mod, small_cases, name):
+    w = small_cases[name]
+    W0 = _zero_base(w)
+    say("adapter term alone %s T=%d" % (name, w.T))
+    y = cts.apply(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(W0), dev(w.U), dev(w.Vt), dev(w.Sigma))
+    yu = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(W0), dev(w.A), dev(w.B))
+    torch.cuda.synchronize()
+    ref = oracle_mod.apply(w.x, w.adapter_id, w.cluster_of, W0, w.U, w.Vt, w.Sigma)
+    refu = oracle_mod.apply_uncompressed(w.x, w.adapter_id, W0, w.A, w.B)
+    assert np.abs(ref).max() > 0
+    err, erru = row_rel_err(host(y), ref), row_rel_err(host(yu), refu)
+    assert err <= TOL["bf16"], err
+    assert erru <= TOL["bf16"], erru
+
+
+@pytest.mark.parametrize("name", ["bf16_ragged", "bf16_decode_split4", "bf16_ring_ragged", "bf16_wide_split"])
+def test_adapter_term_alone_variants(oracle_mod, small_cases, name):
+    """W = 0 through the diagonal-Sigma, mixed-rank and multi-module entry
+    points."""
+    w = small_cases[name]
+    kw = SMALL[name]
+    W0 = _zero_base(w)
+    x, aid, cof = dev(w.x), dev(w.adapter_id), dev(w.cluster_of)
+    say("adapter term alone (diag, ranked, multi) %s" % name)
+    sig = wl.sigma_diagonals(kw["cfg"], w.n, w.r, w.dtype)
+    yd = cts.apply_diag(x, aid, cof, dev(W0), dev(w.U), dev(w.Vt), dev(sig))
+    rk = wl.mixed_ranks(kw["cfg"], w.K, w.r, lo=8)
+    yr = cts.apply_ranked(x, aid, cof, dev(W0), dev(w.U), dev(w.Vt), dev(w.Sigma), dev(rk))
+    ra = wl.mixed_ranks(kw["cfg"] + 500, w.n, w.r_l, lo=8)
+    yur = cts.apply_uncompressed_ranked(x, aid, dev(W0), dev(w.A), dev(w.B), dev(ra))
+    # two modules: the layer's own arrays and a second set with W = 0 too
+    w2 = wl.synthetic(name + "_m2", **dict(kw, cfg=kw["cfg"] + 900, with_lora=False))
+    Vt2 = np.concatenate([w.Vt, w2.Vt], axis=1)
+    ym = cts.apply_multi(x, aid, cof, [dev(W0), dev(np.zeros_like(w2.W))], [dev(w.U), dev(w2.U)], dev(Vt2),
+                         [dev(w.Sigma), dev(w2.Sigma)])
+    torch.cuda.synchronize()
+    checks = [
+        (yd, oracle_mod.apply_diag(w.x, w.adapter_id, w.cluster_of, W0, w.U, w.Vt, sig)),
+        (yr, oracle_mod.apply_ranked(w.x, w.adapter_id, w.cluster_of, W0, w.U, w.Vt, w.Sigma, rk)),
+        (yur, oracle_mod.apply_uncompressed_ranked(w.x, w.adapter_id, W0, w.A, w.B, ra)),
+    ] + list(zip(ym, oracle_mod.apply_multi(w.x, w.adapter_id, w.cluster_of, [W0, np.zeros_like(w2.W)],
+                                            [w.U, w2.U], Vt2, [w.Sigma, w2.Sigma])))
+    for i, (y, ref) in enumerate(checks):
+        assert np.abs(ref).max() > 0, i
+        err = row_rel_err(host(y), ref)
+        assert err <= TOL["bf16"], (i, err)
 
 
 def test_tiny_exact_compressed_equals_uncompressed(oracle_mod):
@@ -271,19 +393,23 @@ def test_shrink_split_follows_tile_count(oracle_mod):
 # --------------------------------------------------------------------------
 # full-size workloads: sampled tokens
 
-def _sample_tokens(w, oracle_mod, extra=6, cap=14):
+def _sample_tokens(w, oracle_mod, extra=6, max_bounds=8):
+    """Tokens at the positions a tiling can get wrong, in the cluster-sorted
+    order: the first and last position, both sides of every multiple of 64
+    (one token per 64-column tile at least), and both sides of the first
+    max_bounds cluster boundaries; then `extra` random positions.  Every
+    position of the first two kinds is kept (the oracle's cost is one
+    d_out x d_in update per distinct adapter among them)."""
     perm, offs = oracle_mod.sort_by_cluster(w.adapter_id, w.cluster_of, w.n, w.K)
     pos = {0, w.T - 1}
-    for b in (63, 64, 127, 128):
-        if b < w.T:
-            pos.add(b)
-    for k in range(1, min(w.K, 4)):
-        if 0 < offs[k] < w.T:
-            pos.update({int(offs[k]) - 1, int(offs[k])})
+    for b in range(64, w.T, 64):
+        pos.update({b - 1, b})
+    bounds = [int(o) for o in offs[1:-1] if 0 < o < w.T]
+    for o in sorted(set(bounds))[:max_bounds]:
+        pos.update({o - 1, o})
     rs = np.random.default_rng(w.T)
     pos.update(rs.integers(0, w.T, extra).tolist())
-    toks = sorted({int(perm[j]) for j in pos})
-    return np.array(toks[:cap], np.int64)
+    return np.array(sorted({int(perm[j]) for j in pos}), np.int64)
 
 
 @pytest.fixture(scope="module")
@@ -301,7 +427,7 @@ def _full(full_cases, name):
 @pytest.mark.parametrize("name", ["decode_q", "prefill_mix", "mlp_up"])
 def test_full_config_sampled(oracle_mod, full_cases, name):
     w = _full(full_cases, name)
-    toks = _sample_tokens(w, oracle_mod, cap=14 if name != "mlp_up" else 8)
+    toks = _sample_tokens(w, oracle_mod)
     say("apply %s (full size), %d sampled tokens" % (name, len(toks)))
     y = cts.apply(*_inputs(w))
     torch.cuda.synchronize()
@@ -316,7 +442,7 @@ def test_full_config_sampled(oracle_mod, full_cases, name):
 def test_stack_projection_sampled(oracle_mod, full_cases, name):
     """Each distinct projection shape of the 32-layer decoder stack at full size."""
     w = _full(full_cases, name)
-    toks = _sample_tokens(w, oracle_mod, cap=8)
+    toks = _sample_tokens(w, oracle_mod, max_bounds=4)
     say("apply %s (full size), %d sampled tokens" % (name, len(toks)))
     y = cts.apply(*_inputs(w))
     torch.cuda.synchronize()
@@ -331,7 +457,7 @@ def test_stack_projection_sampled(oracle_mod, full_cases, name):
 @pytest.mark.parametrize("name", ["decode_q", "prefill_mix", "mlp_up"])
 def test_full_config_uncompressed_sampled(oracle_mod, full_cases, name):
     w = _full(full_cases, name)
-    toks = _sample_tokens(w, oracle_mod, cap=10 if name != "mlp_up" else 6)
+    toks = _sample_tokens(w, oracle_mod)
     say("apply_uncompressed %s (full size), %d sampled tokens" % (name, len(toks)))
     y = cts.apply_uncompressed(dev(w.x), dev(w.adapter_id), dev(w.W), dev(w.A), dev(w.B))
     torch.cuda.synchronize()

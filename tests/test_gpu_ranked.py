@@ -93,7 +93,7 @@ def test_apply_ranked_prefill_full_size(oracle_mod):
     w = wl.make("prefill_mix")
     rk = wl.mixed_ranks(wl.CONFIGS["prefill_mix"]["cfg"], w.K, w.r)
     U, Vt, S = _poisoned_compressed(w, rk)
-    toks = _sample_tokens(w, oracle_mod, cap=10)
+    toks = _sample_tokens(w, oracle_mod)
     say("apply_ranked prefill_mix (full size), %d sampled tokens" % len(toks))
     y = cts.apply_ranked(dev(w.x), dev(w.adapter_id), dev(w.cluster_of), dev(w.W), dev(U), dev(Vt),
                          dev(S), dev(rk))
