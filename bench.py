@@ -17,6 +17,11 @@ step) are reported under "graph_replay".  Single-layer inputs are rotated over e
 total) that the 256 MB last-level cache cannot hold them between steps; the
 stack's weights (about 32 GB) are distinct per projection anyway.
 
+By default (--workload all) the line's throughput is prefill_mix's (4096
+tokens of a 4096 x 4096 projection, 1000 LoRAs in 25 clusters), and the other
+four configurations (decode_q, mlp_up, tiny_fp32, stack32) are measured in
+the same run and reported under "configs", each with the keys below.
+
 One JSON line is printed.  Besides the throughput it carries:
   roofline        the dominant kernel (the fused GEMM): algorithmic flops or
                   bytes of one launch over its mean duration, measured here
@@ -29,6 +34,8 @@ One JSON line is printed.  Besides the throughput it carries:
   single_adapter  the same batch with every token on one LoRA (n = K = 1);
                   ratio = this throughput / that one
   stages_us       mean duration of each stage of the layer (per step)
+  layer_roofline  the whole layer call (all stages, ms_per_step) against the
+                  chip: algorithmic flops or bytes of the layer over the step
 
 --workload jd_full measures the offline compressor instead (cts_jd_full, the
 eigenvalue iteration of App. A.2 on 1000 rank-16 LoRAs of a 4096 x 4096
@@ -87,6 +94,26 @@ def main_kernel_model(w, touched_clusters, ranks=None):
     return flops, nbytes
 
 
+def layer_model(T, d_in, d_out, r, e, touched_clusters, distinct_adapters, sigma_elems=None):
+    """Algorithmic flops and bytes of one whole layer call: W X + U_k Sigma_i
+    V_k^T X with every touched U_k, V_k and Sigma_i read once, X read and Y
+    written once (the bucketing's ids and the intermediates Z, Z' are under
+    1% and not counted)."""
+    sig = r * r if sigma_elems is None else sigma_elems
+    flops = 2.0 * T * d_in * d_out + 2.0 * T * (d_in * r + sig + d_out * r)
+    nbytes = e * (d_out * d_in + T * d_in + T * d_out + touched_clusters * r * (d_in + d_out)
+                  + distinct_adapters * sig)
+    return flops, nbytes
+
+
+def layer_roofline(flops, nbytes, t_s, dtype):
+    """The whole layer call against the chip: its algorithmic flops or bytes
+    (whichever bound is tighter) over the measured step time."""
+    roof = roofline_of(flops, nbytes, t_s, dtype)
+    return {"bound": roof["bound"], "achieved": roof["achieved"], "unit": roof["unit"], "frac": roof["frac"],
+            "algorithmic_flops": flops, "algorithmic_bytes": nbytes}
+
+
 def cpu_baseline(w, target_s, sigma=None, ranks=None):
     """The oracle on a prefix of the batch (in batch order), grown until about
     target_s seconds of oracle time; tokens/s = tokens / oracle seconds.  With
@@ -108,10 +135,21 @@ def cpu_baseline(w, target_s, sigma=None, ranks=None):
         per_tok = spent / done
         chunk = int(max(1, min(w.T - done, (target_s - spent) / per_tok + 1)))
     distinct = len(set(w.adapter_id[:done].tolist()))
+    sample = "first %d of %d tokens of the batch (%d distinct adapters)" % (done, w.T, distinct)
+    # a batch the oracle finishes early is run again, whole, until about
+    # target_s seconds (at most 20 passes)
+    passes = 1
+    if done == w.T:
+        while spent < target_s and passes < 20:
+            tm = {}
+            fn(f64[0], w.adapter_id, w.cluster_of, f64[1], f64[2], f64[3], f64[4], timing=tm)
+            spent += tm["s"]
+            done += w.T
+            passes += 1
+        sample = "the whole batch of %d tokens (%d distinct adapters), %d pass%s" % (
+            w.T, distinct, passes, "" if passes == 1 else "es")
     return {"value": done / spent, "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": "first %d of %d tokens of the batch (%d distinct adapters), %.1f s of "
-                      "fp64 oracle time" % (done, w.T, distinct, spent)}
+            "kind": "oracle", "sample": sample + ", %.1f s of fp64 oracle time" % spent}
 
 
 def copy_calibration(torch, device, nbytes=256 << 20, reps=3):
@@ -439,7 +477,9 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         layer1 = lambda *a, **k: cts.apply_ranked(*a, rk_d[:1], **k)
 
     set_bytes = sum(a.nbytes for a in (w.x, w.W, w.U, w.Vt, w.Sigma))
-    n_sets = max(1, math.ceil(2 * MALL_BYTES / set_bytes))
+    # (at most 64: a set that small stays in the last-level cache whatever
+    # the rotation, and its launches, not its bytes, set the pace)
+    n_sets = min(64, max(1, math.ceil(2 * MALL_BYTES / set_bytes)))
     base = [to_dev(a, device) for a in (w.x, w.W, w.U, w.Vt, w.Sigma)]
     sets = [base] + [[t.clone() for t in base] for _ in range(n_sets - 1)]
     aid = to_dev(w.adapter_id, device)
@@ -508,6 +548,9 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     value = w.T / (ms * 1e-3)
     value1 = w.T / (ms1 * 1e-3)
+    distinct = len(set(w.adapter_id.tolist()))
+    lf, lb = layer_model(w.T, w.d_in, w.d_out, w.r, 2 if w.dtype == "bf16" else 4, touched, distinct,
+                         sigma_elems=w.r if diag else None)
     return {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
@@ -519,6 +562,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
                    "n_adapters": w.n, "n_clusters": w.K, "touched_clusters": touched,
                    "distinct_adapters": len(set(w.adapter_id.tolist())), "parallelism": "single GPU"},
         "roofline": roof,
+        "layer_roofline": layer_roofline(lf, lb, ms * 1e-3, w.dtype),
         "cpu_baseline": cpu,
         "uncompressed": {"value": round(w.T / (ms_u * 1e-3), 1), "unit": "tokens/s",
                          "ms_per_step": round(ms_u, 5), "graph_replay_ms_per_step": round(ms_u_g, 5),
@@ -634,6 +678,31 @@ def bench_stack(args, torch, np, cts, B, wl, device):
     log("timing the stack with one adapter")
     ms1, ms1_g = time_launches(step1, [None], args, torch)
 
+    # the uncompressed comparison: every projection with its 1000 rank-16
+    # LoRAs (A_i, B_i) resident, one cts_apply_uncompressed call each
+    r_l = 16
+    log("generating the stack's uncompressed LoRAs on the device")
+    loras = [{name: wl.stack_lora(torch, device, li, name, r_l) for name, _, _ in wl.STACK_PROJ}
+             for li in range(wl.STACK_LAYERS)]
+    lora_bytes = sum(t.numel() * t.element_size() for L in loras for v in L.values() for t in v)
+    wszu = 1
+    for name, d_in, d_out in wl.STACK_PROJ:
+        pu = cts.make_problem(T, d_in, d_out, n_adapters=n, r_lora=r_l, dtype=B.CTS_BF16)
+        wszu = max(wszu, cts.workspace_size(pu, compressed=False))
+    wsu = torch.empty(wszu, dtype=torch.uint8, device=device)
+
+    def step_u(_):
+        for L, LA in zip(projs, loras):
+            for name, _, _ in wl.STACK_PROJ:
+                x, W, _U, _V, _S, y = L[name]
+                A_, B_ = LA[name]
+                cts.apply_uncompressed(x, aid, W, A_, B_, out=y, workspace=wsu)
+
+    log("timing the uncompressed stack: %.1f GB of LoRAs" % (lora_bytes / 1e9))
+    ms_u, ms_u_g = time_launches(step_u, [None], args, torch)
+    del loras, wsu
+    torch.cuda.empty_cache()
+
     # per-call stage events over a few steps: the GEMM time of a step
     n_ev = min(args.steps, 3)
     calls = wl.STACK_LAYERS * len(wl.STACK_PROJ)
@@ -684,6 +753,12 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                  "mean_us": round(gemm_us / calls, 2), "event_interval_us": round(g_int / calls, 2),
                  "marker_us": round(g_mark / calls, 2),
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes})
+    lf = lb = 0.0
+    distinct = len(set(aid_h.tolist()))
+    for name, d_in, d_out in wl.STACK_PROJ:
+        f, b = layer_model(T, d_in, d_out, r, 2, touched, distinct)
+        lf += f * wl.STACK_LAYERS
+        lb += b * wl.STACK_LAYERS
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (about %.0f s)" % args.cpu_seconds)
@@ -705,11 +780,48 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                    "n_clusters": K, "touched_clusters": touched,
                    "distinct_adapters": len(set(aid_h.tolist())), "parallelism": "single GPU"},
         "roofline": roof,
+        "layer_roofline": layer_roofline(lf, lb, ms * 1e-3, "bf16"),
         "cpu_baseline": cpu,
         "single_adapter": {"value": round(value1, 1), "unit": "tokens/s", "ms_per_step": round(ms1, 5),
                            "graph_replay_ms_per_step": round(ms1_g, 5), "ratio": round(value / value1, 4)},
+        "uncompressed": {"value": round(T / (ms_u * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms_u, 5),
+                         "graph_replay_ms_per_step": round(ms_u_g, 5), "r_lora": r_l,
+                         "resident_lora_gb": round(lora_bytes / 1e9, 1),
+                         "note": "every projection its own cts_apply_uncompressed call"},
         "stages_us": {k: round(v, 2) for k, v in stages.items()},
     }
+
+
+# Every configuration of the layer: the headline line (prefill_mix) carries
+# the other four under "configs", each measured the same way in this run.
+ALL_CONFIGS = ("decode_q", "mlp_up", "tiny_fp32", "stack32")
+SUB_KEYS = ("value", "unit", "ms_per_step", "graph_replay", "dtype", "data", "config", "roofline",
+            "layer_roofline", "cpu_baseline", "uncompressed", "single_adapter", "separate_calls", "stages_us")
+
+
+def bench_all(args, torch, np, cts, B, wl, device):
+    import copy
+    import gc
+    a = copy.copy(args)
+    a.workload = "prefill_mix"
+    rec = bench_layer(a, torch, np, cts, B, wl, device)
+    rec["configs"] = {}
+    for name in ALL_CONFIGS:
+        gc.collect()
+        torch.cuda.empty_cache()
+        a = copy.copy(args)
+        a.workload = name
+        t0 = time.time()
+        sub = bench_stack(a, torch, np, cts, B, wl, device) if name == "stack32" else \
+            bench_layer(a, torch, np, cts, B, wl, device)
+        sub = {k: sub[k] for k in SUB_KEYS if k in sub}
+        sub["steps"], sub["warmup"] = a.steps, a.warmup
+        sub["bench_seconds"] = round(time.time() - t0, 1)
+        rec["configs"][name] = sub
+        log("%s: %.1f tokens/s, %.5f ms per step" % (name, sub["value"], sub["ms_per_step"]))
+    gc.collect()
+    torch.cuda.empty_cache()
+    return rec
 
 
 def main():
@@ -717,8 +829,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="prefill_mix",
-                    choices=["prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32", "jd_full", "jd_diag"])
+    ap.add_argument("--workload", default="all",
+                    choices=["all", "prefill_mix", "decode_q", "mlp_up", "tiny_fp32", "stack32", "jd_full",
+                             "jd_diag"],
+                    help="all (the default): prefill_mix as the headline line, the other four "
+                         "configurations under its key 'configs'")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sigma", default="full", choices=["full", "diag"],
@@ -733,7 +848,7 @@ def main():
     if args.sigma == "diag" and args.ranks == "mixed":
         print("--sigma diag and --ranks mixed are separate variants", file=sys.stderr)
         sys.exit(2)
-    if args.workload in ("stack32", "jd_full", "jd_diag") and (args.sigma != "full" or args.ranks != "uniform"):
+    if args.workload in ("all", "stack32", "jd_full", "jd_diag") and (args.sigma != "full" or args.ranks != "uniform"):
         print("--sigma diag and --ranks mixed apply to the single-layer workloads", file=sys.stderr)
         sys.exit(2)
 
@@ -756,6 +871,8 @@ def main():
     copy_calibration(torch, device)
     if args.workload in ("jd_full", "jd_diag"):
         rec = bench_jd(args, torch, np, cts, B, device)
+    elif args.workload == "all":
+        rec = bench_all(args, torch, np, cts, B, wl, device)
     elif args.workload == "stack32":
         rec = bench_stack(args, torch, np, cts, B, wl, device)
     else:

@@ -270,3 +270,17 @@ def stack_module(torch, device, layer: int, proj: str):
         shape, var = shapes[t]
         out.append(_stack_draw(torch, device, _STACK_SEED + 100_000 + 1000 * layer + 10 * pi + ti, shape, var))
     return tuple(out)
+
+
+def stack_lora(torch, device, layer: int, proj: str, r_l: int = 16):
+    """(A, B) of one projection's uncompressed rank-16 LoRAs for the
+    comparison path (bf16, on device): A ~N(0,1/d_in), B ~N(0,1/(64 r_l)),
+    so the adapter term is about 1/8 of the base term, as for the shared
+    bases."""
+    names = [p[0] for p in STACK_PROJ]
+    pi = names.index(proj)
+    _, d_in, d_out = STACK_PROJ[pi]
+    n = STACK["n"]
+    seed = _STACK_SEED + 200_000 + 1000 * layer + 10 * pi
+    return (_stack_draw(torch, device, seed, (n, r_l, d_in), 1.0 / d_in),
+            _stack_draw(torch, device, seed + 1, (n, d_out, r_l), 1.0 / (64 * r_l)))
