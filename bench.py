@@ -614,15 +614,14 @@ def bench_stack(args, torch, np, cts, B, wl, device):
     xs = {4096: wl.stack_x(torch, device, 4096), 14336: wl.stack_x(torch, device, 14336)}
     x_o = wl.stack_x_o(torch, device)
     ys = {d: torch.empty((T, d), dtype=torch.bfloat16, device=device) for d in (1024, 4096, 14336)}
-    projs, wsz, wsz1 = [], 1, 1
+    projs, wsz = [], 1
     for li in range(wl.STACK_LAYERS):
         layer = {}
         for name, d_in, d_out in wl.STACK_PROJ:
             layer[name] = ((x_o if name == "o" else xs[d_in]),) + wl.stack_module(torch, device, li, name) + \
                 (ys[d_out],)
             pb = cts.make_problem(T, d_in, d_out, r=r, n_adapters=n, n_clusters=K, dtype=B.CTS_BF16)
-            p1 = cts.make_problem(T, d_in, d_out, r=r, n_adapters=1, n_clusters=1, dtype=B.CTS_BF16)
-            wsz, wsz1 = max(wsz, cts.workspace_size(pb)), max(wsz1, cts.workspace_size(p1))
+            wsz = max(wsz, cts.workspace_size(pb))
         projs.append(layer)
     # multi-module batching: q/k/v and gate/up each read one x; their V_k^T
     # stacked along r (separate outputs, since the modules run in one call)
@@ -635,16 +634,26 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         stacked.append({grp: torch.cat([L[nm][3] for nm in grp], dim=1).contiguous() for grp in groups})
     outs_of = {("q", "k", "v"): [ys[4096], extra_y[("k",)], extra_y[("v",)]],
                ("gate", "up"): [ys[14336], extra_y[("up",)]]}
-    wszm = 1
-    for grp in groups:
+    wszm = wszm1 = 1
+    for grp in groups + (("o",), ("down",)):
         d_in = dict((nm, di) for nm, di, _ in wl.STACK_PROJ)[grp[0]]
         dims = [dict((nm, do) for nm, _, do in wl.STACK_PROJ)[g_] for g_ in grp]
         pm = cts.make_problem(T, d_in, 8, r=r, n_adapters=n, n_clusters=K, dtype=B.CTS_BF16)
         wszm = max(wszm, cts.workspace_size_multi(pm, dims))
+        pm1 = cts.make_problem(T, d_in, 8, r=r, n_adapters=1, n_clusters=1, dtype=B.CTS_BF16)
+        wszm1 = max(wszm1, cts.workspace_size_multi(pm1, dims))
     torch.cuda.synchronize()
     ws = torch.empty(wsz, dtype=torch.uint8, device=device)
-    ws1 = torch.empty(wsz1, dtype=torch.uint8, device=device)
     wsm = torch.empty(wszm, dtype=torch.uint8, device=device)
+    wsm1 = torch.empty(wszm1, dtype=torch.uint8, device=device)
+    # one bucketing of the batch for the whole step (every projection shares
+    # the cluster map): perm and the sort's workspace
+    perm_s = torch.empty(T, dtype=torch.int32, device=device)
+    offs_s = torch.empty(K + 1, dtype=torch.int32, device=device)
+    bk = torch.empty(cts.bucketing_size(T, n, K), dtype=torch.uint8, device=device)
+    perm_1 = torch.empty(T, dtype=torch.int32, device=device)
+    offs_1 = torch.empty(2, dtype=torch.int32, device=device)
+    bk1 = torch.empty(cts.bucketing_size(T, 1, 1), dtype=torch.uint8, device=device)
     aid1 = torch.zeros_like(aid)
     cof1 = torch.zeros(1, dtype=torch.int32, device=device)
     resident = sum(t.numel() * t.element_size() for L in projs for v in L.values() for t in v[1:5])
@@ -665,16 +674,37 @@ def bench_stack(args, torch, np, cts, B, wl, device):
                     cts.apply_multi(L[grp[0]][0], aid, cof, [L[nm][1] for nm in grp], [L[nm][2] for nm in grp],
                                     SV[grp], [L[nm][4] for nm in grp], outs=outs_of[grp], workspace=wsm)
 
+    def step_shared(_):
+        cts.sort_by_cluster(aid, cof, n, K, perm=perm_s, offsets=offs_s, bucketing=bk)
+        for L, SV in zip(projs, stacked):
+            for grp in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+                if len(grp) == 1:
+                    x, W, U, Vt, S, y = L[grp[0]]
+                    cts.apply_multi_sorted(perm_s, bk, x, [W], [U], Vt, [S], outs=[y], workspace=wsm)
+                else:
+                    cts.apply_multi_sorted(perm_s, bk, L[grp[0]][0], [L[nm][1] for nm in grp],
+                                           [L[nm][2] for nm in grp], SV[grp], [L[nm][4] for nm in grp],
+                                           outs=outs_of[grp], workspace=wsm)
+
     def step1(_):
-        for L in projs:
-            for name, _, _ in wl.STACK_PROJ:
-                x, W, U, Vt, S, y = L[name]
-                cts.apply(x, aid1, cof1, W, U[:1], Vt[:1], S[:1], out=y, workspace=ws1)
+        # the same calls with every token on LoRA 0 of cluster 0 (n = K = 1)
+        cts.sort_by_cluster(aid1, cof1, 1, 1, perm=perm_1, offsets=offs_1, bucketing=bk1)
+        for L, SV in zip(projs, stacked):
+            for grp in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+                if len(grp) == 1:
+                    x, W, U, Vt, S, y = L[grp[0]]
+                    cts.apply_multi_sorted(perm_1, bk1, x, [W], [U[:1]], Vt[:1], [S[:1]], outs=[y], workspace=wsm1)
+                else:
+                    cts.apply_multi_sorted(perm_1, bk1, L[grp[0]][0], [L[nm][1] for nm in grp],
+                                           [L[nm][2][:1] for nm in grp], SV[grp][:1], [L[nm][4][:1] for nm in grp],
+                                           outs=outs_of[grp], workspace=wsm1)
 
     log("timing the stack: %.1f GB of weights, %d warmup + %d steps" % (resident / 1e9, args.warmup, args.steps))
     ms_sep, ms_sep_g = time_launches(step, [None], args, torch)
-    log("timing the stack with q/k/v and gate/up batched (cts_apply_multi)")
-    ms, ms_g = time_launches(step_multi, [None], args, torch)
+    log("timing the stack with q/k/v and gate/up batched (cts_apply_multi), a sort per call")
+    ms_m, ms_m_g = time_launches(step_multi, [None], args, torch)
+    log("timing the stack with one sort per step (cts_apply_multi_sorted)")
+    ms, ms_g = time_launches(step_shared, [None], args, torch)
     log("timing the stack with one adapter")
     ms1, ms1_g = time_launches(step1, [None], args, torch)
 
@@ -768,6 +798,10 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         "separate_calls": {"value": round(T / (ms_sep * 1e-3), 1), "ms_per_step": round(ms_sep, 5),
                            "graph_replay_ms_per_step": round(ms_sep_g, 5),
                            "note": "every projection its own cts_apply call"},
+        "sort_per_call": {"value": round(T / (ms_m * 1e-3), 1), "ms_per_step": round(ms_m, 5),
+                          "graph_replay_ms_per_step": round(ms_m_g, 5),
+                          "note": "q/k/v and gate/up per cts_apply_multi call, o and down per cts_apply call, "
+                                  "each call sorting the ids itself"},
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -775,7 +809,8 @@ def bench_stack(args, torch, np, cts, B, wl, device):
         "dtype": "bf16",
         "data": "synthetic (seeded, generated on the device; %.1f GB of weights resident in HBM)" % (resident / 1e9),
         "config": {"workload": "stack32", "T": T, "layers": wl.STACK_LAYERS,
-                   "batching": "q/k/v and gate/up per cts_apply_multi call, o and down per cts_apply call",
+                   "batching": "one cts_sort_by_cluster per step; q/k/v and gate/up per "
+                               "cts_apply_multi_sorted call (V_k^T stacked), o and down per call of their own",
                    "projections": [list(pr) for pr in wl.STACK_PROJ], "r": r, "n_adapters": n,
                    "n_clusters": K, "touched_clusters": touched,
                    "distinct_adapters": len(set(aid_h.tolist())), "parallelism": "single GPU"},
@@ -796,7 +831,8 @@ def bench_stack(args, torch, np, cts, B, wl, device):
 # the other four under "configs", each measured the same way in this run.
 ALL_CONFIGS = ("decode_q", "mlp_up", "tiny_fp32", "stack32")
 SUB_KEYS = ("value", "unit", "ms_per_step", "graph_replay", "dtype", "data", "config", "roofline",
-            "layer_roofline", "cpu_baseline", "uncompressed", "single_adapter", "separate_calls", "stages_us")
+            "layer_roofline", "cpu_baseline", "uncompressed", "single_adapter", "separate_calls", "sort_per_call",
+            "stages_us")
 
 
 def bench_all(args, torch, np, cts, B, wl, device):

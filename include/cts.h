@@ -124,10 +124,18 @@ int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* of
  *   perm[j]            = token with the j-th smallest key        (int32 [T])
  *   cluster_offsets[k] = number of tokens whose cluster is < k   (int32 [K+1])
  * cluster_of == NULL means every adapter is its own cluster (then K == n).
- * All arrays are device memory; T == 0 writes only cluster_offsets (zeros). */
+ * workspace: NULL, or device memory of at least cts_bucketing_size(T, n, K)
+ * bytes (16-byte aligned), which then receives the rest of the bucketing the
+ * layer uses (each sorted position's cluster and adapter, the runs of one
+ * adapter and of one cluster): with perm, it is the `bucketing` argument of
+ * cts_apply_multi_sorted, so that the modules of a whole model share one sort
+ * per batch.  All arrays are device memory; T == 0 writes only
+ * cluster_offsets (zeros).  Limits: T <= 8192, n and K <= 65536. */
+size_t cts_bucketing_size(int32_t T, int32_t n, int32_t K);
 int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of,
                         int32_t T, int32_t n, int32_t K,
-                        int32_t* perm, int32_t* cluster_offsets, void* stream);
+                        int32_t* perm, int32_t* cluster_offsets,
+                        void* workspace, size_t workspace_bytes, void* stream);
 
 /* Compressed multi-adapter layer: overwrites y[t] with
  * W x_t + U_k Sigma_i V_k^T x_t for every token (Sec. 3.1, 3.2, App. D).
@@ -219,6 +227,23 @@ int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const
 int cts_apply_noalloc(const cts_problem* p, const void* x, const int32_t* adapter_id,
                       const int32_t* cluster_of, const void* W, const void* U,
                       const void* Vt, const void* Sigma, void* y, void* stream);
+
+/* cts_apply_multi with a bucketing computed once for the batch by
+ * cts_sort_by_cluster (perm and its workspace `bucketing`, bucketing_bytes
+ * >= cts_bucketing_size(T, n, K)) instead of sorting the ids again: every
+ * module of every layer of a model whose LoRAs share one cluster map
+ * (Sec. 3.2) can take the same bucketing.  The sort must have been made with
+ * p->T tokens, n = p->n_adapters and K = p->n_clusters and a cluster map
+ * (not NULL), and have completed on `stream` (or a stream ordered before
+ * it); the ids themselves are not arguments.  M = 1 is cts_apply's layer.
+ * Same limits, layouts, results and errors as cts_apply_multi, and the same
+ * workspace (cts_workspace_size_multi bytes); outputs must not overlap perm
+ * or the bucketing either. */
+int cts_apply_multi_sorted(const cts_problem* p, int32_t M, const int32_t* d_out,
+                           const int32_t* perm, const void* bucketing, size_t bucketing_bytes,
+                           const void* x, const void* const* W, const void* const* U,
+                           const void* Vt, const void* const* Sigma, void* const* y,
+                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* Synchronous id check for tests and debugging: copies the ids to the host
  * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is

@@ -25,7 +25,7 @@ EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncom
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
             "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi", "cts_apply_noalloc",
-            "cts_workspace_bucketing",
+            "cts_workspace_bucketing", "cts_bucketing_size", "cts_apply_multi_sorted",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
             "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
@@ -70,8 +70,10 @@ def lib() -> ctypes.CDLL:
                 L.cts_workspace_size_uncompressed.restype = sz
                 L.cts_workspace_bucketing.argtypes = [pp, i32, ctypes.POINTER(sz)]
                 L.cts_workspace_bucketing.restype = ctypes.c_int
-                L.cts_sort_by_cluster.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp]
+                L.cts_sort_by_cluster.argtypes = [vp, vp, i32, i32, i32, vp, vp, vp, sz, vp]
                 L.cts_sort_by_cluster.restype = ctypes.c_int
+                L.cts_bucketing_size.argtypes = [i32, i32, i32]
+                L.cts_bucketing_size.restype = sz
                 L.cts_apply.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
                 L.cts_apply.restype = ctypes.c_int
                 L.cts_apply_noalloc.argtypes = [pp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -94,6 +96,8 @@ def lib() -> ctypes.CDLL:
                 L.cts_workspace_size_multi.restype = sz
                 L.cts_apply_multi.argtypes = [pp, i32, i32p, vp, vp, vp, vpp, vpp, vp, vpp, vpp, vp, sz, vp]
                 L.cts_apply_multi.restype = ctypes.c_int
+                L.cts_apply_multi_sorted.argtypes = [pp, i32, i32p, vp, vp, sz, vp, vpp, vpp, vp, vpp, vpp, vp, sz, vp]
+                L.cts_apply_multi_sorted.restype = ctypes.c_int
                 jp, fl = ctypes.POINTER(JdProblem), ctypes.c_float
                 L.cts_jd_workspace_size.argtypes = [jp]
                 L.cts_jd_workspace_size.restype = sz
@@ -185,9 +189,18 @@ def workspace_bucketing(p: Problem, compressed: bool = True) -> dict:
     return dict(zip(("perm", "seg", "aid", "items", "n_items"), (int(v) for v in offs)))
 
 
+def bucketing_size(T: int, n: int, K: int) -> int:
+    return int(lib().cts_bucketing_size(T, n, K))
+
+
 def sort_by_cluster(adapter_id: torch.Tensor, cluster_of: torch.Tensor | None, n: int, K: int,
-                    perm: torch.Tensor | None = None, offsets: torch.Tensor | None = None):
-    """(perm, cluster_offsets): tokens sorted by (cluster, adapter, token)."""
+                    perm: torch.Tensor | None = None, offsets: torch.Tensor | None = None,
+                    bucketing=None):
+    """(perm, cluster_offsets): tokens sorted by (cluster, adapter, token).
+    bucketing: None, True (a new buffer) or a uint8 tensor of at least
+    bucketing_size(T, n, K) bytes that receives the rest of the bucketing;
+    then (perm, cluster_offsets, bucketing) is returned, and (perm,
+    bucketing) can be passed to apply_multi_sorted."""
     dev = adapter_id.device
     T = adapter_id.numel()
     if perm is None:
@@ -198,8 +211,15 @@ def sort_by_cluster(adapter_id: torch.Tensor, cluster_of: torch.Tensor | None, n
     c = _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)) if cluster_of is not None else None
     pp = _dev(perm, "perm", dev, torch.int32, (T,))
     oo = _dev(offsets, "offsets", dev, torch.int32, (K + 1,))
-    _check(lib().cts_sort_by_cluster(a, c, T, n, K, pp, oo, _stream(dev)), "cts_sort_by_cluster")
-    return perm, offsets
+    bk, bp, bn = None, None, 0
+    if bucketing is not None:
+        bk = bucketing if isinstance(bucketing, torch.Tensor) else \
+            torch.empty(max(bucketing_size(T, n, K), 1), dtype=torch.uint8, device=dev)
+        if bk.device != dev or bk.dtype != torch.uint8:
+            raise ValueError("bucketing must be a uint8 tensor on %s" % dev)
+        bp, bn = ctypes.c_void_p(bk.data_ptr()), bk.numel()
+    _check(lib().cts_sort_by_cluster(a, c, T, n, K, pp, oo, bp, bn, _stream(dev)), "cts_sort_by_cluster")
+    return (perm, offsets) if bk is None else (perm, offsets, bk)
 
 
 def apply(x, adapter_id, cluster_of, W, U, Vt, Sigma, out=None, out_dtype=None, workspace=None):
@@ -415,6 +435,43 @@ def apply_multi(x, adapter_id, cluster_of, Ws, Us, Vt, Sigmas, outs=None, out_dt
                                  _dev(cluster_of, "cluster_of", dev, torch.int32, (n,)), Wp, Up,
                                  _dev(Vt, "Vt", dev, tdt, (K, M * r, d_in)), Sp, Yp,
                                  ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)), "cts_apply_multi")
+    return outs
+
+
+def apply_multi_sorted(perm, bucketing, x, Ws, Us, Vt, Sigmas, outs=None, out_dtype=None, workspace=None):
+    """apply_multi with the bucketing of one sort_by_cluster(..., bucketing=...)
+    call for this batch (cts_apply_multi_sorted): no ids, no sort here.
+    Returns the list of outputs y_m [T][d_out_m]."""
+    dev = x.device
+    T, d_in = x.shape
+    M = len(Ws)
+    if not (len(Us) == len(Sigmas) == M):
+        raise ValueError("Ws, Us and Sigmas must have one entry per module")
+    K, _, r = Us[0].shape
+    n = Sigmas[0].shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    odt = tdt if out_dtype is None else out_dtype
+    d_out = [int(w.shape[0]) for w in Ws]
+    if outs is None:
+        outs = [torch.empty((T, dm), dtype=odt, device=dev) for dm in d_out]
+    p = make_problem(T, d_in, 8, r=r, n_adapters=n, n_clusters=K, dtype=dt, out_dtype=_dt(outs[0], "out"))
+    vp = ctypes.c_void_p
+    Wp = (vp * M)(*[_dev(w, "W[%d]" % m, dev, tdt, (d_out[m], d_in)) for m, w in enumerate(Ws)])
+    Up = (vp * M)(*[_dev(u, "U[%d]" % m, dev, tdt, (K, d_out[m], r)) for m, u in enumerate(Us)])
+    Sp = (vp * M)(*[_dev(sg, "Sigma[%d]" % m, dev, tdt, (n, r, r)) for m, sg in enumerate(Sigmas)])
+    Yp = (vp * M)(*[_dev(y, "out[%d]" % m, dev, None, (T, d_out[m])) for m, y in enumerate(outs)])
+    dims = (ctypes.c_int32 * M)(*d_out)
+    if bucketing.device != dev or bucketing.dtype != torch.uint8:
+        raise ValueError("bucketing must be a uint8 tensor on %s" % dev)
+    nbytes = workspace_size_multi(p, d_out)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_multi_sorted(ctypes.byref(p), M, dims, _dev(perm, "perm", dev, torch.int32, (T,)),
+                                        ctypes.c_void_p(bucketing.data_ptr()), bucketing.numel(),
+                                        _dev(x, "x", dev, tdt, (T, d_in)), Wp, Up,
+                                        _dev(Vt, "Vt", dev, tdt, (K, M * r, d_in)), Sp, Yp,
+                                        ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)),
+           "cts_apply_multi_sorted")
     return outs
 
 

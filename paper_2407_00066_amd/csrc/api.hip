@@ -184,6 +184,24 @@ hipError_t mark(int i, hipStream_t s) {
   return (g_stage_on && g_stage_events[i]) ? hipEventRecord(g_stage_events[i], s) : hipSuccess;
 }
 
+// The bucketing cts_sort_by_cluster leaves in its workspace (perm is its own
+// argument): each sorted position's cluster and adapter, the core-product
+// items and their count, the shrink tiles and their count.
+struct BucketLayout { size_t seg, aid, items, nitems, ctiles, nctiles, total; };
+
+bool bucket_layout(int T, int n, int K, BucketLayout* L) {
+  if (T < 0 || n < 1 || K < 1 || T > cts::kSortMaxT || n > 65536 || K > 65536) return false;
+  size_t off = 0;
+  L->seg = off;     off = align_up(off + 4ull * T);
+  L->aid = off;     off = align_up(off + 4ull * T);
+  L->items = off;   off = align_up(off + 4ull * (cts::max_sigma_items(T, n) + 1));
+  L->nitems = off;  off = align_up(off + 4);
+  L->ctiles = off;  off = align_up(off + 4ull * (cts::max_seg_tiles(T, K) + 1));
+  L->nctiles = off; off = align_up(off + 4);
+  L->total = off;
+  return true;
+}
+
 struct Range { const void* p; size_t bytes; };
 
 // Every float array is read or written in 16-byte vectors: its address must be
@@ -339,23 +357,37 @@ int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* of
   return CTS_OK;
 }
 
+size_t cts_bucketing_size(int32_t T, int32_t n, int32_t K) {
+  BucketLayout L;
+  return bucket_layout(T, n, K, &L) ? L.total : 0;
+}
+
 int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, int32_t T, int32_t n,
-                        int32_t K, int32_t* perm, int32_t* cluster_offsets, void* stream) {
+                        int32_t K, int32_t* perm, int32_t* cluster_offsets, void* workspace,
+                        size_t workspace_bytes, void* stream) {
   if (T < 0 || n < 1 || K < 1 || !cluster_offsets) return CTS_ERR_INVALID_ARG;
   if (!cluster_of && K != n) return CTS_ERR_INVALID_ARG;
   if (T > 0 && (!adapter_id || !perm)) return CTS_ERR_INVALID_ARG;
   if (misaligned(adapter_id, 4) || misaligned(cluster_of, 4) || misaligned(perm, 4) ||
-      misaligned(cluster_offsets, 4))
+      misaligned(cluster_offsets, 4) || misaligned(workspace, 16))
     return CTS_ERR_INVALID_ARG;
   if (T > cts::kSortMaxT || n > 65536 || K > 65536) return CTS_ERR_UNSUPPORTED;
-  const Range out[2] = {{perm, 4ull * T}, {cluster_offsets, 4ull * (K + 1)}};
+  BucketLayout L;
+  bucket_layout(T, n, K, &L);
+  if (workspace && workspace_bytes < L.total) return CTS_ERR_WORKSPACE;
+  const Range out[3] = {{perm, 4ull * T}, {cluster_offsets, 4ull * (K + 1)},
+                        {workspace, workspace ? L.total : 0}};
   const Range in[2] = {{adapter_id, 4ull * T}, {cluster_of, cluster_of ? 4ull * n : 0}};
-  if (overlap(out[0], out[1])) return CTS_ERR_INVALID_ARG;
+  for (int a = 0; a < 3; ++a)
+    for (int b = a + 1; b < 3; ++b)
+      if (overlap(out[a], out[b])) return CTS_ERR_INVALID_ARG;
   for (const Range& o : out)
     for (const Range& i : in)
       if (overlap(o, i)) return CTS_ERR_INVALID_ARG;
-  const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets,
-                                        nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+  char* ws = static_cast<char*>(workspace);
+  auto at = [&](size_t off) { return ws ? reinterpret_cast<int32_t*>(ws + off) : nullptr; };
+  const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets, at(L.seg),
+                                        at(L.aid), at(L.items), at(L.nitems), at(L.ctiles), at(L.nctiles),
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
@@ -493,10 +525,12 @@ int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan
   return CTS_OK;
 }
 
+// ext_perm / ext_bucket: a bucketing from cts_sort_by_cluster (then the ids
+// are not read and no sort runs here).
 int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, const void* x,
               const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
               const void* const* U, const void* Vt, const void* const* Sigma, void* const* y, void* workspace,
-              hipStream_t stream) {
+              hipStream_t stream, const int32_t* ext_perm = nullptr, const void* ext_bucket = nullptr) {
   const Plan& pl = mp.mod[0];
   char* ws = static_cast<char*>(workspace);
   int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
@@ -507,6 +541,19 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
   int32_t* ctiles = reinterpret_cast<int32_t*>(ws + pl.off_ctiles);
   int32_t* n_ctiles = reinterpret_cast<int32_t*>(ws + pl.off_nctiles);
+  const bool ext = ext_perm != nullptr;
+  if (ext) {
+    BucketLayout L;
+    bucket_layout(p->T, p->n_adapters, p->n_clusters, &L);
+    char* b = static_cast<char*>(const_cast<void*>(ext_bucket));
+    perm = const_cast<int32_t*>(ext_perm);
+    sseg = reinterpret_cast<int32_t*>(b + L.seg);
+    said = reinterpret_cast<int32_t*>(b + L.aid);
+    items = reinterpret_cast<int32_t*>(b + L.items);
+    n_items = reinterpret_cast<int32_t*>(b + L.nitems);
+    ctiles = reinterpret_cast<int32_t*>(b + L.ctiles);
+    n_ctiles = reinterpret_cast<int32_t*>(b + L.nctiles);
+  }
   float* zpart = reinterpret_cast<float*>(ws + mp.off_zpart);
   char* zp = ws + mp.off_zp;
   float* ypart = reinterpret_cast<float*>(ws + mp.off_ypart);
@@ -514,8 +561,8 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
 
   hipError_t e = mark(0, stream);
   if (e != hipSuccess) return CTS_ERR_HIP;
-  const bool fuse_sort = T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
-  if (!fuse_sort) {
+  const bool fuse_sort = !ext && T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
+  if (!fuse_sort && !ext) {
     e = cts::launch_sort(adapter_id, cluster_of, T, p->n_adapters, pl.nseg, perm, offs, sseg, said, items, n_items,
                          ctiles, n_ctiles, stream);
     if (e != hipSuccess) return CTS_ERR_HIP;
@@ -592,15 +639,28 @@ size_t cts_workspace_size_multi(const cts_problem* p, int32_t M, const int32_t* 
   return make_multi_plan(p, M, d_out, &mp) == CTS_OK ? mp.total : 0;
 }
 
-int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
-                    const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
-                    const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
-                    void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+// The checks of cts_apply_multi and cts_apply_multi_sorted: either the ids
+// (adapter_id, cluster_of) or a bucketing (perm, bucket of bucket_bytes).
+int apply_multi_checked(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
+                        const int32_t* adapter_id, const int32_t* cluster_of, const int32_t* perm,
+                        const void* bucket, size_t bucket_bytes, const void* const* W, const void* const* U,
+                        const void* Vt, const void* const* Sigma, void* const* y, void* workspace,
+                        size_t workspace_bytes, void* stream) {
   MultiPlan mp;
   const int rc = make_multi_plan(p, M, d_out, &mp);
   if (rc != CTS_OK) return rc;
   if (p->T == 0) return CTS_OK;
-  if (!x || !adapter_id || !cluster_of || !W || !U || !Vt || !Sigma || !y || !workspace) return CTS_ERR_INVALID_ARG;
+  const bool sorted = perm != nullptr || bucket != nullptr;
+  if (sorted ? (!perm || !bucket) : (!adapter_id || !cluster_of)) return CTS_ERR_INVALID_ARG;
+  if (!x || !W || !U || !Vt || !Sigma || !y || !workspace) return CTS_ERR_INVALID_ARG;
+  BucketLayout L{};
+  if (sorted) {
+    bucket_layout(p->T, p->n_adapters, p->n_clusters, &L);
+    if (misaligned(perm, 4) || misaligned(bucket, 16)) return CTS_ERR_INVALID_ARG;
+    if (bucket_bytes < L.total) return CTS_ERR_WORKSPACE;
+  }
   for (int m = 0; m < M; ++m)
     if (!W[m] || !U[m] || !Sigma[m] || !y[m] || misaligned(W[m], 16) || misaligned(U[m], 16) ||
         misaligned(Sigma[m], 16) || misaligned(y[m], 16))
@@ -612,8 +672,14 @@ int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const
   const size_t e = mp.mod[0].elt;
   const size_t T = p->T, di = p->d_in, r = p->r, n = p->n_adapters, K = p->n_clusters;
   // every output against the workspace, every input and the other outputs
-  std::vector<Range> in = {{x, T * di * e}, {adapter_id, 4 * T}, {cluster_of, 4 * n},
-                           {Vt, K * static_cast<size_t>(mp.rtot) * di * e}};
+  std::vector<Range> in = {{x, T * di * e}, {Vt, K * static_cast<size_t>(mp.rtot) * di * e}};
+  if (sorted) {
+    in.push_back({perm, 4 * T});
+    in.push_back({bucket, L.total});
+  } else {
+    in.push_back({adapter_id, 4 * T});
+    in.push_back({cluster_of, 4 * n});
+  }
   for (int m = 0; m < M; ++m) {
     const size_t dm = d_out[m];
     in.push_back({W[m], dm * di * e});
@@ -628,7 +694,26 @@ int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const
       if (overlap(ym, {y[k], T * static_cast<size_t>(d_out[k]) * mp.mod[k].out_elt})) return CTS_ERR_INVALID_ARG;
   }
   return run_multi(p, mp, d_out, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
-                   static_cast<hipStream_t>(stream));
+                   static_cast<hipStream_t>(stream), sorted ? perm : nullptr, sorted ? bucket : nullptr);
+}
+
+}  // namespace
+
+int cts_apply_multi(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
+                    const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
+                    const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  return apply_multi_checked(p, M, d_out, x, adapter_id, cluster_of, nullptr, nullptr, 0, W, U, Vt, Sigma, y,
+                             workspace, workspace_bytes, stream);
+}
+
+int cts_apply_multi_sorted(const cts_problem* p, int32_t M, const int32_t* d_out, const int32_t* perm,
+                           const void* bucketing, size_t bucketing_bytes, const void* x, const void* const* W,
+                           const void* const* U, const void* Vt, const void* const* Sigma, void* const* y,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  if (p && p->T > 0 && (!perm || !bucketing)) return CTS_ERR_INVALID_ARG;
+  return apply_multi_checked(p, M, d_out, x, nullptr, nullptr, perm, bucketing, bucketing_bytes, W, U, Vt,
+                             Sigma, y, workspace, workspace_bytes, stream);
 }
 
 namespace {

@@ -147,7 +147,7 @@ def test_workspace_grows_with_problem():
 
 def test_sort_validation():
     L = cts.lib()
-    f = lambda *a: L.cts_sort_by_cluster(*a, None)
+    f = lambda *a: L.cts_sort_by_cluster(*a, None, 0, None)
     assert f(FAKE, FAKE, -1, 4, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG
     assert f(FAKE, FAKE, 4, 0, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG
     assert f(FAKE, None, 4, 4, 2, FAKE, FAKE) == B.CTS_ERR_INVALID_ARG   # K must equal n
@@ -418,3 +418,48 @@ def test_noalloc_scratch_size_matches_header():
     src = open(os.path.join(ROOT, "include", "cts.h")).read()
     m = re.search(r"#define CTS_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
     assert m and int(m.group(1)) << int(m.group(2)) == B.NOALLOC_SCRATCH_BYTES
+
+
+def test_sort_bucketing_workspace_validation():
+    """cts_sort_by_cluster's workspace (the bucketing for cts_apply_multi_sorted):
+    its size, refused when too small, misaligned or overlapping an array."""
+    L = cts.lib()
+    assert cts.bucketing_size(512, 1000, 50) > 3 * 4 * 512
+    assert cts.bucketing_size(0, 4, 2) > 0
+    assert cts.bucketing_size(-1, 4, 2) == 0 and cts.bucketing_size(8193, 4, 2) == 0
+    assert cts.bucketing_size(8, 0, 2) == 0 and cts.bucketing_size(8, 4, 65537) == 0
+    need = cts.bucketing_size(64, 4, 2)
+    a, c, pm, of = (ctypes.c_void_p(0x1000_0000 * (i + 1)) for i in range(4))
+    ws = ctypes.c_void_p(0x8000_0000)
+    f = lambda w, nb: L.cts_sort_by_cluster(a, c, 64, 4, 2, pm, of, w, nb, None)
+    assert f(ws, need - 1) == B.CTS_ERR_WORKSPACE
+    assert f(ctypes.c_void_p(0x8000_0008), need) == B.CTS_ERR_INVALID_ARG          # misaligned
+    assert f(ctypes.c_void_p(0x3000_0000 + 64), need) == B.CTS_ERR_INVALID_ARG     # overlaps perm
+    assert f(ctypes.c_void_p(0x1000_0000), need) == B.CTS_ERR_INVALID_ARG          # overlaps adapter_id
+
+
+def _multi_sorted(p, perm, bk, bk_bytes, y=None, ws=None, M=1, d_out=None):
+    d_out = d_out or [p.d_out] * M
+    dims = (ctypes.c_int32 * M)(*d_out)
+    vp = ctypes.c_void_p
+    W = (vp * M)(*[vp(0x5000_0000_0000 + (m << 32)) for m in range(M)])
+    U = (vp * M)(*[vp(0x5100_0000_0000 + (m << 32)) for m in range(M)])
+    S = (vp * M)(*[vp(0x5200_0000_0000 + (m << 32)) for m in range(M)])
+    Y = (vp * M)(*[vp((y or 0x7000_0000_0000) + (m << 32)) for m in range(M)])
+    return cts.lib().cts_apply_multi_sorted(ctypes.byref(p), M, dims, perm, bk, bk_bytes,
+                                            vp(0x5300_0000_0000), W, U, vp(0x5400_0000_0000), S, Y,
+                                            vp(ws or 0x6000_0000_0000), 1 << 40, None)
+
+
+def test_multi_sorted_validation():
+    p = _p(T=512, d_in=4096, d_out=4096, r=64, n_adapters=1000, n_clusters=50)
+    perm, bk = ctypes.c_void_p(0x4000_0000_0000), ctypes.c_void_p(0x4100_0000_0000)
+    need = cts.bucketing_size(512, 1000, 50)
+    assert _multi_sorted(p, perm, bk, need - 1) == B.CTS_ERR_WORKSPACE
+    assert _multi_sorted(p, None, bk, need) == B.CTS_ERR_INVALID_ARG
+    assert _multi_sorted(p, perm, None, need) == B.CTS_ERR_INVALID_ARG
+    assert _multi_sorted(p, perm, ctypes.c_void_p(0x4100_0000_0008), need) == B.CTS_ERR_INVALID_ARG
+    # an output over the bucketing
+    assert _multi_sorted(p, perm, bk, need, y=0x4100_0000_0000) == B.CTS_ERR_INVALID_ARG
+    assert _multi_sorted(_p(T=512, r=12), perm, bk, need) == B.CTS_ERR_UNSUPPORTED
+    assert _multi_sorted(_p(T=0), None, None, 0) == B.CTS_OK

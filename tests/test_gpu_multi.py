@@ -61,3 +61,53 @@ def test_apply_multi_one_module_is_apply():
     y1 = cts.apply(*args, dev(w0.W), dev(w0.U), dev(w0.Vt), dev(w0.Sigma))
     torch.cuda.synchronize()
     assert torch.equal(ys[0], y1)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_apply_multi_sorted_shares_one_bucketing(oracle_mod, name):
+    """One cts_sort_by_cluster for the batch, then cts_apply_multi_sorted for
+    every module group and for single modules (M = 1): bit for bit the
+    results of cts_apply_multi / cts_apply, which sort the ids themselves."""
+    w0, mods, Vt = _modules(CASES[name])
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    say("apply_multi_sorted %s (M=%d)" % (name, len(mods)))
+    perm, offs, bk = cts.sort_by_cluster(aid, cof, w0.n, w0.K, bucketing=True)
+    ys = cts.apply_multi_sorted(perm, bk, x, [dev(m.W) for m in mods], [dev(m.U) for m in mods], dev(Vt),
+                                [dev(m.Sigma) for m in mods])
+    ref = cts.apply_multi(x, aid, cof, [dev(m.W) for m in mods], [dev(m.U) for m in mods], dev(Vt),
+                          [dev(m.Sigma) for m in mods])
+    singles = [cts.apply_multi_sorted(perm, bk, x, [dev(m.W)], [dev(m.U)], dev(m.Vt), [dev(m.Sigma)])[0]
+               for m in mods]
+    torch.cuda.synchronize()
+    for m in range(len(mods)):
+        assert torch.equal(ys[m], ref[m]), m
+        y1 = cts.apply(x, aid, cof, dev(mods[m].W), dev(mods[m].U), dev(mods[m].Vt), dev(mods[m].Sigma))
+        torch.cuda.synchronize()
+        assert torch.equal(singles[m], y1), m
+    oref = oracle_mod.apply_multi(w0.x, w0.adapter_id, w0.cluster_of, [m.W for m in mods], [m.U for m in mods],
+                                  Vt, [m.Sigma for m in mods])
+    for m in range(len(mods)):
+        assert row_rel_err(host(ys[m]), oref[m]) <= TOL[w0.dtype], m
+
+
+def test_apply_multi_sorted_many_calls_one_sort(oracle_mod):
+    """As a decoder step: one sort, then several layers' calls on the same
+    bucketing (other inputs each), interleaved with a different batch's
+    sort on another buffer."""
+    kw = dict(cfg=145, T=512, d_in=256, d_outs=(256, 128), r=32, n=200, K=10)
+    w0, mods, Vt = _modules(kw)
+    other = wl.synthetic("other_ids", cfg=146, T=512, d_in=64, d_out=64, r=8, n=200, K=10, with_lora=False)
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    say("apply_multi_sorted: one sort, four calls")
+    perm, _, bk = cts.sort_by_cluster(aid, cof, w0.n, w0.K, bucketing=True)
+    cts.sort_by_cluster(dev(other.adapter_id), cof, w0.n, w0.K, bucketing=True)
+    outs = [cts.apply_multi_sorted(perm, bk, x, [dev(m.W) for m in mods], [dev(m.U) for m in mods], dev(Vt),
+                                   [dev(m.Sigma) for m in mods]) for _ in range(4)]
+    torch.cuda.synchronize()
+    for ys in outs[1:]:
+        for a, b in zip(ys, outs[0]):
+            assert torch.equal(a, b)
+    oref = oracle_mod.apply_multi(w0.x, w0.adapter_id, w0.cluster_of, [m.W for m in mods], [m.U for m in mods],
+                                  Vt, [m.Sigma for m in mods])
+    for m in range(len(mods)):
+        assert row_rel_err(host(outs[0][m]), oref[m]) <= TOL["bf16"], m
