@@ -34,19 +34,28 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "cts_oracle.c")
-_LIB = os.path.join(_HERE, "libcts_oracle.so")
+# CTS_ORACLE_LIB names another build of the oracle (the sanitizer check's)
+_LIB = os.environ.get("CTS_ORACLE_LIB") or os.path.join(_HERE, "libcts_oracle.so")
 _lib = None
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (fp64, OpenMP, no fast-math)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-std=c11", "-O3", "-fopenmp", "-fPIC", "-shared",
-               "-Wall", "-Wextra", "-o", tmp, _SRC]
+def build(force: bool = True, out: str | None = None, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP, no fast-math).  sanitize:
+    with ROCm's clang and -fsanitize=address,undefined (the shared sanitizer
+    runtime) into `out`, for the sanitizer check of the CPU tests."""
+    lib = out or _LIB
+    if force or not os.path.exists(lib):
+        tmp = lib + ".tmp%d" % os.getpid()
+        if sanitize:
+            cmd = ["/opt/rocm/llvm/bin/clang", "-std=c11", "-O1", "-g", "-fno-omit-frame-pointer",
+                   "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libsan",
+                   "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC]
+        else:
+            cmd = ["gcc", "-std=c11", "-O3", "-fopenmp", "-fPIC", "-shared",
+                   "-Wall", "-Wextra", "-o", tmp, _SRC]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, lib)
+    return lib
 
 
 def _load():

@@ -13,7 +13,8 @@ import threading
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcts.so")
+# CTS_LIB names another build of the library (the sanitizer check's)
+_LIB_PATH = os.environ.get("CTS_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcts.so")
 _lib = None
 _lock = threading.Lock()
 
