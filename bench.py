@@ -164,13 +164,17 @@ def copy_calibration(torch, device, nbytes=256 << 20, reps=3):
     del src, dst
 
 
-def traffic_from_profile(kernel_src):
+GEMM_SOURCES = [os.path.join(ROOT, "paper_2407_00066_amd", "csrc", f) for f in ("gemm.hip", "ldsdma.h")]
+
+
+def traffic_from_profile(workload):
     """HBM bytes per launch of the fused GEMM measured with rocprofv3 --pmc
     (FETCH_SIZE + WRITE_SIZE, each scaled by the copy calibration), read from
-    the committed summary; None when there is none or the kernel source has
-    changed since the counters were taken."""
+    the committed summary of this workload; None when there is none or the
+    GEMM's sources (gemm.hip followed by ldsdma.h) have changed since the
+    counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic_seg_gemm_prefill_mix.md")
+    path = os.path.join(ROOT, "profiles", "traffic_seg_gemm_%s.md" % workload)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -178,8 +182,10 @@ def traffic_from_profile(kernel_src):
         if line.startswith("- ") and ":" in line:
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    digest = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()
-    if fields.get("kernel_source_sha256") != digest or "hbm_bytes_per_launch" not in fields:
+    h = hashlib.sha256()
+    for src in GEMM_SOURCES:
+        h.update(open(src, "rb").read())
+    if fields.get("kernel_source_sha256") != h.hexdigest() or "hbm_bytes_per_launch" not in fields:
         return None
     return float(fields["hbm_bytes_per_launch"])
 
@@ -534,8 +540,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
     # the GEMM's duration: its event interval less the marker interval
     gemm_us = g_int - g_mark
     roof = roofline_of(flops, nbytes, gemm_us * 1e-6, w.dtype)
-    if args.workload == "prefill_mix":
-        roof["traffic"] = traffic_from_profile(os.path.join(ROOT, "paper_2407_00066_amd", "csrc", "gemm.hip"))
+    roof["traffic"] = traffic_from_profile(args.workload)
     gemm_kernel = "seg_gemm_dma_kernel" if w.dtype == "bf16" else "seg_gemm_kernel"
     roof.update({"kernel": gemm_kernel + " (fused W X + U_k Z')", "mean_us": round(gemm_us, 2),
                  "event_interval_us": round(g_int, 2), "marker_us": round(g_mark, 2),
