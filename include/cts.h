@@ -70,7 +70,7 @@ typedef enum {
 typedef enum { CTS_F32 = 0, CTS_BF16 = 1 } cts_dtype;
 
 /* Problem description (host memory).  Limits (else CTS_ERR_UNSUPPORTED):
- *   0 <= T <= 8192, d_in and d_out multiples of 8,
+ *   T >= 0, d_in and d_out multiples of 8,
  *   r: multiple of 8 in [8, 128]; r_lora: multiple of 4 (f32) or 8 (bf16)
  *   in [4, 128]; 1 <= n_adapters <= 65536; 1 <= n_clusters <= 65536;
  *   dtype F32 with out_dtype F32, or dtype BF16 with out_dtype BF16 or F32.
@@ -78,7 +78,14 @@ typedef enum { CTS_F32 = 0, CTS_BF16 = 1 } cts_dtype;
  * on bf16 matrix cores with fp32 accumulation; V^T x is kept in fp32, Sigma
  * is applied in fp32, and the result is rounded to the input type before the
  * U (or B) product.  Fields a call does not use are ignored (r, n_clusters
- * for the uncompressed path; r_lora for the compressed one). */
+ * for the uncompressed path; r_lora for the compressed one).
+ * Batches of more than 8192 tokens (the bucketing sorts at most 8192 tokens
+ * in one workgroup) run as ceil(T / 8192) consecutive pieces of near-equal
+ * size, the larger ones first, each a complete layer call on its rows of x,
+ * adapter_id and y: every output row depends on its own token alone, so
+ * the result is the whole batch's.  The workspace sizes cover the largest
+ * piece; the bucketing read-back, cts_sort_by_cluster and
+ * cts_apply_multi_sorted take at most 8192 tokens. */
 typedef struct {
     int32_t T;            /* tokens in the batch */
     int32_t d_in;         /* input features of the layer */
@@ -114,7 +121,9 @@ size_t cts_workspace_size_uncompressed(const cts_problem* p);
  *                                 a multiple of 16, ascending, then items[c] = T
  *   offsets[4]  int32 c           the number of items
  * `offsets` is a host array of 5 entries.  Returns CTS_ERR_INVALID_ARG or
- * CTS_ERR_UNSUPPORTED for a problem the call would refuse. */
+ * CTS_ERR_UNSUPPORTED for a problem the call would refuse, and
+ * CTS_ERR_UNSUPPORTED for T > 8192 (each piece of such a call overwrites
+ * the bucketing of the one before). */
 int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* offsets);
 
 /* Token bucketing (the grouping of tokens by cluster that makes the shared-
@@ -236,9 +245,9 @@ int cts_apply_noalloc(const cts_problem* p, const void* x, const int32_t* adapte
  * p->T tokens, n = p->n_adapters and K = p->n_clusters and a cluster map
  * (not NULL), and have completed on `stream` (or a stream ordered before
  * it); the ids themselves are not arguments.  M = 1 is cts_apply's layer.
- * Same limits, layouts, results and errors as cts_apply_multi, and the same
- * workspace (cts_workspace_size_multi bytes); outputs must not overlap perm
- * or the bucketing either. */
+ * Same limits (and T <= 8192, the sort's), layouts, results and errors as
+ * cts_apply_multi, and the same workspace (cts_workspace_size_multi bytes);
+ * outputs must not overlap perm or the bucketing either. */
 int cts_apply_multi_sorted(const cts_problem* p, int32_t M, const int32_t* d_out,
                            const int32_t* perm, const void* bucketing, size_t bucketing_bytes,
                            const void* x, const void* const* W, const void* const* U,

@@ -69,9 +69,40 @@ int shrink_split_of(int T, int rank, int nseg, int d_in, Tile t) {
   return std::max(1, std::min(std::min(ceil_div(target, tiles), std::max(1, nk / kmin)), 64));
 }
 
-// Validates the sizes of `p` for the compressed (compressed=true) or the
-// uncompressed path and fills the launch plan.  Pure host arithmetic.
-int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
+// Batches of more than kSortMaxT tokens (the one-workgroup bucketing's
+// limit) run as consecutive pieces of near-equal size, each at most
+// kSortMaxT tokens and a complete layer call of its own: y_t depends on
+// token t alone (its x_t and its adapter), so the pieces' rows are the
+// batch's rows.  The first `rem` pieces hold q + 1 tokens, the rest q.
+struct Pieces { int n, q, rem; };
+
+Pieces pieces_of(int T) {
+  Pieces pc;
+  pc.n = T <= cts::kSortMaxT ? 1 : ceil_div(T, cts::kSortMaxT);
+  pc.q = T / pc.n;
+  pc.rem = T % pc.n;
+  return pc;
+}
+
+// Runs fn(piece problem, first token) over the pieces of p->T in token order;
+// stops at the first status that is not CTS_OK.
+template <typename F> int for_pieces(const cts_problem* p, F&& fn) {
+  const Pieces pc = pieces_of(p->T);
+  cts_problem q = *p;
+  int t0 = 0;
+  for (int i = 0; i < pc.n; ++i) {
+    q.T = pc.q + (i < pc.rem ? 1 : 0);
+    const int rc = fn(q, static_cast<size_t>(t0));
+    if (rc != CTS_OK) return rc;
+    t0 += q.T;
+  }
+  return CTS_OK;
+}
+
+// Validates the sizes of `p` (T <= kSortMaxT) for the compressed
+// (compressed=true) or the uncompressed path and fills the launch plan.
+// Pure host arithmetic.
+int plan_piece(const cts_problem* p, bool compressed, Plan* pl) {
   if (!p) return CTS_ERR_INVALID_ARG;
   if (p->T < 0 || p->d_in < 1 || p->d_out < 1 || p->n_adapters < 1) return CTS_ERR_INVALID_ARG;
   if (compressed && (p->r < 1 || p->n_clusters < 1)) return CTS_ERR_INVALID_ARG;
@@ -79,7 +110,7 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   if (p->dtype != CTS_F32 && p->dtype != CTS_BF16) return CTS_ERR_UNSUPPORTED;
   if (p->out_dtype != CTS_F32 && p->out_dtype != CTS_BF16) return CTS_ERR_UNSUPPORTED;
   if (p->dtype == CTS_F32 && p->out_dtype != CTS_F32) return CTS_ERR_UNSUPPORTED;
-  if (p->T > cts::kSortMaxT) return CTS_ERR_UNSUPPORTED;
+  if (p->T > cts::kSortMaxT) return CTS_ERR_UNSUPPORTED;   // a piece
   if (p->d_in % 8 || p->d_out % 8) return CTS_ERR_UNSUPPORTED;
   if (p->n_adapters > 65536) return CTS_ERR_UNSUPPORTED;
   pl->elt = p->dtype == CTS_BF16 ? 2 : 4;
@@ -173,6 +204,24 @@ int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
   pl->off_ypart = off;
   if (pl->main_split > 1) off = align_up(off + 4ull * pl->main_split * T * p->d_out);
   pl->total = off;
+  return CTS_OK;
+}
+
+// The plan of p: for a batch of pieces, the plan of its largest piece, with
+// a workspace that also fits the smaller piece size.
+int make_plan(const cts_problem* p, bool compressed, Plan* pl) {
+  if (!p) return CTS_ERR_INVALID_ARG;
+  if (p->T <= cts::kSortMaxT) return plan_piece(p, compressed, pl);
+  const Pieces pc = pieces_of(p->T);
+  cts_problem q = *p;
+  q.T = pc.q + (pc.rem ? 1 : 0);
+  int rc = plan_piece(&q, compressed, pl);
+  if (rc != CTS_OK || !pc.rem) return rc;
+  Plan small;
+  q.T = pc.q;
+  rc = plan_piece(&q, compressed, &small);
+  if (rc != CTS_OK) return rc;
+  pl->total = std::max(pl->total, small.total);
   return CTS_OK;
 }
 
@@ -349,6 +398,7 @@ int cts_workspace_bucketing(const cts_problem* p, int32_t compressed, size_t* of
   Plan pl;
   const int rc = make_plan(p, compressed != 0, &pl);
   if (rc != CTS_OK) return rc;
+  if (p->T > cts::kSortMaxT) return CTS_ERR_UNSUPPORTED;   // each piece buckets on its own
   offsets[0] = pl.off_perm;
   offsets[1] = pl.off_seg;
   offsets[2] = pl.off_aid;
@@ -452,8 +502,14 @@ int apply_compressed(const cts_problem* p, const void* x, const int32_t* adapter
     const int sc = scratch_of_current_device(&workspace);
     if (sc != CTS_OK) return sc;
   }
-  return run_layer(p, pl, true, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
-                   static_cast<hipStream_t>(stream), sigma_diag, ranked ? rank_of_cluster : nullptr);
+  return for_pieces(p, [&](const cts_problem& q, size_t t0) {
+    Plan pq;
+    const int rq = make_plan(&q, true, &pq);
+    if (rq != CTS_OK) return rq;
+    return run_layer(&q, pq, true, static_cast<const char*>(x) + t0 * di * e, adapter_id + t0, cluster_of, W,
+                     U, Vt, Sigma, static_cast<char*>(y) + t0 * dout * pl.out_elt, workspace,
+                     static_cast<hipStream_t>(stream), sigma_diag, ranked ? rank_of_cluster : nullptr);
+  });
 }
 
 }  // namespace
@@ -497,7 +553,7 @@ struct MultiPlan {
   size_t off_zpart, off_zp, off_ypart, total;
 };
 
-int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan* mp) {
+int multi_plan_piece(const cts_problem* p, int M, const int32_t* d_out, MultiPlan* mp) {
   if (!p || M < 1 || !d_out) return CTS_ERR_INVALID_ARG;
   if (M > CTS_MAX_MODULES) return CTS_ERR_UNSUPPORTED;
   mp->M = M;
@@ -522,6 +578,24 @@ int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan
     if (mp->mod[m].main_split > 1) yp = std::max<size_t>(yp, 4ull * mp->mod[m].main_split * T * d_out[m]);
   off = align_up(off + yp);
   mp->total = off;
+  return CTS_OK;
+}
+
+// As make_plan: a batch of pieces takes its largest piece's plan, with a
+// workspace that also fits the smaller piece size.
+int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan* mp) {
+  if (!p) return CTS_ERR_INVALID_ARG;
+  if (p->T <= cts::kSortMaxT) return multi_plan_piece(p, M, d_out, mp);
+  const Pieces pc = pieces_of(p->T);
+  cts_problem q = *p;
+  q.T = pc.q + (pc.rem ? 1 : 0);
+  int rc = multi_plan_piece(&q, M, d_out, mp);
+  if (rc != CTS_OK || !pc.rem) return rc;
+  MultiPlan small;
+  q.T = pc.q;
+  rc = multi_plan_piece(&q, M, d_out, &small);
+  if (rc != CTS_OK) return rc;
+  mp->total = std::max(mp->total, small.total);
   return CTS_OK;
 }
 
@@ -657,6 +731,7 @@ int apply_multi_checked(const cts_problem* p, int32_t M, const int32_t* d_out, c
   if (!x || !W || !U || !Vt || !Sigma || !y || !workspace) return CTS_ERR_INVALID_ARG;
   BucketLayout L{};
   if (sorted) {
+    if (p->T > cts::kSortMaxT) return CTS_ERR_UNSUPPORTED;
     bucket_layout(p->T, p->n_adapters, p->n_clusters, &L);
     if (misaligned(perm, 4) || misaligned(bucket, 16)) return CTS_ERR_INVALID_ARG;
     if (bucket_bytes < L.total) return CTS_ERR_WORKSPACE;
@@ -693,8 +768,19 @@ int apply_multi_checked(const cts_problem* p, int32_t M, const int32_t* d_out, c
     for (int k = 0; k < m; ++k)
       if (overlap(ym, {y[k], T * static_cast<size_t>(d_out[k]) * mp.mod[k].out_elt})) return CTS_ERR_INVALID_ARG;
   }
-  return run_multi(p, mp, d_out, x, adapter_id, cluster_of, W, U, Vt, Sigma, y, workspace,
-                   static_cast<hipStream_t>(stream), sorted ? perm : nullptr, sorted ? bucket : nullptr);
+  if (sorted)   // one bucketing of the whole batch (cts_sort_by_cluster: T <= kSortMaxT)
+    return run_multi(p, mp, d_out, x, nullptr, nullptr, W, U, Vt, Sigma, y, workspace,
+                     static_cast<hipStream_t>(stream), perm, bucket);
+  return for_pieces(p, [&](const cts_problem& q, size_t t0) {
+    MultiPlan mq;
+    const int rq = make_multi_plan(&q, M, d_out, &mq);
+    if (rq != CTS_OK) return rq;
+    void* yq[CTS_MAX_MODULES];
+    for (int m = 0; m < M; ++m)
+      yq[m] = static_cast<char*>(y[m]) + t0 * static_cast<size_t>(d_out[m]) * mp.mod[m].out_elt;
+    return run_multi(&q, mq, d_out, static_cast<const char*>(x) + t0 * di * e, adapter_id + t0, cluster_of, W,
+                     U, Vt, Sigma, yq, workspace, static_cast<hipStream_t>(stream));
+  });
 }
 
 }  // namespace
@@ -739,8 +825,14 @@ int apply_uncompressed(const cts_problem* p, const void* x, const int32_t* adapt
                        {rank_of_adapter, ranked ? 4 * n : 0}};
   if (any_overlap({y, T * dout * pl.out_elt}, {workspace, workspace_bytes}, in, 6))
     return CTS_ERR_INVALID_ARG;
-  return run_layer(p, pl, false, x, adapter_id, nullptr, W, B, A, nullptr, y, workspace,
-                   static_cast<hipStream_t>(stream), false, ranked ? rank_of_adapter : nullptr);
+  return for_pieces(p, [&](const cts_problem& q, size_t t0) {
+    Plan pq;
+    const int rq = make_plan(&q, false, &pq);
+    if (rq != CTS_OK) return rq;
+    return run_layer(&q, pq, false, static_cast<const char*>(x) + t0 * di * e, adapter_id + t0, nullptr, W, B,
+                     A, nullptr, static_cast<char*>(y) + t0 * dout * pl.out_elt, workspace,
+                     static_cast<hipStream_t>(stream), false, ranked ? rank_of_adapter : nullptr);
+  });
 }
 
 }  // namespace

@@ -66,7 +66,7 @@ def _apply_u(p, ws_bytes=1 << 40):
     (dict(n_adapters=0), B.CTS_ERR_INVALID_ARG), (dict(n_clusters=0), B.CTS_ERR_INVALID_ARG),
     (dict(d_in=4100), B.CTS_ERR_UNSUPPORTED), (dict(d_out=12), B.CTS_ERR_UNSUPPORTED),
     (dict(r=12), B.CTS_ERR_UNSUPPORTED), (dict(r=136), B.CTS_ERR_UNSUPPORTED),
-    (dict(T=8193), B.CTS_ERR_UNSUPPORTED), (dict(n_adapters=65537), B.CTS_ERR_UNSUPPORTED),
+    (dict(n_adapters=65537), B.CTS_ERR_UNSUPPORTED),
     (dict(dtype=2), B.CTS_ERR_UNSUPPORTED), (dict(out_dtype=7), B.CTS_ERR_UNSUPPORTED),
     (dict(dtype=B.CTS_F32, out_dtype=B.CTS_BF16), B.CTS_ERR_UNSUPPORTED),
 ])
@@ -138,6 +138,36 @@ def test_uncompressed_ignores_compressed_fields():
     assert _apply_u(p, ws_bytes=1) == B.CTS_ERR_WORKSPACE
 
 
+def _pieces(T, cap=8192):
+    """Token counts of the pieces a batch of T tokens runs as: ceil(T / cap)
+    near-equal pieces, the larger ones first."""
+    n = max(1, -(-T // cap))
+    q, rem = divmod(T, n)
+    return [q + 1] * rem + [q] * (n - rem)
+
+
+@pytest.mark.parametrize("T", [8193, 16384, 16385, 20000, 100000])
+def test_large_batches_run_in_pieces(T):
+    """Above 8192 tokens a call runs as pieces of at most 8192 tokens: its
+    workspace is the largest any piece needs, for every entry point, and the
+    pieces' validation is the whole batch's."""
+    pieces = _pieces(T)
+    assert sum(pieces) == T and max(pieces) <= 8192 and max(pieces) - min(pieces) <= 1
+    kw = dict(n_clusters=25, n_adapters=1000)
+    ws = cts.workspace_size(_p(T=T, **kw))
+    assert ws > 0 and ws == max(cts.workspace_size(_p(T=q, **kw)) for q in set(pieces))
+    wsu = cts.workspace_size(_p(T=T, **kw), compressed=False)
+    assert wsu == max(cts.workspace_size(_p(T=q, **kw), compressed=False) for q in set(pieces))
+    wsm = cts.workspace_size_multi(_p(T=T, **kw), [64, 128])
+    assert wsm == max(cts.workspace_size_multi(_p(T=q, **kw), [64, 128]) for q in set(pieces))
+    # an undersized workspace is still refused for the whole call
+    assert _apply(_p(T=T, **kw), ws_bytes=ws - 1) == B.CTS_ERR_WORKSPACE
+    # the bucketing read-back describes one piece's sort: refused for pieces
+    offs = (ctypes.c_size_t * 5)()
+    assert cts.lib().cts_workspace_bucketing(ctypes.byref(_p(T=T, **kw)), 1, offs) == B.CTS_ERR_UNSUPPORTED
+    assert cts.lib().cts_workspace_bucketing(ctypes.byref(_p(T=8192, **kw)), 1, offs) == B.CTS_OK
+
+
 def test_workspace_grows_with_problem():
     small = cts.workspace_size(_p(T=32))
     big = cts.workspace_size(_p(T=4096, n_clusters=25, n_adapters=1000))
@@ -186,7 +216,7 @@ def _apply_d(p, ptrs=None, ws_bytes=1 << 40, y=None, ws=None):
 @pytest.mark.parametrize("kw,code", [
     (dict(T=-1), B.CTS_ERR_INVALID_ARG), (dict(r=0), B.CTS_ERR_INVALID_ARG),
     (dict(n_clusters=0), B.CTS_ERR_INVALID_ARG), (dict(r=12), B.CTS_ERR_UNSUPPORTED),
-    (dict(T=8193), B.CTS_ERR_UNSUPPORTED), (dict(dtype=2), B.CTS_ERR_UNSUPPORTED),
+    (dict(dtype=2), B.CTS_ERR_UNSUPPORTED),
 ])
 def test_apply_diag_rejects_bad_problem(kw, code):
     assert _apply_d(_p(**kw)) == code
@@ -462,4 +492,6 @@ def test_multi_sorted_validation():
     # an output over the bucketing
     assert _multi_sorted(p, perm, bk, need, y=0x4100_0000_0000) == B.CTS_ERR_INVALID_ARG
     assert _multi_sorted(_p(T=512, r=12), perm, bk, need) == B.CTS_ERR_UNSUPPORTED
+    # a bucketing covers at most 8192 tokens (the sort's limit)
+    assert _multi_sorted(_p(T=8193), perm, bk, 1 << 30) == B.CTS_ERR_UNSUPPORTED
     assert _multi_sorted(_p(T=0), None, None, 0) == B.CTS_OK
