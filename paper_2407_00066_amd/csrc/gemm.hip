@@ -453,7 +453,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   __shared__ int32_t n_sched_s;
   __shared__ uint32_t pf_sink[PFD > 0 ? 64 : 1];
   constexpr int FS = FSORT ? kFuseSortMaxT : 1;
-  __shared__ uint32_t fs_raw[FS], fs_key[FS];                // keys in token order, sorted
+  __shared__ uint64_t fs_raw[FS];                          // (key << 8) | token, in token order
+  __shared__ uint32_t fs_key[FS];                          // keys, sorted
   __shared__ int32_t fs_perm[FS], fs_tile[FS + 1];
   __shared__ int32_t fs_cnt[2];
 
@@ -476,18 +477,17 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
         c = c < 0 ? 0 : (c >= p.fs_K ? p.fs_K - 1 : c);
         key |= static_cast<uint32_t>(c) << p.fs_bits_n;
       }
-      fs_raw[tid] = key;
+      fs_raw[tid] = (static_cast<uint64_t>(key) << 8) | static_cast<uint32_t>(tid);
     }
     __syncthreads();
     if (tid < T) {
-      const uint32_t key = fs_raw[tid];
+      // the token index makes every composite distinct: the rank is the
+      // number of smaller composites
+      const uint64_t c = fs_raw[tid];
       int rank = 0;
-      for (int j = 0; j < T; ++j) {
-        const uint32_t kj = fs_raw[j];
-        rank += (kj < key || (kj == key && j < tid)) ? 1 : 0;
-      }
+      for (int j = 0; j < T; ++j) rank += fs_raw[j] < c ? 1 : 0;
       fs_perm[rank] = tid;
-      fs_key[rank] = key;
+      fs_key[rank] = static_cast<uint32_t>(c >> 8);
     }
     __syncthreads();
     // wave 0: tile starts (a multiple of kSegTile or a new cluster) and, for

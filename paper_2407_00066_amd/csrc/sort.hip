@@ -106,8 +106,9 @@ __global__ __launch_bounds__(NT) void sort_kernel(
   __shared__ uint16_t vbuf[2][C::MAXT];
   __shared__ uint32_t hist[kWaves * kRadix];   // [wave][digit]
   __shared__ uint32_t wsum[kWaves];
-  // run keys padded with 16 entries that rank below nothing (all ones)
-  __shared__ __attribute__((aligned(16))) uint32_t run_key[kMaxRuns + 16];
+  // run keys with their run index, (key << 8) | run, padded with 16 entries
+  // that rank below nothing (all ones: a real entry is below 2^40)
+  __shared__ __attribute__((aligned(16))) uint64_t run_key[kMaxRuns + 16];
   __shared__ uint32_t run_start[kMaxRuns + 1], run_order[kMaxRuns], run_off[kMaxRuns];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -183,30 +184,29 @@ __global__ __launch_bounds__(NT) void sort_kernel(
       kp = (j0 > 0 && j0 < T) ? kbuf[0][j0 - 1] : 0u;
       for (int j = j0; j < j1; ++j) {
         const uint32_t k = kbuf[0][j];
-        if (j == 0 || k != kp) { run_start[r] = j; run_key[r] = k; ++r; }
+        if (j == 0 || k != kp) {
+          run_start[r] = j;
+          run_key[r] = (static_cast<uint64_t>(k) << 8) | r;
+          ++r;
+        }
         kp = k;
       }
       if (tid == 0) run_start[R] = T;
-      if (tid < 16) run_key[R + tid] = 0xffffffffu;            // keys use at most 31 bits
+      if (tid < 16) run_key[R + tid] = ~0ull;
       __syncthreads();
       if (static_cast<uint32_t>(tid) < R) {
-        const uint32_t kr = run_key[tid];
+        // (key, first token) order is (key, run index) order, and the run
+        // index makes every composite distinct: the rank is the number of
+        // smaller composites.  16 per step, eight 16-byte reads in flight.
+        const uint64_t kr = run_key[tid];
         uint32_t rank = 0;
-        const uint4* rk = reinterpret_cast<const uint4*>(run_key);
-        // 16 keys per step, four 16-byte reads in flight
+        const ulong2* rk = reinterpret_cast<const ulong2*>(run_key);
         for (uint32_t q = 0; q < R; q += 16) {
-          uint4 v[4];
+          ulong2 v[8];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[i] = rk[q / 4 + i];
+          for (int i = 0; i < 8; ++i) v[i] = rk[q / 2 + i];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint32_t kq[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const uint32_t qi = q + 4 * i + j;
-              rank += (kq[j] < kr || (kq[j] == kr && qi < static_cast<uint32_t>(tid))) ? 1u : 0u;
-            }
-          }
+          for (int i = 0; i < 8; ++i) rank += (v[i].x < kr ? 1u : 0u) + (v[i].y < kr ? 1u : 0u);
         }
         run_order[rank] = tid;
       }

@@ -1,9 +1,11 @@
 """GPU parity on the 32-layer decoder stack's own inputs: the tensors the
 benchmark times (workloads.stack_*, drawn on the device from per-projection
 seeds), layers 0, 15 and 31, all seven projections, run through the same
-calls as the benchmark's step (q/k/v and gate/up through cts_apply_multi with
-their V_k^T stacked along r, o and down through cts_apply), and 64 of the
-512 tokens compared with the fp64 oracle per projection."""
+calls as the benchmark's step (one cts_sort_by_cluster for the batch, then
+q/k/v and gate/up through cts_apply_multi_sorted with their V_k^T stacked
+along r, o and down through it with one module), and 64 of the 512 tokens
+compared with the fp64 oracle per projection.  The calls that sort for
+themselves (cts_apply_multi, cts_apply) give the same bits."""
 import numpy as np
 import pytest
 import torch
@@ -50,18 +52,24 @@ def test_stack_bench_inputs_sampled(oracle_mod, layer):
     mods = {nm: wl.stack_module(torch, "cuda", layer, nm) for nm, _, _ in wl.STACK_PROJ}
     xin = {nm: (x_o if nm == "o" else xs[d_in[nm]]) for nm in mods}
     say("stack layer %d: the benchmark's calls" % layer)
-    ys = {}
+    n, K = wl.STACK["n"], wl.STACK["K"]
+    perm = torch.empty(len(aid_h), dtype=torch.int32, device="cuda")
+    offs = torch.empty(K + 1, dtype=torch.int32, device="cuda")
+    bk = torch.empty(cts.bucketing_size(len(aid_h), n, K), dtype=torch.uint8, device="cuda")
+    cts.sort_by_cluster(aid, cof, n, K, perm=perm, offsets=offs, bucketing=bk)
+    ys, ys_own = {}, {}
     for grp in GROUPS:
         x = xin[grp[0]]
+        Vt = torch.cat([mods[nm][2] for nm in grp], dim=1).contiguous()
+        Ws, Us, Ss = ([mods[nm][i] for nm in grp] for i in (0, 1, 3))
+        ys.update(zip(grp, cts.apply_multi_sorted(perm, bk, x, Ws, Us, Vt, Ss)))
         if len(grp) == 1:
-            W, U, Vt, S = mods[grp[0]]
-            ys[grp[0]] = cts.apply(x, aid, cof, W, U, Vt, S)
+            ys_own[grp[0]] = cts.apply(x, aid, cof, Ws[0], Us[0], Vt, Ss[0])
         else:
-            Vt = torch.cat([mods[nm][2] for nm in grp], dim=1).contiguous()
-            outs = cts.apply_multi(x, aid, cof, [mods[nm][0] for nm in grp], [mods[nm][1] for nm in grp], Vt,
-                                   [mods[nm][3] for nm in grp])
-            ys.update(zip(grp, outs))
+            ys_own.update(zip(grp, cts.apply_multi(x, aid, cof, Ws, Us, Vt, Ss)))
     torch.cuda.synchronize()
+    for nm in ys:
+        assert torch.equal(ys[nm], ys_own[nm]), nm
     toks = _tokens(oracle_mod, aid_h, cof_h)
     assert len(toks) == 64
     for nm, _, _ in wl.STACK_PROJ:
