@@ -143,8 +143,43 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;
   if (sorted_rank && tid < nt) sorted_rank[lo + tid] = rk;
 
-  // Sigma_a -> LDS as fp32: every 16-byte load of this thread is issued
-  // before the first is widened and stored (one round trip, not a chain)
+  // Loads first, uses after: this thread's split partials (they depend on
+  // the item only) and its 16-byte pieces of Sigma_a (on the adapter) are
+  // all in flight before the first is waited for.  z = sum over the
+  // shrink's k-splits in fixed order; 4 consecutive values per thread and
+  // round, 16 splits' loads in flight at a time.  Rows of zpart and zp are
+  // ldz apart (ldz = r, or the stacked rank of several modules).
+  const int64_t split_stride = static_cast<int64_t>(T) * ldz;
+  const float* zbase = zpart + static_cast<int64_t>(lo) * ldz;
+  constexpr int ZR = (kSigmaChunk * MAXR / 4 + kSigThreads - 1) / kSigThreads;   // rounds of 4 values
+  f32x4 zacc[ZR];
+  f32x4 zv[ZR][16];
+#pragma unroll
+  for (int u = 0; u < ZR; ++u) zacc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto zload = [&](int q) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < ZR; ++u) {
+      const int e4 = (tid + u * kSigThreads) * 4;
+      const bool ok = e4 < cnt && e4 % r < rk;
+      const int64_t zo = static_cast<int64_t>(e4 / r) * ldz + e4 % r;
+#pragma unroll
+      for (int w = 0; w < 16; ++w)
+        if (ok && q + w < S) zv[u][w] = *reinterpret_cast<const f32x4*>(zbase + (q + w) * split_stride + zo);
+    }
+  };
+  auto zsum = [&](int q) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < ZR; ++u) {
+      const int e4 = (tid + u * kSigThreads) * 4;
+      const bool ok = e4 < cnt && e4 % r < rk;
+#pragma unroll
+      for (int w = 0; w < 16; ++w)
+        if (ok && q + w < S) zacc[u] += zv[u][w];
+    }
+  };
+  zload(0);
+
+  // Sigma_a -> LDS as fp32
   if (Sigma != nullptr) {
     int a = sorted_aid[lo];
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
@@ -159,6 +194,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
       const int row = (e * V) / r, col = (e * V) % r;
       raw[u] = (e < nv && row < rk && col < rk) ? sa[e] : uint4{0u, 0u, 0u, 0u};
     }
+    zsum(0);
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = tid + u * kSigThreads;
@@ -171,26 +207,21 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
           *reinterpret_cast<f32x4*>(sig + row * kSigLd + col + q) = f32x4{w[q], w[q + 1], w[q + 2], w[q + 3]};
       }
     }
+  } else {
+    zsum(0);
   }
-  // z = sum over the shrink's k-splits in fixed order; 4 consecutive values
-  // per thread, 16 splits' loads in flight at a time.  Rows of zpart and zp
-  // are ldz apart (ldz = r, or the stacked rank of several modules).
-  const int64_t split_stride = static_cast<int64_t>(T) * ldz;
-  const float* zbase = zpart + static_cast<int64_t>(lo) * ldz;
-  for (int e4 = tid * 4; e4 < cnt; e4 += kSigThreads * 4) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const int64_t zo = static_cast<int64_t>(e4 / r) * ldz + e4 % r;
-    for (int q = 0; e4 % r < rk && q < S; q += 16) {
-      f32x4 v[16];
+  // splits past the first 16
+  for (int q = 16; q < S; q += 16) {
+    zload(q);
+    zsum(q);
+  }
 #pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (q + u < S) v[u] = *reinterpret_cast<const f32x4*>(zbase + (q + u) * split_stride + zo);
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (q + u < S) acc += v[u];
+  for (int u = 0; u < ZR; ++u) {
+    const int e4 = (tid + u * kSigThreads) * 4;
+    if (e4 < cnt) {
+      const int i = e4 / r, c = e4 % r;
+      *reinterpret_cast<f32x4*>(z + i * kSigLd + c) = zacc[u];
     }
-    const int i = e4 / r, c = e4 % r;
-    *reinterpret_cast<f32x4*>(z + i * kSigLd + c) = acc;
   }
   __syncthreads();
 
