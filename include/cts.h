@@ -254,6 +254,25 @@ int cts_apply_multi_sorted(const cts_problem* p, int32_t M, const int32_t* d_out
                            const void* Vt, const void* const* Sigma, void* const* y,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* cts_apply_multi (ids) or cts_apply_multi_sorted (a bucketing) writing one
+ * packed output: the serving engine's fused projection output, into which
+ * each module adds its slice (App. F's add_lora_slice_with_sigma writes the
+ * columns [y_offset, y_offset + y_slice_size) of one y).  Module m writes
+ * the columns [c_m, c_m + d_out[m]) of every row of y, c_m = d_out[0] + ... +
+ * d_out[m-1]; the rows are ldy elements apart (ldy >= the sum of d_out, a
+ * multiple of 8; y 16-byte aligned), and columns past the sum are left
+ * untouched.  Exactly one of the pairs (adapter_id, cluster_of) and (perm,
+ * bucketing) is given (the other NULL).  Same problem limits, workspace
+ * (cts_workspace_size_multi), results and errors as the two calls it merges;
+ * the packed range y[0 .. (T-1) ldy + sum of d_out) must not overlap an
+ * input or the workspace. */
+int cts_apply_multi_packed(const cts_problem* p, int32_t M, const int32_t* d_out,
+                           const int32_t* adapter_id, const int32_t* cluster_of,
+                           const int32_t* perm, const void* bucketing, size_t bucketing_bytes,
+                           const void* x, const void* const* W, const void* const* U,
+                           const void* Vt, const void* const* Sigma, void* y, int32_t ldy,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 /* Synchronous id check for tests and debugging: copies the ids to the host
  * (waiting for `stream`) and returns CTS_ERR_BAD_IDS if any adapter_id is
  * outside [0, n) or any cluster_of outside [0, K) (cluster_of may be NULL). */

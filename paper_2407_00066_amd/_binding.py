@@ -26,7 +26,7 @@ EXPORTED = ("cts_status_string", "cts_workspace_size", "cts_workspace_size_uncom
             "cts_sort_by_cluster", "cts_apply", "cts_apply_diag", "cts_apply_ranked",
             "cts_apply_uncompressed", "cts_apply_uncompressed_ranked", "cts_validate_ids",
             "cts_set_stage_events", "cts_workspace_size_multi", "cts_apply_multi", "cts_apply_noalloc",
-            "cts_workspace_bucketing", "cts_bucketing_size", "cts_apply_multi_sorted",
+            "cts_workspace_bucketing", "cts_bucketing_size", "cts_apply_multi_sorted", "cts_apply_multi_packed",
             # include/cts_compress.h
             "cts_jd_workspace_size", "cts_jd_cluster_workspace_size", "cts_lora_norms2", "cts_jd_full",
             "cts_jd_diag", "cts_jd_sigma", "cts_jd_cluster")
@@ -99,6 +99,9 @@ def lib() -> ctypes.CDLL:
                 L.cts_apply_multi.restype = ctypes.c_int
                 L.cts_apply_multi_sorted.argtypes = [pp, i32, i32p, vp, vp, sz, vp, vpp, vpp, vp, vpp, vpp, vp, sz, vp]
                 L.cts_apply_multi_sorted.restype = ctypes.c_int
+                L.cts_apply_multi_packed.argtypes = [pp, i32, i32p, vp, vp, vp, vp, sz, vp, vpp, vpp, vp, vpp, vp, i32,
+                                                     vp, sz, vp]
+                L.cts_apply_multi_packed.restype = ctypes.c_int
                 jp, fl = ctypes.POINTER(JdProblem), ctypes.c_float
                 L.cts_jd_workspace_size.argtypes = [jp]
                 L.cts_jd_workspace_size.restype = sz
@@ -474,6 +477,52 @@ def apply_multi_sorted(perm, bucketing, x, Ws, Us, Vt, Sigmas, outs=None, out_dt
                                         ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)),
            "cts_apply_multi_sorted")
     return outs
+
+
+def apply_multi_packed(x, Ws, Us, Vt, Sigmas, adapter_id=None, cluster_of=None, perm=None, bucketing=None,
+                       out=None, out_dtype=None, workspace=None):
+    """The multi-module layer into one packed output (cts_apply_multi_packed):
+    module m's columns follow module m-1's in every row of out [T][ldy]
+    (ldy = out's row length, at least the sum of the modules' d_out).  Give
+    either (adapter_id, cluster_of) or (perm, bucketing) from
+    sort_by_cluster.  Returns out."""
+    dev = x.device
+    T, d_in = x.shape
+    M = len(Ws)
+    if not (len(Us) == len(Sigmas) == M):
+        raise ValueError("Ws, Us and Sigmas must have one entry per module")
+    if (adapter_id is None) == (perm is None) or (adapter_id is None) != (cluster_of is None) or \
+            (perm is None) != (bucketing is None):
+        raise ValueError("give either (adapter_id, cluster_of) or (perm, bucketing)")
+    K, _, r = Us[0].shape
+    n = Sigmas[0].shape[0]
+    dt = _dt(x, "x")
+    tdt = x.dtype
+    d_out = [int(w.shape[0]) for w in Ws]
+    if out is None:
+        out = torch.empty((T, sum(d_out)), dtype=tdt if out_dtype is None else out_dtype, device=dev)
+    if out.dim() != 2 or out.shape[0] != T:
+        raise ValueError("out must be [T][ldy]")
+    p = make_problem(T, d_in, 8, r=r, n_adapters=n, n_clusters=K, dtype=dt, out_dtype=_dt(out, "out"))
+    vp = ctypes.c_void_p
+    Wp = (vp * M)(*[_dev(w, "W[%d]" % m, dev, tdt, (d_out[m], d_in)) for m, w in enumerate(Ws)])
+    Up = (vp * M)(*[_dev(u, "U[%d]" % m, dev, tdt, (K, d_out[m], r)) for m, u in enumerate(Us)])
+    Sp = (vp * M)(*[_dev(sg, "Sigma[%d]" % m, dev, tdt, (n, r, r)) for m, sg in enumerate(Sigmas)])
+    dims = (ctypes.c_int32 * M)(*d_out)
+    if bucketing is not None and (bucketing.device != dev or bucketing.dtype != torch.uint8):
+        raise ValueError("bucketing must be a uint8 tensor on %s" % dev)
+    ids = (_dev(adapter_id, "adapter_id", dev, torch.int32, (T,)), _dev(cluster_of, "cluster_of", dev, torch.int32,
+                                                                      (n,))) if adapter_id is not None else (None, None)
+    srt = (_dev(perm, "perm", dev, torch.int32, (T,)), ctypes.c_void_p(bucketing.data_ptr()),
+           bucketing.numel()) if perm is not None else (None, None, 0)
+    nbytes = workspace_size_multi(p, d_out)
+    ws = _workspace(dev, nbytes, workspace)
+    _check(lib().cts_apply_multi_packed(ctypes.byref(p), M, dims, *ids, *srt, _dev(x, "x", dev, tdt, (T, d_in)),
+                                        Wp, Up, _dev(Vt, "Vt", dev, tdt, (K, M * r, d_in)), Sp,
+                                        _dev(out, "out", dev, None, tuple(out.shape)), int(out.shape[1]),
+                                        ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(dev)),
+           "cts_apply_multi_packed")
+    return out
 
 
 def validate_ids(adapter_id, cluster_of, n: int, K: int = 1) -> bool:

@@ -604,7 +604,8 @@ int make_multi_plan(const cts_problem* p, int M, const int32_t* d_out, MultiPlan
 int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, const void* x,
               const int32_t* adapter_id, const int32_t* cluster_of, const void* const* W,
               const void* const* U, const void* Vt, const void* const* Sigma, void* const* y, void* workspace,
-              hipStream_t stream, const int32_t* ext_perm = nullptr, const void* ext_bucket = nullptr) {
+              hipStream_t stream, const int32_t* ext_perm = nullptr, const void* ext_bucket = nullptr,
+              int64_t ldy = 0) {
   const Plan& pl = mp.mod[0];
   char* ws = static_cast<char*>(workspace);
   int32_t* perm = reinterpret_cast<int32_t*>(ws + pl.off_perm);
@@ -694,11 +695,12 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
     f.perm = perm; f.sorted_seg = sseg;
     f.ksplit = pm.main_split;
     f.part = pm.main_split > 1 ? ypart : nullptr;
-    f.out = y[m]; f.ldo = dm; f.out_perm = 1; f.out_dtype = p->out_dtype;
+    const int64_t ldm = ldy > 0 ? ldy : dm;              // output row stride (packed: the slices' total)
+    f.out = y[m]; f.ldo = ldm; f.out_perm = 1; f.out_dtype = p->out_dtype;
     e = cts::launch_seg_gemm(f, p->dtype, pm.main_tile, stream);
     if (e != hipSuccess) return CTS_ERR_HIP;
     if (pm.main_split > 1) {
-      e = cts::launch_splitk_reduce(ypart, pm.main_split, T, dm, perm, y[m], dm, p->out_dtype, stream);
+      e = cts::launch_splitk_reduce(ypart, pm.main_split, T, dm, perm, y[m], ldm, p->out_dtype, stream);
       if (e != hipSuccess) return CTS_ERR_HIP;
     }
   }
@@ -717,14 +719,31 @@ namespace {
 
 // The checks of cts_apply_multi and cts_apply_multi_sorted: either the ids
 // (adapter_id, cluster_of) or a bucketing (perm, bucket of bucket_bytes).
+// ypk != null: the packed output of cts_apply_multi_packed (module m's
+// columns at the sum of the earlier d_out, rows ldy elements apart) instead of
+// the array y.
 int apply_multi_checked(const cts_problem* p, int32_t M, const int32_t* d_out, const void* x,
                         const int32_t* adapter_id, const int32_t* cluster_of, const int32_t* perm,
                         const void* bucket, size_t bucket_bytes, const void* const* W, const void* const* U,
                         const void* Vt, const void* const* Sigma, void* const* y, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+                        size_t workspace_bytes, void* stream, void* ypk = nullptr, int32_t ldy = 0) {
   MultiPlan mp;
   const int rc = make_multi_plan(p, M, d_out, &mp);
   if (rc != CTS_OK) return rc;
+  void* yp[CTS_MAX_MODULES];
+  int64_t cols = 0;
+  for (int m = 0; m < M; ++m) cols += d_out[m];
+  if (ypk) {
+    // columns of module m: [c_m, c_m + d_out[m]), c_m a multiple of 8 (d_out
+    // is); rows ldy elements apart, a multiple of 8 (16-byte rows)
+    if (ldy < cols || ldy % 8) return CTS_ERR_INVALID_ARG;
+    int64_t c = 0;
+    for (int m = 0; m < M; ++m) {
+      yp[m] = static_cast<char*>(ypk) + c * mp.mod[m].out_elt;
+      c += d_out[m];
+    }
+    y = yp;
+  }
   if (p->T == 0) return CTS_OK;
   const bool sorted = perm != nullptr || bucket != nullptr;
   if (sorted ? (!perm || !bucket) : (!adapter_id || !cluster_of)) return CTS_ERR_INVALID_ARG;
@@ -761,25 +780,34 @@ int apply_multi_checked(const cts_problem* p, int32_t M, const int32_t* d_out, c
     in.push_back({U[m], K * dm * r * e});
     in.push_back({Sigma[m], n * r * r * e});
   }
-  for (int m = 0; m < M; ++m) {
-    const Range ym{y[m], T * static_cast<size_t>(d_out[m]) * mp.mod[m].out_elt};
-    if (any_overlap(ym, {workspace, workspace_bytes}, in.data(), static_cast<int>(in.size())))
+  if (ypk) {
+    // the packed slices are disjoint by construction: one range for all
+    const Range yr{ypk, (T - 1) * static_cast<size_t>(ldy) * mp.mod[0].out_elt +
+                            static_cast<size_t>(cols) * mp.mod[0].out_elt};
+    if (any_overlap(yr, {workspace, workspace_bytes}, in.data(), static_cast<int>(in.size())))
       return CTS_ERR_INVALID_ARG;
-    for (int k = 0; k < m; ++k)
-      if (overlap(ym, {y[k], T * static_cast<size_t>(d_out[k]) * mp.mod[k].out_elt})) return CTS_ERR_INVALID_ARG;
+  } else {
+    for (int m = 0; m < M; ++m) {
+      const Range ym{y[m], T * static_cast<size_t>(d_out[m]) * mp.mod[m].out_elt};
+      if (any_overlap(ym, {workspace, workspace_bytes}, in.data(), static_cast<int>(in.size())))
+        return CTS_ERR_INVALID_ARG;
+      for (int k = 0; k < m; ++k)
+        if (overlap(ym, {y[k], T * static_cast<size_t>(d_out[k]) * mp.mod[k].out_elt})) return CTS_ERR_INVALID_ARG;
+    }
   }
+  const int64_t ld = ypk ? ldy : 0;
   if (sorted)   // one bucketing of the whole batch (cts_sort_by_cluster: T <= kSortMaxT)
     return run_multi(p, mp, d_out, x, nullptr, nullptr, W, U, Vt, Sigma, y, workspace,
-                     static_cast<hipStream_t>(stream), perm, bucket);
+                     static_cast<hipStream_t>(stream), perm, bucket, ld);
   return for_pieces(p, [&](const cts_problem& q, size_t t0) {
     MultiPlan mq;
     const int rq = make_multi_plan(&q, M, d_out, &mq);
     if (rq != CTS_OK) return rq;
     void* yq[CTS_MAX_MODULES];
     for (int m = 0; m < M; ++m)
-      yq[m] = static_cast<char*>(y[m]) + t0 * static_cast<size_t>(d_out[m]) * mp.mod[m].out_elt;
+      yq[m] = static_cast<char*>(y[m]) + t0 * static_cast<size_t>(ld > 0 ? ld : d_out[m]) * mp.mod[m].out_elt;
     return run_multi(&q, mq, d_out, static_cast<const char*>(x) + t0 * di * e, adapter_id + t0, cluster_of, W,
-                     U, Vt, Sigma, yq, workspace, static_cast<hipStream_t>(stream));
+                     U, Vt, Sigma, yq, workspace, static_cast<hipStream_t>(stream), nullptr, nullptr, ld);
   });
 }
 
@@ -800,6 +828,18 @@ int cts_apply_multi_sorted(const cts_problem* p, int32_t M, const int32_t* d_out
   if (p && p->T > 0 && (!perm || !bucketing)) return CTS_ERR_INVALID_ARG;
   return apply_multi_checked(p, M, d_out, x, nullptr, nullptr, perm, bucketing, bucketing_bytes, W, U, Vt,
                              Sigma, y, workspace, workspace_bytes, stream);
+}
+
+int cts_apply_multi_packed(const cts_problem* p, int32_t M, const int32_t* d_out, const int32_t* adapter_id,
+                           const int32_t* cluster_of, const int32_t* perm, const void* bucketing,
+                           size_t bucketing_bytes, const void* x, const void* const* W, const void* const* U,
+                           const void* Vt, const void* const* Sigma, void* y, int32_t ldy, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  const bool ids = adapter_id || cluster_of, sorted = perm || bucketing;
+  if (p && p->T > 0 && ids == sorted) return CTS_ERR_INVALID_ARG;     // exactly one of the two
+  if (p && p->T > 0 && !y) return CTS_ERR_INVALID_ARG;
+  return apply_multi_checked(p, M, d_out, x, adapter_id, cluster_of, perm, bucketing, bucketing_bytes, W, U, Vt,
+                             Sigma, nullptr, workspace, workspace_bytes, stream, y, ldy);
 }
 
 namespace {

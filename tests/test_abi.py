@@ -495,3 +495,41 @@ def test_multi_sorted_validation():
     # a bucketing covers at most 8192 tokens (the sort's limit)
     assert _multi_sorted(_p(T=8193), perm, bk, 1 << 30) == B.CTS_ERR_UNSUPPORTED
     assert _multi_sorted(_p(T=0), None, None, 0) == B.CTS_OK
+
+
+def _packed(p, d_out=(64, 32), ids=True, srt=False, y=0x7000_0000_0000, ldy=96, ws_bytes=1 << 30,
+            ws=0x6000_0000_0000, bk_bytes=1 << 20):
+    vp = ctypes.c_void_p
+    M = len(d_out)
+    dims = (ctypes.c_int32 * M)(*d_out)
+    arr = lambda base: (vp * M)(*[vp(base + (m << 32)) for m in range(M)])
+    a, c = (vp(0x5500_0000_0000), vp(0x5600_0000_0000)) if ids else (None, None)
+    pm, bk = (vp(0x5700_0000_0000), vp(0x5800_0000_0000)) if srt else (None, None)
+    return cts.lib().cts_apply_multi_packed(ctypes.byref(p), M, dims, a, c, pm, bk, bk_bytes if srt else 0,
+                                            vp(0x5300_0000_0000), arr(0x5000_0000_0000), arr(0x5100_0000_0000),
+                                            vp(0x5400_0000_0000), arr(0x5200_0000_0000), vp(y) if y else None,
+                                            ldy, vp(ws) if ws else None, ws_bytes, None)
+
+
+def test_multi_packed_validation():
+    """cts_apply_multi_packed: exactly one of the ids and a bucketing, a row
+    stride that holds every module's columns, one packed range checked
+    against the inputs and the workspace."""
+    p = B.make_problem(32, 64, 8, r=16, n_adapters=4, n_clusters=2)
+    need = cts.workspace_size_multi(p, [64, 32])
+    assert _packed(p, ids=False, srt=False) == B.CTS_ERR_INVALID_ARG             # neither
+    assert _packed(p, ids=True, srt=True) == B.CTS_ERR_INVALID_ARG               # both
+    assert _packed(p, y=0) == B.CTS_ERR_INVALID_ARG
+    assert _packed(p, ldy=88) == B.CTS_ERR_INVALID_ARG                           # < 64 + 32
+    assert _packed(p, ldy=100) == B.CTS_ERR_INVALID_ARG                          # not a multiple of 8
+    assert _packed(p, y=0x7000_0000_0008) == B.CTS_ERR_INVALID_ARG               # misaligned
+    assert _packed(p, ws_bytes=need - 1) == B.CTS_ERR_WORKSPACE
+    assert _packed(p, ids=False, srt=True, ws_bytes=need - 1) == B.CTS_ERR_WORKSPACE
+    assert _packed(p, ids=False, srt=True, bk_bytes=8) == B.CTS_ERR_WORKSPACE    # bucketing too small
+    # the packed range reaches x (rows 1024 apart: row 31 ends past 0x5300...)
+    assert _packed(p, y=0x5300_0000_0000 - 31 * 1024 * 2, ldy=1024, ws_bytes=need) == B.CTS_ERR_INVALID_ARG
+    assert _packed(p, y=0x6000_0000_0000, ws=0x6000_0000_0000, ws_bytes=need) == B.CTS_ERR_INVALID_ARG
+    p0 = B.make_problem(0, 64, 8, r=16, n_adapters=4, n_clusters=2)
+    assert _packed(p0, ids=False, y=0, ws=0, ws_bytes=0) == B.CTS_OK
+    assert cts.lib().cts_apply_multi_packed(None, 2, None, *[None] * 4, 0, *[None] * 6, 0, None, 0, None) \
+        == B.CTS_ERR_INVALID_ARG

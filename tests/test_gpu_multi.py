@@ -111,3 +111,46 @@ def test_apply_multi_sorted_many_calls_one_sort(oracle_mod):
                                   Vt, [m.Sigma for m in mods])
     for m in range(len(mods)):
         assert row_rel_err(host(outs[0][m]), oref[m]) <= TOL["bf16"], m
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_apply_multi_packed(name):
+    """cts_apply_multi_packed: the modules' outputs as column slices of one
+    packed y with padded rows, from the ids and from a shared bucketing; each
+    slice bit for bit cts_apply_multi's output for that module, the padding
+    columns untouched."""
+    w0, mods, Vt = _modules(CASES[name])
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    Ws, Us, Ss = [dev(m.W) for m in mods], [dev(m.U) for m in mods], [dev(m.Sigma) for m in mods]
+    d_out = [m.d_out for m in mods]
+    ldy = sum(d_out) + 16
+    odt = x.dtype
+    say("apply_multi_packed %s (M=%d, ldy=%d)" % (name, len(mods), ldy))
+    ref = cts.apply_multi(x, aid, cof, Ws, Us, dev(Vt), Ss)
+    y_ids = torch.full((w0.T, ldy), 7.0, dtype=odt, device="cuda")
+    cts.apply_multi_packed(x, Ws, Us, dev(Vt), Ss, adapter_id=aid, cluster_of=cof, out=y_ids)
+    perm, _, bk = cts.sort_by_cluster(aid, cof, w0.n, w0.K, bucketing=True)
+    y_srt = torch.full((w0.T, ldy), 7.0, dtype=odt, device="cuda")
+    cts.apply_multi_packed(x, Ws, Us, dev(Vt), Ss, perm=perm, bucketing=bk, out=y_srt)
+    torch.cuda.synchronize()
+    for y in (y_ids, y_srt):
+        c = 0
+        for m, dm in enumerate(d_out):
+            assert torch.equal(y[:, c:c + dm], ref[m]), m
+            c += dm
+        assert bool((y[:, c:] == 7.0).all())
+
+
+def test_apply_multi_packed_pieces(oracle_mod):
+    """A packed output over a batch of 9000 tokens (two pieces)."""
+    w0, mods, Vt = _modules(dict(cfg=147, T=9000, d_in=128, d_outs=(64, 32), r=16, n=30, K=3, ids="zipf"))
+    x, aid, cof = dev(w0.x), dev(w0.adapter_id), dev(w0.cluster_of)
+    say("apply_multi_packed over 9000 tokens")
+    y = cts.apply_multi_packed(x, [dev(m.W) for m in mods], [dev(m.U) for m in mods], dev(Vt),
+                               [dev(m.Sigma) for m in mods], adapter_id=aid, cluster_of=cof)
+    torch.cuda.synchronize()
+    oref = oracle_mod.apply_multi(w0.x, w0.adapter_id, w0.cluster_of, [m.W for m in mods], [m.U for m in mods],
+                                  Vt, [m.Sigma for m in mods])
+    yh = host(y)
+    assert row_rel_err(yh[:, :64], oref[0]) <= TOL["bf16"]
+    assert row_rel_err(yh[:, 64:], oref[1]) <= TOL["bf16"]
