@@ -107,6 +107,8 @@ struct GemmParams {
   // ceil(M / BM) max_tiles + split_target (enough for every n) and workgroup
   // 0 writes S to split_out[0] for the core-product stage.
   int split_target; int32_t* split_out;
+  // m-tiles per group of the XCD-aware tile order (set by the launcher)
+  int group_m;
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide

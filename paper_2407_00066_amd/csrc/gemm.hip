@@ -99,9 +99,12 @@ __device__ __forceinline__ int split_lo(int n, int ks, int S) { return (int)((in
 // grid size.
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
-__device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, int* ks, int nb_used = 0) {
+// group_m: m-tiles per group (0: kGroupM).
+__device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, int* ks, int nb_used = 0,
+                                              int group_m = 0) {
   const int b = blockIdx.x;
   const int nb_mn = gm * gn;
+  const int G = group_m > 0 ? group_m : kGroupM;
   // nb_mn * ksplit workgroups (the grid, or its first nb_used)
   const int nb = nb_used > 0 ? nb_used : static_cast<int>(gridDim.x);
   const int q = nb / kXcds, rem = nb % kXcds;
@@ -109,12 +112,27 @@ __device__ __forceinline__ void tile_of_block(int gm, int gn, int* mt, int* nt, 
   const int L = x * q + min(x, rem) + i;
   *ks = L / nb_mn;
   const int l = L % nb_mn;
-  const int per_group = kGroupM * gn;
+  const int per_group = G * gn;
   const int g = l / per_group;
-  const int gsz = min(kGroupM, gm - g * kGroupM);   // m-tiles in this group
+  const int gsz = min(G, gm - g * G);               // m-tiles in this group
   const int r = l % per_group;
-  *mt = g * kGroupM + r % gsz;
+  *mt = g * G + r % gsz;
   *nt = r / gsz;
+}
+
+// The group size for a grid of gm x gn tiles split S ways: kGroupM when each
+// XCD's share of the grid is a whole number of groups or of group columns;
+// otherwise, when that share is a whole number of m-tiles with all their
+// n-tiles, the share itself (one group per XCD), so that no weight row tile
+// is fetched into two XCDs' L2s (e.g. 56 x 4 tiles: 7 m-tiles per XCD, not
+// groups of 8 that straddle two XCDs).
+int xcd_group_m(int gm, int gn, int S) {
+  const int64_t nb = static_cast<int64_t>(gm) * gn * S;
+  if (nb % kXcds) return kGroupM;
+  const int64_t c = nb / kXcds, pg = static_cast<int64_t>(kGroupM) * gn, nmn = static_cast<int64_t>(gm) * gn;
+  if (pg % c == 0 || c % pg == 0) return kGroupM;
+  if (c % gn == 0 && nmn % c == 0) return static_cast<int>(c / gn);
+  return kGroupM;
 }
 
 // STAGES: register stages of global loads in flight; OCC: waves per SIMD the
@@ -543,7 +561,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     if (static_cast<int>(blockIdx.x) >= used) return;
     tile_of_block(gm, ntl, &mt, &nt, &ks, used);
   } else {
-    tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks);
+    tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks, 0,
+                  tlist ? 0 : p.group_m);
   }
   const int S = s_pieces;
   int j0, jn;
@@ -1091,8 +1110,13 @@ hipError_t launch_dma1(const GemmParams& p, hipStream_t stream) {
     const int64_t gmt = (p.M + BM - 1) / BM;
     grid = dim3(static_cast<unsigned>(std::min<int64_t>(gmt * gn + p.split_target, gmt * gn * p.ksplit)));
   }
+  GemmParams q = p;
+  // the L2 prefetch splits its lines over groups of kGroupM row tiles
+  q.group_m = (p.tile_start || FSORT || PFD > 0)
+                  ? 0
+                  : xcd_group_m((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, p.ksplit);
   hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT, RANKED>),
-                     grid, dim3(WM * WN * 64), 0, stream, p);
+                     grid, dim3(WM * WN * 64), 0, stream, q);
   return hipGetLastError();
 }
 
