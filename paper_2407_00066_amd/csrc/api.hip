@@ -547,9 +547,18 @@ int cts_apply_ranked(const cts_problem* p, const void* x, const int32_t* adapter
 namespace {
 
 // ---- several modules sharing x, the adapter ids and the cluster map
+// Workgroups of a grouped multi-module launch: one round over 256 compute
+// units.
+constexpr int64_t kGroupedMaxWorkgroups = 256;
+
 struct MultiPlan {
   Plan mod[CTS_MAX_MODULES];   // per-module plans (fused GEMM tile and split)
   int M, rtot, shrink_split;
+  // grouped: every module's fused GEMM in one launch, with the tile and split
+  // of one GEMM as wide as all the modules together (bf16 inputs, M > 1)
+  bool grouped;
+  Tile g_tile;
+  int g_split, d_sum;
   size_t off_zpart, off_zp, off_ypart, total;
 };
 
@@ -573,9 +582,37 @@ int multi_plan_piece(const cts_problem* p, int M, const int32_t* d_out, MultiPla
   mp->off_zpart = off; off = align_up(off + 4ull * mp->shrink_split * T * mp->rtot);
   mp->off_zp = off;    off = align_up(off + static_cast<size_t>(p0.elt) * T * mp->rtot);
   mp->off_ypart = off;
+  mp->d_sum = 0;
+  for (int m = 0; m < M; ++m) mp->d_sum += d_out[m];
+  // grouped when the one launch fits one round of workgroups over the
+  // compute units (q/k/v at T = 512: 192 workgroups instead of three launches
+  // and three split-K sums); two launches of a round each are kept apart
+  // (gate/up at T = 512: 448 grouped workgroups were slower than 2 x 224)
+  mp->grouped = false;
+  if (M > 1 && p0.elt == 2) {
+    cts_problem q = *p;
+    q.d_out = mp->d_sum;
+    Plan gp;
+    if (plan_piece(&q, true, &gp) == CTS_OK) {
+      int BM, BN, BK;
+      cts::tile_dims(gp.main_tile, &BM, &BN, &BK);
+      int64_t rt = 0;
+      for (int m = 0; m < M; ++m) rt += ceil_div(d_out[m], BM);
+      const int64_t wgs = rt * ceil_div(std::max(T, 1), BN) * gp.main_split;
+      if (wgs <= kGroupedMaxWorkgroups) {
+        mp->grouped = true;
+        mp->g_tile = gp.main_tile;
+        mp->g_split = gp.main_split;
+      }
+    }
+  }
   size_t yp = 0;
-  for (int m = 0; m < M; ++m)
-    if (mp->mod[m].main_split > 1) yp = std::max<size_t>(yp, 4ull * mp->mod[m].main_split * T * d_out[m]);
+  if (mp->grouped) {
+    if (mp->g_split > 1) yp = 4ull * mp->g_split * T * mp->d_sum;
+  } else {
+    for (int m = 0; m < M; ++m)
+      if (mp->mod[m].main_split > 1) yp = std::max<size_t>(yp, 4ull * mp->mod[m].main_split * T * d_out[m]);
+  }
   off = align_up(off + yp);
   mp->total = off;
   return CTS_OK;
@@ -678,6 +715,57 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
                         zp, p->dtype, stream, false, sseg, nullptr, nullptr, rt, ssplit, Sigma, mp.M);
   if (e != hipSuccess) return CTS_ERR_HIP;
   if (mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
+
+  if (mp.grouped) {
+    // one launch: module m's row tiles follow module m-1's
+    int BM, BN, BK;
+    cts::tile_dims(mp.g_tile, &BM, &BN, &BK);
+    cts::GemmParams f{};
+    f.M = d_out[0]; f.N = T;
+    f.A0 = W[0]; f.lda0 = p->d_in; f.B0 = x; f.ldb0 = p->d_in; f.K0 = p->d_in;
+    f.A1 = U[0]; f.lda1 = r; f.B1 = zp; f.ldb1 = rt; f.K1 = r; f.b1_gather = 0;
+    f.b0_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
+    f.perm = perm; f.sorted_seg = sseg;
+    f.ksplit = mp.g_split;
+    f.part = mp.g_split > 1 ? ypart : nullptr;
+    f.part_ld = mp.d_sum;
+    f.out = y[0]; f.ldo = ldy > 0 ? ldy : d_out[0]; f.out_perm = 1; f.out_dtype = p->out_dtype;
+    f.n_mod = mp.M;
+    cts::SplitkMods sm{};
+    sm.n = mp.M;
+    int rt_acc = 0, col = 0;
+    for (int m = 0; m < mp.M; ++m) {
+      const int dm = d_out[m];
+      f.mod_rt[m] = rt_acc;
+      f.mod_M[m] = dm;
+      f.mod_col[m] = col;
+      f.mod_A0[m] = W[m];
+      f.mod_a0_bytes[m] = static_cast<uint32_t>(static_cast<uint64_t>(dm) * p->d_in * pl.elt);
+      f.mod_A1[m] = U[m];
+      f.mod_a1_seg_bytes[m] = static_cast<uint32_t>(static_cast<uint64_t>(dm) * r * pl.elt);
+      f.mod_B1[m] = zp + static_cast<size_t>(m) * r * pl.elt;
+      f.mod_b1_bytes[m] =
+          static_cast<uint32_t>((static_cast<uint64_t>(T) * rt - static_cast<uint64_t>(m) * r) * pl.elt);
+      f.mod_out[m] = y[m];
+      f.mod_ldo[m] = ldy > 0 ? ldy : dm;
+      sm.col[m] = col;
+      sm.out[m] = y[m];
+      sm.ldo[m] = f.mod_ldo[m];
+      rt_acc += (dm + BM - 1) / BM;
+      col += dm;
+    }
+    f.mod_rt[mp.M] = rt_acc;
+    sm.col[mp.M] = col;
+    f.a0_bytes = f.mod_a0_bytes[0]; f.a1_seg_bytes = f.mod_a1_seg_bytes[0]; f.b1_bytes = f.mod_b1_bytes[0];
+    e = cts::launch_seg_gemm(f, p->dtype, mp.g_tile, stream);
+    if (e != hipSuccess) return CTS_ERR_HIP;
+    if (mp.g_split > 1) {
+      e = cts::launch_splitk_reduce(ypart, mp.g_split, T, mp.d_sum, perm, nullptr, 0, p->out_dtype, stream, &sm);
+      if (e != hipSuccess) return CTS_ERR_HIP;
+    }
+    if (mark(4, stream) != hipSuccess) return CTS_ERR_HIP;
+    return mark(5, stream) == hipSuccess ? CTS_OK : CTS_ERR_HIP;
+  }
 
   // fused W_m X + U_k^(m) Z'^(m) per module
   for (int m = 0; m < mp.M; ++m) {

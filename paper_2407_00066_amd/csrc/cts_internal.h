@@ -61,6 +61,8 @@ hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int
                        hipStream_t stream);
 
 // ----------------------------------------------------- segmented MFMA GEMM
+// Modules one fused-GEMM launch can hold.
+constexpr int kMaxGemmModules = 8;
 // out[j][m] (m < M rows of the weight operand, j < N sorted token positions) =
 //     sum_k A0[m][k] * B0[map(j)][k]                       (dense phase, K0)
 //   + sum_k A1_{seg(j)}[m][k] * B1[map1(j)][k]             (segment phase, K1)
@@ -109,6 +111,22 @@ struct GemmParams {
   int split_target; int32_t* split_out;
   // m-tiles per group of the XCD-aware tile order (set by the launcher)
   int group_m;
+  // Several modules in one launch (n_mod > 0; LDS-ring tiles, no token
+  // tiles): module m owns the grid's row tiles [mod_rt[m], mod_rt[m+1]),
+  // mod_rt[m+1] - mod_rt[m] = ceil(mod_M[m] / BM), and its M, A0, A1, B1,
+  // out, ldo and operand sizes replace the fields above.  Its split partials
+  // are the columns [mod_col[m], mod_col[m] + mod_M[m]) of rows part_ld floats
+  // apart (0: M).
+  int n_mod;
+  int mod_rt[kMaxGemmModules + 1];
+  int mod_M[kMaxGemmModules], mod_col[kMaxGemmModules];
+  const void* mod_A0[kMaxGemmModules];
+  const void* mod_A1[kMaxGemmModules];
+  const void* mod_B1[kMaxGemmModules];
+  void* mod_out[kMaxGemmModules];
+  int64_t mod_ldo[kMaxGemmModules];
+  uint32_t mod_a0_bytes[kMaxGemmModules], mod_a1_seg_bytes[kMaxGemmModules], mod_b1_bytes[kMaxGemmModules];
+  int64_t part_ld;
 };
 
 // Tile shapes of the segmented GEMM (BM x BN x BK).  Large 256x256x64, Wide
@@ -151,8 +169,20 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
 // it is on; a no-op otherwise.
 hipError_t stage_mark(int i, hipStream_t s);
 
-// y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype.
+// Outputs of several modules' split partials reduced in one launch: the
+// partials' columns [col[q], col[q+1]) (multiples of 8, col[0] = 0,
+// col[n] = M) go to module q's output out[q] with rows ldo[q] apart.
+struct SplitkMods {
+  int n;
+  int col[kMaxGemmModules + 1];
+  void* out[kMaxGemmModules];
+  int64_t ldo[kMaxGemmModules];
+};
+
+// y[perm[j]][m] = sum_s part[s][j][m], converted to out_dtype (with mods:
+// into the module that owns column m, at its column m - col[q]).
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,
-                                void* out, int64_t ldo, int out_dtype, hipStream_t stream);
+                                void* out, int64_t ldo, int out_dtype, hipStream_t stream,
+                                const SplitkMods* mods = nullptr);
 
 }  // namespace cts

@@ -450,8 +450,9 @@ struct DmaCfg {
 // RANKED: the segments have ranks (p.seg_rank, with each column's rank in
 // p.sorted_rank): a cluster run takes only its adapter k-tiles below its
 // rank, from a schedule listed in LDS.
+// MODS: the launch may hold several modules (p.n_mod > 0).
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT, int PFD = 0, int WSPL = 1,
-          int FSORT = 0, int RANKED = 0>
+          int FSORT = 0, int RANKED = 0, int MODS = 0>
 __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const GemmParams p) {
   using C = DmaCfg<BM, BN, BK, WM, WN, MB, P, DIRECT>;
   static_assert(PFD == 0 || P <= 3, "prefetch wait counts cover rings of two or three stages");
@@ -561,9 +562,35 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     if (static_cast<int>(blockIdx.x) >= used) return;
     tile_of_block(gm, ntl, &mt, &nt, &ks, used);
   } else {
-    tile_of_block((p.M + BM - 1) / BM, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks, 0,
-                  tlist ? 0 : p.group_m);
+    const int gm_all = (MODS && !tlist && p.n_mod > 0) ? p.mod_rt[p.n_mod] : (p.M + BM - 1) / BM;
+    tile_of_block(gm_all, tlist ? p.max_tiles : (p.N + BN - 1) / BN, &mt, &nt, &ks, 0, tlist ? 0 : p.group_m);
   }
+  // the operands of this workgroup's module: with several modules in the
+  // launch, row tiles [mod_rt[m], mod_rt[m+1]) are module m's
+  const int mt_grid = mt;
+  int Mv = p.M;
+  const void* A0v = p.A0;
+  const void* A1v = p.A1;
+  const void* B1v = p.B1;
+  void* outv = p.out;
+  float* partv = p.part;
+  int64_t ldov = p.ldo;
+  uint32_t a0v_bytes = p.a0_bytes, a1_seg_bytes = p.a1_seg_bytes, b1v_bytes = p.b1_bytes;
+  if (MODS && !tlist && p.n_mod > 0) {
+    int mod = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxGemmModules; ++q) mod += (q < p.n_mod && mt >= p.mod_rt[q]) ? 1 : 0;
+    mod = __builtin_amdgcn_readfirstlane(mod);
+    mt -= p.mod_rt[mod];
+    Mv = p.mod_M[mod];
+    A0v = p.mod_A0[mod]; a0v_bytes = p.mod_a0_bytes[mod];
+    A1v = p.mod_A1[mod]; a1_seg_bytes = p.mod_a1_seg_bytes[mod];
+    B1v = p.mod_B1[mod]; b1v_bytes = p.mod_b1_bytes[mod];
+    outv = p.mod_out[mod]; ldov = p.mod_ldo[mod];
+    if (partv) partv += p.mod_col[mod];
+  }
+  // row stride of the split partials (the modules' total width with several)
+  const int64_t part_ld = (MODS && p.part_ld > 0) ? p.part_ld : Mv;
   const int S = s_pieces;
   int j0, jn;
   if (tlist) {
@@ -575,17 +602,17 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     j0 = nt * BN;
     jn = min(BN, p.N - j0);
   }
-  const void* A0 = p.A0;
+  const void* A0 = A0v;
   const void* B0 = p.B0;
-  uint32_t a0_bytes = p.a0_bytes, b0_bytes = p.b0_bytes;
+  uint32_t a0_bytes = a0v_bytes, b0_bytes = p.b0_bytes;
   int64_t lda0 = p.lda0, ldb0 = p.ldb0;
   int K0 = p.K0, K1 = p.K1;
   bool b0_gather = true;
   if (tlist) {
     const int seg = FSORT ? static_cast<int>(fs_key[j0] >> fs_cshift) : p.sorted_seg[j0];
-    A0 = static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes;
-    a0_bytes = p.a1_seg_bytes; lda0 = p.lda1; K0 = p.K1;
-    B0 = p.B1; b0_bytes = p.b1_bytes; ldb0 = p.ldb1; b0_gather = p.b1_gather != 0;
+    A0 = static_cast<const char*>(A1v) + static_cast<int64_t>(seg) * a1_seg_bytes;
+    a0_bytes = a1_seg_bytes; lda0 = p.lda1; K0 = p.K1;
+    B0 = B1v; b0_bytes = b1v_bytes; ldb0 = p.ldb1; b0_gather = p.b1_gather != 0;
     K1 = 0;
   }
   const int m0 = mt * BM;
@@ -625,7 +652,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 #pragma unroll
   for (int j = 0; j < C::QA; ++j) {
     const int m = m0 + C::RPI * (wave + C::NW * j) + lrow;
-    const bool ok = m < p.M;
+    const bool ok = m < Mv;
     a0_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT + cbytes : kOob;
     a1_v[j] = ok ? static_cast<uint32_t>(m) * static_cast<uint32_t>(p.lda1) * ELT + cbytes : kOob;
   }
@@ -752,7 +779,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     b1_v[j] = r1 * static_cast<uint32_t>(p.ldb1) * ELT + cbytes;
   }
   const __amdgpu_buffer_rsrc_t rB0 = make_rsrc(B0, b0_bytes);
-  const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(p.B1, p.b1_bytes);
+  const __amdgpu_buffer_rsrc_t rB1 = make_rsrc(B1v, b1v_bytes);
   int lt = 0, lq = 0, lkt = s_lo;
 
   // L2 prefetch: this lane's weight row or token row (kOob when none)
@@ -763,9 +790,9 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
                                BN % (8 * PFW) == 0 && BN / 8 / PFW <= 64), "prefetch lanes");
     if (pf_w) {
       const int m = m0 + WSPL * (wave * (BM / WSPL / PFW) + lane) + (nt % WSPL);
-      if (lane < BM / WSPL / PFW && m < p.M) pf_v = static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT;
+      if (lane < BM / WSPL / PFW && m < Mv) pf_v = static_cast<uint32_t>(m) * static_cast<uint32_t>(lda0) * ELT;
     } else {
-      const int jl = 8 * ((wave - PFW) * (BN / 8 / PFW) + lane) + (mt & 7);
+      const int jl = 8 * ((wave - PFW) * (BN / 8 / PFW) + lane) + (mt_grid & 7);
       if (lane < BN / 8 / PFW && jl < jn) {
         const uint32_t r0 = b0_gather ? static_cast<uint32_t>(t_perm[jl]) : static_cast<uint32_t>(j0 + jl);
         pf_v = r0 * static_cast<uint32_t>(ldb0) * ELT;
@@ -809,8 +836,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       L.lo = static_cast<int>(ex & 511u);
       L.span = (ex >> 9) & 511u;
       const int seg = static_cast<int>(ey & 0xffffu);
-      L.rA = make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
-                       p.a1_seg_bytes);
+      L.rA = make_rsrc(static_cast<const char*>(A1v) + static_cast<int64_t>(seg) * a1_seg_bytes,
+                       a1_seg_bytes);
       L.rB = rB1;
       L.dsel = 0u;
       k0 = (ex >> 18) * BK;
@@ -822,8 +849,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       L.lo = run_start[q];
       const int hi = run_start[q + 1];
       const int seg = __builtin_amdgcn_readfirstlane(t_seg[L.lo]);
-      L.rA = make_rsrc(static_cast<const char*>(p.A1) + static_cast<int64_t>(seg) * p.a1_seg_bytes,
-                       p.a1_seg_bytes);
+      L.rA = make_rsrc(static_cast<const char*>(A1v) + static_cast<int64_t>(seg) * a1_seg_bytes,
+                       a1_seg_bytes);
       L.rB = rB1;
       L.span = static_cast<uint32_t>(hi - L.lo);
       // phase select by mask arithmetic (a conditional pick between the two
@@ -910,8 +937,11 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   constexpr int NR = C::FM + C::FN;                          // fragment reads per step
   constexpr int NLG = C::NKS > 2 ? C::NKS / 2 : 1;           // steps that issue loads
   constexpr int GPS = (C::LPT + NLG - 1) / NLG;              // loads per such step
-  static_assert(GPS <= (NM > NR ? NM : NR), "every load gets an issue slot");
-  static_assert(NPF == 0 || GPS < (NM > NR ? NM : NR), "a slot for the prefetch");
+  // issue slots per multiply step: one per MFMA or fragment read, or one per
+  // load where a step has more loads than both (load-heavy, narrow tiles)
+  constexpr int NSL0 = NM > NR ? NM : NR;
+  constexpr int NSL = NSL0 > GPS ? NSL0 : GPS;
+  static_assert(NPF == 0 || GPS < NSL, "a slot for the prefetch");
   bf16x8 fa[2][C::FM], fb[2][C::FN];
   auto read_frag = [&](int buf, int r, uint32_t sa, uint32_t sb, uint32_t sl) __attribute__((always_inline)) {
     if (r < C::FM) lds_read16(fa[buf][r], sa + sl + r * MB * C::ROWB);
@@ -969,7 +999,7 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
       for (int j = 0; j < C::FN; ++j) pin(fb[b][j]);
       if (s2 + 1 < C::NKS) {
 #pragma unroll
-        for (int m = 0; m < (NM > NR ? NM : NR); ++m) {
+        for (int m = 0; m < NSL; ++m) {
           if (m < NM) mma(b, m);
           if (m < NR) read_frag(b ^ 1, m, sa, sb, slot[s2 + 1]);
           if (s2 < NLG && m < GPS) iss(s2 * GPS + m, s2 * GPS + m + 1);
@@ -1025,17 +1055,17 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 #pragma unroll
         for (int v = 0; v < MT::NACC; v += 4) {
           const int m = m0 + wm * C::WTM + i * MB + acc_row<MB>(lane, v);
-          if (!jok || m >= p.M) continue;
+          if (!jok || m >= Mv) continue;
           const f32x4 val = f32x4{acc[i][j][v], acc[i][j][v + 1], acc[i][j][v + 2], acc[i][j][v + 3]};
-          if (p.part) {
-            *reinterpret_cast<f32x4*>(p.part + (static_cast<int64_t>(ks) * p.N + j0 + jl) * p.M + m) = val;
+          if (partv) {
+            *reinterpret_cast<f32x4*>(partv + (static_cast<int64_t>(ks) * p.N + j0 + jl) * part_ld + m) = val;
           } else if (p.out_dtype == 1) {
             uint2 w;
             w.x = f32_to_bf16(val[0]) | (static_cast<uint32_t>(f32_to_bf16(val[1])) << 16);
             w.y = f32_to_bf16(val[2]) | (static_cast<uint32_t>(f32_to_bf16(val[3])) << 16);
-            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + orow * p.ldo + m) = w;
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(outv) + orow * ldov + m) = w;
           } else {
-            *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + orow * p.ldo + m) = val;
+            *reinterpret_cast<f32x4*>(static_cast<float*>(outv) + orow * ldov + m) = val;
           }
         }
     }
@@ -1057,21 +1087,21 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
     }
   __syncthreads();
 
-  if (p.part) {
-    float* part = p.part + static_cast<int64_t>(ks) * p.N * p.M;
+  if (partv) {
+    float* part = partv + static_cast<int64_t>(ks) * p.N * part_ld;
     constexpr int CPRO = BM / 4;
     for (int c = tid; c < BN * CPRO; c += C::NT) {
       const int jl = c / CPRO, mc = (c % CPRO) * 4;
-      if (jl < jn && m0 + mc < p.M)
-        *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(j0 + jl) * p.M + m0 + mc) =
+      if (jl < jn && m0 + mc < Mv)
+        *reinterpret_cast<f32x4*>(part + static_cast<int64_t>(j0 + jl) * part_ld + m0 + mc) =
             *reinterpret_cast<const f32x4*>(stg + jl * C::ST_ROW + mc);
     }
   } else if (p.out_dtype == 1) {
     constexpr int CPRO = BM / 8;
-    uint16_t* out = static_cast<uint16_t*>(p.out);
+    uint16_t* out = static_cast<uint16_t*>(outv);
     for (int c = tid; c < BN * CPRO; c += C::NT) {
       const int jl = c / CPRO, mc = (c % CPRO) * 8;
-      if (jl < jn && m0 + mc < p.M) {
+      if (jl < jn && m0 + mc < Mv) {
         const float* s = stg + jl * C::ST_ROW + mc;
         const f32x4 lo = *reinterpret_cast<const f32x4*>(s);
         const f32x4 hi = *reinterpret_cast<const f32x4*>(s + 4);
@@ -1081,17 +1111,17 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
         v.z = f32_to_bf16(hi[0]) | (static_cast<uint32_t>(f32_to_bf16(hi[1])) << 16);
         v.w = f32_to_bf16(hi[2]) | (static_cast<uint32_t>(f32_to_bf16(hi[3])) << 16);
         const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
-        *reinterpret_cast<uint4*>(out + row * p.ldo + m0 + mc) = v;
+        *reinterpret_cast<uint4*>(out + row * ldov + m0 + mc) = v;
       }
     }
   } else {
     constexpr int CPRO = BM / 4;
-    float* out = static_cast<float*>(p.out);
+    float* out = static_cast<float*>(outv);
     for (int c = tid; c < BN * CPRO; c += C::NT) {
       const int jl = c / CPRO, mc = (c % CPRO) * 4;
-      if (jl < jn && m0 + mc < p.M) {
+      if (jl < jn && m0 + mc < Mv) {
         const int64_t row = p.out_perm ? t_perm[jl] : static_cast<int64_t>(j0 + jl);
-        *reinterpret_cast<f32x4*>(out + row * p.ldo + m0 + mc) =
+        *reinterpret_cast<f32x4*>(out + row * ldov + m0 + mc) =
             *reinterpret_cast<const f32x4*>(stg + jl * C::ST_ROW + mc);
       }
     }
@@ -1099,10 +1129,19 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0, int PFD = 0,
-          int WSPL = 1, int FSORT = 0, int RANKED = 0>
+          int WSPL = 1, int FSORT = 0, int RANKED = 0, int MODS = 0>
 hipError_t launch_dma1(const GemmParams& p, hipStream_t stream) {
   const int gn = (p.tile_start || FSORT) ? p.max_tiles : (p.N + BN - 1) / BN;
-  dim3 grid(((p.M + BM - 1) / BM) * gn * p.ksplit);
+  // row tiles: the modules' together when the launch holds several
+  const bool mods = MODS && !(p.tile_start || FSORT) && p.n_mod > 0;
+  if (!MODS && p.n_mod > 0) return hipErrorInvalidValue;
+  if (mods) {
+    if (p.n_mod > kMaxGemmModules || p.mod_rt[0] != 0) return hipErrorInvalidValue;
+    for (int m = 0; m < p.n_mod; ++m)
+      if (p.mod_rt[m + 1] - p.mod_rt[m] != (p.mod_M[m] + BM - 1) / BM) return hipErrorInvalidValue;
+  }
+  const int gm = mods ? p.mod_rt[p.n_mod] : (p.M + BM - 1) / BM;
+  dim3 grid(gm * gn * p.ksplit);
   if ((p.tile_start || FSORT) && p.split_target > 0) {
     if (!(BM == 64 && BN == 64 && BK == 64)) return hipErrorInvalidValue;   // no adaptive split here
     // gm n S workgroups are used: fewer than gm max_tiles + split_target, and
@@ -1112,10 +1151,8 @@ hipError_t launch_dma1(const GemmParams& p, hipStream_t stream) {
   }
   GemmParams q = p;
   // the L2 prefetch splits its lines over groups of kGroupM row tiles
-  q.group_m = (p.tile_start || FSORT || PFD > 0)
-                  ? 0
-                  : xcd_group_m((p.M + BM - 1) / BM, (p.N + BN - 1) / BN, p.ksplit);
-  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT, RANKED>),
+  q.group_m = (p.tile_start || FSORT || PFD > 0) ? 0 : xcd_group_m(gm, (p.N + BN - 1) / BN, p.ksplit);
+  hipLaunchKernelGGL((seg_gemm_dma_kernel<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT, RANKED, MODS>),
                      grid, dim3(WM * WN * 64), 0, stream, q);
   return hipGetLastError();
 }
@@ -1126,6 +1163,10 @@ template <int BM, int BN, int BK, int WM, int WN, int MB, int P, int DIRECT = 0,
           int WSPL = 1, int FSORT = 0>
 hipError_t launch_dma(const GemmParams& p, hipStream_t stream) {
   const bool ranked = p.seg_rank && p.sorted_seg && p.K1 > 0 && !p.tile_start && !FSORT;
+  if (p.n_mod > 0) {
+    if (ranked || p.tile_start || FSORT) return hipErrorInvalidValue;
+    if constexpr (FSORT == 0) return launch_dma1<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, 0, 0, 1>(p, stream);
+  }
   if (!ranked) return launch_dma1<BM, BN, BK, WM, WN, MB, P, DIRECT, PFD, WSPL, FSORT>(p, stream);
   if (p.K1 > 2 * BK || !p.sorted_rank) return hipErrorInvalidValue;
   if constexpr (FSORT == 0)
@@ -1169,6 +1210,9 @@ void tile_dims(Tile tile, int* BM, int* BN, int* BK) {
 }
 
 hipError_t launch_seg_gemm(const GemmParams& p, int in_dtype, Tile tile, hipStream_t stream) {
+  // several modules in one launch: the LDS-ring tiles only, without token tiles
+  if (p.n_mod > 0 && (in_dtype == 0 || tile == Tile::Small || p.tile_start || p.fs_adapter))
+    return hipErrorInvalidValue;
   // explicit token tiles (at most kSegTile columns) only with the 64-wide tiles
   if (p.tile_start &&
       !(tile == Tile::Decode || tile == Tile::Shrink || tile == Tile::Small || tile == Tile::F32))

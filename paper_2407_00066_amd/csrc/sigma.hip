@@ -259,17 +259,29 @@ template <int OUT_BF16>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int S,
                                                             int N, int M,
                                                             const int32_t* __restrict__ perm,
-                                                            void* __restrict__ out, int64_t ldo) {
+                                                            void* __restrict__ out, int64_t ldo,
+                                                            const SplitkMods mods) {
   constexpr int V = OUT_BF16 ? 8 : 4;
   const int cpr = M / V;
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (c >= static_cast<int64_t>(N) * cpr) return;
-  const int j = static_cast<int>(c / cpr), m = static_cast<int>(c % cpr) * V;
+  const int j = static_cast<int>(c / cpr), mc = static_cast<int>(c % cpr) * V;
+  // several modules: columns [col[q], col[q+1]) of the partials are module
+  // q's output (each a multiple of 8 wide, so a chunk lies in one module)
+  int m = mc;
+  if (mods.n > 0) {
+    int q = 0;
+#pragma unroll
+    for (int u = 1; u < kMaxGemmModules; ++u) q += (u < mods.n && mc >= mods.col[u]) ? 1 : 0;
+    out = mods.out[q];
+    ldo = mods.ldo[q];
+    m = mc - mods.col[q];
+  }
   float acc[V];
 #pragma unroll
   for (int v = 0; v < V; ++v) acc[v] = 0.f;
   for (int s = 0; s < S; ++s) {
-    const float* src = part + (static_cast<int64_t>(s) * N + j) * M + m;
+    const float* src = part + (static_cast<int64_t>(s) * N + j) * M + mc;
 #pragma unroll
     for (int v = 0; v < V; v += 4) {
       const f32x4 x = *reinterpret_cast<const f32x4*>(src + v);
@@ -339,14 +351,23 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
 }
 
 hipError_t launch_splitk_reduce(const float* part, int S, int N, int M, const int32_t* perm,
-                                void* out, int64_t ldo, int out_dtype, hipStream_t stream) {
+                                void* out, int64_t ldo, int out_dtype, hipStream_t stream,
+                                const SplitkMods* mods) {
   const int V = out_dtype == 1 ? 8 : 4;
+  SplitkMods md{};
+  if (mods) {
+    if (mods->n < 1 || mods->n > kMaxGemmModules || mods->col[0] != 0 || mods->col[mods->n] != M)
+      return hipErrorInvalidValue;
+    for (int q = 0; q < mods->n; ++q)
+      if (mods->col[q + 1] <= mods->col[q] || mods->col[q] % 8) return hipErrorInvalidValue;
+    md = *mods;
+  }
   const int64_t chunks = static_cast<int64_t>(N) * (M / V);
   dim3 grid(static_cast<unsigned>((chunks + 255) / 256));
   if (out_dtype == 1)
-    hipLaunchKernelGGL(splitk_reduce_kernel<1>, grid, dim3(256), 0, stream, part, S, N, M, perm, out, ldo);
+    hipLaunchKernelGGL(splitk_reduce_kernel<1>, grid, dim3(256), 0, stream, part, S, N, M, perm, out, ldo, md);
   else
-    hipLaunchKernelGGL(splitk_reduce_kernel<0>, grid, dim3(256), 0, stream, part, S, N, M, perm, out, ldo);
+    hipLaunchKernelGGL(splitk_reduce_kernel<0>, grid, dim3(256), 0, stream, part, S, N, M, perm, out, ldo, md);
   return hipGetLastError();
 }
 
