@@ -38,7 +38,7 @@ struct Plan {
   int main_split, shrink_split;
   int max_items, max_ctiles;
   size_t off_perm, off_seg, off_aid, off_srank, off_offs, off_items, off_nitems, off_ctiles, off_nctiles,
-      off_ssplit, off_zpart, off_zp, off_ypart, total;
+      off_iaid, off_cseg, off_ssplit, off_zpart, off_zp, off_ypart, total;
 };
 
 constexpr uint64_t kMaxOperandBytes = 0x7fffffffull;   // buffer-load offsets are 31-bit
@@ -198,6 +198,8 @@ int plan_piece(const cts_problem* p, bool compressed, Plan* pl) {
   pl->off_nitems = off; off = align_up(off + 4);
   pl->off_ctiles = off; off = align_up(off + 4ull * (pl->max_ctiles + 1));
   pl->off_nctiles = off; off = align_up(off + 4);
+  pl->off_iaid = off;  off = align_up(off + 4ull * (pl->max_items + 1));
+  pl->off_cseg = off;  off = align_up(off + 4ull * (pl->max_ctiles + 1));
   pl->off_ssplit = off; off = align_up(off + 4);
   pl->off_zpart = off; off = align_up(off + 4ull * pl->shrink_split * T * pl->rank);
   pl->off_zp = off;    off = align_up(off + static_cast<size_t>(pl->elt) * T * pl->rank);
@@ -236,7 +238,7 @@ hipError_t mark(int i, hipStream_t s) {
 // The bucketing cts_sort_by_cluster leaves in its workspace (perm is its own
 // argument): each sorted position's cluster and adapter, the core-product
 // items and their count, the shrink tiles and their count.
-struct BucketLayout { size_t seg, aid, items, nitems, ctiles, nctiles, total; };
+struct BucketLayout { size_t seg, aid, items, nitems, ctiles, nctiles, iaid, cseg, total; };
 
 bool bucket_layout(int T, int n, int K, BucketLayout* L) {
   if (T < 0 || n < 1 || K < 1 || T > cts::kSortMaxT || n > 65536 || K > 65536) return false;
@@ -247,6 +249,8 @@ bool bucket_layout(int T, int n, int K, BucketLayout* L) {
   L->nitems = off;  off = align_up(off + 4);
   L->ctiles = off;  off = align_up(off + 4ull * (cts::max_seg_tiles(T, K) + 1));
   L->nctiles = off; off = align_up(off + 4);
+  L->iaid = off;    off = align_up(off + 4ull * (cts::max_sigma_items(T, n) + 1));
+  L->cseg = off;    off = align_up(off + 4ull * (cts::max_seg_tiles(T, K) + 1));
   L->total = off;
   return true;
 }
@@ -288,6 +292,8 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
   int32_t* ctiles = reinterpret_cast<int32_t*>(ws + pl.off_ctiles);
   int32_t* n_ctiles = reinterpret_cast<int32_t*>(ws + pl.off_nctiles);
+  int32_t* iaid = reinterpret_cast<int32_t*>(ws + pl.off_iaid);
+  int32_t* cseg = reinterpret_cast<int32_t*>(ws + pl.off_cseg);
   float* zpart = reinterpret_cast<float*>(ws + pl.off_zpart);
   void* zp = ws + pl.off_zp;
   float* ypart = reinterpret_cast<float*>(ws + pl.off_ypart);
@@ -299,7 +305,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   const bool fuse_sort = T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
   if (!fuse_sort) {
     e = cts::launch_sort(adapter_id, compressed ? cluster_of : nullptr, T, p->n_adapters,
-                         pl.nseg, perm, offs, sseg, said, items, n_items, ctiles, n_ctiles, stream);
+                         pl.nseg, perm, offs, sseg, said, items, n_items, ctiles, n_ctiles, stream, iaid, cseg);
     if (e != hipSuccess) return CTS_ERR_HIP;
   }
   if (mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
@@ -314,14 +320,15 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
   g.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = pl.shrink_split; g.part = zpart;
-  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles; g.tile_seg = cseg;
   int32_t* ssplit = nullptr;
   if (shrink_adaptive(T, pl.shrink_tile)) {
     ssplit = reinterpret_cast<int32_t*>(ws + pl.off_ssplit);
     g.split_target = kShrinkAdaptiveTarget; g.split_out = ssplit;
   }
   if (fuse_sort) {
-    g.tile_start = nullptr; g.n_tiles = nullptr;
+    g.tile_start = nullptr; g.n_tiles = nullptr; g.tile_seg = nullptr;
+    g.fs_item_aid = iaid;
     g.fs_adapter = adapter_id; g.fs_cluster = compressed ? cluster_of : nullptr;
     g.fs_n = p->n_adapters; g.fs_K = pl.nseg;
     int bits_n = 0;
@@ -334,7 +341,7 @@ int run_layer(const cts_problem* p, const Plan& pl, bool compressed, const void*
 
   e = cts::launch_sigma(zpart, pl.shrink_split, T, rank, said, p->n_adapters, items, n_items,
                         pl.max_items, compressed ? Sigma : nullptr, zp, p->dtype, stream, sigma_diag,
-                        sseg, seg_rank, seg_rank ? srank : nullptr, 0, ssplit);
+                        sseg, seg_rank, seg_rank ? srank : nullptr, 0, ssplit, nullptr, 0, iaid);
   if (e != hipSuccess || mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 
   cts::GemmParams f{};
@@ -438,7 +445,7 @@ int cts_sort_by_cluster(const int32_t* adapter_id, const int32_t* cluster_of, in
   auto at = [&](size_t off) { return ws ? reinterpret_cast<int32_t*>(ws + off) : nullptr; };
   const hipError_t e = cts::launch_sort(adapter_id, cluster_of, T, n, K, perm, cluster_offsets, at(L.seg),
                                         at(L.aid), at(L.items), at(L.nitems), at(L.ctiles), at(L.nctiles),
-                                        static_cast<hipStream_t>(stream));
+                                        static_cast<hipStream_t>(stream), at(L.iaid), at(L.cseg));
   return e == hipSuccess ? CTS_OK : CTS_ERR_HIP;
 }
 
@@ -653,6 +660,8 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   int32_t* n_items = reinterpret_cast<int32_t*>(ws + pl.off_nitems);
   int32_t* ctiles = reinterpret_cast<int32_t*>(ws + pl.off_ctiles);
   int32_t* n_ctiles = reinterpret_cast<int32_t*>(ws + pl.off_nctiles);
+  int32_t* iaid = reinterpret_cast<int32_t*>(ws + pl.off_iaid);
+  int32_t* cseg = reinterpret_cast<int32_t*>(ws + pl.off_cseg);
   const bool ext = ext_perm != nullptr;
   if (ext) {
     BucketLayout L;
@@ -665,6 +674,8 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
     n_items = reinterpret_cast<int32_t*>(b + L.nitems);
     ctiles = reinterpret_cast<int32_t*>(b + L.ctiles);
     n_ctiles = reinterpret_cast<int32_t*>(b + L.nctiles);
+    iaid = reinterpret_cast<int32_t*>(b + L.iaid);
+    cseg = reinterpret_cast<int32_t*>(b + L.cseg);
   }
   float* zpart = reinterpret_cast<float*>(ws + mp.off_zpart);
   char* zp = ws + mp.off_zp;
@@ -676,7 +687,7 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   const bool fuse_sort = !ext && T <= cts::kFuseSortMaxT && pl.shrink_tile == Tile::Shrink;
   if (!fuse_sort && !ext) {
     e = cts::launch_sort(adapter_id, cluster_of, T, p->n_adapters, pl.nseg, perm, offs, sseg, said, items, n_items,
-                         ctiles, n_ctiles, stream);
+                         ctiles, n_ctiles, stream, iaid, cseg);
     if (e != hipSuccess) return CTS_ERR_HIP;
   }
   if (mark(1, stream) != hipSuccess) return CTS_ERR_HIP;
@@ -692,14 +703,15 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
   g.b1_bytes = static_cast<uint32_t>(static_cast<uint64_t>(T) * p->d_in * pl.elt);
   g.perm = perm; g.sorted_seg = sseg;
   g.ksplit = mp.shrink_split; g.part = zpart;
-  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles;
+  g.tile_start = ctiles; g.n_tiles = n_ctiles; g.max_tiles = pl.max_ctiles; g.tile_seg = cseg;
   int32_t* ssplit = nullptr;
   if (shrink_adaptive(T, pl.shrink_tile)) {
     ssplit = reinterpret_cast<int32_t*>(ws + pl.off_ssplit);
     g.split_target = kShrinkAdaptiveTarget; g.split_out = ssplit;
   }
   if (fuse_sort) {
-    g.tile_start = nullptr; g.n_tiles = nullptr;
+    g.tile_start = nullptr; g.n_tiles = nullptr; g.tile_seg = nullptr;
+    g.fs_item_aid = iaid;
     g.fs_adapter = adapter_id; g.fs_cluster = cluster_of;
     g.fs_n = p->n_adapters; g.fs_K = pl.nseg;
     int bits_n = 0;
@@ -712,7 +724,7 @@ int run_multi(const cts_problem* p, const MultiPlan& mp, const int32_t* d_out, c
 
   // core product of every module on its slice of Z (rows M r apart), one launch
   e = cts::launch_sigma(zpart, mp.shrink_split, T, r, said, p->n_adapters, items, n_items, pl.max_items, Sigma[0],
-                        zp, p->dtype, stream, false, sseg, nullptr, nullptr, rt, ssplit, Sigma, mp.M);
+                        zp, p->dtype, stream, false, sseg, nullptr, nullptr, rt, ssplit, Sigma, mp.M, iaid);
   if (e != hipSuccess) return CTS_ERR_HIP;
   if (mark(3, stream) != hipSuccess) return CTS_ERR_HIP;
 

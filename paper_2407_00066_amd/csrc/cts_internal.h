@@ -54,11 +54,14 @@ inline int max_seg_tiles(int T, int nseg) {
 // are the sorted positions where a run of one adapter starts or crosses a
 // multiple of kSigmaChunk, items[c] = T, and n_items[0] = c; likewise the
 // segment tiles ctiles/n_ctiles for runs of one cluster and kSegTile.
+// Optionally item_aid[i] (the adapter of item i) and ctile_seg[i] (the
+// cluster of tile i), so that the later stages need not look them up
+// through the sorted positions.
 // cluster_of may be null (every adapter its own cluster, K == n).
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
                        int32_t* items, int32_t* n_items, int32_t* ctiles, int32_t* n_ctiles,
-                       hipStream_t stream);
+                       hipStream_t stream, int32_t* item_aid = nullptr, int32_t* ctile_seg = nullptr);
 
 // ----------------------------------------------------- segmented MFMA GEMM
 // Modules one fused-GEMM launch can hold.
@@ -94,6 +97,8 @@ struct GemmParams {
   // [tile_start[t], tile_start[t+1]) (at most the tile width); n_tiles[0]
   // tiles exist and the grid is sized for max_tiles (the rest exit at once)
   const int32_t* tile_start; const int32_t* n_tiles; int max_tiles;
+  // optional segment of each explicit tile (else sorted_seg[tile_start[t]])
+  const int32_t* tile_seg;
   // optional bucketing inside the kernel (token-tile mode, N <= kFuseSortMaxT;
   // fs_adapter != null): every workgroup sorts the N tokens by (cluster,
   // adapter, token) in LDS and takes its tile, perm and segments from there;
@@ -103,6 +108,7 @@ struct GemmParams {
   const int32_t* fs_adapter; const int32_t* fs_cluster;   // fs_cluster null: key = adapter
   int fs_n, fs_K, fs_bits_n;
   int32_t* fs_perm; int32_t* fs_seg; int32_t* fs_aid; int32_t* fs_items; int32_t* fs_nitems;
+  int32_t* fs_item_aid;   // optional: the adapter of each core-product item
   // token-tile mode of the LDS-ring tiles: split_target > 0 makes the split
   // along k follow the tile count n known on the device: S = min(ksplit,
   // ceil(split_target / (ceil(M / BM) n))) pieces.  The grid is then sized
@@ -163,7 +169,8 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         bool diag = false, const int32_t* sorted_seg = nullptr,
                         const int32_t* seg_rank = nullptr, int32_t* sorted_rank = nullptr,
                         int ldz = 0, const int32_t* split_dev = nullptr,
-                        const void* const* sigmas = nullptr, int nmod = 0);
+                        const void* const* sigmas = nullptr, int nmod = 0,
+                        const int32_t* item_aid = nullptr);
 
 // Records stage event i of the profiling aid (cts_set_stage_events) on s when
 // it is on; a no-op otherwise.

@@ -487,12 +487,24 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   if (FSORT) {
     static_assert(!FSORT || (C::NT >= kFuseSortMaxT && BN >= 64), "one token per thread; 64-token tiles");
     const int T = p.N;
+    // A cluster map that fits the ring's LDS (unused until the k loop) is
+    // staged there: its loads go out with the adapter ids', one round trip
+    // instead of a second, dependent one.
+    const bool map_lds = p.fs_cluster && p.fs_n <= static_cast<int>(C::SMEM / 4);
+    int32_t* const cmap = reinterpret_cast<int32_t*>(smem);
+    int a = 0;
     if (tid < T) {
-      int a = p.fs_adapter[tid];
+      a = p.fs_adapter[tid];
       a = a < 0 ? 0 : (a >= p.fs_n ? p.fs_n - 1 : a);
+    }
+    if (map_lds) {
+      for (int i = tid; i < p.fs_n; i += C::NT) cmap[i] = p.fs_cluster[i];
+      __syncthreads();
+    }
+    if (tid < T) {
       uint32_t key = static_cast<uint32_t>(a);
       if (p.fs_cluster) {
-        int c = p.fs_cluster[a];
+        int c = map_lds ? cmap[a] : p.fs_cluster[a];
         c = c < 0 ? 0 : (c >= p.fs_K ? p.fs_K - 1 : c);
         key |= static_cast<uint32_t>(c) << p.fs_bits_n;
       }
@@ -523,7 +535,11 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
         const bool si = valid && (j % kSigmaChunk == 0 || k != kp);
         const uint64_t bt = __ballot(st), bi = __ballot(si);
         if (st) fs_tile[nt_ + __popcll(bt & lt_mask)] = j;
-        if (si && blockIdx.x == 0) p.fs_items[ni_ + __popcll(bi & lt_mask)] = j;
+        if (si && blockIdx.x == 0) {
+          p.fs_items[ni_ + __popcll(bi & lt_mask)] = j;
+          if (p.fs_item_aid)
+            p.fs_item_aid[ni_ + __popcll(bi & lt_mask)] = static_cast<int32_t>(k & ((1u << p.fs_bits_n) - 1u));
+        }
         nt_ += __popcll(bt);
         ni_ += __popcll(bi);
       }
@@ -609,7 +625,8 @@ __global__ __launch_bounds__(WM * WN * 64, 1) void seg_gemm_dma_kernel(const Gem
   int K0 = p.K0, K1 = p.K1;
   bool b0_gather = true;
   if (tlist) {
-    const int seg = FSORT ? static_cast<int>(fs_key[j0] >> fs_cshift) : p.sorted_seg[j0];
+    const int seg = FSORT ? static_cast<int>(fs_key[j0] >> fs_cshift)
+                          : (p.tile_seg ? p.tile_seg[nt] : p.sorted_seg[j0]);
     A0 = static_cast<const char*>(A1v) + static_cast<int64_t>(seg) * a1_seg_bytes;
     a0_bytes = a1_seg_bytes; lda0 = p.lda1; K0 = p.K1;
     B0 = B1v; b0_bytes = b1v_bytes; ldb0 = p.ldb1; b0_gather = p.b1_gather != 0;

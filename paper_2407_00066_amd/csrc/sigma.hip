@@ -64,16 +64,25 @@ __global__ __launch_bounds__(kSigThreads) void sigma_diag_kernel(const float* __
                                                                  const int32_t* __restrict__ sorted_seg,
                                                                  const int32_t* __restrict__ seg_rank,
                                                                  int32_t* __restrict__ sorted_rank,
-                                                                 const int32_t* __restrict__ split_dev) {
+                                                                 const int32_t* __restrict__ split_dev,
+                                                                 const int32_t* __restrict__ item_aid) {
   const int item = blockIdx.x;
-  if (item >= n_items[0]) return;
-  if (split_dev) S = min(split_dev[0], S);
-  const int tid = threadIdx.x;
+  // the item's bounds and adapter are read with the item count (the grid
+  // covers max_items items; the arrays hold max_items + 1 entries)
+  const int n_it = n_items[0];
   const int lo = items[item], hi = items[item + 1];
+  const int a_it = item_aid[item];
+  // the shrink's split count (read from a valid address either way)
+  const int s_dev = (split_dev ? split_dev : n_items)[0];
+  // all five loads before the exit test: one round trip, not a chain
+  asm volatile("" ::"s"(lo), "s"(hi), "s"(a_it), "s"(s_dev));
+  if (item >= n_it) return;
+  if (split_dev) S = min(s_dev, S);
+  const int tid = threadIdx.x;
   const int cnt = (hi - lo) * r;
   const int rk = seg_rank ? seg_rank_of(seg_rank, sorted_seg[lo], r) : r;   // a multiple of 8
   if (sorted_rank && tid < hi - lo) sorted_rank[lo + tid] = rk;
-  int a = sorted_aid[lo];
+  int a = a_it;
   a = a < 0 ? 0 : (a >= n ? n - 1 : a);
   const TI* sa = sigma + static_cast<int64_t>(a) * r;
   const int64_t split_stride = static_cast<int64_t>(T) * r;
@@ -119,13 +128,23 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
                                                             const int32_t* __restrict__ seg_rank,
                                                             int32_t* __restrict__ sorted_rank, int ldz,
                                                             const int32_t* __restrict__ split_dev,
-                                                            const SigmaMods mods, int nmod) {
+                                                            const SigmaMods mods, int nmod,
+                                                            const int32_t* __restrict__ item_aid) {
   constexpr int kSigLd = MAXR + 4;
   __shared__ __attribute__((aligned(16))) float z[kSigmaChunk * kSigLd];
   __shared__ __attribute__((aligned(16))) float sig[MAXR * kSigLd];
 
   const int item = blockIdx.x;
-  if (item >= n_items[0]) return;
+  // the item's bounds and adapter are read with the item count (the grid
+  // covers max_items items; the arrays hold max_items + 1 entries)
+  const int n_it = n_items[0];
+  const int lo = items[item], hi = items[item + 1];
+  const int a_it = item_aid[item];
+  // the shrink's split count (read from a valid address either way)
+  const int s_dev = (split_dev ? split_dev : n_items)[0];
+  // all five loads before the exit test: one round trip, not a chain
+  asm volatile("" ::"s"(lo), "s"(hi), "s"(a_it), "s"(s_dev));
+  if (item >= n_it) return;
   if (nmod > 0) {
     const int m = blockIdx.y;
     Sigma = static_cast<const TI*>(mods.sigma[m]);
@@ -133,9 +152,8 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     zp += static_cast<int64_t>(m) * r;
   }
   // pieces the shrink actually split the reduction into (at most S)
-  if (split_dev) S = min(split_dev[0], S);
+  if (split_dev) S = min(s_dev, S);
   const int tid = threadIdx.x;
-  const int lo = items[item], hi = items[item + 1];
   const int nt = hi - lo;                 // tokens of this item (<= kSigmaChunk), one adapter
   const int cnt = nt * r;                 // outputs of this item
   // rank of the item's segment (a multiple of 8): Sigma's entries past it and
@@ -147,13 +165,16 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   // the item only) and its 16-byte pieces of Sigma_a (on the adapter) are
   // all in flight before the first is waited for.  z = sum over the
   // shrink's k-splits in fixed order; 4 consecutive values per thread and
-  // round, 16 splits' loads in flight at a time.  Rows of zpart and zp are
+  // round, ZB splits' loads in flight at a time.  Rows of zpart and zp are
   // ldz apart (ldz = r, or the stacked rank of several modules).
   const int64_t split_stride = static_cast<int64_t>(T) * ldz;
   const float* zbase = zpart + static_cast<int64_t>(lo) * ldz;
   constexpr int ZR = (kSigmaChunk * MAXR / 4 + kSigThreads - 1) / kSigThreads;   // rounds of 4 values
   f32x4 zacc[ZR];
-  f32x4 zv[ZR][16];
+  // splits whose loads are in flight together: 32 at rank <= 64 (the
+  // in-shrink bucketing's fixed split of a decode batch is up to 32), 16 above
+  constexpr int ZB = MAXR <= 64 ? 32 : 16;
+  f32x4 zv[ZR][ZB];
 #pragma unroll
   for (int u = 0; u < ZR; ++u) zacc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto zload = [&](int q) __attribute__((always_inline)) {
@@ -163,7 +184,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
       const bool ok = e4 < cnt && e4 % r < rk;
       const int64_t zo = static_cast<int64_t>(e4 / r) * ldz + e4 % r;
 #pragma unroll
-      for (int w = 0; w < 16; ++w)
+      for (int w = 0; w < ZB; ++w)
         if (ok && q + w < S) zv[u][w] = *reinterpret_cast<const f32x4*>(zbase + (q + w) * split_stride + zo);
     }
   };
@@ -173,7 +194,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
       const int e4 = (tid + u * kSigThreads) * 4;
       const bool ok = e4 < cnt && e4 % r < rk;
 #pragma unroll
-      for (int w = 0; w < 16; ++w)
+      for (int w = 0; w < ZB; ++w)
         if (ok && q + w < S) zacc[u] += zv[u][w];
     }
   };
@@ -181,7 +202,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
 
   // Sigma_a -> LDS as fp32
   if (Sigma != nullptr) {
-    int a = sorted_aid[lo];
+    int a = a_it;
     a = a < 0 ? 0 : (a >= n ? n - 1 : a);
     constexpr int V = Vec16<TI>::N;
     constexpr int PER = (MAXR * MAXR / V + kSigThreads - 1) / kSigThreads;
@@ -211,7 +232,7 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
     zsum(0);
   }
   // splits past the first 16
-  for (int q = 16; q < S; q += 16) {
+  for (int q = ZB; q < S; q += ZB) {
     zload(q);
     zsum(q);
   }
@@ -309,8 +330,9 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
                         const void* Sigma, void* zp, int in_dtype, hipStream_t stream,
                         bool diag, const int32_t* sorted_seg, const int32_t* seg_rank,
                         int32_t* sorted_rank, int ldz, const int32_t* split_dev,
-                        const void* const* sigmas, int nmod) {
+                        const void* const* sigmas, int nmod, const int32_t* item_aid) {
   if (seg_rank && !sorted_seg) return hipErrorInvalidValue;
+  if (!item_aid) return hipErrorInvalidValue;
   if (sorted_rank && !seg_rank) return hipErrorInvalidValue;
   if (ldz <= 0) ldz = r;
   if (ldz != r && (diag || ldz < r || ldz % 4)) return hipErrorInvalidValue;
@@ -323,30 +345,30 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
     if (in_dtype == 0)
       hipLaunchKernelGGL(sigma_diag_kernel<float>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                         static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev);
+                         static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev, item_aid);
     else
       hipLaunchKernelGGL(sigma_diag_kernel<bf16_t>, grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                          sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev);
+                         static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, split_dev, item_aid);
     return hipGetLastError();
   }
   if (r > 128) return hipErrorInvalidValue;
   if (in_dtype == 0 && r <= 64)
     hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
   else if (in_dtype == 0)
     hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
+                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
   else if (r <= 64)
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
   else
     hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
                        sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod);
+                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
   return hipGetLastError();
 }
 

@@ -99,7 +99,7 @@ __global__ __launch_bounds__(NT) void sort_kernel(
     int K, int bits_n, int bits_k, int32_t* __restrict__ perm, int32_t* __restrict__ offs,
     int32_t* __restrict__ sorted_seg, int32_t* __restrict__ sorted_aid,
     int32_t* __restrict__ items, int32_t* __restrict__ n_items, int32_t* __restrict__ ctiles,
-    int32_t* __restrict__ n_ctiles) {
+    int32_t* __restrict__ n_ctiles, int32_t* __restrict__ item_aid, int32_t* __restrict__ ctile_seg) {
   using C = SortCfg<NT>;
   constexpr int kWaves = C::W;
   __shared__ uint32_t kbuf[2][C::MAXT];
@@ -327,8 +327,14 @@ __global__ __launch_bounds__(NT) void sort_kernel(
       const uint32_t k = kbuf[in][j];
       const bool si = (j % kSigmaChunk == 0) || k != kp;
       const bool sc = (j % kSegTile == 0) || (k >> cshift) != (kp >> cshift);
-      if (si && items) items[bi] = j;
-      if (sc && ctiles) ctiles[bc] = j;
+      if (si && items) {
+        items[bi] = j;
+        if (item_aid) item_aid[bi] = static_cast<int32_t>(k & amask);
+      }
+      if (sc && ctiles) {
+        ctiles[bc] = j;
+        if (ctile_seg) ctile_seg[bc] = static_cast<int32_t>(k >> cshift);
+      }
       bi += si ? 1u : 0u;
       bc += sc ? 1u : 0u;
       kp = k;
@@ -361,17 +367,17 @@ int ceil_log2(int v) {
 hipError_t launch_sort(const int32_t* adapter_id, const int32_t* cluster_of, int T, int n, int K,
                        int32_t* perm, int32_t* offs, int32_t* sorted_seg, int32_t* sorted_aid,
                        int32_t* items, int32_t* n_items, int32_t* ctiles, int32_t* n_ctiles,
-                       hipStream_t stream) {
+                       hipStream_t stream, int32_t* item_aid, int32_t* ctile_seg) {
   const int bits_n = ceil_log2(n);
   const int bits_k = cluster_of ? ceil_log2(K) : 0;  // key is the adapter alone when K == n
   if (T <= kSortSmallT)
     hipLaunchKernelGGL(sort_kernel<256>, dim3(1), dim3(256), 0, stream, adapter_id, cluster_of,
                        T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
-                       ctiles, n_ctiles);
+                       ctiles, n_ctiles, item_aid, ctile_seg);
   else
     hipLaunchKernelGGL(sort_kernel<1024>, dim3(1), dim3(1024), 0, stream, adapter_id, cluster_of,
                        T, n, K, bits_n, bits_k, perm, offs, sorted_seg, sorted_aid, items, n_items,
-                       ctiles, n_ctiles);
+                       ctiles, n_ctiles, item_aid, ctile_seg);
   return hipGetLastError();
 }
 
