@@ -116,7 +116,10 @@ struct SigmaMods {
   const void* sigma[CTS_MAX_MODULES];
 };
 
-template <typename TI, int MAXR>
+// ZB: split partials whose loads are in flight together per thread (the
+// host picks the smallest of 8, 16 or 32 that covers the split; fewer
+// registers mean more workgroups resident when there are many items)
+template <typename TI, int MAXR, int ZB>
 __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restrict__ zpart, int S,
                                                             int T, int r,
                                                             const int32_t* __restrict__ sorted_aid,
@@ -171,9 +174,6 @@ __global__ __launch_bounds__(kSigThreads) void sigma_kernel(const float* __restr
   const float* zbase = zpart + static_cast<int64_t>(lo) * ldz;
   constexpr int ZR = (kSigmaChunk * MAXR / 4 + kSigThreads - 1) / kSigThreads;   // rounds of 4 values
   f32x4 zacc[ZR];
-  // splits whose loads are in flight together: 32 at rank <= 64 (the
-  // in-shrink bucketing's fixed split of a decode batch is up to 32), 16 above
-  constexpr int ZB = MAXR <= 64 ? 32 : 16;
   f32x4 zv[ZR][ZB];
 #pragma unroll
   for (int u = 0; u < ZR; ++u) zacc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -353,22 +353,29 @@ hipError_t launch_sigma(const float* zpart, int S, int T, int r, const int32_t* 
     return hipGetLastError();
   }
   if (r > 128) return hipErrorInvalidValue;
-  if (in_dtype == 0 && r <= 64)
-    hipLaunchKernelGGL((sigma_kernel<float, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
-  else if (in_dtype == 0)
-    hipLaunchKernelGGL((sigma_kernel<float, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, items, n_items, static_cast<const float*>(Sigma),
-                       static_cast<float*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
-  else if (r <= 64)
-    hipLaunchKernelGGL((sigma_kernel<bf16_t, 64>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
-  else
-    hipLaunchKernelGGL((sigma_kernel<bf16_t, 128>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r,
-                       sorted_aid, n, items, n_items, static_cast<const bf16_t*>(Sigma),
-                       static_cast<bf16_t*>(zp), sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid);
+  // S: the most pieces the shrink may have split into (the device-chosen
+  // split is at most S)
+  const int zb = S <= 8 ? 8 : (S <= 16 || r > 64) ? 16 : 32;
+#define CTS_SIGMA_LAUNCH(TI_, MAXR_, ZB_)                                                              \
+  hipLaunchKernelGGL((sigma_kernel<TI_, MAXR_, ZB_>), grid, dim3(kSigThreads), 0, stream, zpart, S, T, r, \
+                     sorted_aid, n, items, n_items, static_cast<const TI_*>(Sigma), static_cast<TI_*>(zp), \
+                     sorted_seg, seg_rank, sorted_rank, ldz, split_dev, mods, nmod, item_aid)
+  if (in_dtype == 0 && r <= 64) {
+    if (zb == 8) CTS_SIGMA_LAUNCH(float, 64, 8);
+    else if (zb == 16) CTS_SIGMA_LAUNCH(float, 64, 16);
+    else CTS_SIGMA_LAUNCH(float, 64, 32);
+  } else if (in_dtype == 0) {
+    if (zb == 8) CTS_SIGMA_LAUNCH(float, 128, 8);
+    else CTS_SIGMA_LAUNCH(float, 128, 16);
+  } else if (r <= 64) {
+    if (zb == 8) CTS_SIGMA_LAUNCH(bf16_t, 64, 8);
+    else if (zb == 16) CTS_SIGMA_LAUNCH(bf16_t, 64, 16);
+    else CTS_SIGMA_LAUNCH(bf16_t, 64, 32);
+  } else {
+    if (zb == 8) CTS_SIGMA_LAUNCH(bf16_t, 128, 8);
+    else CTS_SIGMA_LAUNCH(bf16_t, 128, 16);
+  }
+#undef CTS_SIGMA_LAUNCH
   return hipGetLastError();
 }
 
