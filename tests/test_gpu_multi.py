@@ -22,6 +22,11 @@ CASES = {
                             n_seq=12, seq_len=(60, 300)),
     # fp32, ragged
     "f32_pair": dict(cfg=143, T=77, d_in=128, d_outs=(96, 64), r=16, n=10, K=3, dtype="f32"),
+    # the modules' GEMMs in one launch split along d_in (decode tile, split 4) with one split-K sum
+    # over all modules' partials
+    "qkv_grouped_split": dict(cfg=148, T=64, d_in=2048, d_outs=(512, 128, 128), r=32, n=40, K=4),
+    # the same with 128x64 tiles (split 2), a module narrower than one row tile, Zipf ids
+    "mixed_grouped_split": dict(cfg=149, T=200, d_in=1024, d_outs=(256, 128, 64), r=16, n=60, K=5, ids="zipf"),
 }
 
 
