@@ -11,9 +11,12 @@ down) with their own weights: q/k/v and gate/up through one cts_apply_multi
 call each (they read the same x), o and down through cts_apply; the same
 pass with every projection its own cts_apply call is reported beside it.  The timed region is
 K consecutive steps between two HIP events on the stream the library launches
-on; the steps are launched call by call.  The same steps replayed from HIP
-graphs captured from their cts_apply calls (as a serving loop replays a decode
-step) are reported under "graph_replay".  Single-layer inputs are rotated over enough device copies (>= 512 MB in
+on; the steps are launched call by call.  The same steps replayed from a HIP
+graph captured from their calls are reported under "graph_replay": one graph
+holds the calls on every rotated input set in turn (for stack32, one whole
+step), as a serving loop replays one graph per forward pass; single-layer
+lines also give the time with one graph per call ("one_call_graph_ms_per_step"),
+which pays the graph's launch every call.  Single-layer inputs are rotated over enough device copies (>= 512 MB in
 total) that the 256 MB last-level cache cannot hold them between steps; the
 stack's weights (about 32 GB) are distinct per projection anyway.
 
@@ -219,14 +222,44 @@ def captured(fn, sets, torch):
     return graphs
 
 
-def time_launches(fn, sets, args, torch):
+def time_chain(fn, sets, steps, warmup, torch):
+    """ms per step of one HIP graph holding fn(set) for every input set in
+    turn, replayed until at least `steps` steps have run: consecutive calls on
+    different inputs, as a serving loop replays one graph holding the calls of
+    a whole forward pass (the launch of a graph, ~5-10 us on this ROCm, is paid
+    once per replay, not once per call)."""
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for st in sets:
+            fn(st)
+    torch.cuda.synchronize()
+    reps = max(1, math.ceil(steps / len(sets)))
+    for _ in range(max(1, math.ceil(warmup / len(sets)))):
+        g.replay()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(reps):
+        g.replay()
+    ev1.record()
+    torch.cuda.synchronize()
+    del g
+    return ev0.elapsed_time(ev1) / (reps * len(sets))
+
+
+def time_launches(fn, sets, args, torch, one_call=False):
     """(eager ms, graph-replay ms) per step: the step launched call by call,
-    then from its captured graph."""
+    then from one captured graph holding the calls of every input set in turn;
+    with one_call, also (third) one graph per call, replayed call by call."""
     eager = time_steps(fn, sets, args.steps, args.warmup, torch)
+    chain = time_chain(fn, sets, args.steps, args.warmup, torch)
+    if not one_call:
+        return eager, chain
     graphs = captured(fn, sets, torch)
-    graph = time_steps(lambda g: g.replay(), graphs, args.steps, args.warmup, torch)
+    single = time_steps(lambda g: g.replay(), graphs, args.steps, args.warmup, torch)
     del graphs
-    return eager, graph
+    return eager, chain, single
 
 
 STAGES = ["sort", "shrink", "sigma", "fused_gemm", "splitk_reduce"]
@@ -501,7 +534,7 @@ def bench_layer(args, torch, np, cts, B, wl, device):
 
     log("timing cts_apply: %d sets of %.1f MB, %d warmup + %d steps" %
         (n_sets, set_bytes / 1e6, args.warmup, args.steps))
-    ms, ms_g = time_launches(step, sets, args, torch)
+    ms, ms_g, ms_g1 = time_launches(step, sets, args, torch, one_call=True)
     stages = stage_times(step, sets, args.steps, torch, B)
     g_int, g_mark = gemm_times(step, sets, args.steps, args.warmup, torch, B)
 
@@ -560,7 +593,8 @@ def bench_layer(args, torch, np, cts, B, wl, device):
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "graph_replay": {"value": round(w.T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5)},
+        "graph_replay": {"value": round(w.T / (ms_g * 1e-3), 1), "ms_per_step": round(ms_g, 5),
+                         "calls_per_graph": len(sets), "one_call_graph_ms_per_step": round(ms_g1, 5)},
         "dtype": w.dtype, "data": "synthetic (seeded; inputs resident in HBM, rotated over %d copies)" % n_sets,
         "config": {"workload": args.workload, "sigma": args.sigma, "ranks": args.ranks,
                    "cluster_ranks": None if rk is None else rk.tolist(), "T": w.T, "d_in": w.d_in, "d_out": w.d_out, "r": w.r,
