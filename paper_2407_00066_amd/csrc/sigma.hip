@@ -298,18 +298,38 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     ldo = mods.ldo[q];
     m = mc - mods.col[q];
   }
+  const int64_t row = perm ? perm[j] : j;     // read with the partials
   float acc[V];
 #pragma unroll
   for (int v = 0; v < V; ++v) acc[v] = 0.f;
-  for (int s = 0; s < S; ++s) {
-    const float* src = part + (static_cast<int64_t>(s) * N + j) * M + mc;
+  // the partials are summed in piece order; four pieces' loads go out before
+  // their sums, so a launch waits for one round trip per four pieces (not one
+  // per piece)
+  const float* src0 = part + static_cast<int64_t>(j) * M + mc;
+  const int64_t pstride = static_cast<int64_t>(N) * M;
+  int s = 0;
+  for (; s + 4 <= S; s += 4) {
+    f32x4 x[4][V / 4];
 #pragma unroll
-    for (int v = 0; v < V; v += 4) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(src + v);
-      acc[v] += x[0]; acc[v + 1] += x[1]; acc[v + 2] += x[2]; acc[v + 3] += x[3];
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < V / 4; ++v)
+        x[u][v] = *reinterpret_cast<const f32x4*>(src0 + (s + u) * pstride + 4 * v);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int v = 0; v < V / 4; ++v) {
+        acc[4 * v] += x[u][v][0]; acc[4 * v + 1] += x[u][v][1];
+        acc[4 * v + 2] += x[u][v][2]; acc[4 * v + 3] += x[u][v][3];
+      }
+  }
+  for (; s < S; ++s) {
+#pragma unroll
+    for (int v = 0; v < V / 4; ++v) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(src0 + s * pstride + 4 * v);
+      acc[4 * v] += x[0]; acc[4 * v + 1] += x[1]; acc[4 * v + 2] += x[2]; acc[4 * v + 3] += x[3];
     }
   }
-  const int64_t row = perm ? perm[j] : j;
   if (OUT_BF16) {
     uint4 w;
     w.x = f32_to_bf16(acc[0]) | (static_cast<uint32_t>(f32_to_bf16(acc[1])) << 16);
